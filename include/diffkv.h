@@ -1,0 +1,254 @@
+/*
+ * diffkv.h -- C ABI of the DiffKV decode hot path for AMD Instinct MI355X
+ * (gfx950).  DiffKV: arXiv 2412.03131, "Differentiated Memory Management
+ * for Large Language Models with Parallel KV Compaction".
+ *
+ * What the library computes
+ *   A differentiated, paged KV cache: keys are kept at more bits than values
+ *   (K8V4 for high-precision tokens, K4V2 for low-precision tokens, Sec. 4),
+ *   each token is kept high, kept low or pruned by its significance score
+ *   (Sec. 4), and every (sequence, KV head) pair -- a "table" -- keeps its own
+ *   number of tokens of each kind.  Memory is managed with unified pages, a
+ *   circular free page list and bidirectional page tables (Sec. 5.2); decode
+ *   attention reads the compressed pages directly (Sec. 6.2).
+ *
+ * Conventions
+ *   - All entry points are C, take plain pointers and sizes, never allocate,
+ *     free or synchronise, and keep no state between calls.
+ *   - "device" pointers point to GPU memory of the current HIP device;
+ *     "host" pointers to CPU memory.  The caller owns every buffer.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     All work is enqueued on it and the call returns immediately.  Calls
+ *     on one cache must be ordered on one stream; different caches are
+ *     independent.
+ *   - Return value: host-detectable errors (bad arguments, unsupported
+ *     layout, small workspace, launch failure).  On any non-OK return
+ *     nothing was enqueued (except DIFFKV_E_LAUNCH, which reports that an
+ *     enqueue failed).
+ *   - Device-detected conditions set sticky bits in *cache->status (device
+ *     word, never cleared by the library).  The operations that can set them
+ *     are all-or-nothing: when a bit is raised by a call, that call changed
+ *     nothing in the cache.  The caller reads the word after a sync and
+ *     recovers (e.g. releases finished sequences through compaction, then
+ *     retries), and clears it.
+ *   - fp16 values are passed as IEEE binary16 bit patterns (uint16_t).
+ */
+#ifndef DIFFKV_H
+#define DIFFKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t diffkv_status;
+enum {
+    DIFFKV_OK = 0,
+    DIFFKV_E_INVAL = 1,       /* null pointer, negative or inconsistent size       */
+    DIFFKV_E_UNSUPPORTED = 2, /* layout/shape the gfx950 kernels do not implement  */
+    DIFFKV_E_WORKSPACE = 3,   /* ws_bytes smaller than diffkv_workspace_size()     */
+    DIFFKV_E_LAUNCH = 4       /* a HIP launch or runtime call failed               */
+};
+
+/* sticky bits of *diffkv_cache.status */
+enum {
+    DIFFKV_ST_OUT_OF_PAGES = 1u,   /* the free region (tail - head) was too small     */
+    DIFFKV_ST_TABLE_OVERFLOW = 2u, /* a table would hold more than p_max pages        */
+    DIFFKV_ST_BAD_INPUT = 4u       /* new_len disagreed with total_new / max_new      */
+};
+
+enum { DIFFKV_HIGH = 0, DIFFKV_LOW = 1 };
+
+/*
+ * Page layout (Sec. 5.2, "unified pages").  Every page has the same byte
+ * stride; its precision is fixed when a table takes it.  A page of
+ * precision p holds T = tokens_per_page[p] tokens in six segments, in this
+ * order, each starting on a 64-byte boundary of the page:
+ *   K codes   [head_dim*k_bits/128 chunks][T][16 B]: chunk c holds dims
+ *             c*(128/k_bits) .. +128/k_bits-1 of one token, element e at
+ *             bit e*k_bits of the 16 bytes;
+ *   K meta    [T][head_dim/group] {fp16 scale, fp16 zero};
+ *   V codes   [head_dim][T*v_bits/8 B]: token slot s of dim d at bit s*v_bits
+ *             of the dim's row;
+ *   V meta    [head_dim/group][T] {fp16 scale, fp16 zero};
+ *   scores    [T] fp32 (significance score as given);
+ *   positions [T] int32 (token position in its sequence).
+ * Bits are little-endian within bytes.  page_bytes = the larger of the two
+ * precisions' sizes.  A fresh page (one whose slot 0 is being written) is
+ * cleared first, so unused slots are zero bytes.
+ * Table width p_max = ceil(max_seq_len / tokens_per_page[HIGH]) + 1: one
+ * more than the paper's max_len / T_high, since a partial high page and a
+ * partial low page can coexist.
+ */
+typedef struct diffkv_layout {
+    int32_t head_dim, group;
+    int32_t k_bits[2], v_bits[2];      /* [HIGH], [LOW]                       */
+    int32_t tokens_per_page[2];        /* [HIGH], [LOW]                       */
+    int32_t max_seq_len, p_max;
+    int64_t page_bytes;
+    int32_t off_kcode[2], off_kmeta[2], off_vcode[2], off_vmeta[2];
+    int32_t off_score[2], off_pos[2], used_bytes[2];
+} diffkv_layout;
+
+/*
+ * Cache state (all device memory, all caller-owned).  Table t = b*num_kv_heads
+ * + h is the bidirectional page table of sequence b, KV head h (Sec. 5.2):
+ * high-precision page IDs grow from slot 0 to the right, low-precision page
+ * IDs from slot p_max-1 to the left; empty slots hold -1.  Token u of a
+ * section lives in slot u % T of the section's page u / T, in position
+ * order.  The free page list is a ring of num_pages IDs; the free IDs are
+ * ring[head % n .. tail % n) with head/tail monotone int64 counters
+ * (start pointer allocates, end pointer recycles).
+ */
+typedef struct diffkv_cache {
+    uint8_t*  pool;          /* device [num_pages][page_bytes]                     */
+    int64_t   num_pages;
+    int32_t*  page_table;    /* device [num_tables][p_max]                         */
+    int32_t*  pages;         /* device [num_tables][2] pages held per section      */
+    int32_t*  len;           /* device [num_tables][2] tokens held per section     */
+    int32_t*  seq_len;       /* device [num_seqs] tokens seen per sequence (incl.
+                                pruned); the threshold form's N                   */
+    int32_t*  ring;          /* device [num_pages] circular free page list         */
+    int64_t*  ring_ptr;      /* device [2] {head, tail}; tail - head = free pages  */
+    uint32_t* status;        /* device [1] sticky DIFFKV_ST_* bits                 */
+    int32_t   num_seqs;      /* B                                                  */
+    int32_t   num_kv_heads;  /* Hkv; num_tables = B * Hkv                          */
+} diffkv_cache;
+
+/* Fill *out (host) from the parameters: segment offsets, page_bytes, p_max.
+ * Bits must be 1, 2, 4 or 8, head_dim*k_bits a multiple of 128,
+ * T*v_bits a multiple of 8, tokens_per_page[LOW] >= tokens_per_page[HIGH].
+ * DIFFKV_E_INVAL otherwise.  Any valid layout is accepted here; the
+ * append and attention kernels implement head_dim 128, group 32, K8V4/K4V2
+ * and 16/32 tokens per page (DIFFKV_E_UNSUPPORTED otherwise); allocation
+ * and compaction accept any valid layout. */
+diffkv_status diffkv_layout_init(diffkv_layout* out, int32_t head_dim, int32_t group,
+                                 const int32_t k_bits[2], const int32_t v_bits[2],
+                                 const int32_t tokens_per_page[2], int32_t max_seq_len);
+
+enum {
+    DIFFKV_OP_APPEND = 0,
+    DIFFKV_OP_ATTENTION = 1,
+    DIFFKV_OP_COMPACT = 2,
+    DIFFKV_OP_ALLOC = 3
+};
+
+/* Bytes of device workspace the operation needs (host out-parameter).
+ * APPEND: num_seqs, num_kv_heads, total_new.  ATTENTION: num_seqs,
+ * num_q_heads, num_splits (0 = the automatic choice for these sizes).
+ * COMPACT / ALLOC: num_seqs*num_kv_heads tables.  Unused sizes are ignored. */
+diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout,
+                                    int32_t num_seqs, int32_t num_q_heads,
+                                    int32_t num_kv_heads, int64_t total_new,
+                                    int32_t num_splits, size_t* bytes);
+
+/* The split count diffkv_decode_attention uses for num_splits = 0. */
+int32_t diffkv_auto_splits(const diffkv_layout* layout, int32_t num_seqs, int32_t num_kv_heads);
+
+/*
+ * KV compressor (Sec. 4) + page placement (Sec. 5.2, 5.3): classes the new
+ * tokens of every table, reserves the pages both sections now need with one
+ * prefix-sum schedule over all tables, then quantizes and stores every kept
+ * token.
+ *
+ *   new_len  device int32 [num_seqs]: new tokens of sequence b; their rows in
+ *            k/v/score are new_off(b) .. +new_len[b]-1, new_off(b) =
+ *            sum of new_len[0..b).  Must sum to total_new with every entry in
+ *            [0, max_new], else DIFFKV_ST_BAD_INPUT is raised and nothing
+ *            changes.
+ *   k, v     device fp16 [total_new][num_kv_heads][head_dim].
+ *   score    device fp32 [total_new][num_kv_heads]: significance (not NaN).
+ *   quota    device int32 [num_seqs][num_kv_heads][2] = {n_high, n_low}, or
+ *            NULL.  Quota form: the non-window new tokens are ranked by
+ *            (score descending, position ascending; -0 == +0); the first
+ *            min(n_high, avail) are high, the next min(n_low, avail - n_high')
+ *            low, the rest pruned.  Threshold form (quota == NULL; Sec. 4,
+ *            Algorithm 1): high iff score >= alpha_h / N, else low iff
+ *            score >= alpha_l / N, else pruned, N = seq_len[b] + new_len[b]
+ *            and both thresholds computed in fp32.
+ *   recent_window  the last W new tokens of each sequence are high precision
+ *            and outside the quotas (W >= 0).
+ *
+ * Quantization (Sec. 2.2) per 32-dim group of each kept K and V vector:
+ *   s = fp16_rne((max - min) / (2^b - 1)) in fp32, z = min (with -0 -> +0),
+ *   code = clamp(rint((x - z) / s), 0, 2^b - 1) in fp32 with the stored fp16
+ *   s and z, code = 0 when s == 0; b = k_bits/v_bits of the token's class.
+ * Placement: kept tokens of a section take section indices len .. in
+ *   position order.  Page demand per section = ceil((len + added) / T) -
+ *   pages (if positive).  Tables take their new IDs from the ring region
+ *   after the demands of all lower tables, high pages first; head advances
+ *   by the total.  Raises OUT_OF_PAGES / TABLE_OVERFLOW all-or-nothing.
+ * Updates pool, page_table, pages, len, seq_len (+= new_len), ring_ptr[0].
+ * Workspace: diffkv_workspace_size(DIFFKV_OP_APPEND, ...).
+ */
+diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_cache* cache,
+                                     int64_t total_new, int32_t max_new,
+                                     const int32_t* new_len,
+                                     const uint16_t* k, const uint16_t* v,
+                                     const float* score, const int32_t* quota,
+                                     float alpha_h, float alpha_l, int32_t recent_window,
+                                     void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Decode attention over the compressed cache, Eq. (1) of Sec. 2.1, one new
+ * query per sequence and query head (Sec. 6.2):
+ *   out[b][hq] = sum_j softmax_j(sm_scale * q[b][hq] . k_hat_j) v_hat_j
+ * over every kept token of table b*Hkv + hq/(Hq/Hkv): the high section, then
+ * the low section; k_hat = s*code + z per group.  fp32 accumulation.
+ *   q    device fp16 [num_seqs][num_q_heads][head_dim]
+ *   out  device fp32 [num_seqs][num_q_heads][head_dim]
+ *   lse  device fp32 [num_seqs][num_q_heads] (natural log of the softmax
+ *        denominator incl. the max) or NULL.  An empty table gives out = 0,
+ *        lse = -inf.
+ *   num_splits  0 = automatic, 1 = one workgroup per table, S > 1 = the
+ *        table's page list is cut into S page-aligned ranges whose partial
+ *        (max, sum, acc) states are merged afterwards (Sec. 6.2 sequence
+ *        split).  Results are deterministic for a given S.
+ * num_q_heads must be a multiple of num_kv_heads, with at most 8 query heads
+ * per KV head.
+ */
+diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_cache* cache,
+                                      int32_t num_q_heads, const uint16_t* q, float sm_scale,
+                                      float* out, float* lse, int32_t num_splits,
+                                      void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Parallel free-list compaction (Sec. 5.2 recycling, Sec. 5.3): for the
+ * first num_tables tables, every live slot whose release byte is nonzero
+ * gives its page back.  With one prefix sum over tables, table t writes its
+ * released IDs -- in ascending slot order -- to ring[(tail + off_t + i) % n];
+ * tail advances by the total.  Each table is then squeezed in place: kept
+ * high IDs packed from slot 0 and kept low IDs from slot p_max-1, both in
+ * their section order; vacated slots become -1.  A released page removes its
+ * tokens from the section (T, or the tail page's fill; later pages shift
+ * down).  Request completion = releasing every live slot of its tables.
+ *   release  device uint8 [num_tables][p_max]; bytes of non-live slots are
+ *            ignored.
+ * Never fails on the device (released IDs always fit the ring).
+ */
+diffkv_status diffkv_compact_free_list(const diffkv_layout* layout, const diffkv_cache* cache,
+                                       int32_t num_tables, const uint8_t* release,
+                                       void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Page allocation alone (Sec. 5.2 allocation; the prompt phase's
+ * conservative reservation of Sec. 5.3): table t appends demand[t][HIGH]
+ * pages to its high side and demand[t][LOW] to its low side, reading IDs
+ * from the ring region after the demands of tables 0..t-1; head advances by
+ * the total.  len is unchanged (the new pages are spare until an append
+ * fills them).  All-or-nothing OUT_OF_PAGES / TABLE_OVERFLOW.
+ *   demand  device int32 [num_tables][2], entries >= 0.
+ */
+diffkv_status diffkv_alloc_pages(const diffkv_layout* layout, const diffkv_cache* cache,
+                                 int32_t num_tables, const int32_t* demand,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/* Static string for a diffkv_status value. */
+const char* diffkv_status_str(diffkv_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,361 @@
+// api.cpp -- the C ABI of include/diffkv.h: argument checks, workspace
+// carving and kernel dispatch.  No allocation, no synchronisation.
+#include <string.h>
+
+#include "internal.hpp"
+
+using namespace dkv;
+
+namespace {
+
+int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+int32_t align64(int64_t x) { return (int32_t)((x + 63) & ~(int64_t)63); }
+bool bits_ok(int b) { return b == 1 || b == 2 || b == 4 || b == 8; }
+
+diffkv_status fill_layout(diffkv_layout* L, int32_t head_dim, int32_t group, const int32_t kb[2],
+                          const int32_t vb[2], const int32_t tp[2], int32_t max_seq_len)
+{
+    if (!L || !kb || !vb || !tp) return DIFFKV_E_INVAL;
+    if (head_dim <= 0 || group <= 0 || head_dim % group != 0 || group > 256 || max_seq_len <= 0)
+        return DIFFKV_E_INVAL;
+    for (int p = 0; p < 2; ++p) {
+        if (!bits_ok(kb[p]) || !bits_ok(vb[p]) || tp[p] <= 0) return DIFFKV_E_INVAL;
+        if ((head_dim * kb[p]) % 128 != 0 || (tp[p] * vb[p]) % 8 != 0) return DIFFKV_E_INVAL;
+    }
+    if (tp[1] < tp[0]) return DIFFKV_E_INVAL;
+    diffkv_layout o;
+    memset(&o, 0, sizeof(o));
+    o.head_dim = head_dim;
+    o.group = group;
+    o.max_seq_len = max_seq_len;
+    const int ng = head_dim / group;
+    int64_t page = 0;
+    for (int p = 0; p < 2; ++p) {
+        const int T = tp[p];
+        o.k_bits[p] = kb[p];
+        o.v_bits[p] = vb[p];
+        o.tokens_per_page[p] = T;
+        int64_t off = 0;
+        o.off_kcode[p] = (int32_t)off;
+        off = align64(off + (int64_t)(head_dim * kb[p] / 128) * T * 16);
+        o.off_kmeta[p] = (int32_t)off;
+        off = align64(off + (int64_t)T * ng * 4);
+        o.off_vcode[p] = (int32_t)off;
+        off = align64(off + (int64_t)head_dim * (T * vb[p] / 8));
+        o.off_vmeta[p] = (int32_t)off;
+        off = align64(off + (int64_t)ng * T * 4);
+        o.off_score[p] = (int32_t)off;
+        off = align64(off + (int64_t)T * 4);
+        o.off_pos[p] = (int32_t)off;
+        off = align64(off + (int64_t)T * 4);
+        o.used_bytes[p] = (int32_t)off;
+        if (off > page) page = off;
+    }
+    o.page_bytes = page;
+    o.p_max = (max_seq_len + tp[0] - 1) / tp[0] + 1;
+    *L = o;
+    return DIFFKV_OK;
+}
+
+// A layout passed in must be one diffkv_layout_init produced.
+bool layout_valid(const diffkv_layout* L)
+{
+    if (!L) return false;
+    diffkv_layout r;
+    if (fill_layout(&r, L->head_dim, L->group, L->k_bits, L->v_bits, L->tokens_per_page,
+                    L->max_seq_len) != DIFFKV_OK)
+        return false;
+    return memcmp(&r, L, sizeof(r)) == 0;
+}
+
+bool layout_kernels_supported(const diffkv_layout* L)
+{
+    return L->head_dim == kD && L->group == kG && L->k_bits[0] == 8 && L->k_bits[1] == 4 &&
+           L->v_bits[0] == 4 && L->v_bits[1] == 2 && L->tokens_per_page[0] == kTHi &&
+           L->tokens_per_page[1] == kTLo;
+}
+
+bool cache_valid(const diffkv_cache* c)
+{
+    return c && c->page_table && c->pages && c->len && c->ring && c->ring_ptr && c->status &&
+           c->num_pages > 0 && c->num_pages <= INT32_MAX && c->num_seqs >= 0 && c->num_kv_heads > 0 &&
+           (int64_t)c->num_seqs * c->num_kv_heads <= INT32_MAX;
+}
+
+void fill_layout_args(LayoutArgs& a, const diffkv_layout* L)
+{
+    a.p_max = L->p_max;
+    a.page_bytes = L->page_bytes;
+    for (int p = 0; p < 2; ++p) {
+        a.T[p] = L->tokens_per_page[p];
+        a.off_kcode[p] = L->off_kcode[p];
+        a.off_kmeta[p] = L->off_kmeta[p];
+        a.off_vcode[p] = L->off_vcode[p];
+        a.off_vmeta[p] = L->off_vmeta[p];
+        a.off_score[p] = L->off_score[p];
+        a.off_pos[p] = L->off_pos[p];
+    }
+}
+
+struct AppendWs {
+    int64_t flags, tstate, sold, row_off, ord, jobs, total;
+    int64_t max_jobs;
+};
+
+AppendWs append_ws(int64_t B, int64_t Hkv, int64_t total_new)
+{
+    AppendWs w;
+    const int64_t T = B * Hkv;
+    w.max_jobs = Hkv * ((3 * total_new + 31) / 32 + 4 * B);
+    int64_t o = 0;
+    w.flags = o;   o = align256(o + (int64_t)sizeof(CallFlags));
+    w.tstate = o;  o = align256(o + T * (int64_t)sizeof(TState));
+    w.sold = o;    o = align256(o + B * 4);
+    w.row_off = o; o = align256(o + B * 4);
+    w.ord = o;     o = align256(o + total_new * Hkv * 4);
+    w.jobs = o;    o = align256(o + w.max_jobs * 8);
+    w.total = o;
+    return w;
+}
+
+int64_t attn_ws(int64_t B, int64_t Hq, int64_t splits)
+{
+    return splits > 1 ? align256(splits * B * Hq * (kD + 2) * 4) : 0;
+}
+
+int64_t compact_ws(int64_t T) { return align256(sizeof(CallFlags)) + 2 * align256(T * 4); }
+int64_t alloc_ws(int64_t T) { return align256(sizeof(CallFlags)) + align256(T * 16); }
+
+int32_t auto_splits(const diffkv_layout* L, int64_t B, int64_t Hkv)
+{
+    const int64_t tables = B * Hkv;
+    if (tables <= 0) return 1;
+    int64_t s = (1024 + tables - 1) / tables;
+    const int64_t cap = L->p_max / 8 > 1 ? L->p_max / 8 : 1;
+    if (s > 16) s = 16;
+    if (s > cap) s = cap;
+    return (int32_t)(s < 1 ? 1 : s);
+}
+
+}  // namespace
+
+extern "C" {
+
+diffkv_status diffkv_layout_init(diffkv_layout* out, int32_t head_dim, int32_t group,
+                                 const int32_t k_bits[2], const int32_t v_bits[2],
+                                 const int32_t tokens_per_page[2], int32_t max_seq_len)
+{
+    return fill_layout(out, head_dim, group, k_bits, v_bits, tokens_per_page, max_seq_len);
+}
+
+int32_t diffkv_auto_splits(const diffkv_layout* layout, int32_t num_seqs, int32_t num_kv_heads)
+{
+    if (!layout_valid(layout)) return 1;
+    return auto_splits(layout, num_seqs, num_kv_heads);
+}
+
+diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout, int32_t num_seqs,
+                                    int32_t num_q_heads, int32_t num_kv_heads, int64_t total_new,
+                                    int32_t num_splits, size_t* bytes)
+{
+    if (!bytes || !layout_valid(layout) || num_seqs < 0) return DIFFKV_E_INVAL;
+    switch (op) {
+    case DIFFKV_OP_APPEND:
+        if (num_kv_heads <= 0 || total_new < 0) return DIFFKV_E_INVAL;
+        *bytes = (size_t)append_ws(num_seqs, num_kv_heads, total_new).total;
+        return DIFFKV_OK;
+    case DIFFKV_OP_ATTENTION: {
+        if (num_q_heads <= 0 || num_kv_heads <= 0 || num_splits < 0) return DIFFKV_E_INVAL;
+        const int32_t s = num_splits == 0 ? auto_splits(layout, num_seqs, num_kv_heads) : num_splits;
+        *bytes = (size_t)attn_ws(num_seqs, num_q_heads, s);
+        return DIFFKV_OK;
+    }
+    case DIFFKV_OP_COMPACT:
+        if (num_kv_heads <= 0) return DIFFKV_E_INVAL;
+        *bytes = (size_t)compact_ws((int64_t)num_seqs * num_kv_heads);
+        return DIFFKV_OK;
+    case DIFFKV_OP_ALLOC:
+        if (num_kv_heads <= 0) return DIFFKV_E_INVAL;
+        *bytes = (size_t)alloc_ws((int64_t)num_seqs * num_kv_heads);
+        return DIFFKV_OK;
+    default:
+        return DIFFKV_E_INVAL;
+    }
+}
+
+diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_cache* cache,
+                                     int64_t total_new, int32_t max_new, const int32_t* new_len,
+                                     const uint16_t* k, const uint16_t* v, const float* score,
+                                     const int32_t* quota, float alpha_h, float alpha_l,
+                                     int32_t recent_window, void* ws, size_t ws_bytes, void* stream)
+{
+    if (!layout_valid(layout) || !cache_valid(cache) || !cache->pool || !cache->seq_len)
+        return DIFFKV_E_INVAL;
+    if (total_new < 0 || max_new < 0 || recent_window < 0) return DIFFKV_E_INVAL;
+    if (total_new > INT32_MAX / 4) return DIFFKV_E_INVAL;
+    if (!layout_kernels_supported(layout)) return DIFFKV_E_UNSUPPORTED;
+    const int64_t B = cache->num_seqs, H = cache->num_kv_heads;
+    if (B == 0) return DIFFKV_OK;
+    if (!new_len) return DIFFKV_E_INVAL;
+    if (total_new > 0 && (!k || !v || !score)) return DIFFKV_E_INVAL;
+    if (total_new * H > INT32_MAX) return DIFFKV_E_INVAL;
+    const AppendWs w = append_ws(B, H, total_new);
+    if (!ws || (int64_t)ws_bytes < w.total) return DIFFKV_E_WORKSPACE;
+    if (w.max_jobs > INT32_MAX) return DIFFKV_E_INVAL;
+    AppendArgs a;
+    memset(&a, 0, sizeof(a));
+    fill_layout_args(a, layout);
+    a.pool = cache->pool;
+    a.num_pages = cache->num_pages;
+    a.page_table = cache->page_table;
+    a.pages = cache->pages;
+    a.len = cache->len;
+    a.seq_len = cache->seq_len;
+    a.ring = cache->ring;
+    a.ring_ptr = cache->ring_ptr;
+    a.status = cache->status;
+    a.B = (int)B;
+    a.Hkv = (int)H;
+    a.total_new = total_new;
+    a.max_new = max_new;
+    a.new_len = new_len;
+    a.k = k;
+    a.v = v;
+    a.score = score;
+    a.quota = quota;
+    a.alpha_h = alpha_h;
+    a.alpha_l = alpha_l;
+    a.window = recent_window;
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    a.flags = reinterpret_cast<CallFlags*>(base + w.flags);
+    a.tstate = reinterpret_cast<TState*>(base + w.tstate);
+    a.sold = reinterpret_cast<int32_t*>(base + w.sold);
+    a.row_off = reinterpret_cast<int32_t*>(base + w.row_off);
+    a.ord = reinterpret_cast<int32_t*>(base + w.ord);
+    a.jobs = reinterpret_cast<int2*>(base + w.jobs);
+    int64_t grid = w.max_jobs < 4096 ? w.max_jobs : 4096;
+    if (grid < 1) grid = 1;
+    hipError_t e = launch_append(a, (int)grid, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
+}
+
+diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_cache* cache,
+                                      int32_t num_q_heads, const uint16_t* q, float sm_scale,
+                                      float* out, float* lse, int32_t num_splits, void* ws,
+                                      size_t ws_bytes, void* stream)
+{
+    if (!layout_valid(layout) || !cache_valid(cache) || !cache->pool) return DIFFKV_E_INVAL;
+    if (num_q_heads <= 0 || num_q_heads % cache->num_kv_heads != 0 || num_splits < 0)
+        return DIFFKV_E_INVAL;
+    if (!layout_kernels_supported(layout)) return DIFFKV_E_UNSUPPORTED;
+    if (num_q_heads / cache->num_kv_heads > 8) return DIFFKV_E_UNSUPPORTED;
+    if (cache->num_seqs == 0) return DIFFKV_OK;
+    if (!q || !out) return DIFFKV_E_INVAL;
+    if (cache->num_seqs > 65535 || cache->num_kv_heads > 65535) return DIFFKV_E_UNSUPPORTED;
+    const int32_t S = num_splits == 0 ? auto_splits(layout, cache->num_seqs, cache->num_kv_heads)
+                                      : num_splits;
+    if (S > 65535) return DIFFKV_E_INVAL;
+    const int64_t need = attn_ws(cache->num_seqs, num_q_heads, S);
+    if (need > 0 && (!ws || (int64_t)ws_bytes < need)) return DIFFKV_E_WORKSPACE;
+    AttnArgs a;
+    memset(&a, 0, sizeof(a));
+    a.p_max = layout->p_max;
+    a.page_bytes = layout->page_bytes;
+    a.num_pages = cache->num_pages;
+    for (int p = 0; p < 2; ++p) {
+        a.off_kcode[p] = layout->off_kcode[p];
+        a.off_kmeta[p] = layout->off_kmeta[p];
+        a.off_vcode[p] = layout->off_vcode[p];
+        a.off_vmeta[p] = layout->off_vmeta[p];
+    }
+    a.pool = cache->pool;
+    a.page_table = cache->page_table;
+    a.len = cache->len;
+    a.B = cache->num_seqs;
+    a.Hkv = cache->num_kv_heads;
+    a.Hq = num_q_heads;
+    a.q = q;
+    a.scale_log2 = sm_scale * 1.4426950408889634f;
+    a.out = out;
+    a.lse = lse;
+    a.splits = S;
+    a.part = static_cast<float*>(ws);
+    hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
+}
+
+diffkv_status diffkv_compact_free_list(const diffkv_layout* layout, const diffkv_cache* cache,
+                                       int32_t num_tables, const uint8_t* release, void* ws,
+                                       size_t ws_bytes, void* stream)
+{
+    if (!layout_valid(layout) || !cache_valid(cache)) return DIFFKV_E_INVAL;
+    if (num_tables < 0 || (int64_t)num_tables > (int64_t)cache->num_seqs * cache->num_kv_heads)
+        return DIFFKV_E_INVAL;
+    if (num_tables == 0) return DIFFKV_OK;
+    if (!release) return DIFFKV_E_INVAL;
+    if (layout->p_max > 8192) return DIFFKV_E_UNSUPPORTED;  // LDS staging of one row
+    const int64_t need = compact_ws(num_tables);
+    if (!ws || (int64_t)ws_bytes < need) return DIFFKV_E_WORKSPACE;
+    CompactArgs a;
+    memset(&a, 0, sizeof(a));
+    a.p_max = layout->p_max;
+    a.T[0] = layout->tokens_per_page[0];
+    a.T[1] = layout->tokens_per_page[1];
+    a.num_pages = cache->num_pages;
+    a.page_table = cache->page_table;
+    a.pages = cache->pages;
+    a.len = cache->len;
+    a.ring = cache->ring;
+    a.ring_ptr = cache->ring_ptr;
+    a.num_tables = num_tables;
+    a.release = release;
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    a.flags = reinterpret_cast<CallFlags*>(base);
+    a.count = reinterpret_cast<int32_t*>(base + align256(sizeof(CallFlags)));
+    a.offset = reinterpret_cast<int32_t*>(base + align256(sizeof(CallFlags)) + align256((int64_t)num_tables * 4));
+    hipError_t e = launch_compact(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
+}
+
+diffkv_status diffkv_alloc_pages(const diffkv_layout* layout, const diffkv_cache* cache,
+                                 int32_t num_tables, const int32_t* demand, void* ws,
+                                 size_t ws_bytes, void* stream)
+{
+    if (!layout_valid(layout) || !cache_valid(cache)) return DIFFKV_E_INVAL;
+    if (num_tables < 0 || (int64_t)num_tables > (int64_t)cache->num_seqs * cache->num_kv_heads)
+        return DIFFKV_E_INVAL;
+    if (num_tables == 0) return DIFFKV_OK;
+    if (!demand) return DIFFKV_E_INVAL;
+    const int64_t need = alloc_ws(num_tables);
+    if (!ws || (int64_t)ws_bytes < need) return DIFFKV_E_WORKSPACE;
+    AllocArgs a;
+    memset(&a, 0, sizeof(a));
+    a.p_max = layout->p_max;
+    a.num_pages = cache->num_pages;
+    a.page_table = cache->page_table;
+    a.pages = cache->pages;
+    a.ring = cache->ring;
+    a.ring_ptr = cache->ring_ptr;
+    a.status = cache->status;
+    a.num_tables = num_tables;
+    a.demand = demand;
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    a.flags = reinterpret_cast<CallFlags*>(base);
+    a.tstate = reinterpret_cast<int4*>(base + align256(sizeof(CallFlags)));
+    hipError_t e = launch_alloc(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
+}
+
+const char* diffkv_status_str(diffkv_status s)
+{
+    switch (s) {
+    case DIFFKV_OK: return "ok";
+    case DIFFKV_E_INVAL: return "invalid argument";
+    case DIFFKV_E_UNSUPPORTED: return "layout or shape not supported by the gfx950 kernels";
+    case DIFFKV_E_WORKSPACE: return "workspace too small";
+    case DIFFKV_E_LAUNCH: return "HIP launch failed";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

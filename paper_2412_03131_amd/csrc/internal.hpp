@@ -1,0 +1,103 @@
+// internal.hpp -- argument blocks and launchers shared by the API and kernels.
+#pragma once
+
+#include "common.hpp"
+
+namespace dkv {
+
+struct TState {        // per-table scratch of one append call
+    int32_t cnt[2];    // kept new tokens per section
+    int32_t lold[2];   // section lengths before the call
+    int32_t pold[2];   // pages held before the call
+    int32_t ring_off;  // first ring index of this table's new pages, from head_old
+    int32_t n;         // new tokens of the table's sequence
+};
+
+struct LayoutArgs {
+    int p_max;
+    int T[2];
+    long long page_bytes;
+    int off_kcode[2], off_kmeta[2], off_vcode[2], off_vmeta[2], off_score[2], off_pos[2];
+};
+
+struct AppendArgs : LayoutArgs {
+    uint8_t* pool;
+    long long num_pages;
+    int32_t* page_table;
+    int32_t* pages;
+    int32_t* len;
+    int32_t* seq_len;
+    int32_t* ring;
+    int64_t* ring_ptr;
+    uint32_t* status;
+    int B, Hkv;
+    long long total_new;
+    int max_new;
+    const int32_t* new_len;
+    const uint16_t* k;
+    const uint16_t* v;
+    const float* score;
+    const int32_t* quota;
+    float alpha_h, alpha_l;
+    int window;
+    CallFlags* flags;
+    TState* tstate;
+    int32_t* sold;
+    int32_t* row_off;
+    int32_t* ord;
+    int2* jobs;
+};
+
+struct AllocArgs {
+    int p_max;
+    long long num_pages;
+    int32_t* page_table;
+    int32_t* pages;
+    int32_t* ring;
+    int64_t* ring_ptr;
+    uint32_t* status;
+    int num_tables;
+    const int32_t* demand;
+    CallFlags* flags;
+    int4* tstate;  // {pages_hi_old, pages_lo_old, ring_off, demand_hi}
+};
+
+struct CompactArgs {
+    int p_max;
+    int T[2];
+    long long num_pages;
+    int32_t* page_table;
+    int32_t* pages;
+    int32_t* len;
+    int32_t* ring;
+    int64_t* ring_ptr;
+    int num_tables;
+    const uint8_t* release;
+    CallFlags* flags;
+    int32_t* count;
+    int32_t* offset;
+};
+
+struct AttnArgs {
+    int p_max;
+    long long page_bytes;
+    long long num_pages;
+    int off_kcode[2], off_kmeta[2], off_vcode[2], off_vmeta[2];
+    const uint8_t* pool;
+    const int32_t* page_table;
+    const int32_t* len;
+    int B, Hkv, Hq;
+    const uint16_t* q;
+    float scale_log2;  // sm_scale * log2(e)
+    float* out;
+    float* lse;
+    int splits;
+    float* part;  // [splits][B][Hq][kD + 2] when splits > 1
+};
+
+hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st);
+hipError_t launch_alloc(const AllocArgs& a, hipStream_t st);
+hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
+hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
+
+}  // namespace dkv

@@ -1,0 +1,625 @@
+// k_memory.hip -- KV compressor, page allocation and free-list compaction
+// kernels for gfx950 (DiffKV Sec. 4, Sec. 5.2, Sec. 5.3).
+//
+// The compressor runs as three launches on the caller's stream:
+//   append_classify  one workgroup per table: classes its new tokens (quota
+//                    form by a two-target radix select on the score bits, or
+//                    the Algorithm 1 threshold comparisons), ranks the kept
+//                    tokens of each section in position order;
+//   append_plan      one workgroup for the whole call: page demand of every
+//                    table, prefix sums over tables, all-or-nothing check
+//                    against the free region and the table width, state
+//                    update and the list of (table, section, page) jobs;
+//   append_quant     persistent waves over the job list: resolve the page ID
+//                    (new pages come from the ring region the plan assigned),
+//                    quantize each token's 32-dim groups and write the page.
+// Allocation alone (alloc_plan + alloc_write) and compaction (compact_count,
+// compact_scan, compact_apply) follow the same planning/coordination split:
+// per-table work is fully parallel, one prefix sum gives every table a
+// disjoint ring region.
+#include "internal.hpp"
+
+namespace dkv {
+
+// ---------------------------------------------------------------------------
+// shared small pieces
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t score_key(float s)
+{
+    uint32_t u = __float_as_uint(s);
+    if (u == 0x80000000u) u = 0;  // -0 == +0
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------------------------
+// append_classify: grid (Hkv, B), block 256
+// ---------------------------------------------------------------------------
+constexpr int kClsThreads = 256;
+
+__global__ __launch_bounds__(kClsThreads) void append_classify(
+    AppendArgs a)
+{
+    const int h = blockIdx.x, b = blockIdx.y;
+    const int H = a.Hkv;
+    const int t = b * H + h;
+    const int tid = threadIdx.x;
+    __shared__ long long s_scan[kClsThreads / kWave + 1];
+    __shared__ int s_hist[2][256];
+    __shared__ int s_red[kClsThreads / kWave];
+    __shared__ int s_sel[8];
+
+    // row offset of this sequence (sum of new_len over lower sequences)
+    int part = 0;
+    for (int i = tid; i < b; i += kClsThreads) part += a.new_len[i];
+    part = wave_isum_w<kWave>(part);
+    if (lane_id() == 0) s_red[tid / kWave] = part;
+    __syncthreads();
+    int off_b = 0;
+    for (int i = 0; i < kClsThreads / kWave; ++i) off_b += s_red[i];
+    const int n = a.new_len[b];
+    TState* ts = a.tstate + t;
+    const bool bad = n < 0 || n > a.max_new || (long long)off_b + n > a.total_new ||
+                     (b == a.B - 1 && (long long)off_b + n != a.total_new);
+    if (bad) {
+        if (tid == 0) {  // the plan kernel turns n < 0 into DIFFKV_ST_BAD_INPUT
+            ts->cnt[0] = ts->cnt[1] = 0;
+            ts->n = -1;
+        }
+        return;
+    }
+    if (h == 0 && tid == 0) {
+        a.sold[b] = a.seq_len[b];
+        a.row_off[b] = off_b;
+    }
+    const int W = a.window < n ? a.window : n;
+    const int avail = n - W;
+    const float* sc = a.score + (long long)off_b * H + h;
+    int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
+
+    // ---- quota form: two-target radix select (k-th largest key) ----------
+    int k_sel[2] = {0, 0};
+    uint32_t K[2] = {0, 0};
+    int need[2] = {0, 0};
+    const bool quota = a.quota != nullptr;
+    float thr_h = 0.f, thr_l = 0.f;
+    if (quota) {
+        int q0 = a.quota[2 * t], q1 = a.quota[2 * t + 1];
+        int nh = q0 < 0 ? 0 : (q0 > avail ? avail : q0);
+        int nl = q1 < 0 ? 0 : (q1 > avail - nh ? avail - nh : q1);
+        k_sel[0] = nh;
+        k_sel[1] = nh + nl;
+        uint32_t prefix[2] = {0, 0}, mask = 0;
+        int kk[2] = {k_sel[0], k_sel[1]};
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            for (int i = tid; i < 512; i += kClsThreads) (&s_hist[0][0])[i] = 0;
+            __syncthreads();
+            for (int j = tid; j < avail; j += kClsThreads) {
+                uint32_t key = score_key(sc[(long long)j * H]);
+                uint32_t dig = (key >> shift) & 255u;
+#pragma unroll
+                for (int s = 0; s < 2; ++s)
+                    if (kk[s] > 0 && (key & mask) == prefix[s]) atomicAdd(&s_hist[s][dig], 1);
+            }
+            __syncthreads();
+            if (tid < 2) {
+                const int s = tid;
+                if (kk[s] > 0) {
+                    int above = 0, d = 255;
+                    for (; d > 0; --d) {
+                        if (above + s_hist[s][d] >= kk[s]) break;
+                        above += s_hist[s][d];
+                    }
+                    s_sel[2 * s] = d;
+                    s_sel[2 * s + 1] = above;
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                if (kk[s] > 0) {
+                    prefix[s] |= (uint32_t)s_sel[2 * s] << shift;
+                    kk[s] -= s_sel[2 * s + 1];
+                }
+            }
+            mask |= 255u << shift;
+            __syncthreads();
+        }
+        K[0] = prefix[0];
+        K[1] = prefix[1];
+        need[0] = kk[0];  // tokens with key == K that still belong above the cut
+        need[1] = kk[1];
+    } else {
+        const float N = (float)(a.seq_len[b] + n);
+        thr_h = a.alpha_h / N;
+        thr_l = a.alpha_l / N;
+    }
+
+    // ---- classes and in-section ranks, in position order ------------------
+    long long carry_tie = 0, carry_rank = 0;
+    for (int base = 0; base < n; base += kClsThreads) {
+        const int j = base + tid;
+        const bool valid = j < n;
+        const bool win = valid && j >= avail;
+        float s = 0.f;
+        uint32_t key = 0;
+        if (valid && !win) {
+            s = sc[(long long)j * H];
+            key = score_key(s);
+        }
+        bool hi = win, lo = false;
+        if (quota) {
+            const bool e0 = valid && !win && k_sel[0] > 0 && key == K[0];
+            const bool e1 = valid && !win && k_sel[1] > 0 && key == K[1];
+            long long tot;
+            long long ex = block_excl_scan<long long>((long long)e0 | ((long long)e1 << 32), s_scan, &tot);
+            ex += carry_tie;
+            carry_tie += tot;
+            const int r0 = (int)(ex & 0xffffffffll), r1 = (int)(ex >> 32);
+            if (valid && !win) {
+                hi = k_sel[0] > 0 && (key > K[0] || (e0 && r0 < need[0]));
+                lo = !hi && k_sel[1] > 0 && (key > K[1] || (e1 && r1 < need[1]));
+            }
+        } else if (valid && !win) {
+            hi = s >= thr_h;
+            lo = !hi && s >= thr_l;
+        }
+        long long tot;
+        long long ex = block_excl_scan<long long>((long long)hi | ((long long)lo << 32), s_scan, &tot);
+        ex += carry_rank;
+        carry_rank += tot;
+        if (hi) ord[(int)(ex & 0xffffffffll)] = j;
+        if (lo) ord[n - 1 - (int)(ex >> 32)] = j;
+    }
+    if (tid == 0) {
+        ts->cnt[0] = (int)(carry_rank & 0xffffffffll);
+        ts->cnt[1] = (int)(carry_rank >> 32);
+        ts->n = n;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// append_plan: one workgroup of 1024 threads
+// ---------------------------------------------------------------------------
+constexpr int kPlanThreads = 1024;
+
+__global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
+{
+    const int tid = threadIdx.x;
+    const int NT = a.B * a.Hkv;
+    const int P = a.p_max;
+    const int T[2] = {a.T[0], a.T[1]};
+    __shared__ long long s_scan[kPlanThreads / kWave + 1];
+    __shared__ int s_bad;
+    __shared__ long long s_head, s_tail;
+    if (tid == 0) {
+        s_bad = 0;
+        s_head = a.ring_ptr[0];
+        s_tail = a.ring_ptr[1];
+    }
+    __syncthreads();
+    for (int t = tid; t < NT; t += kPlanThreads)
+        if (a.tstate[t].n < 0) s_bad = 1;
+    __syncthreads();
+    if (s_bad) {
+        if (tid == 0) {
+            atomicOr(a.status, (uint32_t)DIFFKV_ST_BAD_INPUT);
+            a.flags->ok = 0;
+            a.flags->njobs = 0;
+        }
+        return;
+    }
+    // pass 1: demand and overflow
+    long long total = 0;
+    int ovf = 0;
+    for (int t = tid; t < NT; t += kPlanThreads) {
+        const TState& s = a.tstate[t];
+        int need_sum = 0;
+        int held = 0;
+        for (int sec = 0; sec < 2; ++sec) {
+            int want = ceil_div(a.len[2 * t + sec] + s.cnt[sec], T[sec]);
+            int have = a.pages[2 * t + sec];
+            need_sum += want > have ? want - have : 0;
+            held += have > want ? have : want;
+        }
+        total += need_sum;
+        if (held > P) ovf = 1;
+    }
+    long long tot;
+    block_excl_scan<long long>(total | ((long long)ovf << 62), s_scan, &tot);
+    const long long total_all = tot & ((1ll << 62) - 1);
+    const bool overflow = (tot >> 62) != 0;
+    uint32_t bits = 0;
+    if (total_all > s_tail - s_head) bits |= DIFFKV_ST_OUT_OF_PAGES;
+    if (overflow) bits |= DIFFKV_ST_TABLE_OVERFLOW;
+    if (bits) {
+        if (tid == 0) {
+            atomicOr(a.status, bits);
+            a.flags->ok = 0;
+            a.flags->njobs = 0;
+        }
+        return;
+    }
+    // pass 2: ring offsets, job offsets, state update
+    long long ring_carry = 0, job_carry = 0;
+    for (int t0 = 0; t0 < NT; t0 += kPlanThreads) {
+        const int t = t0 + tid;
+        int need[2] = {0, 0}, jobs[2] = {0, 0};
+        int lold[2] = {0, 0}, pold[2] = {0, 0}, cnt[2] = {0, 0};
+        if (t < NT) {
+            for (int sec = 0; sec < 2; ++sec) {
+                cnt[sec] = a.tstate[t].cnt[sec];
+                lold[sec] = a.len[2 * t + sec];
+                pold[sec] = a.pages[2 * t + sec];
+                int want = ceil_div(lold[sec] + cnt[sec], T[sec]);
+                need[sec] = want > pold[sec] ? want - pold[sec] : 0;
+                jobs[sec] = cnt[sec] ? (lold[sec] + cnt[sec] - 1) / T[sec] - lold[sec] / T[sec] + 1 : 0;
+            }
+        }
+        long long tr, tj;
+        long long ro = block_excl_scan<long long>(need[0] + need[1], s_scan, &tr) + ring_carry;
+        long long jo = block_excl_scan<long long>(jobs[0] + jobs[1], s_scan, &tj) + job_carry;
+        ring_carry += tr;
+        job_carry += tj;
+        if (t < NT) {
+            TState& s = a.tstate[t];
+            s.lold[0] = lold[0];
+            s.lold[1] = lold[1];
+            s.pold[0] = pold[0];
+            s.pold[1] = pold[1];
+            s.ring_off = (int)ro;
+            for (int sec = 0; sec < 2; ++sec) {
+                a.len[2 * t + sec] = lold[sec] + cnt[sec];
+                a.pages[2 * t + sec] = pold[sec] + need[sec];
+                const int p0 = lold[sec] / T[sec];
+                for (int i = 0; i < jobs[sec]; ++i)
+                    a.jobs[jo++] = make_int2(t, (sec << 30) | (p0 + i));
+            }
+        }
+    }
+    for (int b = tid; b < a.B; b += kPlanThreads) a.seq_len[b] = a.sold[b] + a.new_len[b];
+    if (tid == 0) {
+        a.flags->head_old = s_head;
+        a.flags->njobs = (int)job_carry;
+        a.flags->ok = 1;
+        a.ring_ptr[0] = s_head + ring_carry;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// append_quant: persistent single-wave workgroups over the job list
+// ---------------------------------------------------------------------------
+// Quantize one 32-dim group spread over 16 lanes (2 values per lane).
+// Arithmetic is IEEE fp32 with no contraction, identical to the text of the
+// quantizer: s = fp16((max-min)/L), z = fp16(min), code = clamp(rint((x-z)/s)).
+__device__ __forceinline__ void quant_pair(uint32_t xbits, int lb, uint32_t& sz, uint32_t& c0,
+                                           uint32_t& c1)
+{
+#pragma clang fp contract(off)
+    float x0 = h2f(xbits & 0xffffu) + 0.0f;
+    float x1 = h2f(xbits >> 16) + 0.0f;
+    float mn = wave_min_w<16>(fminf(x0, x1));
+    float mx = wave_max_w<16>(fmaxf(x0, x1));
+    float s32 = (mx - mn) / (float)lb;
+    uint32_t s16 = f2h_rne(s32);
+    uint32_t z16 = f2h_rne(mn);
+    float s = h2f(s16), z = h2f(z16);
+    if (s16 == 0) {
+        c0 = c1 = 0;
+    } else {
+        float r0 = rintf((x0 - z) / s);
+        float r1 = rintf((x1 - z) / s);
+        r0 = fminf(fmaxf(r0, 0.0f), (float)lb);
+        r1 = fminf(fmaxf(r1, 0.0f), (float)lb);
+        c0 = (uint32_t)r0;
+        c1 = (uint32_t)r1;
+    }
+    sz = s16 | (z16 << 16);
+}
+
+__global__ __launch_bounds__(kWave) void append_quant(AppendArgs a)
+{
+    if (!a.flags->ok) return;
+    const int njobs = a.flags->njobs;
+    const long long head_old = a.flags->head_old;
+    const int lane = threadIdx.x;
+    const int grp = lane >> 4;
+    const int H = a.Hkv;
+    const int P = a.p_max;
+    const long long page_bytes = a.page_bytes;
+    for (int job = blockIdx.x; job < njobs; job += gridDim.x) {
+        const int2 jb = a.jobs[job];
+        const int t = jb.x;
+        const int sec = jb.y >> 30;
+        const int p = jb.y & ((1 << 30) - 1);
+        const int b = t / H, h = t - b * H;
+        const TState ts = a.tstate[t];
+        const int T = sec ? kTLo : kTHi;
+        const int u0 = max(ts.lold[sec], p * T);
+        const int u1 = min(ts.lold[sec] + ts.cnt[sec], (p + 1) * T);
+        const int tslot = sec ? P - 1 - p : p;
+        int32_t* trow = a.page_table + (long long)t * P;
+        int id;
+        if (p < ts.pold[sec]) {
+            id = trow[tslot];
+        } else {
+            const int need_hi = a.pages[2 * t] - ts.pold[0];
+            long long r = head_old + ts.ring_off + (sec ? need_hi : 0) + (p - ts.pold[sec]);
+            id = a.ring[r % a.num_pages];
+            if (lane == 0) trow[tslot] = id;
+        }
+        if ((unsigned)id >= (unsigned)a.num_pages) continue;  // never write outside the pool
+        uint8_t* pg = a.pool + (long long)id * page_bytes;
+        const bool fresh = (u0 == p * T);
+        if (fresh) {
+            uint4 z = make_uint4(0, 0, 0, 0);
+            for (long long o = (long long)lane * 16; o < page_bytes; o += kWave * 16)
+                *reinterpret_cast<uint4*>(pg + o) = z;
+            __threadfence();  // the zeros land before this job's data stores
+        }
+        const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
+        const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
+        const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
+        uint64_t row0 = 0, row1 = 0;
+        if (!fresh) {
+            const uint4 r = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
+            row0 = ((uint64_t)r.y << 32) | r.x;
+            row1 = ((uint64_t)r.w << 32) | r.z;
+        }
+        const int n = ts.n;
+        const int off_b = a.row_off[b];
+        const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
+        for (int u = u0; u < u1; ++u) {
+            const int s = u - p * T;
+            const int r = u - ts.lold[sec];
+            const int j = sec ? ord[n - 1 - r] : ord[r];
+            const long long row = (long long)(off_b + j) * H + h;
+            const uint32_t kx = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
+            const uint32_t vx = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
+            uint32_t sz, c0, c1;
+            quant_pair(kx, (1 << kb) - 1, sz, c0, c1);
+            if (kb == 8) {
+                uint16_t* dst = reinterpret_cast<uint16_t*>(pg + off_kc + ((lane >> 3) * T + s) * 16 +
+                                                            ((2 * lane) & 15));
+                *dst = (uint16_t)(c0 | (c1 << 8));
+            } else {
+                uint8_t* dst = pg + off_kc + (grp * T + s) * 16 + (lane & 15);
+                *dst = (uint8_t)(c0 | (c1 << 4));
+            }
+            if ((lane & 15) == 0)
+                *reinterpret_cast<uint32_t*>(pg + off_km + (s * kNG + grp) * 4) = sz;
+            quant_pair(vx, (1 << vb) - 1, sz, c0, c1);
+            row0 |= (uint64_t)c0 << (s * vb);
+            row1 |= (uint64_t)c1 << (s * vb);
+            if ((lane & 15) == 0)
+                *reinterpret_cast<uint32_t*>(pg + off_vm + (grp * T + s) * 4) = sz;
+            if (lane == 0) {
+                reinterpret_cast<float*>(pg + a.off_score[sec])[s] = a.score[row];
+                reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[s] = a.sold[b] + j;
+            }
+        }
+        *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
+            make_uint4((uint32_t)row0, (uint32_t)(row0 >> 32), (uint32_t)row1, (uint32_t)(row1 >> 32));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Allocation alone: alloc_plan (one workgroup) + alloc_write (wave per table)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kPlanThreads) void alloc_plan(AllocArgs a)
+{
+    const int tid = threadIdx.x;
+    const int NT = a.num_tables;
+    __shared__ long long s_scan[kPlanThreads / kWave + 1];
+    __shared__ long long s_head, s_tail;
+    if (tid == 0) {
+        s_head = a.ring_ptr[0];
+        s_tail = a.ring_ptr[1];
+    }
+    __syncthreads();
+    long long total = 0;
+    int ovf = 0, neg = 0;
+    for (int t = tid; t < NT; t += kPlanThreads) {
+        int d0 = a.demand[2 * t], d1 = a.demand[2 * t + 1];
+        if (d0 < 0 || d1 < 0) neg = 1;
+        total += (long long)(d0 > 0 ? d0 : 0) + (d1 > 0 ? d1 : 0);
+        if ((long long)a.pages[2 * t] + a.pages[2 * t + 1] + d0 + d1 > a.p_max) ovf = 1;
+    }
+    long long tot;
+    block_excl_scan<long long>(total | ((long long)ovf << 62) | ((long long)neg << 61), s_scan, &tot);
+    uint32_t bits = 0;
+    if ((tot >> 61) & 1) bits |= DIFFKV_ST_BAD_INPUT;
+    if ((tot >> 62) & 1) bits |= DIFFKV_ST_TABLE_OVERFLOW;
+    if ((tot & ((1ll << 61) - 1)) > s_tail - s_head) bits |= DIFFKV_ST_OUT_OF_PAGES;
+    if (bits) {
+        if (tid == 0) {
+            atomicOr(a.status, bits);
+            a.flags->ok = 0;
+        }
+        return;
+    }
+    long long carry = 0;
+    for (int t0 = 0; t0 < NT; t0 += kPlanThreads) {
+        const int t = t0 + tid;
+        int d0 = 0, d1 = 0;
+        if (t < NT) {
+            d0 = a.demand[2 * t];
+            d1 = a.demand[2 * t + 1];
+        }
+        long long tr;
+        long long off = block_excl_scan<long long>(d0 + d1, s_scan, &tr) + carry;
+        carry += tr;
+        if (t < NT) {
+            int4 st = make_int4(a.pages[2 * t], a.pages[2 * t + 1], (int)off, d0);
+            a.tstate[t] = st;
+            a.pages[2 * t] = st.x + d0;
+            a.pages[2 * t + 1] = st.y + d1;
+        }
+    }
+    if (tid == 0) {
+        a.flags->head_old = s_head;
+        a.flags->ok = 1;
+        a.ring_ptr[0] = s_head + carry;
+    }
+}
+
+__global__ __launch_bounds__(kWave) void alloc_write(AllocArgs a)
+{
+    if (!a.flags->ok) return;
+    const int t = blockIdx.x;
+    const int4 st = a.tstate[t];
+    const int d1 = a.pages[2 * t + 1] - st.y;
+    const long long base = a.flags->head_old + st.z;
+    int32_t* row = a.page_table + (long long)t * a.p_max;
+    for (int i = threadIdx.x; i < st.w; i += kWave) row[st.x + i] = a.ring[(base + i) % a.num_pages];
+    for (int i = threadIdx.x; i < d1; i += kWave)
+        row[a.p_max - 1 - (st.y + i)] = a.ring[(base + st.w + i) % a.num_pages];
+}
+
+// ---------------------------------------------------------------------------
+// Compaction: compact_count (wave per table), compact_scan (one workgroup),
+// compact_apply (wave per table)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool slot_live(int slot, int ph, int pl, int P)
+{
+    return slot < ph || slot >= P - pl;
+}
+
+__global__ __launch_bounds__(kWave) void compact_count(CompactArgs a)
+{
+    const int t = blockIdx.x;
+    const int P = a.p_max;
+    int ph = a.pages[2 * t], pl = a.pages[2 * t + 1];
+    ph = ph < 0 ? 0 : (ph > P ? P : ph);
+    pl = pl < 0 ? 0 : (pl > P - ph ? P - ph : pl);
+    const uint8_t* rel = a.release + (long long)t * P;
+    int c = 0;
+    for (int s = threadIdx.x; s < P; s += kWave) c += (rel[s] != 0 && slot_live(s, ph, pl, P));
+    c = wave_isum_w<kWave>(c);
+    if (threadIdx.x == 0) a.count[t] = c;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void compact_scan(CompactArgs a)
+{
+    const int tid = threadIdx.x;
+    __shared__ long long s_scan[kPlanThreads / kWave + 1];
+    __shared__ long long s_tail;
+    if (tid == 0) s_tail = a.ring_ptr[1];
+    __syncthreads();
+    long long carry = 0;
+    for (int t0 = 0; t0 < a.num_tables; t0 += kPlanThreads) {
+        const int t = t0 + tid;
+        const int c = t < a.num_tables ? a.count[t] : 0;
+        long long tr;
+        long long off = block_excl_scan<long long>(c, s_scan, &tr) + carry;
+        carry += tr;
+        if (t < a.num_tables) a.offset[t] = (int)off;
+    }
+    if (tid == 0) {
+        a.flags->tail_old = s_tail;
+        a.ring_ptr[1] = s_tail + carry;
+    }
+}
+
+// One wave per table; the live part of the row is staged in LDS (dynamic
+// shared memory of 2*p_max ints) so the squeeze can write in place.
+__global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
+{
+    extern __shared__ int32_t s_row[];  // [0, P): old IDs, [P, 2P): new row
+    const int t = blockIdx.x;
+    const int lane = threadIdx.x;
+    const int P = a.p_max;
+    int ph = a.pages[2 * t], pl = a.pages[2 * t + 1];
+    ph = ph < 0 ? 0 : (ph > P ? P : ph);  // same clamp as compact_count
+    pl = pl < 0 ? 0 : (pl > P - ph ? P - ph : pl);
+    const int len0 = a.len[2 * t], len1 = a.len[2 * t + 1];
+    const int T0 = a.T[0], T1 = a.T[1];
+    const uint8_t* rel = a.release + (long long)t * P;
+    int32_t* row = a.page_table + (long long)t * P;
+    int32_t* s_new = s_row + P;
+    const long long base = a.flags->tail_old + a.offset[t];
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int s = lane; s < ph; s += kWave) s_row[s] = row[s];
+    for (int s = P - pl + lane; s < P; s += kWave) s_row[s] = row[s];
+    __syncthreads();
+    // released IDs to the ring in ascending slot order; kept high IDs packed left
+    int rank = 0, hi_keep = 0, drop0 = 0, drop1 = 0;
+    for (int c = 0; c < ph; c += kWave) {
+        const int s = c + lane;
+        const bool live = s < ph;
+        const bool r = live && rel[s] != 0;
+        const uint64_t mr = __ballot(r);
+        const uint64_t mk = __ballot(live && !r);
+        if (r) {
+            a.ring[(base + rank + __popcll(mr & below)) % a.num_pages] = s_row[s];
+            int f = len0 - s * T0;
+            drop0 += f < 0 ? 0 : (f > T0 ? T0 : f);
+        }
+        if (live && !r) s_new[hi_keep + __popcll(mk & below)] = s_row[s];
+        rank += __popcll(mr);
+        hi_keep += __popcll(mk);
+    }
+    for (int c = P - pl; c < P; c += kWave) {
+        const int s = c + lane;
+        const bool r = s < P && rel[s] != 0;
+        const uint64_t mr = __ballot(r);
+        if (r) {
+            a.ring[(base + rank + __popcll(mr & below)) % a.num_pages] = s_row[s];
+            int f = len1 - (P - 1 - s) * T1;
+            drop1 += f < 0 ? 0 : (f > T1 ? T1 : f);
+        }
+        rank += __popcll(mr);
+    }
+    // kept low IDs packed right, in section order (section page k sits at slot P-1-k)
+    int lo_keep = 0;
+    for (int c = 0; c < pl; c += kWave) {
+        const int k = c + lane;
+        const int s = P - 1 - k;
+        const bool keep = k < pl && rel[s] == 0;
+        const uint64_t mk = __ballot(keep);
+        if (keep) s_new[P - 1 - (lo_keep + __popcll(mk & below))] = s_row[s];
+        lo_keep += __popcll(mk);
+    }
+    __syncthreads();
+    for (int s = lane; s < ph; s += kWave) row[s] = s < hi_keep ? s_new[s] : -1;
+    for (int s = P - pl + lane; s < P; s += kWave) row[s] = s >= P - lo_keep ? s_new[s] : -1;
+    drop0 = wave_isum_w<kWave>(drop0);
+    drop1 = wave_isum_w<kWave>(drop1);
+    if (lane == 0) {
+        a.pages[2 * t] = hi_keep;
+        a.pages[2 * t + 1] = lo_keep;
+        a.len[2 * t] = len0 - drop0;
+        a.len[2 * t + 1] = len1 - drop1;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st)
+{
+    hipLaunchKernelGGL(append_classify, dim3(a.Hkv, a.B), dim3(kClsThreads), 0, st, a);
+    hipLaunchKernelGGL(append_plan, dim3(1), dim3(kPlanThreads), 0, st, a);
+    hipLaunchKernelGGL(append_quant, dim3(grid_quant), dim3(kWave), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_alloc(const AllocArgs& a, hipStream_t st)
+{
+    hipLaunchKernelGGL(alloc_plan, dim3(1), dim3(kPlanThreads), 0, st, a);
+    if (a.num_tables > 0) hipLaunchKernelGGL(alloc_write, dim3(a.num_tables), dim3(kWave), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_compact(const CompactArgs& a, hipStream_t st)
+{
+    if (a.num_tables == 0) return hipSuccess;
+    hipLaunchKernelGGL(compact_count, dim3(a.num_tables), dim3(kWave), 0, st, a);
+    hipLaunchKernelGGL(compact_scan, dim3(1), dim3(kPlanThreads), 0, st, a);
+    hipLaunchKernelGGL(compact_apply, dim3(a.num_tables), dim3(kWave),
+                       (size_t)2 * a.p_max * sizeof(int32_t), st, a);
+    return hipGetLastError();
+}
+
+}  // namespace dkv

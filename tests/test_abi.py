@@ -1,0 +1,101 @@
+"""The C-ABI library: it loads, exports every symbol include/diffkv.h declares, and its
+host-side entry points (layout, workspace sizes, argument checks) behave (CPU only;
+no call here reaches a kernel)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "diffkv.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:diffkv_status|int32_t|const char\*)\s+(diffkv_\w+)\s*\(",
+                                 txt, re.M)))
+
+
+@pytest.fixture(scope="module")
+def dk():
+    from paper_2412_03131_amd import diffkv
+    if not os.path.exists(diffkv.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    diffkv.lib()
+    return diffkv
+
+
+def test_exports_every_declared_symbol(dk):
+    names = _declared()
+    assert len(names) >= 8
+    raw = C.CDLL(dk.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+    assert set(names) == set(dk.EXPORTS)
+
+
+def test_layout_matches_oracle(dk, orc):
+    for kw in [dict(), dict(tokens_per_page=(2, 4), max_seq_len=6),
+               dict(k_bits=(8, 8), v_bits=(8, 4), tokens_per_page=(16, 16), max_seq_len=999)]:
+        a = dk.layout(**kw)
+        b = orc.layout(**kw)
+        for f, _ in dk.Layout._fields_:
+            va, vb = getattr(a, f), getattr(b, f)
+            if hasattr(va, "__len__"):
+                va, vb = list(va), list(vb)
+            assert va == vb, f
+
+
+def test_layout_rejects_bad_parameters(dk):
+    for kw in [dict(head_dim=100), dict(k_bits=(3, 4)), dict(tokens_per_page=(32, 16)),
+               dict(tokens_per_page=(16, 3)), dict(max_seq_len=0)]:
+        with pytest.raises(dk.DiffKVError) as e:
+            dk.layout(**kw)
+        assert e.value.code == dk.E_INVAL
+
+
+def test_workspace_sizes(dk):
+    L = dk.layout(max_seq_len=8192)
+    assert dk.workspace_size(dk.OP_ATTENTION, L, 32, 64, 8, 0, 1) == 0
+    s4 = dk.workspace_size(dk.OP_ATTENTION, L, 32, 64, 8, 0, 4)
+    assert s4 >= 4 * 32 * 64 * 130 * 4
+    a1 = dk.workspace_size(dk.OP_APPEND, L, 64, 0, 8, 1000)
+    a2 = dk.workspace_size(dk.OP_APPEND, L, 64, 0, 8, 2000)
+    assert a2 > a1 >= 1000 * 8 * 4
+    assert dk.workspace_size(dk.OP_COMPACT, L, 512, 0, 8) >= 2 * 4096 * 4
+    assert dk.auto_splits(L, 32, 8) == 4
+    assert dk.auto_splits(L, 64, 8) == 2
+    assert dk.auto_splits(L, 1024, 8) == 1
+
+
+def test_argument_checks_enqueue_nothing(dk):
+    """Invalid calls return before touching the device (NULL pointers, bad shapes)."""
+    lib = dk.lib()
+    L = dk.layout(max_seq_len=64)
+    st = dk.CacheStruct(0, 16, 0, 0, 0, 0, 0, 0, 0, 2, 2)
+    rc = lib.diffkv_decode_attention(C.byref(L), C.byref(st), 4, None, 0.1, None, None, 0, None, 0, None)
+    assert rc == dk.E_INVAL
+    fake = 0x1000
+    st = dk.CacheStruct(fake, 16, fake, fake, fake, fake, fake, fake, fake, 2, 2)
+    assert lib.diffkv_decode_attention(C.byref(L), C.byref(st), 3, fake, 0.1, fake, None, 0,
+                                       None, 0, None) == dk.E_INVAL  # Hq % Hkv
+    assert lib.diffkv_decode_attention(C.byref(L), C.byref(st), 18, fake, 0.1, fake, None, 0,
+                                       None, 0, None) == dk.E_UNSUPPORTED  # 9 query heads per KV head
+    assert lib.diffkv_decode_attention(C.byref(L), C.byref(st), 4, fake, 0.1, fake, None, 3,
+                                       None, 0, None) == dk.E_WORKSPACE
+    assert lib.diffkv_quantize_append(C.byref(L), C.byref(st), 10, 5, fake, fake, fake, fake, None,
+                                      0.0, 0.0, 0, fake, 16, None) == dk.E_WORKSPACE
+    assert lib.diffkv_quantize_append(C.byref(L), C.byref(st), -1, 5, fake, fake, fake, fake, None,
+                                      0.0, 0.0, 0, fake, 1 << 30, None) == dk.E_INVAL
+    L2 = dk.layout(tokens_per_page=(16, 16), max_seq_len=64)
+    assert lib.diffkv_quantize_append(C.byref(L2), C.byref(st), 10, 5, fake, fake, fake, fake, None,
+                                      0.0, 0.0, 0, fake, 1 << 30, None) == dk.E_UNSUPPORTED
+    assert lib.diffkv_compact_free_list(C.byref(L), C.byref(st), 5, fake, fake, 1 << 20,
+                                        None) == dk.E_INVAL  # more tables than the cache has
+    assert lib.diffkv_alloc_pages(C.byref(L), C.byref(st), 4, fake, fake, 8, None) == dk.E_WORKSPACE
+    bad = dk.Layout.from_buffer_copy(bytes(L))
+    bad.off_vcode[0] += 64
+    assert lib.diffkv_compact_free_list(C.byref(bad), C.byref(st), 1, fake, fake, 1 << 20,
+                                        None) == dk.E_INVAL  # not a layout diffkv_layout_init made
+    assert dk.status_str(dk.E_WORKSPACE) == "workspace too small"

@@ -1,0 +1,307 @@
+"""GPU parity: the HIP library against the CPU oracle on the same seeded inputs.
+
+Bit-exact: page bytes, page tables, page counts, lengths, sequence lengths, the ring
+and its pointers, the status word.  Attention: max |diff| <= 2e-3 and relative L2
+<= 1e-3 against the fp64 oracle.  Sizes span several pages/tiles with ragged tails.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from oracle import oracle as orc  # noqa: E402
+from paper_2412_03131_amd import diffkv as dk  # noqa: E402
+from paper_2412_03131_amd import inputs  # noqa: E402
+
+from gpu_util import (DEV, assert_attention_close, assert_state_equal,  # noqa: E402
+                      dev_cache_from_oracle, layouts, t)
+
+SCALE = 1.0 / np.sqrt(128.0)
+
+
+def _pair(num_pages, B, Hkv, max_seq_len, seed, garbage=True, **kw):
+    Lo, Ld = layouts(max_seq_len=max_seq_len, **kw)
+    ring = np.random.default_rng(seed).permutation(num_pages).astype(np.int32)
+    oc = orc.Cache(Lo, num_pages, B, Hkv, ring=ring)
+    if garbage:
+        oc.pool[:] = np.random.default_rng(seed + 1).integers(0, 256, oc.pool.shape, dtype=np.uint8)
+    dc = dev_cache_from_oracle(Ld, oc)
+    return Lo, Ld, oc, dc
+
+
+def _append_both(oc, dc, new_len, k, v, score, quota=None, alpha_h=0.0, alpha_l=0.0, window=0):
+    orc.quantize_append(oc, new_len, k, v, score, quota=quota, alpha_h=alpha_h, alpha_l=alpha_l,
+                        window=window)
+    dk.quantize_append(dc, t(np.asarray(new_len, np.int32)), t(k), t(v), t(score),
+                       quota=None if quota is None else t(np.asarray(quota, np.int32)),
+                       alpha_h=alpha_h, alpha_l=alpha_l, window=window,
+                       total_new=int(np.sum(new_len)), max_new=int(np.max(new_len, initial=0)))
+
+
+# ---------------------------------------------------------------- append --
+def test_append_tiny_config_bitexact():
+    w = inputs.prefill("tiny")
+    print("case: tiny append B=%d Hkv=%d L=512" % (w["B"], w["Hkv"]), flush=True)
+    Lo, Ld, oc, dc = _pair(256, w["B"], w["Hkv"], 640, seed=3)
+    _append_both(oc, dc, w["new_len"], w["k"], w["v"], w["score"], quota=w["quota"])
+    assert_state_equal(dc, oc, what="tiny")
+    assert oc.status[0] == 0 and oc.len[0].tolist() == [204, 206]
+
+
+def test_append_ragged_threshold_form():
+    rng = np.random.default_rng(11)
+    B, Hkv = 5, 2
+    new_len = np.array([0, 1, 17, 300, 65], np.int32)
+    n = int(new_len.sum())
+    k = (rng.standard_normal((n, Hkv, 128)) * 3).astype(np.float16).view(np.uint16)
+    v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    score = (rng.random((n, Hkv)) * 0.02).astype(np.float32)
+    print("case: ragged threshold append", flush=True)
+    Lo, Ld, oc, dc = _pair(200, B, Hkv, 1024, seed=4)
+    oc.seq_len[:] = [3, 0, 50, 7, 1]
+    dc.seq_len.copy_(t(oc.seq_len))
+    _append_both(oc, dc, new_len, k, v, score, alpha_h=1.0, alpha_l=0.2, window=4)
+    assert_state_equal(dc, oc, what="threshold")
+    assert oc.len[:, 1].sum() > 0 and oc.len[:, 0].sum() > 0
+
+
+def test_append_quota_ties_signed_zero_window():
+    rng = np.random.default_rng(12)
+    B, Hkv = 3, 4
+    new_len = np.array([100, 257, 31], np.int32)
+    n = int(new_len.sum())
+    vals = np.array([0.0, -0.0, 0.5, 0.25, 1.0, -2.0, 3.0], np.float32)
+    score = vals[rng.integers(0, len(vals), (n, Hkv))]
+    k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    k[5, 0, :32] = 0x8000  # a group of -0
+    k[6, 1, :] = np.float16(1.5).view(np.uint16)  # constant groups
+    quota = rng.integers(-2, 200, (B, Hkv, 2)).astype(np.int32)
+    print("case: quota ties", flush=True)
+    Lo, Ld, oc, dc = _pair(300, B, Hkv, 600, seed=5)
+    _append_both(oc, dc, new_len, k, v, score, quota=quota, window=3)
+    assert_state_equal(dc, oc, what="ties")
+
+
+def test_append_decode_steps_into_partial_pages():
+    w = inputs.prefill("llama8b", B=3, L=(40, 90))
+    B, Hkv = w["B"], w["Hkv"]
+    print("case: decode steps", flush=True)
+    Lo, Ld, oc, dc = _pair(400, B, Hkv, 256, seed=6)
+    _append_both(oc, dc, w["new_len"], w["k"], w["v"], w["score"], quota=w["quota"])
+    assert_state_equal(dc, oc, what="prefill")
+    rng = np.random.default_rng(13)
+    for step in range(40):
+        d = inputs.decode_token("llama8b", step, B, w["Hq"], Hkv, w["outliers"])
+        nl = (rng.random(B) < 0.8).astype(np.int32)
+        rows = np.repeat(np.arange(B), nl)
+        quota = np.where(rng.random((B, Hkv, 1)) < 0.7, [[1, 0]], [[0, 1]]).astype(np.int32)
+        _append_both(oc, dc, nl, d["k"][rows], d["v"][rows], d["score"][rows], quota=quota)
+        if step % 8 == 7:
+            assert_state_equal(dc, oc, what="step %d" % step)
+    assert_state_equal(dc, oc, what="decode end")
+
+
+def test_append_all_or_nothing_on_device():
+    rng = np.random.default_rng(14)
+    B, Hkv = 2, 2
+    new_len = np.array([50, 30], np.int32)
+    n = 80
+    k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    score = rng.random((n, Hkv)).astype(np.float32)
+    quota = np.full((B, Hkv, 2), [20, 20], np.int32)
+    print("case: out of pages", flush=True)
+    Lo, Ld, oc, dc = _pair(6, B, Hkv, 64, seed=7)
+    _append_both(oc, dc, new_len, k, v, score, quota=quota)
+    s = assert_state_equal(dc, oc, what="oop")
+    assert s["status"][0] == dk.ST_OUT_OF_PAGES and s["ring_ptr"][0] == 0
+    print("case: table overflow", flush=True)
+    Lo, Ld, oc, dc = _pair(64, B, Hkv, 20, seed=8)
+    _append_both(oc, dc, new_len, k, v, score, quota=np.full((B, Hkv, 2), [33, 17], np.int32))
+    s = assert_state_equal(dc, oc, what="overflow")
+    assert s["status"][0] == dk.ST_TABLE_OVERFLOW
+    print("case: bad new_len", flush=True)
+    Lo, Ld, oc, dc = _pair(64, B, Hkv, 64, seed=9)
+    before = assert_state_equal(dc, oc, what="before")
+    dk.quantize_append(dc, t(new_len), t(k), t(v), t(score), quota=t(quota), total_new=70,
+                       max_new=50)  # sum(new_len) = 80 != 70
+    from gpu_util import snapshot
+    after = snapshot(dc)
+    assert after["status"][0] == dk.ST_BAD_INPUT
+    for f in ("table", "pages", "len", "seq_len", "ring", "ring_ptr", "pool"):
+        assert np.array_equal(after[f], before[f]), f
+
+
+# ------------------------------------------------------------- attention --
+def _attn_case(name, B, L, splits, seed_pages=20):
+    w = inputs.prefill(name, B=B, L=L)
+    Lo, Ld = layouts(max_seq_len=int(w["max_len"]) + 64)
+    npages = int(w["B"] * w["Hkv"] * (int(w["max_len"]) // 16 + 4))
+    oc = orc.Cache(Lo, npages, w["B"], w["Hkv"],
+                   ring=np.random.default_rng(seed_pages).permutation(npages))
+    orc.quantize_append(oc, w["new_len"], w["k"], w["v"], w["score"], quota=w["quota"])
+    assert oc.status[0] == 0
+    return w, Lo, Ld, oc
+
+
+@pytest.mark.parametrize("name,B,L", [("tiny", None, None), ("llama8b", 6, (300, 1100)),
+                                      ("long32k", 2, 900), ("llama70b", 2, 700)])
+def test_attention_matches_oracle(name, B, L):
+    w, Lo, Ld, oc = _attn_case(name, B, L, 1)
+    ref, ref_lse = orc.attention(oc, w["q"], SCALE)
+    dc = dev_cache_from_oracle(Ld, oc)
+    for splits in (1, 3, 0):
+        print("case: attention %s splits=%d" % (name, splits), flush=True)
+        out, lse = dk.decode_attention(dc, t(w["q"]), SCALE, num_splits=splits)
+        torch.cuda.synchronize()
+        mx, rel = assert_attention_close(out.cpu().numpy(), lse.cpu().numpy(), ref, ref_lse,
+                                         "%s splits=%d" % (name, splits))
+        print("   max abs %.2e rel %.2e" % (mx, rel), flush=True)
+
+
+def test_attention_gpu_built_cache_and_determinism():
+    w = inputs.prefill("llama8b", B=4, L=(200, 700))
+    Lo, Ld = layouts(max_seq_len=800)
+    npages = 4 * 8 * 60
+    ring = np.random.default_rng(21).permutation(npages)
+    oc = orc.Cache(Lo, npages, w["B"], w["Hkv"], ring=ring)
+    dc = dev_cache_from_oracle(Ld, oc)
+    print("case: gpu-built cache attention", flush=True)
+    _append_both(oc, dc, w["new_len"], w["k"], w["v"], w["score"], quota=w["quota"])
+    assert_state_equal(dc, oc, what="built")
+    ref, ref_lse = orc.attention(oc, w["q"], SCALE)
+    o1, l1 = dk.decode_attention(dc, t(w["q"]), SCALE, num_splits=2)
+    o2, l2 = dk.decode_attention(dc, t(w["q"]), SCALE, num_splits=2)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    assert_attention_close(o1.cpu().numpy(), l1.cpu().numpy(), ref, ref_lse, "built")
+
+
+def test_attention_edge_cases():
+    """Empty tables, a single kept token, a lone partial page, more splits than pages."""
+    rng = np.random.default_rng(22)
+    B, Hkv, Hq = 4, 2, 8
+    new_len = np.array([0, 1, 40, 5], np.int32)
+    n = int(new_len.sum())
+    k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    score = rng.random((n, Hkv)).astype(np.float32)
+    quota = np.array([[[0, 0], [0, 0]], [[1, 0], [0, 1]], [[17, 5], [0, 0]], [[0, 3], [2, 2]]],
+                     np.int32)
+    Lo, Ld = layouts(max_seq_len=64)
+    oc = orc.Cache(Lo, 64, B, Hkv, ring=rng.permutation(64))
+    orc.quantize_append(oc, new_len, k, v, score, quota=quota)
+    q = rng.standard_normal((B, Hq, 128)).astype(np.float16).view(np.uint16)
+    ref, ref_lse = orc.attention(oc, q, SCALE)
+    dc = dev_cache_from_oracle(Ld, oc)
+    for splits in (1, 2, 7, 16):
+        print("case: edge splits=%d" % splits, flush=True)
+        out, lse = dk.decode_attention(dc, t(q), SCALE, num_splits=splits)
+        torch.cuda.synchronize()
+        o = out.cpu().numpy()
+        assert np.all(o[0] == 0) and np.all(np.isneginf(lse.cpu().numpy()[0]))
+        assert np.all(o[2, 4:] == 0)  # KV head 1 of sequence 2 keeps nothing
+        assert_attention_close(o, lse.cpu().numpy(), ref, ref_lse, "edge %d" % splits)
+    # sequence 1 keeps one high token on KV head 0 (table 2) and one low token on KV
+    # head 1 (table 3): each output is that token's dequantized value
+    out = dk.decode_attention(dc, t(q), SCALE, num_splits=1)[0].cpu().numpy()
+    _, vh0, _, _ = orc.read_token(oc, 2, 0, 0)
+    _, vh1, _, _ = orc.read_token(oc, 3, 1, 0)
+    assert np.abs(out[1, 0:4] - vh0).max() <= 1e-6
+    assert np.abs(out[1, 4:8] - vh1).max() <= 1e-6
+
+
+# ------------------------------------------------------- compaction/alloc --
+def test_compaction_worked_example_on_gpu():
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                    "prompt_phase_example.json")))
+    Lo, Ld = layouts(tokens_per_page=tuple(g["tokens_per_page"]), max_seq_len=6)
+    oc = orc.Cache(Lo, 13, 1, 2, ring=np.array(g["ring"]), with_pool=False)
+    oc.ring_ptr[:] = g["ring_ptr_before"]
+    dc = dev_cache_from_oracle(Ld, oc, with_pool=False)
+    print("case: worked example", flush=True)
+    dk.alloc_pages(dc, t(np.array(g["conservative_demand"], np.int32)))
+    orc.alloc_pages(oc, np.array(g["conservative_demand"]))
+    s = assert_state_equal(dc, oc, with_pool=False, what="alloc")
+    assert s["table"].tolist() == g["tables_after_alloc"]
+    oc.len[:] = [[2, 4], [4, 3]]  # what the planning placed (2 high + 4 low, 4 high + 3 low)
+    dc.len.copy_(t(oc.len))
+    rel = np.array(g["release"], np.uint8)
+    dk.compact_free_list(dc, t(rel))
+    orc.compact(oc, rel)
+    s = assert_state_equal(dc, oc, with_pool=False, what="compact")
+    assert s["table"].tolist() == g["tables_after_recycle"]
+    assert s["ring"][:3].tolist() == g["recycled_in_order"]
+    assert s["ring_ptr"].tolist() == g["ring_ptr_after_recycle"]
+
+
+def test_compaction_random_rounds_bitexact():
+    rng = np.random.default_rng(31)
+    for trial in range(3):
+        num_pages = int(rng.integers(300, 3000))
+        tables = int(rng.integers(5, 120))
+        Lo, Ld = layouts(max_seq_len=int(rng.integers(100, 2000)))
+        oc = orc.Cache(Lo, num_pages, tables, 1, ring=rng.permutation(num_pages), with_pool=False)
+        dc = dev_cache_from_oracle(Ld, oc, with_pool=False)
+        for rnd in range(12):
+            print("case: compaction trial %d round %d" % (trial, rnd), flush=True)
+            free = int(oc.ring_ptr[1] - oc.ring_ptr[0])
+            dem = np.zeros((tables, 2), np.int32)
+            for tt in range(tables):
+                room = Lo.p_max - int(oc.pages[tt].sum())
+                a = int(rng.integers(0, max(1, min(room, 2 * free // tables) + 1)))
+                hi = int(rng.integers(0, a + 1))
+                dem[tt] = hi, a - hi
+            orc.alloc_pages(oc, dem)
+            dk.alloc_pages(dc, t(dem))
+            oc.len[:] = np.maximum(oc.pages * np.array([16, 32]) - rng.integers(0, 16, (tables, 2)), 0)
+            oc.len[oc.pages == 0] = 0
+            dc.len.copy_(t(oc.len))
+            rel = (rng.random((tables, Lo.p_max)) < rng.random()).astype(np.uint8)
+            orc.compact(oc, rel)
+            dk.compact_free_list(dc, t(rel))
+            assert_state_equal(dc, oc, with_pool=False, what="trial %d round %d" % (trial, rnd))
+    # allocation failures leave everything unchanged
+    st = assert_state_equal(dc, oc, with_pool=False)
+    dem = np.zeros((tables, 2), np.int32)
+    dem[0, 0] = int(oc.ring_ptr[1] - oc.ring_ptr[0]) + 1
+    dk.alloc_pages(dc, t(dem))
+    orc.alloc_pages(oc, dem)
+    st2 = assert_state_equal(dc, oc, with_pool=False, what="alloc failure")
+    assert st2["status"][0] & dk.ST_OUT_OF_PAGES
+    assert np.array_equal(st2["table"], st["table"])
+
+
+def test_compaction_workload_scaled():
+    """The compaction workload's recipe at 1/16 scale: 2^16 pages, 256 tables, 60% held,
+    Bernoulli(0.35) releases, refill, 10 rounds (the ring wraps)."""
+    ring, demand = inputs.compaction_setup(num_pages=1 << 16, tables=256)
+    Lo, Ld = layouts(max_seq_len=255 * 16)
+    assert Lo.p_max == 256
+    oc = orc.Cache(Lo, 1 << 16, 256, 1, ring=ring, with_pool=False)
+    dc = dev_cache_from_oracle(Ld, oc, with_pool=False)
+    orc.alloc_pages(oc, demand)
+    dk.alloc_pages(dc, t(demand))
+    oc.len[:] = oc.pages * np.array([16, 32])
+    dc.len.copy_(t(oc.len))
+    assert_state_equal(dc, oc, with_pool=False, what="setup")
+    for rnd in range(10):
+        print("case: scaled compaction round %d" % rnd, flush=True)
+        rel = inputs.release_mask(4, rnd, 256, 256)
+        before = oc.pages.copy()
+        orc.compact(oc, rel)
+        dk.compact_free_list(dc, t(rel))
+        lost = (before - oc.pages).astype(np.int32)
+        orc.alloc_pages(oc, lost)
+        dk.alloc_pages(dc, t(lost))
+        oc.len[:] = oc.pages * np.array([16, 32])
+        dc.len.copy_(t(oc.len))
+        assert_state_equal(dc, oc, with_pool=False, what="round %d" % rnd)
+    assert oc.ring_ptr[1] > (1 << 16)  # wrapped

@@ -1,0 +1,392 @@
+#!/usr/bin/env python3
+"""Benchmark of the DiffKV decode hot path on one MI355X.
+
+Workload: the Llama-3-8B decode shape (batch 64, 32 query / 8 KV heads, head_dim 128,
+context uniform in [1024, 4096], per-head high fraction U[0.1, 0.5] and pruned fraction
+U[0.2, 0.6], K8V4 / K4V2 with group-32 fp16 scale/zero, 16/32 tokens per page), on
+`--layers` layers that share one page pool (so attention streams from HBM, not from the
+256 MB Infinity Cache).
+
+One step = one continuous-batching decode step of the whole path:
+  1. request r = step mod 64 finishes: its pages in every layer go back to the free list
+     (diffkv_compact_free_list, one call for all layers);
+  2. per layer: a replacement request is prefilled into slot r while the other 63
+     append their newest token (diffkv_quantize_append: classing, allocation,
+     quantization, placement);
+  3. per layer: decode attention over the whole batch (diffkv_decode_attention).
+
+value = KV tokens attended per second of step time, where a KV token is one kept
+(token, KV head) pair.  The JSON line adds the attention kernel's roofline (algorithmic
+compressed bytes / kernel time, HIP events on the launch stream), the compaction
+workload (2^20 pages, 4096 tables, 100 rounds of Bernoulli(0.35) releases) in pages/s,
+and the CPU oracle's attention throughput on a bounded sample.
+"""
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attention KV tokens/s + achieved HBM GB/s (% of peak); compaction pages/s"
+HBM_PEAK_GBPS = 8000.0
+SCALE = 1.0 / np.sqrt(128.0)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--layers", type=int, default=4)
+    ap.add_argument("--splits", type=int, default=0, help="attention split count (0 = auto)")
+    ap.add_argument("--compaction-rounds", type=int, default=100)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=("all", "attention", "copy"), default="all",
+                    help="profiling aids that print no benchmark line: 'attention' builds the "
+                         "cache and times only the attention calls; 'copy' runs a plain 1 GiB "
+                         "device copy (the reference for scaling HBM byte counters)")
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def attn_bytes(len_hi, len_lo, B, Hq, Hkv):
+    """Algorithmic bytes of one attention launch: compressed K/V codes + fp16 scale/zero
+    (224 B per high token, 128 B per low token), the table entries of the used pages,
+    the section lengths, q in, out and lse."""
+    ph = -(-len_hi // 16)
+    pl = -(-len_lo // 32)
+    kv = 224 * int(len_hi.sum()) + 128 * int(len_lo.sum())
+    return kv + 4 * int(ph.sum() + pl.sum()) + 8 * len_hi.size + B * Hq * 128 * (2 + 4) + 4 * B * Hq
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the DiffKV path shards by KV head or by request "
+              "with no exchange between GPUs, so a multi-GPU figure is N independent copies "
+              "of this one (see DESIGN.md, 'More than one GPU').", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2412_03131_amd import diffkv as dk
+    from paper_2412_03131_amd import inputs
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.only == "copy":
+        x = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        y = torch.empty_like(x)
+        for _ in range(args.steps):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        log("copied %d x 1 GiB" % args.steps)
+        return
+    lib = dk.lib()
+    stream = torch.cuda.current_stream()
+    sptr = C.c_void_p(stream.cuda_stream)
+
+    # ------------------------------------------------------------ workload --
+    t0 = time.time()
+    w = inputs.prefill("llama8b")
+    B, Hq, Hkv = w["B"], w["Hq"], w["Hkv"]
+    NL = args.layers
+    nl = w["new_len"].astype(np.int64)
+    off = np.concatenate([[0], np.cumsum(nl)])
+    steps_total = args.warmup + args.steps
+    init_hi = w["quota"][:, :, 0].astype(np.int64)
+    init_lo = w["quota"][:, :, 1].astype(np.int64)
+    L = dk.layout(max_seq_len=int(nl.max()) + steps_total + 16)
+    per_table = (-(-(init_hi + steps_total) // 16)) + (-(-init_lo // 32)) + 2
+    num_pages = int(NL * per_table.sum() * 1.05) + 1024
+    log("workload llama8b: B=%d Hq=%d Hkv=%d layers=%d tokens=%d pages=%d (%.2f GB pool), gen %.1fs"
+        % (B, Hq, Hkv, NL, int(nl.sum()), num_pages, num_pages * L.page_bytes / 1e9, time.time() - t0))
+    cache = dk.Cache(L, num_pages, NL * B, Hkv, device=dev)
+    views = [cache.view(l * B, (l + 1) * B) for l in range(NL)]
+
+    def T(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            a = a.view(np.int16)
+        return torch.from_numpy(a).to(dev)
+
+    k_all, v_all, s_all = T(w["k"]), T(w["v"]), T(w["score"])
+    quota_all, nl_all = T(w["quota"]), T(w["new_len"])
+    ws_a = torch.empty(dk.workspace_size(dk.OP_APPEND, L, B, 0, Hkv, int(nl.sum()) + B) + 256,
+                       dtype=torch.uint8, device=dev)
+    for v in views:  # prompt phase of all 64 requests, every layer
+        dk.quantize_append(v, nl_all, k_all, v_all, s_all, quota=quota_all, total_new=int(nl.sum()),
+                           max_new=int(nl.max()), ws=ws_a)
+    torch.cuda.synchronize()
+    if int(cache.status.item()) != 0:
+        raise RuntimeError("prefill raised status %d" % int(cache.status.item()))
+
+    # per-step inputs: slot r gets a new request (same shape as the one it replaces),
+    # the other sequences one generated token each
+    steps_in = []
+    for s in range(steps_total):
+        r = s % B
+        d = inputs.decode_token("llama8b", s, B, Hq, Hkv, w["outliers"])
+        dk_ = T(d["k"])
+        dv_ = T(d["v"])
+        ds_ = T(d["score"])
+        k_s = torch.cat([dk_[:r], k_all[off[r]:off[r + 1]], dk_[r + 1:]])
+        v_s = torch.cat([dv_[:r], v_all[off[r]:off[r + 1]], dv_[r + 1:]])
+        s_s = torch.cat([ds_[:r], s_all[off[r]:off[r + 1]], ds_[r + 1:]])
+        q_np = d["quota"].copy()
+        q_np[r] = w["quota"][r]
+        n_np = np.ones(B, np.int32)
+        n_np[r] = nl[r]
+        steps_in.append(dict(r=r, k=k_s, v=v_s, score=s_s, quota=T(q_np), new_len=T(n_np),
+                             total=int(n_np.sum()), maxn=int(n_np.max()), q=T(d["q"])))
+    P = L.p_max
+    masks = []
+    for r in range(B):
+        m = torch.zeros((NL * B * Hkv, P), dtype=torch.uint8, device=dev)
+        for l in range(NL):
+            m[(l * B + r) * Hkv:(l * B + r + 1) * Hkv] = 1
+        masks.append(m)
+    S = args.splits if args.splits > 0 else dk.auto_splits(L, B, Hkv)
+    ws_att = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, Hq, Hkv, 0, S)),
+                         dtype=torch.uint8, device=dev)
+    ws_c = torch.empty(dk.workspace_size(dk.OP_COMPACT, L, NL * B, 0, Hkv), dtype=torch.uint8,
+                       device=dev)
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+
+    # pre-built ctypes argument lists: the timed loop only enqueues
+    Lp = C.byref(L)
+    cstructs = [v.struct() for v in views]
+    call_struct = cache.struct()
+    vp = lambda x: C.c_void_p(x.data_ptr())
+    attn_args, app_args = [], []
+    for s, si in enumerate(steps_in):
+        app_args.append([(Lp, C.byref(cs), si["total"], si["maxn"], vp(si["new_len"]), vp(si["k"]),
+                          vp(si["v"]), vp(si["score"]), vp(si["quota"]), 0.0, 0.0, 0, vp(ws_a),
+                          ws_a.numel(), sptr) for cs in cstructs])
+        attn_args.append([(Lp, C.byref(cs), Hq, vp(si["q"]), float(SCALE), vp(out), vp(lse), S,
+                           vp(ws_att), ws_att.numel(), sptr) for cs in cstructs])
+    comp_args = [(Lp, C.byref(call_struct), NL * B * Hkv, vp(m), vp(ws_c), ws_c.numel(), sptr)
+                 for m in masks]
+    seq_rows = [torch.arange(r, NL * B, B, device=dev) for r in range(B)]
+
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(NL)] for _ in range(args.steps)]
+
+    def run_step(s, timed_idx):
+        si = steps_in[s]
+        r = si["r"]
+        rc = lib.diffkv_compact_free_list(*comp_args[r])
+        cache.seq_len.index_fill_(0, seq_rows[r], 0)
+        for l in range(NL):
+            rc |= lib.diffkv_quantize_append(*app_args[s][l])
+            if timed_idx is not None:
+                ev[timed_idx][l][0].record(stream)
+            rc |= lib.diffkv_decode_attention(*attn_args[s][l])
+            if timed_idx is not None:
+                ev[timed_idx][l][1].record(stream)
+        if rc:
+            raise RuntimeError("library call failed at step %d (rc %d)" % (s, rc))
+
+    # host-side expected lengths at every step's attention (for byte / token counts)
+    len_hi, len_lo = init_hi.copy(), init_lo.copy()
+    step_bytes, step_tokens = [], []
+    for s in range(steps_total):
+        r = s % B
+        len_hi += 1
+        len_hi[r] = init_hi[r]
+        len_lo[r] = init_lo[r]
+        step_bytes.append(attn_bytes(len_hi, len_lo, B, Hq, Hkv))
+        step_tokens.append(int(len_hi.sum() + len_lo.sum()))
+
+    if args.only == "attention":
+        for s in range(args.warmup):
+            for l in range(NL):
+                lib.diffkv_decode_attention(*attn_args[0][l])
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for s in range(args.steps):
+            for l in range(NL):
+                lib.diffkv_decode_attention(*attn_args[0][l])
+        torch.cuda.synchronize()
+        el = (time.perf_counter() - t1) / (args.steps * NL)
+        nb = attn_bytes(init_hi, init_lo, B, Hq, Hkv)
+        log("attention only: %.1f us/launch, %.0f GB/s (%d bytes per launch)" % (el * 1e6, nb / el / 1e9, nb))
+        return
+
+    for s in range(args.warmup):
+        run_step(s, None)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        run_step(args.warmup + i, i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    status = int(cache.status.item())
+    got = cache.len.view(NL, B, Hkv, 2)[0].cpu().numpy()
+    if status != 0 or not (np.array_equal(got[..., 0], len_hi) and np.array_equal(got[..., 1], len_lo)):
+        raise RuntimeError("state check failed after the timed steps (status %d)" % status)
+    attn_ms = np.array([[a.elapsed_time(b) for a, b in row] for row in ev])  # [steps, layers]
+    timed = slice(args.warmup, steps_total)
+    tok_layer = np.array(step_tokens[timed], np.float64)
+    bytes_layer = np.array(step_bytes[timed], np.float64)
+    kv_tokens = float(tok_layer.sum()) * NL
+    value = kv_tokens / wall
+    attn_total_s = attn_ms.sum() / 1e3
+    achieved = float(bytes_layer.sum() * NL / attn_total_s / 1e9)
+    log("step %.3f ms, attention %.1f us/launch, %.0f GB/s, %.3g KV tokens/s (whole step)"
+        % (wall / args.steps * 1e3, attn_ms.mean() * 1e3, achieved, value))
+
+    # ---------------------------------------------------------- compaction --
+    comp = compaction_bench(torch, dk, lib, dev, sptr, args.compaction_rounds)
+
+    # -------------------------------------------------------- cpu baseline --
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "KV tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "llama8b decode step: B=64, Hq=32, Hkv=8, D=128, ctx U[1024,4096], "
+                        "f_hi U[0.1,0.5], f_pr U[0.2,0.6], K8V4/K4V2 group 32, 16/32 tokens "
+                        "per page; per step 1 request recycled + re-prefilled, 63 decode "
+                        "appends, attention; %d layers on one page pool" % NL,
+            "global_batch": B,
+            "layers": NL,
+            "attention_splits": S,
+        },
+        "roofline": {
+            "kernel": "attn_decode",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": None,
+            "bytes_per_launch": float(bytes_layer.mean()),
+            "us_per_launch": float(attn_ms.mean() * 1e3),
+        },
+        "attention": {
+            "kv_tokens_per_s": float(tok_layer.sum() * NL / attn_total_s),
+            "kv_tokens_per_launch": float(tok_layer.mean()),
+            "fp16_equivalent_gbps": float(tok_layer.sum() * NL * 512 / attn_total_s / 1e9),
+        },
+        "compaction": comp,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def compaction_bench(torch, dk, lib, dev, sptr, rounds):
+    """2^20-page pool, 4096 tables (60% of pages held), Bernoulli(0.35) release per held
+    page, then a refill of what each table lost; compaction and refill timed apart."""
+    from paper_2412_03131_amd import inputs
+    cfg = inputs.CONFIGS["compact"]
+    ring, demand = inputs.compaction_setup()
+    n_tab, npg = cfg["tables"], cfg["num_pages"]
+    L = dk.layout(max_seq_len=(cfg["p_max"] - 1) * 16)
+    c = dk.Cache(L, npg, n_tab, 1, device=dev, ring=torch.from_numpy(ring), with_pool=False)
+    tpp = torch.tensor([16, 32], dtype=torch.int32, device=dev)
+    dk.alloc_pages(c, torch.from_numpy(demand).to(dev))
+    c.len.copy_(c.pages * tpp)
+    masks = [torch.from_numpy(inputs.release_mask(cfg["seed"], r, n_tab, L.p_max)).to(dev)
+             for r in range(rounds)]
+    ws_c = torch.empty(dk.workspace_size(dk.OP_COMPACT, L, n_tab, 0, 1), dtype=torch.uint8, device=dev)
+    ws_a = torch.empty(dk.workspace_size(dk.OP_ALLOC, L, n_tab, 0, 1), dtype=torch.uint8, device=dev)
+    cs = c.struct()
+    Lp = C.byref(L)
+    live = int(demand.sum())
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(rounds)]
+    before = torch.empty_like(c.pages)
+    lost = torch.empty_like(c.pages)
+    torch.cuda.synchronize()
+    # keep the GPU busy while the host enqueues every round, so the events time
+    # the kernels rather than the Python loop
+    torch.cuda._sleep(int(2.4e9 * 3e-4 * rounds) + 1)
+    for r in range(rounds):
+        before.copy_(c.pages)
+        ev[r][0].record()
+        rc = lib.diffkv_compact_free_list(Lp, C.byref(cs), n_tab, C.c_void_p(masks[r].data_ptr()),
+                                          C.c_void_p(ws_c.data_ptr()), ws_c.numel(), sptr)
+        ev[r][1].record()
+        torch.sub(before, c.pages, out=lost)
+        rc |= lib.diffkv_alloc_pages(Lp, C.byref(cs), n_tab, C.c_void_p(lost.data_ptr()),
+                                     C.c_void_p(ws_a.data_ptr()), ws_a.numel(), sptr)
+        ev[r][2].record()
+        torch.mul(c.pages, tpp, out=c.len)
+        if rc:
+            raise RuntimeError("compaction bench call failed")
+    torch.cuda.synchronize()
+    ring_ptr = c.ring_ptr.cpu().numpy()
+    released = int(ring_ptr[1]) - npg
+    if int(c.status.item()) != 0 or int(c.pages.sum().item()) != live:
+        raise RuntimeError("compaction bench state check failed")
+    cms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    ams = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    res = {
+        "workload": "2^20 pages, 4096 tables, %d held (60%%), Bernoulli(0.35) release, %d rounds"
+                    % (live, rounds),
+        "pages_per_s": live / (cms.mean() / 1e3),
+        "released_pages_per_s": released / rounds / (cms.mean() / 1e3),
+        "us_per_round": float(cms.mean() * 1e3),
+        "us_p10_p90": [float(np.percentile(cms, 10) * 1e3), float(np.percentile(cms, 90) * 1e3)],
+        "refill_us_per_round": float(ams.mean() * 1e3),
+        "released_per_round": released / rounds,
+        "ring_wraps": int(ring_ptr[1] // npg),
+    }
+    log("compaction: %.1f us/round, %.3g pages/s, refill %.1f us" %
+        (res["us_per_round"], res["pages_per_s"], res["refill_us_per_round"]))
+    return res
+
+
+def cpu_baseline(w, seconds):
+    """The oracle's fp64 attention, single-threaded on the host, over the first 8
+    requests of the same workload, repeated until `seconds` of CPU time are spent."""
+    from oracle import oracle as orc
+    nreq = 8
+    Lo = orc.layout(max_seq_len=int(w["new_len"][:nreq].max()) + 16)
+    rows = int(w["new_len"][:nreq].sum())
+    Hkv = w["Hkv"]
+    tabs = nreq * Hkv
+    npg = int(tabs * (int(w["new_len"][:nreq].max()) // 16 + 4))
+    oc = orc.Cache(Lo, npg, nreq, Hkv)
+    orc.quantize_append(oc, w["new_len"][:nreq], w["k"][:rows], w["v"][:rows], w["score"][:rows],
+                        quota=w["quota"][:nreq])
+    q = w["q"][:nreq]
+    tokens = int(oc.len.sum())
+    t0 = time.process_time()
+    reps = 0
+    while True:
+        orc.attention(oc, q, SCALE)
+        reps += 1
+        el = time.process_time() - t0
+        if el >= seconds:
+            break
+    res = {"value": tokens * reps / el, "unit": "KV tokens/s", "cores": 1, "kind": "oracle",
+           "sample": "fp64 oracle attention over requests 0-7 of the llama8b workload "
+                     "(%d KV tokens), %d passes, %.1f s CPU" % (tokens, reps, el)}
+    log("cpu baseline: %.3g KV tokens/s" % res["value"])
+    return res
+
+
+if __name__ == "__main__":
+    main()

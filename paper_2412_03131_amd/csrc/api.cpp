@@ -72,7 +72,7 @@ bool layout_kernels_supported(const diffkv_layout* L)
 {
     return L->head_dim == kD && L->group == kG && L->k_bits[0] == 8 && L->k_bits[1] == 4 &&
            L->v_bits[0] == 4 && L->v_bits[1] == 2 && L->tokens_per_page[0] == kTHi &&
-           L->tokens_per_page[1] == kTLo;
+           L->tokens_per_page[1] == kTLo && attention_layout_matches(L);
 }
 
 bool cache_valid(const diffkv_cache* c)

@@ -59,31 +59,37 @@ __device__ __forceinline__ int wave_isum_w(int x)
     return x;
 }
 
-// Inclusive prefix sum over a full 64-lane wave.
-__device__ __forceinline__ int wave_incl_scan(int x)
+// Inclusive prefix sum over a full 64-lane wave with DPP: shifts of 1, 2, 4
+// and 8 inside each 16-lane row, then row_bcast:15 and row_bcast:31 carry the
+// row totals upward (lanes without a source read 0).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x)
 {
-    const int l = lane_id();
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        int y = __shfl_up(x, o, kWave);
-        if (l >= o) x += y;
-    }
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xF, true);
+}
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x)
+{
+    x += dpp_u32<0x111, 0xF>(x);  // row_shr:1
+    x += dpp_u32<0x112, 0xF>(x);  // row_shr:2
+    x += dpp_u32<0x114, 0xF>(x);  // row_shr:4
+    x += dpp_u32<0x118, 0xF>(x);  // row_shr:8
+    x += dpp_u32<0x142, 0xA>(x);  // row_bcast:15 into rows 1 and 3
+    x += dpp_u32<0x143, 0xC>(x);  // row_bcast:31 into rows 2 and 3
     return x;
 }
+__device__ __forceinline__ int wave_incl_scan(int x) { return (int)wave_incl_scan_u32((uint32_t)x); }
+// two independent 32-bit counters packed in one 64-bit value
 __device__ __forceinline__ long long wave_incl_scan64(long long x)
 {
-    const int l = lane_id();
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        long long y = __shfl_up(x, o, kWave);
-        if (l >= o) x += y;
-    }
-    return x;
+    const uint32_t lo = wave_incl_scan_u32((uint32_t)x);
+    const uint32_t hi = wave_incl_scan_u32((uint32_t)((unsigned long long)x >> 32));
+    return (long long)(((unsigned long long)hi << 32) | lo);
 }
 
 // Exclusive block scan of one value per thread (blockDim.x multiple of 64,
 // at most 1024).  Returns the exclusive prefix; *total gets the block sum.
-// `lds` must hold blockDim.x/64 + 1 entries.
+// `lds` must hold blockDim.x/64 + 1 entries.  64-bit values are two
+// independent 32-bit counters (no carry between the halves).
 template <typename TInt>
 __device__ __forceinline__ TInt block_excl_scan(TInt x, TInt* lds, TInt* total)
 {
@@ -109,6 +115,33 @@ __device__ __forceinline__ TInt block_excl_scan(TInt x, TInt* lds, TInt* total)
     *total = lds[nw];
     __syncthreads();
     return r;
+}
+
+// Block-wide sum of a true 64-bit value and OR of flag bits (all threads get
+// the result).  `lds` must hold blockDim.x/64 + 1 entries.
+__device__ __forceinline__ long long block_sum_or(long long x, uint32_t bits, long long* lds,
+                                                  uint32_t* bits_out)
+{
+    const int w = threadIdx.x / kWave;
+    const int nw = blockDim.x / kWave;
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        x += __shfl_xor(x, o, kWave);
+        bits |= (uint32_t)__shfl_xor((int)bits, o, kWave);
+    }
+    __shared__ uint32_t s_bits;
+    if (threadIdx.x == 0) s_bits = 0;
+    __syncthreads();
+    if (lane_id() == 0) {
+        lds[w] = x;
+        atomicOr(&s_bits, bits);
+    }
+    __syncthreads();
+    long long t = 0;
+    for (int i = 0; i < nw; ++i) t += lds[i];
+    *bits_out = s_bits;
+    __syncthreads();
+    return t;
 }
 
 // ---- fp16 helpers ----------------------------------------------------------

@@ -99,5 +99,6 @@ hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st);
 hipError_t launch_alloc(const AllocArgs& a, hipStream_t st);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
+bool attention_layout_matches(const diffkv_layout* L);
 
 }  // namespace dkv

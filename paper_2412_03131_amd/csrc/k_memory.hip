@@ -34,12 +34,12 @@ __device__ __forceinline__ uint32_t score_key(float s)
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // ---------------------------------------------------------------------------
-// append_classify: grid (Hkv, B), block 256
+// append_classify: grid (Hkv, B), block 1024
 // ---------------------------------------------------------------------------
-constexpr int kClsThreads = 256;
+constexpr int kClsThreads = 1024;
+constexpr int kClsLdsKeys = 8192;  // tables with more new tokens re-read keys from global
 
-__global__ __launch_bounds__(kClsThreads) void append_classify(
-    AppendArgs a)
+__global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
 {
     const int h = blockIdx.x, b = blockIdx.y;
     const int H = a.Hkv;
@@ -47,21 +47,18 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(
     const int tid = threadIdx.x;
     __shared__ long long s_scan[kClsThreads / kWave + 1];
     __shared__ int s_hist[2][256];
-    __shared__ int s_red[kClsThreads / kWave];
-    __shared__ int s_sel[8];
+    __shared__ int s_sel[4];
+    __shared__ uint32_t s_keys[kClsLdsKeys];
 
     // row offset of this sequence (sum of new_len over lower sequences)
-    int part = 0;
+    long long part = 0;
     for (int i = tid; i < b; i += kClsThreads) part += a.new_len[i];
-    part = wave_isum_w<kWave>(part);
-    if (lane_id() == 0) s_red[tid / kWave] = part;
-    __syncthreads();
-    int off_b = 0;
-    for (int i = 0; i < kClsThreads / kWave; ++i) off_b += s_red[i];
+    uint32_t unused;
+    const long long off_b = block_sum_or(part, 0u, s_scan, &unused);
     const int n = a.new_len[b];
     TState* ts = a.tstate + t;
-    const bool bad = n < 0 || n > a.max_new || (long long)off_b + n > a.total_new ||
-                     (b == a.B - 1 && (long long)off_b + n != a.total_new);
+    const bool bad = n < 0 || n > a.max_new || off_b + n > a.total_new ||
+                     (b == a.B - 1 && off_b + n != a.total_new);
     if (bad) {
         if (tid == 0) {  // the plan kernel turns n < 0 into DIFFKV_ST_BAD_INPUT
             ts->cnt[0] = ts->cnt[1] = 0;
@@ -71,12 +68,13 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(
     }
     if (h == 0 && tid == 0) {
         a.sold[b] = a.seq_len[b];
-        a.row_off[b] = off_b;
+        a.row_off[b] = (int)off_b;
     }
     const int W = a.window < n ? a.window : n;
     const int avail = n - W;
-    const float* sc = a.score + (long long)off_b * H + h;
-    int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
+    const float* sc = a.score + off_b * H + h;
+    int32_t* ord = a.ord + off_b * H + (long long)h * n;
+    const bool in_lds = avail <= kClsLdsKeys;
 
     // ---- quota form: two-target radix select (k-th largest key) ----------
     int k_sel[2] = {0, 0};
@@ -85,51 +83,74 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(
     const bool quota = a.quota != nullptr;
     float thr_h = 0.f, thr_l = 0.f;
     if (quota) {
-        int q0 = a.quota[2 * t], q1 = a.quota[2 * t + 1];
-        int nh = q0 < 0 ? 0 : (q0 > avail ? avail : q0);
-        int nl = q1 < 0 ? 0 : (q1 > avail - nh ? avail - nh : q1);
+        const int q0 = a.quota[2 * t], q1 = a.quota[2 * t + 1];
+        const int nh = q0 < 0 ? 0 : (q0 > avail ? avail : q0);
+        const int nl = q1 < 0 ? 0 : (q1 > avail - nh ? avail - nh : q1);
         k_sel[0] = nh;
         k_sel[1] = nh + nl;
-        uint32_t prefix[2] = {0, 0}, mask = 0;
-        int kk[2] = {k_sel[0], k_sel[1]};
-        for (int shift = 24; shift >= 0; shift -= 8) {
-            for (int i = tid; i < 512; i += kClsThreads) (&s_hist[0][0])[i] = 0;
-            __syncthreads();
-            for (int j = tid; j < avail; j += kClsThreads) {
-                uint32_t key = score_key(sc[(long long)j * H]);
-                uint32_t dig = (key >> shift) & 255u;
-#pragma unroll
-                for (int s = 0; s < 2; ++s)
-                    if (kk[s] > 0 && (key & mask) == prefix[s]) atomicAdd(&s_hist[s][dig], 1);
+        // a cut that keeps every non-window token needs no selection
+        const bool sel0 = nh > 0 && nh < avail, sel1 = nh + nl > 0 && nh + nl < avail;
+        if (sel0 || sel1) {
+            if (in_lds) {
+                for (int j = tid; j < avail; j += kClsThreads) s_keys[j] = score_key(sc[(long long)j * H]);
+                __syncthreads();
             }
-            __syncthreads();
-            if (tid < 2) {
-                const int s = tid;
-                if (kk[s] > 0) {
-                    int above = 0, d = 255;
-                    for (; d > 0; --d) {
-                        if (above + s_hist[s][d] >= kk[s]) break;
-                        above += s_hist[s][d];
+            uint32_t prefix[2] = {0, 0}, mask = 0;
+            int kk[2] = {sel0 ? nh : 0, sel1 ? nh + nl : 0};
+            for (int shift = 24; shift >= 0; shift -= 8) {
+                for (int i = tid; i < 512; i += kClsThreads) (&s_hist[0][0])[i] = 0;
+                __syncthreads();
+                for (int j = tid; j < avail; j += kClsThreads) {
+                    const uint32_t key = in_lds ? s_keys[j] : score_key(sc[(long long)j * H]);
+                    const uint32_t dig = (key >> shift) & 255u;
+#pragma unroll
+                    for (int s2 = 0; s2 < 2; ++s2)
+                        if (kk[s2] > 0 && (key & mask) == prefix[s2]) atomicAdd(&s_hist[s2][dig], 1);
+                }
+                __syncthreads();
+                if (tid < 2 * kWave) {  // two waves find the cut bins with a scan from the top
+                    const int s2 = tid / kWave, l = tid & (kWave - 1);
+                    if (kk[s2] > 0) {
+                        // lane l owns bins 255-4l .. 252-4l (descending)
+                        int c[4], tot4 = 0;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) { c[e] = s_hist[s2][255 - 4 * l - e]; tot4 += c[e]; }
+                        const int incl = wave_incl_scan(tot4);
+                        int above = incl - tot4;
+                        if (above < kk[s2] && incl >= kk[s2]) {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                if (above + c[e] >= kk[s2]) {
+                                    s_sel[2 * s2] = 255 - 4 * l - e;
+                                    s_sel[2 * s2 + 1] = above;
+                                    break;
+                                }
+                                above += c[e];
+                            }
+                        }
                     }
-                    s_sel[2 * s] = d;
-                    s_sel[2 * s + 1] = above;
                 }
-            }
-            __syncthreads();
+                __syncthreads();
 #pragma unroll
-            for (int s = 0; s < 2; ++s) {
-                if (kk[s] > 0) {
-                    prefix[s] |= (uint32_t)s_sel[2 * s] << shift;
-                    kk[s] -= s_sel[2 * s + 1];
+                for (int s2 = 0; s2 < 2; ++s2) {
+                    if (kk[s2] > 0) {
+                        prefix[s2] |= (uint32_t)s_sel[2 * s2] << shift;
+                        kk[s2] -= s_sel[2 * s2 + 1];
+                    }
                 }
+                mask |= 255u << shift;
+                __syncthreads();
             }
-            mask |= 255u << shift;
-            __syncthreads();
+            K[0] = prefix[0];
+            K[1] = prefix[1];
+            need[0] = kk[0];  // tokens with key == K that still belong above the cut
+            need[1] = kk[1];
         }
-        K[0] = prefix[0];
-        K[1] = prefix[1];
-        need[0] = kk[0];  // tokens with key == K that still belong above the cut
-        need[1] = kk[1];
+        // cuts at 0 or at avail: every token is above (or below) them
+        if (!sel0) { K[0] = 0; need[0] = nh > 0 ? avail : 0; }
+        if (!sel1) { K[1] = 0; need[1] = nh + nl > 0 ? avail : 0; }
+        if (!sel0 && nh > 0) k_sel[0] = -1;  // marker: all non-window tokens are high
+        if (!sel1 && nh + nl > 0) k_sel[1] = -1;
     } else {
         const float N = (float)(a.seq_len[b] + n);
         thr_h = a.alpha_h / N;
@@ -138,6 +159,7 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(
 
     // ---- classes and in-section ranks, in position order ------------------
     long long carry_tie = 0, carry_rank = 0;
+    const bool need_ties = quota && (k_sel[0] > 0 || k_sel[1] > 0);
     for (int base = 0; base < n; base += kClsThreads) {
         const int j = base + tid;
         const bool valid = j < n;
@@ -145,21 +167,28 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(
         float s = 0.f;
         uint32_t key = 0;
         if (valid && !win) {
-            s = sc[(long long)j * H];
-            key = score_key(s);
+            if (quota && in_lds && need_ties) key = s_keys[j];
+            else {
+                s = sc[(long long)j * H];
+                key = score_key(s);
+            }
         }
         bool hi = win, lo = false;
         if (quota) {
             const bool e0 = valid && !win && k_sel[0] > 0 && key == K[0];
             const bool e1 = valid && !win && k_sel[1] > 0 && key == K[1];
-            long long tot;
-            long long ex = block_excl_scan<long long>((long long)e0 | ((long long)e1 << 32), s_scan, &tot);
-            ex += carry_tie;
-            carry_tie += tot;
-            const int r0 = (int)(ex & 0xffffffffll), r1 = (int)(ex >> 32);
+            int r0 = 0, r1 = 0;
+            if (need_ties) {
+                long long tot;
+                long long ex = block_excl_scan<long long>((long long)e0 | ((long long)e1 << 32), s_scan, &tot);
+                ex += carry_tie;
+                carry_tie += tot;
+                r0 = (int)(ex & 0xffffffffll);
+                r1 = (int)(ex >> 32);
+            }
             if (valid && !win) {
-                hi = k_sel[0] > 0 && (key > K[0] || (e0 && r0 < need[0]));
-                lo = !hi && k_sel[1] > 0 && (key > K[1] || (e1 && r1 < need[1]));
+                hi = k_sel[0] < 0 || (k_sel[0] > 0 && (key > K[0] || (e0 && r0 < need[0])));
+                lo = !hi && (k_sel[1] < 0 || (k_sel[1] > 0 && (key > K[1] || (e1 && r1 < need[1]))));
             }
         } else if (valid && !win) {
             hi = s >= thr_h;
@@ -226,13 +255,10 @@ __global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
         total += need_sum;
         if (held > P) ovf = 1;
     }
-    long long tot;
-    block_excl_scan<long long>(total | ((long long)ovf << 62), s_scan, &tot);
-    const long long total_all = tot & ((1ll << 62) - 1);
-    const bool overflow = (tot >> 62) != 0;
-    uint32_t bits = 0;
+    uint32_t bits;
+    const long long total_all = block_sum_or(total, ovf ? (uint32_t)DIFFKV_ST_TABLE_OVERFLOW : 0u,
+                                             s_scan, &bits);
     if (total_all > s_tail - s_head) bits |= DIFFKV_ST_OUT_OF_PAGES;
-    if (overflow) bits |= DIFFKV_ST_TABLE_OVERFLOW;
     if (bits) {
         if (tid == 0) {
             atomicOr(a.status, bits);
@@ -318,12 +344,21 @@ __device__ __forceinline__ void quant_pair(uint32_t xbits, int lb, uint32_t& sz,
     sz = s16 | (z16 << 16);
 }
 
-__global__ __launch_bounds__(kWave) void append_quant(AppendArgs a)
+// One workgroup of four waves per job (one page of one table); the job's
+// tokens are dealt round-robin to the waves, each wave prefetching its next
+// token's K/V rows while it quantizes the current one.  The dimension-major
+// V code rows of the page are built in registers per wave and OR-ed together
+// through LDS before one store.
+constexpr int kQuantWaves = 4;
+
+__global__ __launch_bounds__(kQuantWaves * kWave) void append_quant(AppendArgs a)
 {
     if (!a.flags->ok) return;
+    __shared__ uint64_t s_rows[kQuantWaves][kWave][2];
     const int njobs = a.flags->njobs;
     const long long head_old = a.flags->head_old;
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
     const int grp = lane >> 4;
     const int H = a.Hkv;
     const int P = a.p_max;
@@ -345,38 +380,54 @@ __global__ __launch_bounds__(kWave) void append_quant(AppendArgs a)
             id = trow[tslot];
         } else {
             const int need_hi = a.pages[2 * t] - ts.pold[0];
-            long long r = head_old + ts.ring_off + (sec ? need_hi : 0) + (p - ts.pold[sec]);
+            const long long r = head_old + ts.ring_off + (sec ? need_hi : 0) + (p - ts.pold[sec]);
             id = a.ring[r % a.num_pages];
-            if (lane == 0) trow[tslot] = id;
+            if (threadIdx.x == 0) trow[tslot] = id;
         }
         if ((unsigned)id >= (unsigned)a.num_pages) continue;  // never write outside the pool
         uint8_t* pg = a.pool + (long long)id * page_bytes;
         const bool fresh = (u0 == p * T);
         if (fresh) {
-            uint4 z = make_uint4(0, 0, 0, 0);
-            for (long long o = (long long)lane * 16; o < page_bytes; o += kWave * 16)
+            const uint4 z = make_uint4(0, 0, 0, 0);
+            for (long long o = (long long)threadIdx.x * 16; o < page_bytes; o += kQuantWaves * kWave * 16)
                 *reinterpret_cast<uint4*>(pg + o) = z;
             __threadfence();  // the zeros land before this job's data stores
+            __syncthreads();
         }
         const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
         const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
         const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
-        uint64_t row0 = 0, row1 = 0;
-        if (!fresh) {
-            const uint4 r = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
-            row0 = ((uint64_t)r.y << 32) | r.x;
-            row1 = ((uint64_t)r.w << 32) | r.z;
-        }
         const int n = ts.n;
         const int off_b = a.row_off[b];
         const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
-        for (int u = u0; u < u1; ++u) {
-            const int s = u - p * T;
+        auto row_of = [&](int u) {
             const int r = u - ts.lold[sec];
             const int j = sec ? ord[n - 1 - r] : ord[r];
+            return j;
+        };
+        uint64_t row0 = 0, row1 = 0;
+        int u = u0 + wave;
+        uint32_t kx = 0, vx = 0;
+        int j = 0;
+        if (u < u1) {
+            j = row_of(u);
             const long long row = (long long)(off_b + j) * H + h;
-            const uint32_t kx = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
-            const uint32_t vx = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
+            kx = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
+            vx = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
+        }
+        for (; u < u1; u += kQuantWaves) {
+            // prefetch the wave's next token
+            const int un = u + kQuantWaves;
+            uint32_t kn = 0, vn = 0;
+            int jn = 0;
+            if (un < u1) {
+                jn = row_of(un);
+                const long long rn = (long long)(off_b + jn) * H + h;
+                kn = reinterpret_cast<const uint32_t*>(a.k + rn * kD)[lane];
+                vn = reinterpret_cast<const uint32_t*>(a.v + rn * kD)[lane];
+            }
+            const int s = u - p * T;
+            const long long row = (long long)(off_b + j) * H + h;
             uint32_t sz, c0, c1;
             quant_pair(kx, (1 << kb) - 1, sz, c0, c1);
             if (kb == 8) {
@@ -398,9 +449,29 @@ __global__ __launch_bounds__(kWave) void append_quant(AppendArgs a)
                 reinterpret_cast<float*>(pg + a.off_score[sec])[s] = a.score[row];
                 reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[s] = a.sold[b] + j;
             }
+            kx = kn;
+            vx = vn;
+            j = jn;
         }
-        *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
-            make_uint4((uint32_t)row0, (uint32_t)(row0 >> 32), (uint32_t)row1, (uint32_t)(row1 >> 32));
+        s_rows[wave][lane][0] = row0;
+        s_rows[wave][lane][1] = row1;
+        __syncthreads();
+        if (wave == 0) {
+            uint64_t r0 = 0, r1 = 0;
+            if (!fresh) {
+                const uint4 r = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
+                r0 = ((uint64_t)r.y << 32) | r.x;
+                r1 = ((uint64_t)r.w << 32) | r.z;
+            }
+#pragma unroll
+            for (int w = 0; w < kQuantWaves; ++w) {
+                r0 |= s_rows[w][lane][0];
+                r1 |= s_rows[w][lane][1];
+            }
+            *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
+                make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
+        }
+        __syncthreads();  // s_rows is reused by the next job
     }
 }
 
@@ -419,19 +490,17 @@ __global__ __launch_bounds__(kPlanThreads) void alloc_plan(AllocArgs a)
     }
     __syncthreads();
     long long total = 0;
-    int ovf = 0, neg = 0;
+    uint32_t flags = 0;
     for (int t = tid; t < NT; t += kPlanThreads) {
         int d0 = a.demand[2 * t], d1 = a.demand[2 * t + 1];
-        if (d0 < 0 || d1 < 0) neg = 1;
+        if (d0 < 0 || d1 < 0) flags |= DIFFKV_ST_BAD_INPUT;
         total += (long long)(d0 > 0 ? d0 : 0) + (d1 > 0 ? d1 : 0);
-        if ((long long)a.pages[2 * t] + a.pages[2 * t + 1] + d0 + d1 > a.p_max) ovf = 1;
+        if ((long long)a.pages[2 * t] + a.pages[2 * t + 1] + d0 + d1 > a.p_max)
+            flags |= DIFFKV_ST_TABLE_OVERFLOW;
     }
-    long long tot;
-    block_excl_scan<long long>(total | ((long long)ovf << 62) | ((long long)neg << 61), s_scan, &tot);
-    uint32_t bits = 0;
-    if ((tot >> 61) & 1) bits |= DIFFKV_ST_BAD_INPUT;
-    if ((tot >> 62) & 1) bits |= DIFFKV_ST_TABLE_OVERFLOW;
-    if ((tot & ((1ll << 61) - 1)) > s_tail - s_head) bits |= DIFFKV_ST_OUT_OF_PAGES;
+    uint32_t bits;
+    const long long total_all = block_sum_or(total, flags, s_scan, &bits);
+    if (total_all > s_tail - s_head) bits |= DIFFKV_ST_OUT_OF_PAGES;
     if (bits) {
         if (tid == 0) {
             atomicOr(a.status, bits);
@@ -601,7 +670,7 @@ hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st)
 {
     hipLaunchKernelGGL(append_classify, dim3(a.Hkv, a.B), dim3(kClsThreads), 0, st, a);
     hipLaunchKernelGGL(append_plan, dim3(1), dim3(kPlanThreads), 0, st, a);
-    hipLaunchKernelGGL(append_quant, dim3(grid_quant), dim3(kWave), 0, st, a);
+    hipLaunchKernelGGL(append_quant, dim3(grid_quant), dim3(kQuantWaves * kWave), 0, st, a);
     return hipGetLastError();
 }
 

@@ -157,6 +157,22 @@ class Cache:
     def num_tables(self):
         return self.num_seqs * self.num_kv_heads
 
+    def view(self, seq_lo, seq_hi):
+        """Cache over sequences [seq_lo, seq_hi) sharing this cache's pool, ring, pointers
+        and status (e.g. one layer of a cache whose "sequences" are layer-major)."""
+        v = Cache.__new__(Cache)
+        v.L = self.L
+        v.num_pages = self.num_pages
+        v.num_seqs = seq_hi - seq_lo
+        v.num_kv_heads = self.num_kv_heads
+        H = self.num_kv_heads
+        v.pool, v.ring, v.ring_ptr, v.status = self.pool, self.ring, self.ring_ptr, self.status
+        v.page_table = self.page_table[seq_lo * H:seq_hi * H]
+        v.pages = self.pages[seq_lo * H:seq_hi * H]
+        v.len = self.len[seq_lo * H:seq_hi * H]
+        v.seq_len = self.seq_len[seq_lo:seq_hi]
+        return v
+
     def struct(self):
         return CacheStruct(self.pool.data_ptr(), self.num_pages, self.page_table.data_ptr(),
                            self.pages.data_ptr(), self.len.data_ptr(), self.seq_len.data_ptr(),

@@ -44,10 +44,13 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--layers", type=int, default=4)
-    ap.add_argument("--splits", type=int, default=0, help="attention split count (0 = auto)")
+    ap.add_argument("--splits", type=int, default=0, help="attention split count (0 = balanced shares)")
     ap.add_argument("--compaction-rounds", type=int, default=100)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--hq", type=int, default=0,
+                    help="with --only attention: query heads per sequence (default: the "
+                         "workload's 32; a multiple of the 8 KV heads, at most 64)")
     ap.add_argument("--only", choices=("all", "attention", "copy"), default="all",
                     help="profiling aids that print no benchmark line: 'attention' builds the "
                          "cache and times only the attention calls; 'copy' runs a plain 1 GiB "
@@ -155,7 +158,7 @@ def main():
         for l in range(NL):
             m[(l * B + r) * Hkv:(l * B + r + 1) * Hkv] = 1
         masks.append(m)
-    S = args.splits if args.splits > 0 else dk.auto_splits(L, B, Hkv)
+    S = args.splits
     ws_att = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, Hq, Hkv, 0, S)),
                          dtype=torch.uint8, device=dev)
     ws_c = torch.empty(dk.workspace_size(dk.OP_COMPACT, L, NL * B, 0, Hkv), dtype=torch.uint8,
@@ -209,6 +212,16 @@ def main():
         step_tokens.append(int(len_hi.sum() + len_lo.sum()))
 
     if args.only == "attention":
+        if args.hq:
+            hq = args.hq
+            qx = torch.randn((B, hq, 128), device=dev).half()
+            outx = torch.empty((B, hq, 128), dtype=torch.float32, device=dev)
+            lsex = torch.empty((B, hq), dtype=torch.float32, device=dev)
+            wsx = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, hq, Hkv, 0, S)),
+                              dtype=torch.uint8, device=dev)
+            attn_args[0] = [(Lp, C.byref(cs), hq, vp(qx), float(SCALE), vp(outx), vp(lsex), S,
+                             vp(wsx), wsx.numel(), sptr) for cs in cstructs]
+            Hq = hq
         for s in range(args.warmup):
             for l in range(NL):
                 lib.diffkv_decode_attention(*attn_args[0][l])

@@ -137,15 +137,12 @@ enum {
 
 /* Bytes of device workspace the operation needs (host out-parameter).
  * APPEND: num_seqs, num_kv_heads, total_new.  ATTENTION: num_seqs,
- * num_q_heads, num_splits (0 = the automatic choice for these sizes).
+ * num_q_heads, num_splits (0 = the balanced mode).
  * COMPACT / ALLOC: num_seqs*num_kv_heads tables.  Unused sizes are ignored. */
 diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout,
                                     int32_t num_seqs, int32_t num_q_heads,
                                     int32_t num_kv_heads, int64_t total_new,
                                     int32_t num_splits, size_t* bytes);
-
-/* The split count diffkv_decode_attention uses for num_splits = 0. */
-int32_t diffkv_auto_splits(const diffkv_layout* layout, int32_t num_seqs, int32_t num_kv_heads);
 
 /*
  * KV compressor (Sec. 4) + page placement (Sec. 5.2, 5.3): classes the new
@@ -202,10 +199,17 @@ diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_c
  *   lse  device fp32 [num_seqs][num_q_heads] (natural log of the softmax
  *        denominator incl. the max) or NULL.  An empty table gives out = 0,
  *        lse = -inf.
- *   num_splits  0 = automatic, 1 = one workgroup per table, S > 1 = the
- *        table's page list is cut into S page-aligned ranges whose partial
- *        (max, sum, acc) states are merged afterwards (Sec. 6.2 sequence
- *        split).  Results are deterministic for a given S.
+ *   num_splits  0 = balanced (default): the page lists of all tables, in
+ *        table order, form one list of work units (a high page 1, a low page
+ *        2) that is cut into one equal share per workgroup the device holds
+ *        at once; a table spread over several shares has their (max, sum,
+ *        acc) states merged in page order (Sec. 6.2 sequence split).
+ *        S >= 1: each table is cut into min(S, pages) equal page ranges,
+ *        merged the same way (S = 1: no split, no merge).  Results are
+ *        deterministic for a given mode and device.
+ *   ws   device workspace of diffkv_workspace_size(DIFFKV_OP_ATTENTION, ...)
+ *        bytes (always needed: it holds the work bookkeeping and partial
+ *        states).
  * num_q_heads must be a multiple of num_kv_heads, with at most 8 query heads
  * per KV head.
  */

@@ -118,24 +118,29 @@ AppendWs append_ws(int64_t B, int64_t Hkv, int64_t total_new)
     return w;
 }
 
-int64_t attn_ws(int64_t B, int64_t Hq, int64_t splits)
+// Attention workspace: balanced mode (splits = 0): per-table first unit, the
+// unit total and one partial state per (share, table) slot k + t; split mode
+// (S > 1): S partial states per table; S = 1 needs none.
+struct AttnWs {
+    int64_t ustart, utot, part, total, nparts;
+};
+
+AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits)
 {
-    return splits > 1 ? align256(splits * B * Hq * (kD + 2) * 4) : 0;
+    AttnWs w;
+    const int64_t T = B * Hkv;
+    const int64_t gq = Hkv > 0 ? Hq / Hkv : 1;
+    w.nparts = splits == 0 ? kAttnMaxWorkers + T : (splits > 1 ? T * splits : 0);
+    int64_t o = 0;
+    w.ustart = o; o = align256(o + T * 8);
+    w.utot = o;   o = align256(o + 8);
+    w.part = o;   o = align256(o + w.nparts * gq * (kD + 2) * 4);
+    w.total = o;
+    return w;
 }
 
 int64_t compact_ws(int64_t T) { return align256(sizeof(CallFlags)) + 2 * align256(T * 4); }
 int64_t alloc_ws(int64_t T) { return align256(sizeof(CallFlags)) + align256(T * 16); }
-
-int32_t auto_splits(const diffkv_layout* L, int64_t B, int64_t Hkv)
-{
-    const int64_t tables = B * Hkv;
-    if (tables <= 0) return 1;
-    int64_t s = (1024 + tables - 1) / tables;
-    const int64_t cap = L->p_max / 8 > 1 ? L->p_max / 8 : 1;
-    if (s > 16) s = 16;
-    if (s > cap) s = cap;
-    return (int32_t)(s < 1 ? 1 : s);
-}
 
 }  // namespace
 
@@ -146,12 +151,6 @@ diffkv_status diffkv_layout_init(diffkv_layout* out, int32_t head_dim, int32_t g
                                  const int32_t tokens_per_page[2], int32_t max_seq_len)
 {
     return fill_layout(out, head_dim, group, k_bits, v_bits, tokens_per_page, max_seq_len);
-}
-
-int32_t diffkv_auto_splits(const diffkv_layout* layout, int32_t num_seqs, int32_t num_kv_heads)
-{
-    if (!layout_valid(layout)) return 1;
-    return auto_splits(layout, num_seqs, num_kv_heads);
 }
 
 diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout, int32_t num_seqs,
@@ -166,8 +165,7 @@ diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout, int
         return DIFFKV_OK;
     case DIFFKV_OP_ATTENTION: {
         if (num_q_heads <= 0 || num_kv_heads <= 0 || num_splits < 0) return DIFFKV_E_INVAL;
-        const int32_t s = num_splits == 0 ? auto_splits(layout, num_seqs, num_kv_heads) : num_splits;
-        *bytes = (size_t)attn_ws(num_seqs, num_q_heads, s);
+        *bytes = (size_t)attn_ws(num_seqs, num_q_heads, num_kv_heads, num_splits).total;
         return DIFFKV_OK;
     }
     case DIFFKV_OP_COMPACT:
@@ -252,11 +250,11 @@ diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_
     if (cache->num_seqs == 0) return DIFFKV_OK;
     if (!q || !out) return DIFFKV_E_INVAL;
     if (cache->num_seqs > 65535 || cache->num_kv_heads > 65535) return DIFFKV_E_UNSUPPORTED;
-    const int32_t S = num_splits == 0 ? auto_splits(layout, cache->num_seqs, cache->num_kv_heads)
-                                      : num_splits;
-    if (S > 65535) return DIFFKV_E_INVAL;
-    const int64_t need = attn_ws(cache->num_seqs, num_q_heads, S);
-    if (need > 0 && (!ws || (int64_t)ws_bytes < need)) return DIFFKV_E_WORKSPACE;
+    if (num_splits > 65535) return DIFFKV_E_INVAL;
+    const AttnWs w = attn_ws(cache->num_seqs, num_q_heads, cache->num_kv_heads, num_splits);
+    if ((int64_t)cache->num_seqs * cache->num_kv_heads * (num_splits > 0 ? num_splits : 1) > INT32_MAX)
+        return DIFFKV_E_INVAL;
+    if (!ws || (int64_t)ws_bytes < w.total) return DIFFKV_E_WORKSPACE;
     AttnArgs a;
     memset(&a, 0, sizeof(a));
     a.p_max = layout->p_max;
@@ -278,8 +276,11 @@ diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_
     a.scale_log2 = sm_scale * 1.4426950408889634f;
     a.out = out;
     a.lse = lse;
-    a.splits = S;
-    a.part = static_cast<float*>(ws);
+    a.splits = num_splits;
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    a.ustart = reinterpret_cast<long long*>(base + w.ustart);
+    a.utot = reinterpret_cast<long long*>(base + w.utot);
+    a.part = reinterpret_cast<float*>(base + w.part);
     hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
 }

@@ -88,17 +88,23 @@ struct AttnArgs {
     const int32_t* len;
     int B, Hkv, Hq;
     const uint16_t* q;
-    float scale_log2;  // sm_scale * log2(e)
+    float scale_log2;    // sm_scale * log2(e)
     float* out;
     float* lse;
-    int splits;
-    float* part;  // [splits][B][Hq][kD + 2] when splits > 1
+    int splits;          // 0: balanced shares; S >= 1: min(S, pages) ranges per table
+    int workers;         // balanced mode: shares (= workgroups of attn_decode)
+    long long* ustart;   // [T] first work unit of each table (balanced mode)
+    long long* utot;     // [1] total work units (balanced mode)
+    float* part;         // partial states {max, sum, acc[kD]} per head
 };
+
+// most shares of the balanced attention mode (sizes its workspace)
+constexpr int kAttnMaxWorkers = 2048;
 
 hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st);
 hipError_t launch_alloc(const AllocArgs& a, hipStream_t st);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
-hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
+hipError_t launch_attention(AttnArgs a, hipStream_t st);
 bool attention_layout_matches(const diffkv_layout* L);
 
 }  // namespace dkv

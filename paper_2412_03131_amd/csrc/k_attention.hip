@@ -1,13 +1,14 @@
 // k_attention.hip -- decode attention over the differentiated paged KV cache
 // for gfx950 (DiffKV Eq. (1) of Sec. 2.1, kernel structure of Sec. 6.2).
 //
-// Grid (splits, Hkv, B); a workgroup of four waves owns one table (one
-// sequence, one KV head) -- or one page range of it when the sequence is
-// split -- and all GQ query heads that read it.  Each wave walks its share of
-// the table's pages, high-precision pages first, then low-precision pages,
-// and loads page i+1 into registers while it computes page i.  The wave's
-// page IDs are fetched 64 at a time into one VGPR and read back with
-// v_readlane, so a page's loads wait on nothing but the previous page.
+// Work: a table's pages (high pages first, then low pages) are processed by
+// one four-wave workgroup for all GQ query heads that read them, or -- in the
+// balanced mode -- every table's pages are laid end to end and cut into one
+// equal share per resident workgroup, so the spread of table lengths costs
+// nothing; tables that straddle shares are merged by attn_merge.  Inside a
+// workgroup each wave takes every fourth page and keeps page i+1 in flight
+// (two register buffers in rotation) while it computes page i; page IDs come
+// from scalar loads issued two pages ahead.
 //
 // Lane mapping inside a wave (64 lanes = 4 rows of 16):
 //   key phase    lane = grp*16 + j: token j (and j+16 on 32-token pages),
@@ -15,20 +16,21 @@
 //                pairs and computes sum(q*code) with v_dot2_f32_f16 on codes
 //                turned into fp16 denormals (exact, one v_perm or AND per two
 //                codes), then s*sum + z*sum(q) (scale and zero factored out of
-//                the dot product); the four groups of a token are summed with
-//                v_permlane16/32_swap.
-//   softmax      online, base 2, per query head, with a lazily raised max: the
-//                page max (DPP row ops) is only taken when a logit exceeds
-//                the running max by more than 2^8.
+//                the dot product).  A transposed sum over the four rows
+//                (v_permlane16/32_swap) leaves head 4s + r of token j in
+//                row r, so the softmax costs one exp2 per (token, head).
+//   softmax      online, base 2, with a lazily raised max: the page max (DPP
+//                row ops) is only taken when a logit exceeds the running max
+//                by more than 2^8.
 //   value phase  lane owns dims 2*lane, 2*lane+1 (its row's group).  The
-//                weights p*s_v (fp32) of the row's tokens go through LDS (one
-//                broadcast read per token for all heads) into fp32 FMAs with
-//                the codes; the zero-point term sum(p*z_v) is accumulated per
-//                lane and added once at the end.  (fp16 weights with v_dot2
-//                would halve these FMAs but miss the 2e-3 bound when one
-//                token dominates.)
-// The four waves' (max, sum, acc) states merge through LDS; with splits > 1
-// the per-range states go to the workspace and attn_merge combines them.
+//                weights p*s_v of the row's tokens, rounded to fp16, go
+//                through LDS (one broadcast read per token pair for all heads)
+//                into v_dot2_f32_f16 with two tokens' codes as fp16 denormals;
+//                the zero-point term and the weights' rounding error (charged
+//                at the centre code) are accumulated per lane and added once.
+// The four waves' (max, sum, acc) states merge through LDS.
+#include <atomic>
+
 #include "internal.hpp"
 
 namespace dkv {
@@ -95,70 +97,95 @@ __device__ __forceinline__ float dot2(half2_t a, uint32_t b, float c)
 {
     return __builtin_amdgcn_fdot2(a, __builtin_bit_cast(half2_t, b), c, false);
 }
+// a*b with a zero accumulator as one instruction (the compiler would otherwise
+// materialise the zero for the accumulate-in-place encoding)
+__device__ __forceinline__ float dot2_first(half2_t a, uint32_t b)
+{
+    float d;
+    asm("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(d) : "v"(a), "v"(b));
+    return d;
+}
 
 constexpr float kTwo24 = 16777216.0f;
 
-// Raw bytes of one page as one lane needs them.
+// Raw bytes of one page as one lane needs them.  High and low pages take
+// the same seven loads (two of them unused on high pages, inside the page), so
+// the buffers of a prefetch pipeline never need register copies.
 struct PageRaw {
     uint4 k0, k1;  // high: K8 chunks 2g, 2g+1 of token j; low: K4 chunk g of tokens j, j+16
     uint4 vr;      // V code rows of dims 2*lane, 2*lane+1
-    uint32_t m0, m1, m2, m3;  // high: kmeta, vmeta; low: kmeta j, kmeta j+16, vmeta j, vmeta j+16
+    uint32_t m0;   // K meta {s, z} of token j, group g
+    uint32_t m1;   // low: K meta of token j+16
+    uint32_t m2;   // V meta of token j, group g
+    uint32_t m3;   // low: V meta of token j+16
 };
 
-__device__ __forceinline__ uint4 ld16(const uint8_t* p) { return *reinterpret_cast<const uint4*>(p); }
-__device__ __forceinline__ uint32_t ld4(const uint8_t* p) { return *reinterpret_cast<const uint32_t*>(p); }
+__device__ __forceinline__ uint4 ld16(const uint8_t* p, uint32_t o) { return *reinterpret_cast<const uint4*>(p + o); }
+__device__ __forceinline__ uint32_t ld4(const uint8_t* p, uint32_t o) { return *reinterpret_cast<const uint32_t*>(p + o); }
 
+// Both page types put K chunk c of token j at (c*T + j)*16 with 2 (high) or 1
+// (low) chunks per group, i.e. at 512*g + 16*j (+256) for this lane, and K
+// meta at 2048 + 16*j + 4*g; the V segments differ only in base and the V
+// meta row stride (16 or 32 tokens).
 __device__ __forceinline__ void load_page(PageRaw& r, const uint8_t* pg, bool hi, int lane)
 {
-    const int grp = lane >> 4, jl = lane & 15;
-    if (hi) {
-        r.k0 = ld16(pg + kOffKcHi + ((2 * grp) * kTHi + jl) * 16);
-        r.k1 = ld16(pg + kOffKcHi + ((2 * grp + 1) * kTHi + jl) * 16);
-        r.vr = ld16(pg + kOffVcHi + lane * 16);
-        r.m0 = ld4(pg + kOffKmHi + (jl * kNG + grp) * 4);
-        r.m1 = ld4(pg + kOffVmHi + (grp * kTHi + jl) * 4);
-        r.m2 = r.m3 = 0;
-    } else {
-        r.k0 = ld16(pg + kOffKcLo + (grp * kTLo + jl) * 16);
-        r.k1 = ld16(pg + kOffKcLo + (grp * kTLo + jl + 16) * 16);
-        r.vr = ld16(pg + kOffVcLo + lane * 16);
-        r.m0 = ld4(pg + kOffKmLo + (jl * kNG + grp) * 4);
-        r.m1 = ld4(pg + kOffKmLo + ((jl + 16) * kNG + grp) * 4);
-        r.m2 = ld4(pg + kOffVmLo + (grp * kTLo + jl) * 4);
-        r.m3 = ld4(pg + kOffVmLo + (grp * kTLo + jl + 16) * 4);
-    }
+    const uint32_t grp = (uint32_t)lane >> 4, jl = (uint32_t)lane & 15;
+    static_assert(kOffKcHi == 0 && kOffKcLo == 0 && kOffKmHi == 2048 && kOffKmLo == 2048, "page layout");
+    const uint32_t kc = grp * 512 + jl * 16;
+    const uint32_t km = 2048 + jl * 16 + grp * 4;
+    const uint8_t* pv = pg + (hi ? kOffVcHi : kOffVcLo);
+    const uint8_t* pm = pg + (hi ? kOffVmHi : kOffVmLo);
+    const uint32_t vm = (hi ? grp * (kTHi * 4) : grp * (kTLo * 4)) + jl * 4;
+    r.k0 = ld16(pg, kc);
+    r.k1 = ld16(pg, kc + 256);
+    r.vr = ld16(pv, (uint32_t)lane * 16);
+    r.m0 = ld4(pg, km);
+    r.m1 = ld4(pg, km + 256);
+    r.m2 = ld4(pm, vm);
+    r.m3 = ld4(pm, grp * (kTLo * 4) + jl * 4 + 64);
 }
 
 template <int GQ>
 struct WaveState {
-    float m[GQ];       // running max (log2 domain), wave-uniform
-    float l[GQ];       // this lane's share of the running sum
-    float z[GQ];       // this lane's share of sum(p * z_v) for its row's group
-    float acc[GQ][2];  // dims 2*lane, 2*lane+1
+    static constexpr int NS = (GQ + 3) / 4;  // head slots per lane in the softmax layout
+    float m[NS];       // running max of head 4s + row (log2 domain), row-uniform
+    float l[NS];       // this lane's share of the running sum of head 4s + row
+    float z[GQ];       // this lane's share of the zero-point term of head hh (group = row)
+    float acc[GQ][2];  // dims 2*lane, 2*lane+1, in units of 2^-24
 };
 
-// LDS for the softmax weights of one page: [row][token][head] fp32, rows
-// padded by four floats so the four rows' broadcast reads hit different banks.
+// LDS for the value weights of one page: [row = value group][token pair][head]
+// as fp16 pairs; rows padded by four dwords so the four rows' broadcast reads
+// hit different banks.
 template <int GQ>
 struct CoefLds {
-    static constexpr int kH = GQ <= 4 ? 4 : 8;
-    static constexpr int kRow = kTLo * kH + 4;
-    float v[kAttnWaves][4 * kRow];
+    static constexpr int kH = GQ <= 4 ? 4 : 8;  // heads per pair entry (dwords)
+    static constexpr int kRow = 16 * kH + 4;     // dwords per row (16 pairs)
+    uint32_t v[kAttnWaves][4 * kRow];
 };
 
-template <int GQ>
-__device__ __forceinline__ void read_coef(const float* row, int j, float (&c)[GQ])
+// Sum over the four rows with a transpose: row r of the result holds the sum of
+// argument r (heads a, b, c, d -> rows 0, 1, 2, 3).
+__device__ __forceinline__ float xsum4(float a, float b, float c, float d)
 {
-    const float* p = row + j * CoefLds<GQ>::kH;
-    float t[8];
-    const float4 v0 = *reinterpret_cast<const float4*>(p);
-    t[0] = v0.x; t[1] = v0.y; t[2] = v0.z; t[3] = v0.w;
-    if constexpr (GQ > 4) {
-        const float4 v1 = *reinterpret_cast<const float4*>(p + 4);
-        t[4] = v1.x; t[5] = v1.y; t[6] = v1.z; t[7] = v1.w;
-    }
-#pragma unroll
-    for (int h = 0; h < GQ; ++h) c[h] = t[h];
+    auto ab = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    auto cd = __builtin_amdgcn_permlane16_swap(__float_as_uint(c), __float_as_uint(d), false, false);
+    const float u = __uint_as_float(ab[0]) + __uint_as_float(ab[1]);
+    const float w = __uint_as_float(cd[0]) + __uint_as_float(cd[1]);
+    auto uw = __builtin_amdgcn_permlane32_swap(__float_as_uint(u), __float_as_uint(w), false, false);
+    return __uint_as_float(uw[0]) + __uint_as_float(uw[1]);
+}
+
+// o[r] = x of row r (same column), in every lane
+__device__ __forceinline__ void gather4(float x, float* o)
+{
+    auto eo = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    auto e = __builtin_amdgcn_permlane32_swap(eo[0], eo[0], false, false);
+    auto od = __builtin_amdgcn_permlane32_swap(eo[1], eo[1], false, false);
+    o[0] = __uint_as_float(e[0]);
+    o[1] = __uint_as_float(od[0]);
+    o[2] = __uint_as_float(e[1]);
+    o[3] = __uint_as_float(od[1]);
 }
 
 // Softmax weights are exp2(logit - m) with a running max m that is only
@@ -166,20 +193,31 @@ __device__ __forceinline__ void read_coef(const float* row, int j, float (&c)[GQ
 constexpr float kSlack = 8.0f;
 
 // One page: logits, online softmax, weighted value sum.  NT = tokens per lane.
+//
+// Value weights.  For token j, head h and value group g the weight
+// w = p * s_v is rounded to fp16 (c) and multiplied with the codes on
+// v_dot2_f32_f16 (codes as fp16 denormals, products exact in fp32).  The
+// rounding error (w - c) is charged to the zero-point term at the centre code
+// (7.5 for 4-bit, 1.5 for 2-bit): sum_j p*z_v + centre*(w - c), so what is
+// left of it scales with |code - centre| <= half the code range, at most
+// 2^-12 of the group's value range per unit of softmax weight.  2-bit codes in
+// odd crumbs are extracted as 4*code, and their c carries w/4.
 template <int GQ, int NT>
 __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, const half2_t (&q2)[GQ][16],
                                         const float (&qsum)[GQ], float sl2, int n_valid, int lane,
-                                        float* coef_row)
+                                        uint32_t* coef_row)
 {
+    constexpr int NS = WaveState<GQ>::NS;
+    constexpr int kH = CoefLds<GQ>::kH;
     const int jl = lane & 15;
-    float lg[NT][GQ];
+    // ---- logits: lane (group row, token jl) partial dot products, then a
+    // transposed row sum: afterwards row r holds head 4s + r of token jl + 16*tk
+    float lg[NT][NS];
 #pragma unroll
     for (int tk = 0; tk < NT; ++tk) {
         const uint32_t km = tk ? r.m1 : r.m0;
         const float ks = h2f(km & 0xffffu) * (kTwo24 * sl2), kz = h2f(km >> 16) * sl2;
         float dlo[GQ], dhi[GQ];
-#pragma unroll
-        for (int hh = 0; hh < GQ; ++hh) dlo[hh] = dhi[hh] = 0.f;
         if (NT == 1) {
             // K8: two dwords (8 dims) -> four (d, d+4) pairs, one v_perm each
             const uint32_t w[8] = {r.k0.x, r.k0.y, r.k0.z, r.k0.w, r.k1.x, r.k1.y, r.k1.z, r.k1.w};
@@ -189,7 +227,8 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
                 for (int a2 = 0; a2 < 4; ++a2) {
                     const uint32_t x = perm_pair(w[2 * m + 1], w[2 * m], a2);
 #pragma unroll
-                    for (int hh = 0; hh < GQ; ++hh) dlo[hh] = dot2(q2[hh][4 * m + a2], x, dlo[hh]);
+                    for (int hh = 0; hh < GQ; ++hh)
+                        dlo[hh] = m + a2 == 0 ? dot2_first(q2[hh][0], x) : dot2(q2[hh][4 * m + a2], x, dlo[hh]);
                 }
             }
         } else {
@@ -203,113 +242,150 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
                 const uint32_t x2 = v8 & 0x000F000Fu, x3 = v8 & 0x00F000F0u;
 #pragma unroll
                 for (int hh = 0; hh < GQ; ++hh) {
-                    dlo[hh] = dot2(q2[hh][4 * m + 0], x0, dlo[hh]);
-                    dhi[hh] = dot2(q2[hh][4 * m + 1], x1, dhi[hh]);
+                    dlo[hh] = m == 0 ? dot2_first(q2[hh][0], x0) : dot2(q2[hh][4 * m + 0], x0, dlo[hh]);
+                    dhi[hh] = m == 0 ? dot2_first(q2[hh][1], x1) : dot2(q2[hh][4 * m + 1], x1, dhi[hh]);
                     dlo[hh] = dot2(q2[hh][4 * m + 2], x2, dlo[hh]);
                     dhi[hh] = dot2(q2[hh][4 * m + 3], x3, dhi[hh]);
                 }
             }
         }
+        float part[4 * NS];
+#pragma unroll
+        for (int hh = 0; hh < 4 * NS; ++hh) {
+            if (hh < GQ) {
+                const float d = NT == 1 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
+                part[hh] = fmaf(ks, d, kz * qsum[hh]);
+            } else {
+                part[hh] = 0.f;
+            }
+        }
         const bool valid = jl + 16 * tk < n_valid;
 #pragma unroll
-        for (int hh = 0; hh < GQ; ++hh) {
-            const float d = NT == 1 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
-            const float part = rows_sum4(fmaf(ks, d, kz * qsum[hh]));
-            lg[tk][hh] = valid ? part : -INFINITY;
+        for (int s = 0; s < NS; ++s) {
+            const float x = xsum4(part[4 * s], part[4 * s + 1], part[4 * s + 2], part[4 * s + 3]);
+            lg[tk][s] = valid ? x : -INFINITY;
         }
     }
-    // online softmax with a lazily raised max
+    // ---- online softmax with a lazily raised max (one head per lane and slot)
     bool raise = false;
 #pragma unroll
-    for (int hh = 0; hh < GQ; ++hh)
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
-        for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][hh] > st.m[hh] + kSlack;
+        for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.m[s] + kSlack;
     if (__builtin_amdgcn_ballot_w64(raise)) {
+        float al[4 * NS];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            float mx = lg[0][s];
+            if (NT > 1) mx = fmax_sel(mx, lg[NT - 1][s]);
+            mx = row_max16(mx);
+            const float mnew = fmax_sel(st.m[s], mx);
+            const float alpha = __builtin_amdgcn_exp2f(st.m[s] - mnew);
+            st.m[s] = mnew;
+            st.l[s] *= alpha;
+            gather4(alpha, al + 4 * s);
+        }
 #pragma unroll
         for (int hh = 0; hh < GQ; ++hh) {
-            float mx = lg[0][hh];
-            if (NT > 1) mx = fmax_sel(mx, lg[NT - 1][hh]);
-            mx = row_max16(mx);
-            const float mnew = fmax_sel(st.m[hh], mx);
-            const float alpha = __builtin_amdgcn_exp2f(st.m[hh] - mnew);
-            st.m[hh] = mnew;
-            st.l[hh] *= alpha;
-            st.z[hh] *= alpha;
-            st.acc[hh][0] *= alpha;
-            st.acc[hh][1] *= alpha;
+            st.z[hh] *= al[hh];
+            st.acc[hh][0] *= al[hh];
+            st.acc[hh][1] *= al[hh];
         }
     }
-    float p[NT][GQ];
+    float p[NT][NS];
 #pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) {
+    for (int s = 0; s < NS; ++s) {
 #pragma unroll
         for (int tk = 0; tk < NT; ++tk) {
-            p[tk][hh] = __builtin_amdgcn_exp2f(lg[tk][hh] - st.m[hh]);
-            st.l[hh] += p[tk][hh];
+            p[tk][s] = __builtin_amdgcn_exp2f(lg[tk][s] - st.m[s]);
+            st.l[s] += p[tk][s];
         }
     }
-    // Weights p*s_v (fp32) to LDS for the row's lanes; zero-point term sum(p*z_v)
-    // in registers.
-    constexpr int kH = CoefLds<GQ>::kH;
+    // ---- value weights of token jl + 16*tk for this lane's group (row), all
+    // heads: fp16 to LDS, zero-point and rounding terms into z
+    _Float16* crow = reinterpret_cast<_Float16*>(coef_row);
 #pragma unroll
     for (int tk = 0; tk < NT; ++tk) {
-        const uint32_t vm = NT == 1 ? r.m1 : (tk ? r.m3 : r.m2);
+        float pg[4 * NS];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) gather4(p[tk][s], pg + 4 * s);
+        const uint32_t vm = tk ? r.m3 : r.m2;
         const float vs = h2f(vm & 0xffffu), vz = h2f(vm >> 16);
-        float c[kH];
+        constexpr float centre = NT == 1 ? 7.5f : 1.5f;
+        const bool by4 = NT == 2 && (jl & 1);
+        const float vs_c = by4 ? vs * 0.25f : vs;
+        const float cc = by4 ? 4.f * centre : centre;
+        const float zc = fmaf(centre, vs, vz);
+        const int pi = NT == 1 ? ((jl >> 3) * 4 + (jl & 3)) : (tk * 8 + (jl & 7));
+        const int pos = NT == 1 ? ((jl >> 2) & 1) : (jl >> 3);
+        _Float16* dst = crow + pi * 2 * kH + pos;
 #pragma unroll
-        for (int hh = 0; hh < kH; ++hh) c[hh] = hh < GQ ? p[tk][hh] * vs : 0.f;
-#pragma unroll
-        for (int hh = 0; hh < GQ; ++hh) st.z[hh] = fmaf(p[tk][hh], vz, st.z[hh]);
-        float* dst = coef_row + (jl + 16 * tk) * kH;
-#pragma unroll
-        for (int i = 0; i < kH; i += 4)
-            *reinterpret_cast<float4*>(dst + i) = make_float4(c[i], c[i + 1], c[i + 2], c[i + 3]);
+        for (int hh = 0; hh < GQ; ++hh) {
+            const _Float16 c = (_Float16)(pg[hh] * vs_c);
+            st.z[hh] = fmaf(pg[hh], zc, st.z[hh]);
+            st.z[hh] = fmaf(-cc, (float)c, st.z[hh]);
+            dst[2 * hh] = c;
+        }
     }
     __builtin_amdgcn_wave_barrier();
-    // value phase: tokens of this row's group, codes of dims 2*lane, 2*lane+1.
-    // The weights of 16 tokens are read from LDS in one burst before their
-    // FMAs, so the reads overlap each other instead of stalling per token.
+    // ---- value phase: lane owns dims 2*lane, 2*lane+1 (its row's group); token
+    // pairs of each dword as fp16 denormals, one v_dot2 per pair and head.
     const uint32_t w[4] = {r.vr.x, r.vr.y, r.vr.z, r.vr.w};
+    // weights of token pairs p0 .. p0+3, all heads (four broadcast reads per
+    // pair group, issued together)
+    auto read_cf = [&](int p0, half2_t (&cf)[4][GQ]) {
 #pragma unroll
-    for (int half = 0; half < NT; ++half) {
-        float cf[16][GQ];
+        for (int pp = 0; pp < 4; ++pp) {
+            const uint32_t* src = coef_row + (p0 + pp) * kH;
+            uint32_t t[kH];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) read_coef<GQ>(coef_row, 16 * half + j, cf[j]);
-        if constexpr (NT == 1) {
-            // 16 tokens x 4 bits per 64-bit row: dword (j >> 3), nibble (j & 7)
+            for (int i = 0; i < kH; i += 4) {
+                const uint4 v = *reinterpret_cast<const uint4*>(src + i);
+                t[i] = v.x; t[i + 1] = v.y; t[i + 2] = v.z; t[i + 3] = v.w;
+            }
 #pragma unroll
-            for (int dw = 0; dw < 2; ++dw) {
-                const uint32_t a = w[dw], b = w[2 + dw];
-                const uint32_t alo = a & 0x0F0F0F0Fu, ahi = (a >> 4) & 0x0F0F0F0Fu;
-                const uint32_t blo = b & 0x0F0F0F0Fu, bhi = (b >> 4) & 0x0F0F0F0Fu;
+            for (int hh = 0; hh < GQ; ++hh) cf[pp][hh] = __builtin_bit_cast(half2_t, t[hh]);
+        }
+    };
+    if constexpr (NT == 1) {
+        // 16 tokens x 4 bits per 64-bit row; nibbles k, k+4 of dword dw -> pair 4*dw + k
 #pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const int j = 8 * dw + k;
-                    const uint32_t sa = (k & 1) ? ahi : alo, sb = (k & 1) ? bhi : blo;
-                    const float c0 = (float)((sa >> (8 * (k >> 1))) & 0xFFu);
-                    const float c1 = (float)((sb >> (8 * (k >> 1))) & 0xFFu);
+        for (int dw = 0; dw < 2; ++dw) {
+            half2_t cf[4][GQ];
+            read_cf(4 * dw, cf);
+            const uint32_t a = w[dw], b = w[2 + dw];
 #pragma unroll
-                    for (int hh = 0; hh < GQ; ++hh) {
-                        st.acc[hh][0] = fmaf(cf[j][hh], c0, st.acc[hh][0]);
-                        st.acc[hh][1] = fmaf(cf[j][hh], c1, st.acc[hh][1]);
-                    }
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t xa = (a >> (4 * k)) & 0x000F000Fu, xb = (b >> (4 * k)) & 0x000F000Fu;
+#pragma unroll
+                for (int hh = 0; hh < GQ; ++hh) {
+                    st.acc[hh][0] = dot2(cf[k][hh], xa, st.acc[hh][0]);
+                    st.acc[hh][1] = dot2(cf[k][hh], xb, st.acc[hh][1]);
                 }
             }
-        } else {
-            // 32 tokens x 2 bits per 64-bit row: tokens 16*half.. in dword `half`, crumb j & 15
+        }
+    } else {
+        // 32 tokens x 2 bits per 64-bit row; dword `half` holds tokens 16*half + r
+        // at bits 2r; crumbs r, r+8 -> pair 8*half + (r & 7) (4*code for odd r)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
             const uint32_t a = w[half], b = w[2 + half];
 #pragma unroll
-            for (int sh = 0; sh < 4; ++sh) {
-                const uint32_t sa = (a >> (2 * sh)) & 0x03030303u, sb = (b >> (2 * sh)) & 0x03030303u;
+            for (int q4 = 0; q4 < 2; ++q4) {
+                half2_t cf[4][GQ];
+                read_cf(8 * half + 4 * q4, cf);
 #pragma unroll
-                for (int by = 0; by < 4; ++by) {
-                    const int j = 4 * by + sh;
-                    const float c0 = (float)((sa >> (8 * by)) & 0xFFu);
-                    const float c1 = (float)((sb >> (8 * by)) & 0xFFu);
+                for (int s2 = 0; s2 < 2; ++s2) {
+                    const int s4 = 2 * q4 + s2;
+                    const uint32_t ya = a >> (4 * s4), yb = b >> (4 * s4);
+                    const uint32_t x1a = ya & 0x00030003u, x1b = yb & 0x00030003u;
+                    const uint32_t x4a = ya & 0x000C000Cu, x4b = yb & 0x000C000Cu;
 #pragma unroll
                     for (int hh = 0; hh < GQ; ++hh) {
-                        st.acc[hh][0] = fmaf(cf[j][hh], c0, st.acc[hh][0]);
-                        st.acc[hh][1] = fmaf(cf[j][hh], c1, st.acc[hh][1]);
+                        st.acc[hh][0] = dot2(cf[2 * s2][hh], x1a, st.acc[hh][0]);
+                        st.acc[hh][1] = dot2(cf[2 * s2][hh], x1b, st.acc[hh][1]);
+                        st.acc[hh][0] = dot2(cf[2 * s2 + 1][hh], x4a, st.acc[hh][0]);
+                        st.acc[hh][1] = dot2(cf[2 * s2 + 1][hh], x4b, st.acc[hh][1]);
                     }
                 }
             }
@@ -318,139 +394,236 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
     __builtin_amdgcn_wave_barrier();
 }
 
-template <int GQ>
-__global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
+// ---------------------------------------------------------------------------
+// Tables and their work
+// ---------------------------------------------------------------------------
+// A table's pages in attention order: high pages 0 .. ph-1 (slots 0 ..), then
+// low pages ph .. np-1 (slots p_max-1 downward).  For balancing, a high page
+// is kHighUnits units of work and a low page kLowUnits (twice the tokens; the
+// measured time per page is about 5:3): page p starts at unit kHighUnits*p
+// (p < ph) or kHighUnits*ph + kLowUnits*(p - ph).
+constexpr int kHighUnits = 3;
+constexpr int kLowUnits = 5;
+
+struct TableInfo {
+    int ph, np;
+    int len_hi, len_lo;
+    long long units;
+};
+
+__device__ __forceinline__ TableInfo table_info(const AttnArgs& a, int t)
 {
-    const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-    const int t = b * a.Hkv + h;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    const int grp = lane >> 4;
+    TableInfo ti;
     const int P = a.p_max;
-    const int len_hi = a.len[2 * t], len_lo = a.len[2 * t + 1];
+    ti.len_hi = a.len[2 * t];
+    ti.len_lo = a.len[2 * t + 1];
     // page counts from the section lengths, clamped to the table width
-    int ph = (len_hi + kTHi - 1) / kTHi;
-    int pl = (len_lo + kTLo - 1) / kTLo;
+    int ph = (ti.len_hi + kTHi - 1) / kTHi;
+    int pl = (ti.len_lo + kTLo - 1) / kTLo;
     ph = ph < 0 ? 0 : (ph > P ? P : ph);
     pl = pl < 0 ? 0 : (pl > P - ph ? P - ph : pl);
-    const int np = ph + pl;
-    const int p0 = (int)(((long long)split * np) / a.splits);
-    const int p1 = (int)(((long long)(split + 1) * np) / a.splits);
-    const int nmine = p1 - p0 > wave ? (p1 - p0 - wave + kAttnWaves - 1) / kAttnWaves : 0;
+    ti.ph = ph;
+    ti.np = ph + pl;
+    ti.units = (long long)kHighUnits * ph + (long long)kLowUnits * pl;
+    return ti;
+}
+
+// first page whose first unit is >= x (np if none)
+__device__ __forceinline__ int page_at_unit(long long x, int ph, int np)
+{
+    if (x <= 0) return 0;
+    const long long xh = (long long)kHighUnits * ph;
+    const long long p = x <= xh ? (x + kHighUnits - 1) / kHighUnits : ph + (x - xh + kLowUnits - 1) / kLowUnits;
+    return p > np ? np : (int)p;
+}
+
+template <int GQ>
+struct AttnShared {
+    CoefLds<GQ> coef;
+    float m[kAttnWaves][8];
+    float l[kAttnWaves][8];
+    float acc[kAttnWaves][8][kD];
+    long long scan[kAttnWaves + 1];
+    int t_first;
+    long long u_first;
+};
+
+// Exclusive prefix sum of one 64-bit value per thread of the workgroup.
+__device__ __forceinline__ long long wg_excl_scan(long long x, long long* lds, long long* total)
+{
+    const int l = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+    long long inc = x;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const long long y = __shfl_up(inc, o, kWave);
+        if (l >= o) inc += y;
+    }
+    if (l == kWave - 1) lds[w] = inc;
+    __syncthreads();
+    long long before = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kAttnWaves; ++i) {
+        const long long v = lds[i];
+        before += i < w ? v : 0;
+        tot += v;
+    }
+    __syncthreads();
+    *total = tot;
+    return before + inc - x;
+}
+
+__device__ __forceinline__ void write_empty(const AttnArgs& a, int t, int gq)
+{
+    const int b = t / a.Hkv, h = t - b * a.Hkv;
+    for (int i = threadIdx.x; i < gq * kD; i += blockDim.x) {
+        const int hh = i / kD, d = i - hh * kD;
+        const long long row = (long long)b * a.Hq + h * gq + hh;
+        a.out[row * kD + d] = 0.f;
+        if (d == 0 && a.lse) a.lse[row] = -INFINITY;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// One segment: pages [pa, pb) of table t for all GQ query heads of its KV
+// head.  The four waves take every fourth page; each keeps page i+1 in
+// flight while it computes page i.  Their (max, sum, acc) states merge through LDS
+// into the output (part == nullptr) or into a partial state {max, sum, acc}
+// per head at `part` (pa == pb gives the empty state).
+// ---------------------------------------------------------------------------
+template <int GQ>
+__device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& sh, int t, const TableInfo& ti,
+                                            int pa, int pb, float* part)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int grp = lane >> 4;
+    const int P = a.p_max;
+    const int b = t / a.Hkv, h = t - b * a.Hkv;
+    const int ph = ti.ph;
+    const float sl2 = a.scale_log2;
+    const long long npool = a.num_pages;
+    const long long page_bytes = a.page_bytes;
+    uint32_t* coef_row = &sh.coef.v[wave][grp * CoefLds<GQ>::kRow];
+    const int nmine = pb - pa > wave ? (pb - pa - wave + kAttnWaves - 1) / kAttnWaves : 0;
     const int32_t* trow = a.page_table + (long long)t * P;
 
-    __shared__ CoefLds<GQ> s_coef;
-    float* coef_row = &s_coef.v[wave][grp * CoefLds<GQ>::kRow];
+    // Page IDs come from scalar loads (the page table is read-only here), each
+    // fetched three pages before its page is issued.
+    auto page_of = [&](int i) { return pa + wave + kAttnWaves * i; };
+    auto slot_of = [&](int p) { return p < ph ? p : P - 1 - (p - ph); };
+    const int i_last = nmine > 0 ? nmine - 1 : 0;
+    auto id_at = [&](int i) {
+        const int ic = i < i_last ? i : i_last;
+        return *(const __attribute__((address_space(4))) int32_t*)(trow + slot_of(page_of(ic)));
+    };
+    // Issue the loads of page i (if any) into r; ok = the page lies in the pool.
+    auto issue = [&](int i, int id, PageRaw& r, bool& ok) {
+        ok = i < nmine && (unsigned long long)id < (unsigned long long)npool;  // never read outside the pool
+        if (ok) load_page(r, a.pool + id * page_bytes, page_of(i) < ph, lane);
+    };
+    PageRaw buf0, buf1;
+    bool ok0 = false, ok1 = false;
+    int id0 = 0, id1 = 0;
+    if (nmine > 0) {
+        id0 = id_at(0);
+        id1 = id_at(1);
+        issue(0, id0, buf0, ok0);
+        id0 = id_at(2);
+    }
 
-    // q of this lane's group as fp16 pairs (d, d+4) of each 8-dim block, and its sum
+    // q of this lane's group as fp16 pairs (d, d+4) of each 8-dim block (one
+    // v_perm each), and its sum (v_dot2 with (1, 1))
     half2_t q2[GQ][16];
     float qsum[GQ];
+    constexpr uint32_t kOnes = 0x3C003C00u;  // fp16 pair (1, 1)
 #pragma unroll
     for (int hh = 0; hh < GQ; ++hh) {
         const uint4* qp = reinterpret_cast<const uint4*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
-        float s = 0.f;
+        float sq = 0.f;
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const uint4 v = qp[m];  // dims 8m .. 8m+7 as four fp16 pairs (d, d+1)
+            const uint32_t pr[4] = {__builtin_amdgcn_perm(v.z, v.x, 0x05040100u), __builtin_amdgcn_perm(v.z, v.x, 0x07060302u),
+                                    __builtin_amdgcn_perm(v.w, v.y, 0x05040100u), __builtin_amdgcn_perm(v.w, v.y, 0x07060302u)};
 #pragma unroll
             for (int a2 = 0; a2 < 4; ++a2) {
-                const uint32_t lo = a2 < 2 ? v.x : v.y, hi = a2 < 2 ? v.z : v.w;
-                const uint32_t sh = (a2 & 1) * 16;
-                const uint32_t pr = ((lo >> sh) & 0xffffu) | (((hi >> sh) & 0xffffu) << 16);
-                q2[hh][4 * m + a2] = __builtin_bit_cast(half2_t, pr);
-                s += (float)q2[hh][4 * m + a2].x + (float)q2[hh][4 * m + a2].y;
+                q2[hh][4 * m + a2] = __builtin_bit_cast(half2_t, pr[a2]);
+                sq = dot2(q2[hh][4 * m + a2], kOnes, sq);
             }
         }
-        qsum[hh] = s;
+        qsum[hh] = sq;
     }
 
     WaveState<GQ> st;
 #pragma unroll
+    for (int s = 0; s < WaveState<GQ>::NS; ++s) {
+        st.m[s] = -INFINITY;
+        st.l[s] = 0.f;
+    }
+#pragma unroll
     for (int hh = 0; hh < GQ; ++hh) {
-        st.m[hh] = -INFINITY;
-        st.l[hh] = 0.f;
         st.z[hh] = 0.f;
         st.acc[hh][0] = st.acc[hh][1] = 0.f;
     }
-    const float sl2 = a.scale_log2;
-    const long long npool = a.num_pages;
-    const long long page_bytes = a.page_bytes;
 
-    // page IDs of this wave's pages, 64 per VGPR load
-    auto page_of = [&](int i) { return p0 + wave + kAttnWaves * i; };
-    auto slot_of = [&](int p) { return p < ph ? p : P - 1 - (p - ph); };
-    int idv = -1;
-    auto load_ids = [&](int i0) {
-        const int i = i0 + lane;
-        idv = i < nmine ? trow[slot_of(page_of(i))] : -1;
-    };
-    PageRaw cur, nxt;
-    int id_cur = -1;
-    if (nmine > 0) {
-        load_ids(0);
-        id_cur = __builtin_amdgcn_readfirstlane(idv);
-        if ((unsigned long long)id_cur < (unsigned long long)npool)
-            load_page(cur, a.pool + id_cur * page_bytes, page_of(0) < ph, lane);
-    }
-    for (int i = 0; i < nmine; ++i) {
+    auto compute = [&](int i, const PageRaw& r, bool ok) {
+        if (i >= nmine || !ok) return;
         const int p = page_of(i);
-        const bool hi = p < ph;
-        int id_nxt = -1;
-        if (i + 1 < nmine) {
-            if (((i + 1) & 63) == 0) load_ids(i + 1);
-            id_nxt = __builtin_amdgcn_readlane(idv, (i + 1) & 63);
-            if ((unsigned long long)id_nxt < (unsigned long long)npool)
-                load_page(nxt, a.pool + id_nxt * page_bytes, page_of(i + 1) < ph, lane);
+        if (p < ph) {
+            do_page<GQ, 1>(st, r, q2, qsum, sl2, ti.len_hi - p * kTHi, lane, coef_row);
+        } else {
+            do_page<GQ, 2>(st, r, q2, qsum, sl2, ti.len_lo - (p - ph) * kTLo, lane, coef_row);
         }
-        if ((unsigned long long)id_cur < (unsigned long long)npool) {  // never read outside the pool
-            if (hi) {
-                do_page<GQ, 1>(st, cur, q2, qsum, sl2, len_hi - p * kTHi, lane, coef_row);
-            } else {
-                do_page<GQ, 2>(st, cur, q2, qsum, sl2, len_lo - (p - ph) * kTLo, lane, coef_row);
-            }
-        }
-        cur = nxt;
-        id_cur = id_nxt;
+    };
+    // page i computes from buffer i % 2 while page i+1 is in flight; the ID of
+    // page i is loaded when page i-2 is issued
+    for (int i = 0; i < nmine; i += 2) {
+        issue(i + 1, id1, buf1, ok1);
+        id1 = id_at(i + 3);
+        compute(i, buf0, ok0);
+        issue(i + 2, id0, buf0, ok0);
+        id0 = id_at(i + 4);
+        compute(i + 1, buf1, ok1);
     }
 
-    // ---- finish the wave: row sums of l and of the zero-point term ----------
-    __shared__ float s_m[kAttnWaves][8];
-    __shared__ float s_l[kAttnWaves][8];
-    __shared__ float s_acc[kAttnWaves][8][kD];
+    // ---- finish the wave: row sums of l (head 4s + row) and of the
+    // zero-point term (head hh, group = row); acc back from units of 2^-24
+#pragma unroll
+    for (int s = 0; s < WaveState<GQ>::NS; ++s) {
+        const float l = row_sum16(st.l[s]);
+        if ((lane & 15) == 0 && 4 * s + grp < GQ) {
+            sh.m[wave][4 * s + grp] = st.m[s];
+            sh.l[wave][4 * s + grp] = l;
+        }
+    }
 #pragma unroll
     for (int hh = 0; hh < GQ; ++hh) {
-        const float l = row_sum16(st.l[hh]);
         const float z = row_sum16(st.z[hh]);
-        if (lane == 0) {
-            s_m[wave][hh] = st.m[hh];
-            s_l[wave][hh] = l;
-        }
-        s_acc[wave][hh][2 * lane] = st.acc[hh][0] + z;
-        s_acc[wave][hh][2 * lane + 1] = st.acc[hh][1] + z;
+        sh.acc[wave][hh][2 * lane] = fmaf(st.acc[hh][0], kTwo24, z);
+        sh.acc[wave][hh][2 * lane + 1] = fmaf(st.acc[hh][1], kTwo24, z);
     }
     __syncthreads();
-    // ---- merge the waves ----------------------------------------------------
+    // ---- merge the waves: final output, or this segment's partial state ---
     for (int i = threadIdx.x; i < GQ * kD; i += kAttnThreads) {
         const int hh = i / kD, d = i - hh * kD;
         float M = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < kAttnWaves; ++w) M = fmax_sel(M, s_m[w][hh]);
+        for (int w = 0; w < kAttnWaves; ++w) M = fmax_sel(M, sh.m[w][hh]);
         float L = 0.f, O = 0.f;
         if (M != -INFINITY) {
 #pragma unroll
             for (int w = 0; w < kAttnWaves; ++w) {
-                const float f = __builtin_amdgcn_exp2f(s_m[w][hh] - M);
-                L = fmaf(s_l[w][hh], f, L);
-                O = fmaf(s_acc[w][hh][d], f, O);
+                const float f = __builtin_amdgcn_exp2f(sh.m[w][hh] - M);
+                L = fmaf(sh.l[w][hh], f, L);
+                O = fmaf(sh.acc[w][hh][d], f, O);
             }
         }
-        const int hq = h * GQ + hh;
-        if (a.splits == 1) {
-            a.out[((long long)b * a.Hq + hq) * kD + d] = (L > 0.f) ? O / L : 0.f;
-            if (d == 0 && a.lse)
-                a.lse[(long long)b * a.Hq + hq] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
+        if (part == nullptr) {
+            const long long row = (long long)b * a.Hq + h * GQ + hh;
+            a.out[row * kD + d] = (L > 0.f) ? O / L : 0.f;
+            if (d == 0 && a.lse) a.lse[row] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
         } else {
-            float* pr = a.part + (((long long)split * a.B + b) * a.Hq + hq) * kPartStride;
+            float* pr = part + hh * kPartStride;
             pr[2 + d] = O;
             if (d == 0) {
                 pr[0] = M;
@@ -458,34 +631,237 @@ __global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
             }
         }
     }
+    __syncthreads();  // LDS is reused by the next segment
 }
 
-__global__ __launch_bounds__(kD) void attn_merge(AttnArgs a)
-{
-    const int hq = blockIdx.x, b = blockIdx.y;
-    const int d = threadIdx.x;
-    const long long stride = (long long)a.B * a.Hq * kPartStride;
-    const float* pr = a.part + ((long long)b * a.Hq + hq) * kPartStride;
-    float M = -INFINITY;
-    for (int s = 0; s < a.splits; ++s) M = fmax_sel(M, pr[s * stride]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
-        for (int s = 0; s < a.splits; ++s) {
-            const float* q = pr + s * stride;
-            const float f = __builtin_amdgcn_exp2f(q[0] - M);
-            L = fmaf(q[1], f, L);
-            O = fmaf(q[2 + d], f, O);
-        }
-    }
-    a.out[((long long)b * a.Hq + hq) * kD + d] = (L > 0.f) ? O / L : 0.f;
-    if (d == 0 && a.lse)
-        a.lse[(long long)b * a.Hq + hq] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
-}
-
+// ---------------------------------------------------------------------------
+// attn_decode.
+//  splits = S >= 1: workgroup t*S + c takes range c of table t's pages, cut
+//    into min(S, pages) equal ranges (S = 1: no split).
+//  splits = 0: balanced shares.  All tables' pages, in table order, form one
+//    list of U work units; workgroup k of W owns the pages whose first unit
+//    lies in [k*U/W, (k+1)*U/W).  Each workgroup finds its first table with a
+//    prefix sum over the tables' units, then walks its tables.  A table lying
+//    inside one share is finished in place; otherwise share k writes its
+//    partial state to slot k + t (distinct for every (share, table) pair met
+//    in this walk) and attn_merge combines them.
+// ---------------------------------------------------------------------------
 template <int GQ>
-static void launch_gq(const AttnArgs& a, hipStream_t st)
+__global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
 {
-    hipLaunchKernelGGL(attn_decode<GQ>, dim3(a.splits, a.Hkv, a.B), dim3(kAttnThreads), 0, st, a);
+    __shared__ AttnShared<GQ> sh;
+    const int T = a.B * a.Hkv;
+    if (a.splits > 0) {
+        const int t = blockIdx.x / a.splits, c = blockIdx.x - t * a.splits;
+        const TableInfo ti = table_info(a, t);
+        const int n = ti.np < a.splits ? ti.np : a.splits;
+        if (n == 0) {
+            if (c == 0) write_empty(a, t, GQ);
+            return;
+        }
+        if (c >= n) return;
+        const int pa = (int)((long long)c * ti.np / n), pb = (int)((long long)(c + 1) * ti.np / n);
+        float* part = n == 1 ? nullptr : a.part + ((long long)t * a.splits + c) * GQ * kPartStride;
+        run_segment<GQ>(a, sh, t, ti, pa, pb, part);
+        return;
+    }
+    // ---- balanced shares -------------------------------------------------
+    const long long k = blockIdx.x, W = gridDim.x;
+    const int per = (T + kAttnThreads - 1) / kAttnThreads;
+    const int t0 = threadIdx.x * per;
+    const int t1 = t0 + per < T ? t0 + per : T;
+    constexpr int kKeep = 8;  // units of up to kKeep tables stay in registers
+    long long units[kKeep];
+    long long mine = 0;
+#pragma unroll
+    for (int i = 0; i < kKeep; ++i) {
+        units[i] = t0 + i < t1 ? table_info(a, t0 + i).units : 0;
+        mine += units[i];
+    }
+    for (int t = t0 + kKeep; t < t1; ++t) mine += table_info(a, t).units;
+    long long total;
+    const long long before = wg_excl_scan(mine, sh.scan, &total);
+    if (k == 0 && threadIdx.x == 0) a.utot[0] = total;
+    const long long b_lo = k * total / W, b_hi = (k + 1) * total / W;
+    if (b_lo >= b_hi) return;
+    long long u = before;
+    for (int t = t0; t < t1; ++t) {  // exactly one table holds unit b_lo
+        const int i = t - t0;
+        long long n = 0;
+#pragma unroll
+        for (int j = 0; j < kKeep; ++j) n = i == j ? units[j] : n;
+        if (i >= kKeep) n = table_info(a, t).units;
+        if (u <= b_lo && b_lo < u + n) {
+            sh.t_first = t;
+            sh.u_first = u;
+        }
+        u += n;
+    }
+    __syncthreads();
+    int t = sh.t_first;
+    long long ut = sh.u_first;
+    while (t < T && ut < b_hi) {
+        const TableInfo ti = table_info(a, t);
+        if (ti.units > 0) {
+            const int pa = page_at_unit(b_lo - ut, ti.ph, ti.np);
+            const int pb = page_at_unit(b_hi - ut, ti.ph, ti.np);
+            const bool first = ut >= b_lo;
+            const bool whole = first && ut + ti.units <= b_hi;
+            if (first && threadIdx.x == 0) a.ustart[t] = ut;
+            run_segment<GQ>(a, sh, t, ti, pa, pb, whole ? nullptr : a.part + (k + t) * GQ * kPartStride);
+        }
+        ut += ti.units;
+        ++t;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// attn_merge: one wave per (table, query head) of a table whose pages went to
+// several workgroups; combines their partial states in page order.  Also
+// writes the empty result of empty tables in the balanced mode.  Partial
+// slots of shares with an empty unit range are never read (they hold
+// whatever an earlier call left there).
+// ---------------------------------------------------------------------------
+constexpr int kMergeThreads = 256;
+
+__global__ __launch_bounds__(kMergeThreads) void attn_merge(AttnArgs a)
+{
+    const int gq = a.Hq / a.Hkv;
+    const long long job = (long long)blockIdx.x * (kMergeThreads / kWave) + threadIdx.x / kWave;
+    const int T = a.B * a.Hkv;
+    if (job >= (long long)T * gq) return;
+    const int t = (int)(job / gq), hh = (int)(job - (long long)t * gq);
+    const int lane = threadIdx.x & (kWave - 1);
+    const TableInfo ti = table_info(a, t);
+    const int b = t / a.Hkv, h = t - b * a.Hkv;
+    const long long row = (long long)b * a.Hq + h * gq + hh;
+    // candidate partial slots first + i, i < n; in the balanced mode a share
+    // whose unit range is empty (more shares than units) wrote nothing
+    long long first, kf = 0, U = 1, W = 1;
+    int n;
+    if (a.splits > 0) {
+        n = ti.np < a.splits ? ti.np : a.splits;
+        if (n <= 1) return;  // written by attn_decode
+        first = (long long)t * a.splits;
+    } else {
+        if (ti.units == 0) {
+            a.out[row * kD + 2 * lane] = 0.f;
+            a.out[row * kD + 2 * lane + 1] = 0.f;
+            if (lane == 0 && a.lse) a.lse[row] = -INFINITY;
+            return;
+        }
+        U = a.utot[0];
+        W = a.workers;
+        const long long ut = a.ustart[t];
+        // share owning unit x: the largest k with k*U/W <= x
+        kf = ((ut + 1) * W - 1) / U;
+        const long long kl = ((ut + ti.units) * W - 1) / U;
+        if (kf == kl) return;  // written by attn_decode
+        n = (int)(kl - kf + 1);
+        first = kf + t;
+    }
+    auto wrote = [&](int i) {
+        if (a.splits > 0) return true;
+        const long long k = kf + i;
+        return k * U / W != (k + 1) * U / W;
+    };
+    const float* base = a.part + first * gq * kPartStride + hh * kPartStride;
+    const long long stride = (long long)gq * kPartStride;
+    // the first kPre partials' acc pairs are loaded together with every
+    // partial's (max, sum): one round of loads for the usual 2-4 partials
+    constexpr int kPre = 4;
+    float2 pre[kPre];
+#pragma unroll
+    for (int j = 0; j < kPre; ++j)
+        pre[j] = j < n && wrote(j) ? *reinterpret_cast<const float2*>(base + j * stride + 2 + 2 * lane)
+                                   : make_float2(0.f, 0.f);
+    float M = -INFINITY;
+    for (int i = lane; i < n; i += kWave)
+        if (wrote(i)) M = fmax_sel(M, base[i * stride]);
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) M = fmax_sel(M, __shfl_xor(M, o, kWave));
+    float L = 0.f, O0 = 0.f, O1 = 0.f;
+    if (M != -INFINITY) {
+        float Lp = 0.f;
+        for (int i0 = 0; i0 < n; i0 += kWave) {
+            // weight of partial i0 + lane (0 for slots never written)
+            const int i = i0 + lane;
+            float f = 0.f;
+            if (i < n && wrote(i)) {
+                f = __builtin_amdgcn_exp2f(base[i * stride] - M);
+                Lp = fmaf(base[i * stride + 1], f, Lp);
+            }
+            int j = 0;
+            if (i0 == 0) {
+#pragma unroll
+                for (; j < kPre; ++j) {
+                    const float fj = __shfl(f, j, kWave);
+                    O0 = fmaf(pre[j].x, fj, O0);
+                    O1 = fmaf(pre[j].y, fj, O1);
+                }
+            }
+            const int cnt = n - i0 < kWave ? n - i0 : kWave;
+            for (; j < cnt; ++j) {
+                const float fj = __shfl(f, j, kWave);
+                if (fj == 0.f) continue;  // also skips slots never written
+                const float2 o2 = *reinterpret_cast<const float2*>(base + (i0 + j) * stride + 2 + 2 * lane);
+                O0 = fmaf(o2.x, fj, O0);
+                O1 = fmaf(o2.y, fj, O1);
+            }
+        }
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) Lp += __shfl_xor(Lp, o, kWave);
+        L = Lp;
+    }
+    a.out[row * kD + 2 * lane] = (L > 0.f) ? O0 / L : 0.f;
+    a.out[row * kD + 2 * lane + 1] = (L > 0.f) ? O1 / L : 0.f;
+    if (lane == 0 && a.lse) a.lse[row] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+template <int GQ>
+static const void* decode_kernel()
+{
+    return reinterpret_cast<const void*>(&attn_decode<GQ>);
+}
+
+static const void* decode_kernel_for(int gq)
+{
+    switch (gq) {
+    case 1: return decode_kernel<1>();
+    case 2: return decode_kernel<2>();
+    case 3: return decode_kernel<3>();
+    case 4: return decode_kernel<4>();
+    case 5: return decode_kernel<5>();
+    case 6: return decode_kernel<6>();
+    case 7: return decode_kernel<7>();
+    case 8: return decode_kernel<8>();
+    default: return nullptr;
+    }
+}
+
+// Workgroups of attn_decode<gq> the device holds at once (the balanced mode's
+// share count), cached per device; at most kAttnMaxWorkers.
+static int balanced_workers(int gq)
+{
+    constexpr int kDevs = 64;
+    static std::atomic<int> cache[kDevs][9];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+    const int slot = dev < kDevs ? dev : kDevs - 1;
+    int w = dev < kDevs ? cache[slot][gq].load(std::memory_order_relaxed) : 0;
+    if (w > 0) return w;
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel_for(gq), kAttnThreads, 0) != hipSuccess ||
+        per_cu < 1)
+        per_cu = 1;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 1;
+    w = per_cu * cus;
+    w = w < kAttnMaxWorkers ? w : kAttnMaxWorkers;
+    if (dev < kDevs) cache[slot][gq].store(w, std::memory_order_relaxed);
+    return w;
 }
 
 bool attention_layout_matches(const diffkv_layout* L)
@@ -495,21 +871,29 @@ bool attention_layout_matches(const diffkv_layout* L)
            L->off_vcode[1] == kOffVcLo && L->off_vmeta[1] == kOffVmLo;
 }
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t st)
+hipError_t launch_attention(AttnArgs a, hipStream_t st)
 {
     const int gq = a.Hq / a.Hkv;
-    switch (gq) {
-    case 1: launch_gq<1>(a, st); break;
-    case 2: launch_gq<2>(a, st); break;
-    case 3: launch_gq<3>(a, st); break;
-    case 4: launch_gq<4>(a, st); break;
-    case 5: launch_gq<5>(a, st); break;
-    case 6: launch_gq<6>(a, st); break;
-    case 7: launch_gq<7>(a, st); break;
-    case 8: launch_gq<8>(a, st); break;
-    default: return hipErrorInvalidValue;
+    const void* kern = decode_kernel_for(gq);
+    if (!kern) return hipErrorInvalidValue;
+    const long long T = (long long)a.B * a.Hkv;
+    long long grid;
+    if (a.splits > 0) {
+        grid = T * a.splits;
+        a.workers = 0;
+    } else {
+        a.workers = balanced_workers(gq);
+        grid = a.workers;
     }
-    if (a.splits > 1) hipLaunchKernelGGL(attn_merge, dim3(a.Hq, a.B), dim3(kD), 0, st, a);
+    if (grid < 1 || grid > INT32_MAX) return hipErrorInvalidValue;
+    void* args[] = {&a};
+    hipError_t e = hipLaunchKernel(kern, dim3((unsigned)grid), dim3(kAttnThreads), args, 0, st);
+    if (e != hipSuccess) return e;
+    if (a.splits != 1) {
+        const long long jobs = T * gq;
+        const long long mgrid = (jobs + kMergeThreads / kWave - 1) / (kMergeThreads / kWave);
+        hipLaunchKernelGGL(attn_merge, dim3((unsigned)mgrid), dim3(kMergeThreads), 0, st, a);
+    }
     return hipGetLastError();
 }
 

@@ -49,9 +49,9 @@ class CacheStruct(C.Structure):
     ]
 
 
-EXPORTS = ("diffkv_layout_init", "diffkv_workspace_size", "diffkv_auto_splits",
-           "diffkv_quantize_append", "diffkv_decode_attention", "diffkv_compact_free_list",
-           "diffkv_alloc_pages", "diffkv_status_str")
+EXPORTS = ("diffkv_layout_init", "diffkv_workspace_size", "diffkv_quantize_append",
+           "diffkv_decode_attention", "diffkv_compact_free_list", "diffkv_alloc_pages",
+           "diffkv_status_str")
 
 
 def lib():
@@ -66,7 +66,6 @@ def lib():
         PC = C.POINTER(CacheStruct)
         L.diffkv_layout_init.argtypes = [PL, i32, i32, vp, vp, vp, i32]
         L.diffkv_workspace_size.argtypes = [i32, PL, i32, i32, i32, i64, i32, C.POINTER(sz)]
-        L.diffkv_auto_splits.argtypes = [PL, i32, i32]
         L.diffkv_quantize_append.argtypes = [PL, PC, i64, i32, vp, vp, vp, vp, vp, f32, f32, i32,
                                              vp, sz, vp]
         L.diffkv_decode_attention.argtypes = [PL, PC, i32, vp, f32, vp, vp, i32, vp, sz, vp]
@@ -115,10 +114,6 @@ def workspace_size(op, L, num_seqs, num_q_heads=0, num_kv_heads=1, total_new=0, 
     _check(lib().diffkv_workspace_size(op, C.byref(L), num_seqs, num_q_heads, num_kv_heads,
                                        total_new, num_splits, C.byref(n)), "diffkv_workspace_size")
     return n.value
-
-
-def auto_splits(L, num_seqs, num_kv_heads):
-    return lib().diffkv_auto_splits(C.byref(L), num_seqs, num_kv_heads)
 
 
 def _ws(nbytes, device, ws):

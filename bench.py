@@ -36,6 +36,36 @@ sys.path.insert(0, ROOT)
 METRIC = "decode-attention KV tokens/s + achieved HBM GB/s (% of peak); compaction pages/s"
 HBM_PEAK_GBPS = 8000.0
 SCALE = 1.0 / np.sqrt(128.0)
+# measured HBM traffic of the attention call (rocprofv3 FETCH_SIZE / WRITE_SIZE),
+# valid while the attention sources hash to the value recorded with it
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_llama8b_traffic.txt")
+ATTN_SOURCES = ["k_attention.hip", "internal.hpp", "common.hpp"]
+
+
+def attention_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        with open(os.path.join(ROOT, "paper_2412_03131_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the committed counter summary, or None when
+    it is missing or was taken on different attention sources."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as fh:
+            for ln in fh:
+                if ":" in ln and not ln.startswith("#"):
+                    k, v = ln.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("sources_sha256") != attention_sources_sha256():
+            return None
+        return float(kv["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def parse():
@@ -182,21 +212,25 @@ def main():
                  for m in masks]
     seq_rows = [torch.arange(r, NL * B, B, device=dev) for r in range(B)]
 
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(NL)] for _ in range(args.steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
 
     def run_step(s, timed_idx):
+        # every layer's append, then every layer's attention back to back (the
+        # events around the attention calls then see kernel time, not the dispatch
+        # gap after an append)
         si = steps_in[s]
         r = si["r"]
         rc = lib.diffkv_compact_free_list(*comp_args[r])
         cache.seq_len.index_fill_(0, seq_rows[r], 0)
         for l in range(NL):
             rc |= lib.diffkv_quantize_append(*app_args[s][l])
-            if timed_idx is not None:
-                ev[timed_idx][l][0].record(stream)
+        if timed_idx is not None:
+            ev[timed_idx][0].record(stream)
+        for l in range(NL):
             rc |= lib.diffkv_decode_attention(*attn_args[s][l])
-            if timed_idx is not None:
-                ev[timed_idx][l][1].record(stream)
+        if timed_idx is not None:
+            ev[timed_idx][1].record(stream)
         if rc:
             raise RuntimeError("library call failed at step %d (rc %d)" % (s, rc))
 
@@ -248,7 +282,7 @@ def main():
     got = cache.len.view(NL, B, Hkv, 2)[0].cpu().numpy()
     if status != 0 or not (np.array_equal(got[..., 0], len_hi) and np.array_equal(got[..., 1], len_lo)):
         raise RuntimeError("state check failed after the timed steps (status %d)" % status)
-    attn_ms = np.array([[a.elapsed_time(b) for a, b in row] for row in ev])  # [steps, layers]
+    attn_ms = np.array([[a.elapsed_time(b) / NL] * NL for a, b in ev])  # [steps, layers], per launch
     timed = slice(args.warmup, steps_total)
     tok_layer = np.array(step_tokens[timed], np.float64)
     bytes_layer = np.array(step_bytes[timed], np.float64)
@@ -288,13 +322,13 @@ def main():
             "attention_splits": S,
         },
         "roofline": {
-            "kernel": "attn_decode",
+            "kernel": "diffkv_decode_attention (attn_decode + attn_merge)",
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None,
+            "traffic": measured_traffic(),
             "bytes_per_launch": float(bytes_layer.mean()),
             "us_per_launch": float(attn_ms.mean() * 1e3),
         },

@@ -98,8 +98,8 @@ void fill_layout_args(LayoutArgs& a, const diffkv_layout* L)
 }
 
 struct AppendWs {
-    int64_t flags, tstate, sold, row_off, ord, jobs, total;
-    int64_t max_jobs;
+    int64_t flags, tstate, sold, row_off, ord, total;
+    int64_t max_jobs;  // bound on the call's page jobs (sizes the commit grid)
 };
 
 AppendWs append_ws(int64_t B, int64_t Hkv, int64_t total_new)
@@ -113,7 +113,6 @@ AppendWs append_ws(int64_t B, int64_t Hkv, int64_t total_new)
     w.sold = o;    o = align256(o + B * 4);
     w.row_off = o; o = align256(o + B * 4);
     w.ord = o;     o = align256(o + total_new * Hkv * 4);
-    w.jobs = o;    o = align256(o + w.max_jobs * 8);
     w.total = o;
     return w;
 }
@@ -230,8 +229,9 @@ diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_c
     a.sold = reinterpret_cast<int32_t*>(base + w.sold);
     a.row_off = reinterpret_cast<int32_t*>(base + w.row_off);
     a.ord = reinterpret_cast<int32_t*>(base + w.ord);
-    a.jobs = reinterpret_cast<int2*>(base + w.jobs);
-    int64_t grid = w.max_jobs < 4096 ? w.max_jobs : 4096;
+    // every commit workgroup reads all tables' plan state once, so the grid is
+    // capped; workgroups loop over the jobs beyond it
+    int64_t grid = w.max_jobs < 1024 ? w.max_jobs : 1024;
     if (grid < 1) grid = 1;
     hipError_t e = launch_append(a, (int)grid, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;

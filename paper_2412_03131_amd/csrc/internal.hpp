@@ -45,7 +45,6 @@ struct AppendArgs : LayoutArgs {
     int32_t* sold;
     int32_t* row_off;
     int32_t* ord;
-    int2* jobs;
 };
 
 struct AllocArgs {

@@ -109,8 +109,9 @@ __device__ __forceinline__ float dot2_first(half2_t a, uint32_t b)
 constexpr float kTwo24 = 16777216.0f;
 
 // Raw bytes of one page as one lane needs them.  High and low pages take
-// the same seven loads (two of them unused on high pages, inside the page), so
-// the buffers of a prefetch pipeline never need register copies.
+// the same seven loads (two of them unused on high pages, re-reading lines the
+// page's other loads fetch), so the buffers of a prefetch pipeline never need
+// register copies.
 struct PageRaw {
     uint4 k0, k1;  // high: K8 chunks 2g, 2g+1 of token j; low: K4 chunk g of tokens j, j+16
     uint4 vr;      // V code rows of dims 2*lane, 2*lane+1
@@ -142,7 +143,7 @@ __device__ __forceinline__ void load_page(PageRaw& r, const uint8_t* pg, bool hi
     r.m0 = ld4(pg, km);
     r.m1 = ld4(pg, km + 256);
     r.m2 = ld4(pm, vm);
-    r.m3 = ld4(pm, grp * (kTLo * 4) + jl * 4 + 64);
+    r.m3 = ld4(pm, hi ? vm : vm + 64);  // high pages: a line already fetched
 }
 
 template <int GQ>

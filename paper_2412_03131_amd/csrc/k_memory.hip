@@ -1,18 +1,18 @@
 // k_memory.hip -- KV compressor, page allocation and free-list compaction
 // kernels for gfx950 (DiffKV Sec. 4, Sec. 5.2, Sec. 5.3).
 //
-// The compressor runs as three launches on the caller's stream:
+// The compressor runs as two launches on the caller's stream:
 //   append_classify  one workgroup per table: classes its new tokens (quota
 //                    form by a two-target radix select on the score bits, or
 //                    the Algorithm 1 threshold comparisons), ranks the kept
 //                    tokens of each section in position order;
-//   append_plan      one workgroup for the whole call: page demand of every
-//                    table, prefix sums over tables, all-or-nothing check
-//                    against the free region and the table width, state
-//                    update and the list of (table, section, page) jobs;
-//   append_quant     persistent waves over the job list: resolve the page ID
-//                    (new pages come from the ring region the plan assigned),
-//                    quantize each token's 32-dim groups and write the page.
+//   append_commit    every workgroup derives the plan from the classify
+//                    results (page demand per table, one prefix sum over
+//                    tables, all-or-nothing check against the free region and
+//                    the table width); workgroup 0 writes the new state, and
+//                    all take (table, section, page) jobs: resolve the page ID
+//                    (new pages from the table's ring region), quantize each
+//                    token's 32-dim groups and write the page.
 // Allocation alone (alloc_plan + alloc_write) and compaction (compact_count,
 // compact_scan, compact_apply) follow the same planning/coordination split:
 // per-table work is fully parallel, one prefix sum gives every table a
@@ -50,6 +50,10 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
     __shared__ int s_sel[4];
     __shared__ uint32_t s_keys[kClsLdsKeys];
 
+    if (t == 0 && tid == 0) {  // ring pointers before this call (the commit kernel moves head)
+        a.flags->head_old = a.ring_ptr[0];
+        a.flags->tail_old = a.ring_ptr[1];
+    }
     // row offset of this sequence (sum of new_len over lower sequences)
     long long part = 0;
     for (int i = tid; i < b; i += kClsThreads) part += a.new_len[i];
@@ -59,8 +63,14 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
     TState* ts = a.tstate + t;
     const bool bad = n < 0 || n > a.max_new || off_b + n > a.total_new ||
                      (b == a.B - 1 && off_b + n != a.total_new);
+    if (tid == 0) {  // section lengths and pages before this call
+        ts->lold[0] = a.len[2 * t];
+        ts->lold[1] = a.len[2 * t + 1];
+        ts->pold[0] = a.pages[2 * t];
+        ts->pold[1] = a.pages[2 * t + 1];
+    }
     if (bad) {
-        if (tid == 0) {  // the plan kernel turns n < 0 into DIFFKV_ST_BAD_INPUT
+        if (tid == 0) {  // the commit kernel turns n < 0 into DIFFKV_ST_BAD_INPUT
             ts->cnt[0] = ts->cnt[1] = 0;
             ts->n = -1;
         }
@@ -208,113 +218,17 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
     }
 }
 
-// ---------------------------------------------------------------------------
-// append_plan: one workgroup of 1024 threads
-// ---------------------------------------------------------------------------
 constexpr int kPlanThreads = 1024;
 
-__global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
-{
-    const int tid = threadIdx.x;
-    const int NT = a.B * a.Hkv;
-    const int P = a.p_max;
-    const int T[2] = {a.T[0], a.T[1]};
-    __shared__ long long s_scan[kPlanThreads / kWave + 1];
-    __shared__ int s_bad;
-    __shared__ long long s_head, s_tail;
-    if (tid == 0) {
-        s_bad = 0;
-        s_head = a.ring_ptr[0];
-        s_tail = a.ring_ptr[1];
-    }
-    __syncthreads();
-    for (int t = tid; t < NT; t += kPlanThreads)
-        if (a.tstate[t].n < 0) s_bad = 1;
-    __syncthreads();
-    if (s_bad) {
-        if (tid == 0) {
-            atomicOr(a.status, (uint32_t)DIFFKV_ST_BAD_INPUT);
-            a.flags->ok = 0;
-            a.flags->njobs = 0;
-        }
-        return;
-    }
-    // pass 1: demand and overflow
-    long long total = 0;
-    int ovf = 0;
-    for (int t = tid; t < NT; t += kPlanThreads) {
-        const TState& s = a.tstate[t];
-        int need_sum = 0;
-        int held = 0;
-        for (int sec = 0; sec < 2; ++sec) {
-            int want = ceil_div(a.len[2 * t + sec] + s.cnt[sec], T[sec]);
-            int have = a.pages[2 * t + sec];
-            need_sum += want > have ? want - have : 0;
-            held += have > want ? have : want;
-        }
-        total += need_sum;
-        if (held > P) ovf = 1;
-    }
-    uint32_t bits;
-    const long long total_all = block_sum_or(total, ovf ? (uint32_t)DIFFKV_ST_TABLE_OVERFLOW : 0u,
-                                             s_scan, &bits);
-    if (total_all > s_tail - s_head) bits |= DIFFKV_ST_OUT_OF_PAGES;
-    if (bits) {
-        if (tid == 0) {
-            atomicOr(a.status, bits);
-            a.flags->ok = 0;
-            a.flags->njobs = 0;
-        }
-        return;
-    }
-    // pass 2: ring offsets, job offsets, state update
-    long long ring_carry = 0, job_carry = 0;
-    for (int t0 = 0; t0 < NT; t0 += kPlanThreads) {
-        const int t = t0 + tid;
-        int need[2] = {0, 0}, jobs[2] = {0, 0};
-        int lold[2] = {0, 0}, pold[2] = {0, 0}, cnt[2] = {0, 0};
-        if (t < NT) {
-            for (int sec = 0; sec < 2; ++sec) {
-                cnt[sec] = a.tstate[t].cnt[sec];
-                lold[sec] = a.len[2 * t + sec];
-                pold[sec] = a.pages[2 * t + sec];
-                int want = ceil_div(lold[sec] + cnt[sec], T[sec]);
-                need[sec] = want > pold[sec] ? want - pold[sec] : 0;
-                jobs[sec] = cnt[sec] ? (lold[sec] + cnt[sec] - 1) / T[sec] - lold[sec] / T[sec] + 1 : 0;
-            }
-        }
-        long long tr, tj;
-        long long ro = block_excl_scan<long long>(need[0] + need[1], s_scan, &tr) + ring_carry;
-        long long jo = block_excl_scan<long long>(jobs[0] + jobs[1], s_scan, &tj) + job_carry;
-        ring_carry += tr;
-        job_carry += tj;
-        if (t < NT) {
-            TState& s = a.tstate[t];
-            s.lold[0] = lold[0];
-            s.lold[1] = lold[1];
-            s.pold[0] = pold[0];
-            s.pold[1] = pold[1];
-            s.ring_off = (int)ro;
-            for (int sec = 0; sec < 2; ++sec) {
-                a.len[2 * t + sec] = lold[sec] + cnt[sec];
-                a.pages[2 * t + sec] = pold[sec] + need[sec];
-                const int p0 = lold[sec] / T[sec];
-                for (int i = 0; i < jobs[sec]; ++i)
-                    a.jobs[jo++] = make_int2(t, (sec << 30) | (p0 + i));
-            }
-        }
-    }
-    for (int b = tid; b < a.B; b += kPlanThreads) a.seq_len[b] = a.sold[b] + a.new_len[b];
-    if (tid == 0) {
-        a.flags->head_old = s_head;
-        a.flags->njobs = (int)job_carry;
-        a.flags->ok = 1;
-        a.ring_ptr[0] = s_head + ring_carry;
-    }
-}
-
 // ---------------------------------------------------------------------------
-// append_quant: persistent single-wave workgroups over the job list
+// append_commit: plan + quantize in one launch.
+// Every workgroup first derives the call's plan from the per-table state the
+// classify kernel left (new tokens per section, section lengths and pages
+// before the call): page demand, page jobs, one prefix sum over tables (ring
+// region and first job of every table), and the all-or-nothing checks.  So no
+// workgroup waits on another: workgroup 0 writes the new state (lengths,
+// pages, seq_len, ring head) while all of them -- reading only the snapshot
+// -- take page jobs (table, section, page) in job order.
 // ---------------------------------------------------------------------------
 // Quantize one 32-dim group spread over 16 lanes (2 values per lane).
 // Arithmetic is IEEE fp32 with no contraction, identical to the text of the
@@ -344,134 +258,238 @@ __device__ __forceinline__ void quant_pair(uint32_t xbits, int lb, uint32_t& sz,
     sz = s16 | (z16 << 16);
 }
 
-// One workgroup of four waves per job (one page of one table); the job's
-// tokens are dealt round-robin to the waves, each wave prefetching its next
-// token's K/V rows while it quantizes the current one.  The dimension-major
-// V code rows of the page are built in registers per wave and OR-ed together
-// through LDS before one store.
 constexpr int kQuantWaves = 4;
+constexpr int kCommitThreads = kQuantWaves * kWave;
+constexpr int kTokIlp = 4;  // tokens a wave quantizes side by side
 
-__global__ __launch_bounds__(kQuantWaves * kWave) void append_quant(AppendArgs a)
+struct TablePlan {
+    int need[2], jobs[2];
+    bool held_over;  // more pages than p_max after the call
+};
+
+__device__ __forceinline__ TablePlan table_plan(const TState& s, const int (&T)[2], int P)
 {
-    if (!a.flags->ok) return;
+    TablePlan tp;
+    int held = 0;
+#pragma unroll
+    for (int sec = 0; sec < 2; ++sec) {
+        const int want = ceil_div(s.lold[sec] + s.cnt[sec], T[sec]);
+        tp.need[sec] = want > s.pold[sec] ? want - s.pold[sec] : 0;
+        held += want > s.pold[sec] ? want : s.pold[sec];
+        tp.jobs[sec] = s.cnt[sec] ? (s.lold[sec] + s.cnt[sec] - 1) / T[sec] - s.lold[sec] / T[sec] + 1 : 0;
+    }
+    tp.held_over = held > P;
+    return tp;
+}
+
+struct JobDesc {
+    int t, sec, p, u0, u1, lold, n, id;
+};
+
+__global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
+{
+    const int tid = threadIdx.x;
+    const int NT = a.B * a.Hkv;
+    const int P = a.p_max;
+    const int T[2] = {a.T[0], a.T[1]};
+    __shared__ long long s_scan[kCommitThreads / kWave + 1];
+    __shared__ JobDesc s_job;
     __shared__ uint64_t s_rows[kQuantWaves][kWave][2];
-    const int njobs = a.flags->njobs;
-    const long long head_old = a.flags->head_old;
+    const long long head_old = a.flags->head_old, tail_old = a.flags->tail_old;
+
+    // ---- the plan, in every workgroup (each thread a contiguous run of tables)
+    const int per = (NT + kCommitThreads - 1) / kCommitThreads;
+    const int t0 = tid * per;
+    const int t1 = t0 + per < NT ? t0 + per : NT;
+    long long packed = 0;  // new pages | jobs << 32
+    uint32_t bits = 0;
+    for (int t = t0; t < t1; ++t) {
+        const TState s = a.tstate[t];
+        if (s.n < 0) {
+            bits |= DIFFKV_ST_BAD_INPUT;
+            continue;
+        }
+        const TablePlan tp = table_plan(s, T, P);
+        if (tp.held_over) bits |= DIFFKV_ST_TABLE_OVERFLOW;
+        packed += (tp.need[0] + tp.need[1]) | ((long long)(tp.jobs[0] + tp.jobs[1]) << 32);
+    }
+    long long tot;
+    const long long before = block_excl_scan<long long>(packed, s_scan, &tot);
+    // __syncthreads_or returns whether any thread's value is nonzero: one call per bit
+    const bool any_bad = __syncthreads_or((int)(bits & DIFFKV_ST_BAD_INPUT));
+    const bool any_ovf = __syncthreads_or((int)(bits & DIFFKV_ST_TABLE_OVERFLOW));
+    bits = (any_bad ? DIFFKV_ST_BAD_INPUT : 0u) | (any_ovf ? DIFFKV_ST_TABLE_OVERFLOW : 0u);
+    const long long total_need = tot & 0xffffffffll;
+    const int njobs = (int)(tot >> 32);
+    if (bits & DIFFKV_ST_BAD_INPUT) bits = DIFFKV_ST_BAD_INPUT;
+    else if (total_need > tail_old - head_old) bits |= DIFFKV_ST_OUT_OF_PAGES;
+    if (bits) {  // all or nothing: no state, table or page changes
+        if (blockIdx.x == 0 && tid == 0) atomicOr(a.status, bits);
+        return;
+    }
+
+    // ---- workgroup 0: the state after the call -------------------------------
+    if (blockIdx.x == 0) {
+        for (int t = t0; t < t1; ++t) {
+            const TState s = a.tstate[t];
+            const TablePlan tp = table_plan(s, T, P);
+#pragma unroll
+            for (int sec = 0; sec < 2; ++sec) {
+                a.len[2 * t + sec] = s.lold[sec] + s.cnt[sec];
+                a.pages[2 * t + sec] = s.pold[sec] + tp.need[sec];
+            }
+        }
+        for (int b = tid; b < a.B; b += kCommitThreads) a.seq_len[b] = a.sold[b] + a.new_len[b];
+        if (tid == 0) a.ring_ptr[0] = head_old + total_need;
+    }
+
+    // ---- page jobs ------------------------------------------------------------
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int grp = lane >> 4;
     const int H = a.Hkv;
-    const int P = a.p_max;
     const long long page_bytes = a.page_bytes;
     for (int job = blockIdx.x; job < njobs; job += gridDim.x) {
-        const int2 jb = a.jobs[job];
-        const int t = jb.x;
-        const int sec = jb.y >> 30;
-        const int p = jb.y & ((1 << 30) - 1);
-        const int b = t / H, h = t - b * H;
-        const TState ts = a.tstate[t];
-        const int T = sec ? kTLo : kTHi;
-        const int u0 = max(ts.lold[sec], p * T);
-        const int u1 = min(ts.lold[sec] + ts.cnt[sec], (p + 1) * T);
-        const int tslot = sec ? P - 1 - p : p;
-        int32_t* trow = a.page_table + (long long)t * P;
-        int id;
-        if (p < ts.pold[sec]) {
-            id = trow[tslot];
-        } else {
-            const int need_hi = a.pages[2 * t] - ts.pold[0];
-            const long long r = head_old + ts.ring_off + (sec ? need_hi : 0) + (p - ts.pold[sec]);
-            id = a.ring[r % a.num_pages];
-            if (threadIdx.x == 0) trow[tslot] = id;
-        }
-        if ((unsigned)id >= (unsigned)a.num_pages) continue;  // never write outside the pool
-        uint8_t* pg = a.pool + (long long)id * page_bytes;
-        const bool fresh = (u0 == p * T);
-        if (fresh) {
-            const uint4 z = make_uint4(0, 0, 0, 0);
-            for (long long o = (long long)threadIdx.x * 16; o < page_bytes; o += kQuantWaves * kWave * 16)
-                *reinterpret_cast<uint4*>(pg + o) = z;
-            __threadfence();  // the zeros land before this job's data stores
-            __syncthreads();
-        }
-        const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
-        const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
-        const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
-        const int n = ts.n;
-        const int off_b = a.row_off[b];
-        const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
-        auto row_of = [&](int u) {
-            const int r = u - ts.lold[sec];
-            const int j = sec ? ord[n - 1 - r] : ord[r];
-            return j;
-        };
-        uint64_t row0 = 0, row1 = 0;
-        int u = u0 + wave;
-        uint32_t kx = 0, vx = 0;
-        int j = 0;
-        if (u < u1) {
-            j = row_of(u);
-            const long long row = (long long)(off_b + j) * H + h;
-            kx = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
-            vx = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
-        }
-        for (; u < u1; u += kQuantWaves) {
-            // prefetch the wave's next token
-            const int un = u + kQuantWaves;
-            uint32_t kn = 0, vn = 0;
-            int jn = 0;
-            if (un < u1) {
-                jn = row_of(un);
-                const long long rn = (long long)(off_b + jn) * H + h;
-                kn = reinterpret_cast<const uint32_t*>(a.k + rn * kD)[lane];
-                vn = reinterpret_cast<const uint32_t*>(a.v + rn * kD)[lane];
+        // the thread whose run of tables holds this job describes it
+        long long pre = before;
+        for (int t = t0; t < t1; ++t) {
+            const TState s = a.tstate[t];
+            const TablePlan tp = table_plan(s, T, P);
+            const int jo = (int)(pre >> 32);
+            if (jo <= job && job < jo + tp.jobs[0] + tp.jobs[1]) {
+                const int lj = job - jo;
+                const int sec = lj < tp.jobs[0] ? 0 : 1;
+                const int p = s.lold[sec] / T[sec] + (sec ? lj - tp.jobs[0] : lj);
+                const int tslot = sec ? P - 1 - p : p;
+                int32_t* trow = a.page_table + (long long)t * P;
+                int id;
+                if (p < s.pold[sec]) {
+                    id = trow[tslot];
+                } else {  // new page: this table's ring region, high pages first
+                    const long long r = head_old + (pre & 0xffffffffll) + (sec ? tp.need[0] : 0) + (p - s.pold[sec]);
+                    id = a.ring[r % a.num_pages];
+                    trow[tslot] = id;
+                }
+                const int lo = s.lold[sec], hi_end = s.lold[sec] + s.cnt[sec];
+                s_job.t = t;
+                s_job.sec = sec;
+                s_job.p = p;
+                s_job.u0 = lo > p * T[sec] ? lo : p * T[sec];
+                s_job.u1 = hi_end < (p + 1) * T[sec] ? hi_end : (p + 1) * T[sec];
+                s_job.lold = lo;
+                s_job.n = s.n;
+                s_job.id = id;
             }
-            const int s = u - p * T;
-            const long long row = (long long)(off_b + j) * H + h;
-            uint32_t sz, c0, c1;
-            quant_pair(kx, (1 << kb) - 1, sz, c0, c1);
-            if (kb == 8) {
-                uint16_t* dst = reinterpret_cast<uint16_t*>(pg + off_kc + ((lane >> 3) * T + s) * 16 +
-                                                            ((2 * lane) & 15));
-                *dst = (uint16_t)(c0 | (c1 << 8));
-            } else {
-                uint8_t* dst = pg + off_kc + (grp * T + s) * 16 + (lane & 15);
-                *dst = (uint8_t)(c0 | (c1 << 4));
-            }
-            if ((lane & 15) == 0)
-                *reinterpret_cast<uint32_t*>(pg + off_km + (s * kNG + grp) * 4) = sz;
-            quant_pair(vx, (1 << vb) - 1, sz, c0, c1);
-            row0 |= (uint64_t)c0 << (s * vb);
-            row1 |= (uint64_t)c1 << (s * vb);
-            if ((lane & 15) == 0)
-                *reinterpret_cast<uint32_t*>(pg + off_vm + (grp * T + s) * 4) = sz;
-            if (lane == 0) {
-                reinterpret_cast<float*>(pg + a.off_score[sec])[s] = a.score[row];
-                reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[s] = a.sold[b] + j;
-            }
-            kx = kn;
-            vx = vn;
-            j = jn;
+            pre += (tp.need[0] + tp.need[1]) | ((long long)(tp.jobs[0] + tp.jobs[1]) << 32);
         }
-        s_rows[wave][lane][0] = row0;
-        s_rows[wave][lane][1] = row1;
         __syncthreads();
-        if (wave == 0) {
-            uint64_t r0 = 0, r1 = 0;
-            if (!fresh) {
-                const uint4 r = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
-                r0 = ((uint64_t)r.y << 32) | r.x;
-                r1 = ((uint64_t)r.w << 32) | r.z;
+        const JobDesc jd = s_job;
+        const int t = jd.t, sec = jd.sec, p = jd.p, u0 = jd.u0, u1 = jd.u1, id = jd.id;
+        const int b = t / H, h = t - b * H;
+        const int TT = T[sec];
+        if ((unsigned)id < (unsigned)a.num_pages) {  // never write outside the pool
+            uint8_t* pg = a.pool + (long long)id * page_bytes;
+            const bool fresh = (u0 == p * TT);
+            const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
+            const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
+            const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
+            if (fresh) {
+                // A fresh page reads as zero wherever no token lies: zero the token
+                // slots from u1 on in every per-token segment and the page tail.
+                // These bytes are disjoint from the ones the tokens below write
+                // (V code rows are written whole, zeros included), so the stores
+                // need no ordering among themselves.
+                const int s_end = u1 - p * TT, nfill = TT - s_end;
+                const uint4 z4 = make_uint4(0, 0, 0, 0);
+                for (int i = tid; i < (kb + 1) * nfill; i += kCommitThreads) {
+                    const int c = i / nfill, sl = s_end + (i - c * nfill);  // K chunks (kb per token), then K meta
+                    uint8_t* dst = c < kb ? pg + off_kc + (c * TT + sl) * 16 : pg + off_km + sl * 16;
+                    *reinterpret_cast<uint4*>(dst) = z4;
+                }
+                for (int i = tid; i < (kNG + 2) * nfill; i += kCommitThreads) {
+                    const int g = i / nfill, sl = s_end + (i - g * nfill);  // V meta groups, score, pos
+                    uint8_t* dst = g < kNG ? pg + off_vm + (g * TT + sl) * 4
+                                           : pg + (g == kNG ? a.off_score[sec] : a.off_pos[sec]) + sl * 4;
+                    *reinterpret_cast<uint32_t*>(dst) = 0;
+                }
+                for (long long o = a.off_pos[sec] + (long long)TT * 4 + tid * 16; o < page_bytes;
+                     o += kCommitThreads * 16)
+                    *reinterpret_cast<uint4*>(pg + o) = z4;
             }
+            const int n = jd.n;
+            const int off_b = a.row_off[b];
+            const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
+            // token u of the section is row ord[u - lold] (high, rank order) or
+            // ord[n - 1 - (u - lold)] (low ranks are stored from the back)
+            uint64_t row0 = 0, row1 = 0;
+            for (int ub = u0 + wave; ub < u1; ub += kTokIlp * kQuantWaves) {
+                // this wave's next kTokIlp tokens, quantized side by side
+                uint32_t kx[kTokIlp], vx[kTokIlp];
+                int jj[kTokIlp];
 #pragma unroll
-            for (int w = 0; w < kQuantWaves; ++w) {
-                r0 |= s_rows[w][lane][0];
-                r1 |= s_rows[w][lane][1];
+                for (int i = 0; i < kTokIlp; ++i) {
+                    const int u = ub + i * kQuantWaves;
+                    const int uc = u < u1 ? u : ub;
+                    const int r = uc - jd.lold;
+                    jj[i] = sec ? ord[n - 1 - r] : ord[r];
+                    const long long row = (long long)(off_b + jj[i]) * H + h;
+                    kx[i] = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
+                    vx[i] = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
+                }
+                uint32_t ksz[kTokIlp], kc0[kTokIlp], kc1[kTokIlp], vsz[kTokIlp], vc0[kTokIlp], vc1[kTokIlp];
+#pragma unroll
+                for (int i = 0; i < kTokIlp; ++i) {
+                    quant_pair(kx[i], (1 << kb) - 1, ksz[i], kc0[i], kc1[i]);
+                    quant_pair(vx[i], (1 << vb) - 1, vsz[i], vc0[i], vc1[i]);
+                }
+#pragma unroll
+                for (int i = 0; i < kTokIlp; ++i) {
+                    const int u = ub + i * kQuantWaves;
+                    if (u >= u1) break;
+                    const int sl = u - p * TT;
+                    const long long row = (long long)(off_b + jj[i]) * H + h;
+                    if (kb == 8) {
+                        uint16_t* dst = reinterpret_cast<uint16_t*>(pg + off_kc + ((lane >> 3) * TT + sl) * 16 +
+                                                                    ((2 * lane) & 15));
+                        *dst = (uint16_t)(kc0[i] | (kc1[i] << 8));
+                    } else {
+                        uint8_t* dst = pg + off_kc + (grp * TT + sl) * 16 + (lane & 15);
+                        *dst = (uint8_t)(kc0[i] | (kc1[i] << 4));
+                    }
+                    if ((lane & 15) == 0) {
+                        *reinterpret_cast<uint32_t*>(pg + off_km + (sl * kNG + grp) * 4) = ksz[i];
+                        *reinterpret_cast<uint32_t*>(pg + off_vm + (grp * TT + sl) * 4) = vsz[i];
+                    }
+                    row0 |= (uint64_t)vc0[i] << (sl * vb);
+                    row1 |= (uint64_t)vc1[i] << (sl * vb);
+                    if (lane == 0) {
+                        reinterpret_cast<float*>(pg + a.off_score[sec])[sl] = a.score[row];
+                        reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[sl] = a.sold[b] + jj[i];
+                    }
+                }
             }
-            *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
-                make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
+            // the page's dimension-major V code rows: OR of the waves' bits (and of
+            // the bits already on a page that is being continued), one store
+            s_rows[wave][lane][0] = row0;
+            s_rows[wave][lane][1] = row1;
+            __syncthreads();
+            if (wave == 0) {
+                uint64_t r0 = 0, r1 = 0;
+                if (!fresh) {
+                    const uint4 r = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
+                    r0 = ((uint64_t)r.y << 32) | r.x;
+                    r1 = ((uint64_t)r.w << 32) | r.z;
+                }
+#pragma unroll
+                for (int w = 0; w < kQuantWaves; ++w) {
+                    r0 |= s_rows[w][lane][0];
+                    r1 |= s_rows[w][lane][1];
+                }
+                *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
+                    make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
+            }
         }
-        __syncthreads();  // s_rows is reused by the next job
+        __syncthreads();  // s_job and s_rows are reused by the next job
     }
 }
 
@@ -669,8 +687,7 @@ __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
 hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st)
 {
     hipLaunchKernelGGL(append_classify, dim3(a.Hkv, a.B), dim3(kClsThreads), 0, st, a);
-    hipLaunchKernelGGL(append_plan, dim3(1), dim3(kPlanThreads), 0, st, a);
-    hipLaunchKernelGGL(append_quant, dim3(grid_quant), dim3(kQuantWaves * kWave), 0, st, a);
+    hipLaunchKernelGGL(append_commit, dim3(grid_quant), dim3(kCommitThreads), 0, st, a);
     return hipGetLastError();
 }
 

@@ -517,10 +517,15 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         const int ic = i < i_last ? i : i_last;
         return *(const __attribute__((address_space(4))) int32_t*)(trow + slot_of(page_of(ic)));
     };
-    // Issue the loads of page i (if any) into r; ok = the page lies in the pool.
+    // Issue the loads of page i into r; ok = page i exists and lies in the pool.
+    // The loads are unconditional (past the last page they re-read it, a cache
+    // hit; an ID outside the pool reads page 0 and is not computed), so the
+    // wait before each page's use counts only the loads issued since.
     auto issue = [&](int i, int id, PageRaw& r, bool& ok) {
-        ok = i < nmine && (unsigned long long)id < (unsigned long long)npool;  // never read outside the pool
-        if (ok) load_page(r, a.pool + id * page_bytes, page_of(i) < ph, lane);
+        const bool in_pool = (unsigned long long)id < (unsigned long long)npool;  // never read outside the pool
+        ok = i < nmine && in_pool;
+        const int ic = i < i_last ? i : i_last;
+        load_page(r, a.pool + (in_pool ? id : 0) * page_bytes, page_of(ic) < ph, lane);
     };
     PageRaw buf0, buf1;
     bool ok0 = false, ok1 = false;

@@ -59,7 +59,7 @@ __device__ __forceinline__ float rows_sum4(float x)
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x)
 {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 __device__ __forceinline__ float fmax_sel(float a, float b) { return a > b ? a : b; }
 
@@ -572,24 +572,54 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         st.acc[hh][0] = st.acc[hh][1] = 0.f;
     }
 
-    auto compute = [&](int i, const PageRaw& r, bool ok) {
+    // This wave's pages i < nhi are high pages, the rest low pages.  High and
+    // low pages run in loops of their own (no per-page branch between two
+    // different updates of the softmax state); the prefetch crosses from one
+    // loop to the next.
+    const int nhi = ph - pa - wave > 0 ? min(nmine, (ph - pa - wave + kAttnWaves - 1) / kAttnWaves) : 0;
+    auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
         if (i >= nmine || !ok) return;
         const int p = page_of(i);
-        if (p < ph) {
-            do_page<GQ, 1>(st, r, q2, qsum, sl2, ti.len_hi - p * kTHi, lane, coef_row);
-        } else {
-            do_page<GQ, 2>(st, r, q2, qsum, sl2, ti.len_lo - (p - ph) * kTLo, lane, coef_row);
-        }
+        do_page<GQ, 1>(st, r, q2, qsum, sl2, ti.len_hi - p * kTHi, lane, coef_row);
     };
-    // page i computes from buffer i % 2 while page i+1 is in flight; the ID of
-    // page i is loaded when page i-2 is issued
-    for (int i = 0; i < nmine; i += 2) {
+    auto compute_lo = [&](int i, const PageRaw& r, bool ok) {
+        if (i >= nmine || !ok) return;
+        const int p = page_of(i);
+        do_page<GQ, 2>(st, r, q2, qsum, sl2, ti.len_lo - (p - ph) * kTLo, lane, coef_row);
+    };
+    // page i computes from buffer i % 2 (swapped after an odd number of high
+    // pages) while page i+1 is in flight; the ID of page i is loaded when page
+    // i-2 is issued
+    int i = 0;
+    for (; i + 2 <= nhi; i += 2) {
         issue(i + 1, id1, buf1, ok1);
         id1 = id_at(i + 3);
-        compute(i, buf0, ok0);
+        compute_hi(i, buf0, ok0);
         issue(i + 2, id0, buf0, ok0);
         id0 = id_at(i + 4);
-        compute(i + 1, buf1, ok1);
+        compute_hi(i + 1, buf1, ok1);
+    }
+    if (i < nhi) {  // one more high page (in buf0); the low pages then start in buf1
+        issue(i + 1, id1, buf1, ok1);
+        id1 = id_at(i + 3);
+        compute_hi(i, buf0, ok0);
+        for (++i; i < nmine; i += 2) {
+            issue(i + 1, id0, buf0, ok0);
+            id0 = id_at(i + 3);
+            compute_lo(i, buf1, ok1);
+            issue(i + 2, id1, buf1, ok1);
+            id1 = id_at(i + 4);
+            compute_lo(i + 1, buf0, ok0);
+        }
+    } else {
+        for (; i < nmine; i += 2) {
+            issue(i + 1, id1, buf1, ok1);
+            id1 = id_at(i + 3);
+            compute_lo(i, buf0, ok0);
+            issue(i + 2, id0, buf0, ok0);
+            id0 = id_at(i + 4);
+            compute_lo(i + 1, buf1, ok1);
+        }
     }
 
     // ---- finish the wave: row sums of l (head 4s + row) and of the

@@ -260,7 +260,9 @@ __device__ __forceinline__ void quant_pair(uint32_t xbits, int lb, uint32_t& sz,
 
 constexpr int kQuantWaves = 4;
 constexpr int kCommitThreads = kQuantWaves * kWave;
-constexpr int kTokIlp = 4;  // tokens a wave quantizes side by side
+constexpr int kTokIlp = 4;    // tokens a wave quantizes side by side
+constexpr int kTokLoad = 8;   // tokens a wave loads up front: a 32-token page in one round of loads
+static_assert(kTokLoad * kQuantWaves >= 32, "one round of loads per page");
 
 struct TablePlan {
     int need[2], jobs[2];
@@ -283,7 +285,9 @@ __device__ __forceinline__ TablePlan table_plan(const TState& s, const int (&T)[
 }
 
 struct JobDesc {
-    int t, sec, p, u0, u1, lold, n, id;
+    int t, sec, p, u0, u1, lold, n, tslot;
+    long long ring_idx;  // ring position of a new page, -1 for a page already held
+    int id;
 };
 
 __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
@@ -360,16 +364,6 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
                 const int lj = job - jo;
                 const int sec = lj < tp.jobs[0] ? 0 : 1;
                 const int p = s.lold[sec] / T[sec] + (sec ? lj - tp.jobs[0] : lj);
-                const int tslot = sec ? P - 1 - p : p;
-                int32_t* trow = a.page_table + (long long)t * P;
-                int id;
-                if (p < s.pold[sec]) {
-                    id = trow[tslot];
-                } else {  // new page: this table's ring region, high pages first
-                    const long long r = head_old + (pre & 0xffffffffll) + (sec ? tp.need[0] : 0) + (p - s.pold[sec]);
-                    id = a.ring[r % a.num_pages];
-                    trow[tslot] = id;
-                }
                 const int lo = s.lold[sec], hi_end = s.lold[sec] + s.cnt[sec];
                 s_job.t = t;
                 s_job.sec = sec;
@@ -378,116 +372,142 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
                 s_job.u1 = hi_end < (p + 1) * T[sec] ? hi_end : (p + 1) * T[sec];
                 s_job.lold = lo;
                 s_job.n = s.n;
-                s_job.id = id;
+                s_job.tslot = sec ? P - 1 - p : p;
+                // a new page comes from this table's ring region, high pages first
+                s_job.ring_idx = p < s.pold[sec] ? -1
+                                                 : head_old + (pre & 0xffffffffll) + (sec ? tp.need[0] : 0) + (p - s.pold[sec]);
             }
             pre += (tp.need[0] + tp.need[1]) | ((long long)(tp.jobs[0] + tp.jobs[1]) << 32);
         }
         __syncthreads();
-        const JobDesc jd = s_job;
-        const int t = jd.t, sec = jd.sec, p = jd.p, u0 = jd.u0, u1 = jd.u1, id = jd.id;
+        const int t = s_job.t, sec = s_job.sec, p = s_job.p, u0 = s_job.u0, u1 = s_job.u1;
+        const int lold = s_job.lold, n = s_job.n;
         const int b = t / H, h = t - b * H;
         const int TT = T[sec];
-        if ((unsigned)id < (unsigned)a.num_pages) {  // never write outside the pool
-            uint8_t* pg = a.pool + (long long)id * page_bytes;
-            const bool fresh = (u0 == p * TT);
-            const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
-            const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
-            const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
-            if (fresh) {
-                // A fresh page reads as zero wherever no token lies: zero the token
-                // slots from u1 on in every per-token segment and the page tail.
-                // These bytes are disjoint from the ones the tokens below write
-                // (V code rows are written whole, zeros included), so the stores
-                // need no ordering among themselves.
-                const int s_end = u1 - p * TT, nfill = TT - s_end;
-                const uint4 z4 = make_uint4(0, 0, 0, 0);
-                for (int i = tid; i < (kb + 1) * nfill; i += kCommitThreads) {
-                    const int c = i / nfill, sl = s_end + (i - c * nfill);  // K chunks (kb per token), then K meta
-                    uint8_t* dst = c < kb ? pg + off_kc + (c * TT + sl) * 16 : pg + off_km + sl * 16;
-                    *reinterpret_cast<uint4*>(dst) = z4;
-                }
-                for (int i = tid; i < (kNG + 2) * nfill; i += kCommitThreads) {
-                    const int g = i / nfill, sl = s_end + (i - g * nfill);  // V meta groups, score, pos
-                    uint8_t* dst = g < kNG ? pg + off_vm + (g * TT + sl) * 4
-                                           : pg + (g == kNG ? a.off_score[sec] : a.off_pos[sec]) + sl * 4;
-                    *reinterpret_cast<uint32_t*>(dst) = 0;
-                }
-                for (long long o = a.off_pos[sec] + (long long)TT * 4 + tid * 16; o < page_bytes;
-                     o += kCommitThreads * 16)
-                    *reinterpret_cast<uint4*>(pg + o) = z4;
+        const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
+        // one thread resolves the page ID while the others load their tokens
+        if (tid == 0) {
+            int32_t* trow = a.page_table + (long long)t * P;
+            int id;
+            if (s_job.ring_idx < 0) {
+                id = trow[s_job.tslot];
+            } else {
+                id = a.ring[s_job.ring_idx % a.num_pages];
+                trow[s_job.tslot] = id;
             }
-            const int n = jd.n;
-            const int off_b = a.row_off[b];
-            const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
-            // token u of the section is row ord[u - lold] (high, rank order) or
-            // ord[n - 1 - (u - lold)] (low ranks are stored from the back)
-            uint64_t row0 = 0, row1 = 0;
-            for (int ub = u0 + wave; ub < u1; ub += kTokIlp * kQuantWaves) {
-                // this wave's next kTokIlp tokens, quantized side by side
-                uint32_t kx[kTokIlp], vx[kTokIlp];
-                int jj[kTokIlp];
+            s_job.id = id;
+        }
+        // this wave's tokens u0 + wave + kQuantWaves*i, all loaded up front; token
+        // u of the section is row ord[u - lold] (high, rank order) or
+        // ord[n - 1 - (u - lold)] (low ranks are stored from the back)
+        const int off_b = a.row_off[b];
+        const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
+        int jj[kTokLoad];
+        uint32_t kx[kTokLoad], vx[kTokLoad];
 #pragma unroll
-                for (int i = 0; i < kTokIlp; ++i) {
-                    const int u = ub + i * kQuantWaves;
-                    const int uc = u < u1 ? u : ub;
-                    const int r = uc - jd.lold;
-                    jj[i] = sec ? ord[n - 1 - r] : ord[r];
-                    const long long row = (long long)(off_b + jj[i]) * H + h;
-                    kx[i] = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
-                    vx[i] = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
-                }
-                uint32_t ksz[kTokIlp], kc0[kTokIlp], kc1[kTokIlp], vsz[kTokIlp], vc0[kTokIlp], vc1[kTokIlp];
+        for (int i = 0; i < kTokLoad; ++i) {
+            const int u = u0 + wave + i * kQuantWaves;
+            const int r = (u < u1 ? u : u0) - lold;
+            jj[i] = sec ? ord[n - 1 - r] : ord[r];
+        }
 #pragma unroll
-                for (int i = 0; i < kTokIlp; ++i) {
-                    quant_pair(kx[i], (1 << kb) - 1, ksz[i], kc0[i], kc1[i]);
-                    quant_pair(vx[i], (1 << vb) - 1, vsz[i], vc0[i], vc1[i]);
-                }
+        for (int i = 0; i < kTokLoad; ++i) {
+            const long long row = (long long)(off_b + jj[i]) * H + h;
+            kx[i] = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
+            vx[i] = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
+        }
+        const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
+        const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
+        const bool fresh = (u0 == p * TT);
+        uint8_t* pg = nullptr;
+        bool page_ok = false;
+        uint64_t row0 = 0, row1 = 0;
+        // two passes of kTokIlp tokens: quantize side by side, then store
 #pragma unroll
-                for (int i = 0; i < kTokIlp; ++i) {
-                    const int u = ub + i * kQuantWaves;
-                    if (u >= u1) break;
-                    const int sl = u - p * TT;
-                    const long long row = (long long)(off_b + jj[i]) * H + h;
-                    if (kb == 8) {
-                        uint16_t* dst = reinterpret_cast<uint16_t*>(pg + off_kc + ((lane >> 3) * TT + sl) * 16 +
-                                                                    ((2 * lane) & 15));
-                        *dst = (uint16_t)(kc0[i] | (kc1[i] << 8));
-                    } else {
-                        uint8_t* dst = pg + off_kc + (grp * TT + sl) * 16 + (lane & 15);
-                        *dst = (uint8_t)(kc0[i] | (kc1[i] << 4));
+        for (int pass = 0; pass < kTokLoad / kTokIlp; ++pass) {
+            const int base_u = u0 + wave + pass * kTokIlp * kQuantWaves;
+            if (u0 + pass * kTokIlp * kQuantWaves >= u1) break;  // uniform: no token of this pass in the page
+            uint32_t ksz[kTokIlp], kc0[kTokIlp], kc1[kTokIlp], vsz[kTokIlp], vc0[kTokIlp], vc1[kTokIlp];
+#pragma unroll
+            for (int i = 0; i < kTokIlp; ++i) {
+                quant_pair(kx[pass * kTokIlp + i], (1 << kb) - 1, ksz[i], kc0[i], kc1[i]);
+                quant_pair(vx[pass * kTokIlp + i], (1 << vb) - 1, vsz[i], vc0[i], vc1[i]);
+            }
+            if (pass == 0) {
+                __syncthreads();  // the page ID is in LDS
+                const int id = s_job.id;
+                page_ok = (unsigned)id < (unsigned)a.num_pages;  // never write outside the pool
+                pg = a.pool + (long long)(page_ok ? id : 0) * page_bytes;
+                if (page_ok && fresh) {
+                    // A fresh page reads as zero wherever no token lies: zero the token
+                    // slots from u1 on in every per-token segment and the page tail.
+                    // These bytes are disjoint from the ones the tokens write (V code
+                    // rows are written whole, zeros included), so the stores need no
+                    // ordering among themselves.
+                    const int s_end = u1 - p * TT, nfill = TT - s_end;
+                    const uint4 z4 = make_uint4(0, 0, 0, 0);
+                    for (int i = tid; i < (kb + 1) * nfill; i += kCommitThreads) {
+                        const int c = i / nfill, sl = s_end + (i - c * nfill);  // K chunks (kb per token), then K meta
+                        uint8_t* dst = c < kb ? pg + off_kc + (c * TT + sl) * 16 : pg + off_km + sl * 16;
+                        *reinterpret_cast<uint4*>(dst) = z4;
                     }
-                    if ((lane & 15) == 0) {
-                        *reinterpret_cast<uint32_t*>(pg + off_km + (sl * kNG + grp) * 4) = ksz[i];
-                        *reinterpret_cast<uint32_t*>(pg + off_vm + (grp * TT + sl) * 4) = vsz[i];
+                    for (int i = tid; i < (kNG + 2) * nfill; i += kCommitThreads) {
+                        const int g = i / nfill, sl = s_end + (i - g * nfill);  // V meta groups, score, pos
+                        uint8_t* dst = g < kNG ? pg + off_vm + (g * TT + sl) * 4
+                                               : pg + (g == kNG ? a.off_score[sec] : a.off_pos[sec]) + sl * 4;
+                        *reinterpret_cast<uint32_t*>(dst) = 0;
                     }
-                    row0 |= (uint64_t)vc0[i] << (sl * vb);
-                    row1 |= (uint64_t)vc1[i] << (sl * vb);
-                    if (lane == 0) {
-                        reinterpret_cast<float*>(pg + a.off_score[sec])[sl] = a.score[row];
-                        reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[sl] = a.sold[b] + jj[i];
-                    }
+                    for (long long o = a.off_pos[sec] + (long long)TT * 4 + tid * 16; o < page_bytes;
+                         o += kCommitThreads * 16)
+                        *reinterpret_cast<uint4*>(pg + o) = z4;
                 }
             }
-            // the page's dimension-major V code rows: OR of the waves' bits (and of
-            // the bits already on a page that is being continued), one store
-            s_rows[wave][lane][0] = row0;
-            s_rows[wave][lane][1] = row1;
-            __syncthreads();
-            if (wave == 0) {
-                uint64_t r0 = 0, r1 = 0;
-                if (!fresh) {
-                    const uint4 r = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
-                    r0 = ((uint64_t)r.y << 32) | r.x;
-                    r1 = ((uint64_t)r.w << 32) | r.z;
-                }
 #pragma unroll
-                for (int w = 0; w < kQuantWaves; ++w) {
-                    r0 |= s_rows[w][lane][0];
-                    r1 |= s_rows[w][lane][1];
+            for (int i = 0; i < kTokIlp; ++i) {
+                const int u = base_u + i * kQuantWaves;
+                if (u >= u1) break;
+                const int sl = u - p * TT;
+                row0 |= (uint64_t)vc0[i] << (sl * vb);
+                row1 |= (uint64_t)vc1[i] << (sl * vb);
+                if (!page_ok) continue;
+                const long long row = (long long)(off_b + jj[pass * kTokIlp + i]) * H + h;
+                if (kb == 8) {
+                    uint16_t* dst = reinterpret_cast<uint16_t*>(pg + off_kc + ((lane >> 3) * TT + sl) * 16 +
+                                                                ((2 * lane) & 15));
+                    *dst = (uint16_t)(kc0[i] | (kc1[i] << 8));
+                } else {
+                    uint8_t* dst = pg + off_kc + (grp * TT + sl) * 16 + (lane & 15);
+                    *dst = (uint8_t)(kc0[i] | (kc1[i] << 4));
                 }
-                *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
-                    make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
+                if ((lane & 15) == 0) {
+                    *reinterpret_cast<uint32_t*>(pg + off_km + (sl * kNG + grp) * 4) = ksz[i];
+                    *reinterpret_cast<uint32_t*>(pg + off_vm + (grp * TT + sl) * 4) = vsz[i];
+                }
+                if (lane == 0) {
+                    reinterpret_cast<float*>(pg + a.off_score[sec])[sl] = a.score[row];
+                    reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[sl] = a.sold[b] + jj[pass * kTokIlp + i];
+                }
             }
+        }
+        // the page's dimension-major V code rows: OR of the waves' bits (and of the
+        // bits already on a page being continued), one store per dimension pair
+        s_rows[wave][lane][0] = row0;
+        s_rows[wave][lane][1] = row1;
+        __syncthreads();
+        if (wave == 0 && page_ok) {
+            uint64_t r0 = 0, r1 = 0;
+            if (!fresh) {
+                const uint4 r = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
+                r0 = ((uint64_t)r.y << 32) | r.x;
+                r1 = ((uint64_t)r.w << 32) | r.z;
+            }
+#pragma unroll
+            for (int w = 0; w < kQuantWaves; ++w) {
+                r0 |= s_rows[w][lane][0];
+                r1 |= s_rows[w][lane][1];
+            }
+            *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
+                make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
         }
         __syncthreads();  // s_job and s_rows are reused by the next job
     }

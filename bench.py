@@ -74,7 +74,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--layers", type=int, default=4)
-    ap.add_argument("--splits", type=int, default=0, help="attention split count (0 = balanced shares)")
+    ap.add_argument("--splits", type=int, default=0, help="attention mode: 0 automatic, -1 balanced shares, S >= 1 ranges per table")
     ap.add_argument("--compaction-rounds", type=int, default=100)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -137,7 +137,7 @@ enum {
 
 /* Bytes of device workspace the operation needs (host out-parameter).
  * APPEND: num_seqs, num_kv_heads, total_new.  ATTENTION: num_seqs,
- * num_q_heads, num_splits (0 = the balanced mode).
+ * num_q_heads, num_splits (0 = automatic, -1 = balanced).
  * COMPACT / ALLOC: num_seqs*num_kv_heads tables.  Unused sizes are ignored. */
 diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout,
                                     int32_t num_seqs, int32_t num_q_heads,
@@ -199,14 +199,17 @@ diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_c
  *   lse  device fp32 [num_seqs][num_q_heads] (natural log of the softmax
  *        denominator incl. the max) or NULL.  An empty table gives out = 0,
  *        lse = -inf.
- *   num_splits  0 = balanced (default): the page lists of all tables, in
- *        table order, form one list of work units (a high page 1, a low page
- *        2) that is cut into one equal share per workgroup the device holds
- *        at once; a table spread over several shares has their (max, sum,
- *        acc) states merged in page order (Sec. 6.2 sequence split).
- *        S >= 1: each table is cut into min(S, pages) equal page ranges,
- *        merged the same way (S = 1: no split, no merge).  Results are
- *        deterministic for a given mode and device.
+ *   num_splits  0 = automatic (default): one workgroup per table when there
+ *        are at least as many tables as workgroups the device holds at once
+ *        (waves with more pages left get issue priority, so the longest
+ *        tables are served first), otherwise the balanced mode.
+ *        -1 = balanced: the page lists of all tables, in table order, form one
+ *        list of work units (a high page 3, a low page 5) cut into one equal
+ *        share per resident workgroup; a table spread over several shares has
+ *        their (max, sum, acc) states merged in page order (Sec. 6.2 sequence
+ *        split).  S >= 1: each table is cut into min(S, pages) equal page
+ *        ranges, merged the same way (S = 1: no split, no merge).  Results
+ *        are deterministic for a given mode and device.
  *   ws   device workspace of diffkv_workspace_size(DIFFKV_OP_ATTENTION, ...)
  *        bytes (always needed: it holds the work bookkeeping and partial
  *        states).

@@ -117,9 +117,9 @@ AppendWs append_ws(int64_t B, int64_t Hkv, int64_t total_new)
     return w;
 }
 
-// Attention workspace: balanced mode (splits = 0): per-table first unit, the
-// unit total and one partial state per (share, table) slot k + t; split mode
-// (S > 1): S partial states per table; S = 1 needs none.
+// Attention workspace: automatic (0) or balanced (-1) mode: per-table first
+// unit, the unit total and one partial state per (share, table) slot k + t;
+// split mode (S > 1): S partial states per table; S = 1 needs none.
 struct AttnWs {
     int64_t ustart, utot, part, total, nparts;
 };
@@ -129,7 +129,7 @@ AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits)
     AttnWs w;
     const int64_t T = B * Hkv;
     const int64_t gq = Hkv > 0 ? Hq / Hkv : 1;
-    w.nparts = splits == 0 ? kAttnMaxWorkers + T : (splits > 1 ? T * splits : 0);
+    w.nparts = splits <= 0 ? kAttnMaxWorkers + T : (splits > 1 ? T * splits : 0);
     int64_t o = 0;
     w.ustart = o; o = align256(o + T * 8);
     w.utot = o;   o = align256(o + 8);
@@ -163,7 +163,7 @@ diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout, int
         *bytes = (size_t)append_ws(num_seqs, num_kv_heads, total_new).total;
         return DIFFKV_OK;
     case DIFFKV_OP_ATTENTION: {
-        if (num_q_heads <= 0 || num_kv_heads <= 0 || num_splits < 0) return DIFFKV_E_INVAL;
+        if (num_q_heads <= 0 || num_kv_heads <= 0 || num_splits < -1) return DIFFKV_E_INVAL;
         *bytes = (size_t)attn_ws(num_seqs, num_q_heads, num_kv_heads, num_splits).total;
         return DIFFKV_OK;
     }
@@ -243,7 +243,7 @@ diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_
                                       size_t ws_bytes, void* stream)
 {
     if (!layout_valid(layout) || !cache_valid(cache) || !cache->pool) return DIFFKV_E_INVAL;
-    if (num_q_heads <= 0 || num_q_heads % cache->num_kv_heads != 0 || num_splits < 0)
+    if (num_q_heads <= 0 || num_q_heads % cache->num_kv_heads != 0 || num_splits < -1)
         return DIFFKV_E_INVAL;
     if (!layout_kernels_supported(layout)) return DIFFKV_E_UNSUPPORTED;
     if (num_q_heads / cache->num_kv_heads > 8) return DIFFKV_E_UNSUPPORTED;

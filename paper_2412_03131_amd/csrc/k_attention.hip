@@ -590,8 +590,18 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     // page i computes from buffer i % 2 (swapped after an odd number of high
     // pages) while page i+1 is in flight; the ID of page i is loaded when page
     // i-2 is issued
+    // Wave priority follows the pages this wave still has: on a SIMD shared
+    // with shorter work, the longest work is served first (longest-first
+    // scheduling at the wave level; ties go to the older wave).
+    auto set_prio = [&](int rem) {
+        if (rem > 24) __builtin_amdgcn_s_setprio(3);
+        else if (rem > 12) __builtin_amdgcn_s_setprio(2);
+        else if (rem > 4) __builtin_amdgcn_s_setprio(1);
+        else __builtin_amdgcn_s_setprio(0);
+    };
     int i = 0;
     for (; i + 2 <= nhi; i += 2) {
+        set_prio(nmine - i);
         issue(i + 1, id1, buf1, ok1);
         id1 = id_at(i + 3);
         compute_hi(i, buf0, ok0);
@@ -604,6 +614,7 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         id1 = id_at(i + 3);
         compute_hi(i, buf0, ok0);
         for (++i; i < nmine; i += 2) {
+            set_prio(nmine - i);
             issue(i + 1, id0, buf0, ok0);
             id0 = id_at(i + 3);
             compute_lo(i, buf1, ok1);
@@ -613,6 +624,7 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         }
     } else {
         for (; i < nmine; i += 2) {
+            set_prio(nmine - i);
             issue(i + 1, id1, buf1, ok1);
             id1 = id_at(i + 3);
             compute_lo(i, buf0, ok0);
@@ -914,6 +926,13 @@ hipError_t launch_attention(AttnArgs a, hipStream_t st)
     if (!kern) return hipErrorInvalidValue;
     const long long T = (long long)a.B * a.Hkv;
     long long grid;
+    if (a.splits == 0) {
+        // automatic: one workgroup per table when the tables alone fill the
+        // device (their spread is absorbed by wave priorities and by the
+        // hardware dispatching further tables as workgroups finish), balanced
+        // shares when there are fewer tables than resident workgroups
+        a.splits = T >= balanced_workers(gq) ? 1 : -1;
+    }
     if (a.splits > 0) {
         grid = T * a.splits;
         a.workers = 0;

@@ -61,8 +61,12 @@ def test_workspace_sizes(dk):
     s1 = dk.workspace_size(dk.OP_ATTENTION, L, 32, 64, 8, 0, 1)
     s4 = dk.workspace_size(dk.OP_ATTENTION, L, 32, 64, 8, 0, 4)
     assert s4 >= 4 * 32 * 8 * part and s4 > s1 > 0
-    # balanced mode: one partial slot per (share, table) pair met, at most 2048 shares
+    # automatic / balanced mode: one partial slot per (share, table) pair met, at most
+    # 2048 shares
     assert dk.workspace_size(dk.OP_ATTENTION, L, 32, 64, 8, 0, 0) >= (2048 + 32 * 8) * part
+    assert dk.workspace_size(dk.OP_ATTENTION, L, 32, 64, 8, 0, -1) >= (2048 + 32 * 8) * part
+    with pytest.raises(dk.DiffKVError):
+        dk.workspace_size(dk.OP_ATTENTION, L, 32, 64, 8, 0, -2)
     a1 = dk.workspace_size(dk.OP_APPEND, L, 64, 0, 8, 1000)
     a2 = dk.workspace_size(dk.OP_APPEND, L, 64, 0, 8, 2000)
     assert a2 > a1 >= 1000 * 8 * 4

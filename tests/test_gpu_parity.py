@@ -155,7 +155,7 @@ def test_attention_matches_oracle(name, B, L):
     w, Lo, Ld, oc = _attn_case(name, B, L, 1)
     ref, ref_lse = orc.attention(oc, w["q"], SCALE)
     dc = dev_cache_from_oracle(Ld, oc)
-    for splits in (1, 3, 0):
+    for splits in (1, 3, 0, -1):
         print("case: attention %s splits=%d" % (name, splits), flush=True)
         out, lse = dk.decode_attention(dc, t(w["q"]), SCALE, num_splits=splits)
         torch.cuda.synchronize()
@@ -199,7 +199,7 @@ def test_attention_edge_cases():
     q = rng.standard_normal((B, Hq, 128)).astype(np.float16).view(np.uint16)
     ref, ref_lse = orc.attention(oc, q, SCALE)
     dc = dev_cache_from_oracle(Ld, oc)
-    for splits in (1, 2, 7, 16, 0):
+    for splits in (1, 2, 7, 16, 0, -1):
         print("case: edge splits=%d" % splits, flush=True)
         out, lse = dk.decode_attention(dc, t(q), SCALE, num_splits=splits)
         torch.cuda.synchronize()

@@ -322,7 +322,7 @@ def main():
             "attention_splits": S,
         },
         "roofline": {
-            "kernel": "diffkv_decode_attention (attn_decode + attn_merge)",
+            "kernel": "diffkv_decode_attention (attn_decode, plus attn_merge when the mode splits tables)",
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,

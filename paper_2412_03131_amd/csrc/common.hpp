@@ -86,35 +86,72 @@ __device__ __forceinline__ long long wave_incl_scan64(long long x)
     return (long long)(((unsigned long long)hi << 32) | lo);
 }
 
+// Inclusive OR over a full wave, same DPP pattern as the prefix sum.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_or_step(uint32_t x)
+{
+    return x | dpp_u32<CTRL, ROWS>(x);
+}
+__device__ __forceinline__ uint32_t wave_or_u32(uint32_t x)  // result in lane 63
+{
+    x = dpp_or_step<0x111, 0xF>(x);
+    x = dpp_or_step<0x112, 0xF>(x);
+    x = dpp_or_step<0x114, 0xF>(x);
+    x = dpp_or_step<0x118, 0xF>(x);
+    x = dpp_or_step<0x142, 0xA>(x);
+    x = dpp_or_step<0x143, 0xC>(x);
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
+}
+
+__device__ __forceinline__ int wave_index() { return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave); }
+
+template <typename TInt>
+__device__ __forceinline__ TInt wave_incl_scan_t(TInt x)
+{
+    if constexpr (sizeof(TInt) == 8) return (TInt)wave_incl_scan64((long long)x);
+    else return (TInt)wave_incl_scan((int)x);
+}
+template <typename TInt>
+__device__ __forceinline__ TInt read_lane(TInt x, int l)  // l uniform
+{
+    if constexpr (sizeof(TInt) == 8) {
+        const unsigned long long u = (unsigned long long)x;
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+        return (TInt)(((unsigned long long)hi << 32) | lo);
+    } else {
+        return (TInt)__builtin_amdgcn_readlane((int)x, l);
+    }
+}
+
 // Exclusive block scan of one value per thread (blockDim.x multiple of 64,
 // at most 1024).  Returns the exclusive prefix; *total gets the block sum.
-// `lds` must hold blockDim.x/64 + 1 entries.  64-bit values are two
-// independent 32-bit counters (no carry between the halves).
+// `lds` must hold blockDim.x/64 entries.  64-bit values are two independent
+// 32-bit counters (no carry between the halves).  Every wave scans the wave
+// totals itself, so there is one barrier plus one that frees `lds` for reuse.
+// With `bits`, *bits_out also gets the OR of every thread's bits (`lds_bits`
+// then holds blockDim.x/64 entries).
 template <typename TInt>
-__device__ __forceinline__ TInt block_excl_scan(TInt x, TInt* lds, TInt* total)
+__device__ __forceinline__ TInt block_excl_scan(TInt x, TInt* lds, TInt* total, uint32_t bits = 0,
+                                                uint32_t* lds_bits = nullptr, uint32_t* bits_out = nullptr)
 {
     const int l = lane_id();
-    const int w = threadIdx.x / kWave;
+    const int w = wave_index();
     const int nw = blockDim.x / kWave;
-    TInt inc;
-    if constexpr (sizeof(TInt) == 8) inc = (TInt)wave_incl_scan64((long long)x);
-    else inc = (TInt)wave_incl_scan((int)x);
-    if (l == kWave - 1) lds[w] = inc;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        TInt run = 0;
-        for (int i = 0; i < nw; ++i) {
-            TInt t = lds[i];
-            lds[i] = run;
-            run += t;
-        }
-        lds[nw] = run;
+    const TInt inc = wave_incl_scan_t<TInt>(x);
+    if (lds_bits) bits = wave_or_u32(bits);
+    if (l == kWave - 1) {
+        lds[w] = inc;
+        if (lds_bits) lds_bits[w] = bits;
     }
     __syncthreads();
-    TInt r = lds[w] + inc - x;
-    *total = lds[nw];
+    const TInt tv = l < nw ? lds[l] : (TInt)0;
+    const TInt tinc = wave_incl_scan_t<TInt>(tv);
+    if (lds_bits) *bits_out = wave_or_u32(l < nw ? lds_bits[l] : 0u);
+    const TInt below = read_lane<TInt>(tinc - tv, w);
+    *total = read_lane<TInt>(tinc, nw - 1);
     __syncthreads();
-    return r;
+    return below + inc - x;
 }
 
 // Block-wide sum of a true 64-bit value and OR of flag bits (all threads get

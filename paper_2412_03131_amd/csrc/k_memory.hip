@@ -37,7 +37,31 @@ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; 
 // append_classify: grid (Hkv, B), block 1024
 // ---------------------------------------------------------------------------
 constexpr int kClsThreads = 1024;
-constexpr int kClsLdsKeys = 8192;  // tables with more new tokens re-read keys from global
+constexpr int kClsPer = 8;                       // tokens per thread in one tile
+constexpr int kClsTile = kClsThreads * kClsPer;  // the first tile's scores stay in registers
+constexpr uint32_t kOffSat = 1u << 30;           // row offsets saturate here (above any total_new)
+
+// Sum over the wave of values <= kOffSat, saturating at kOffSat (result in lane 63).
+__device__ __forceinline__ uint32_t wave_sat_sum(uint32_t x)
+{
+    x = min(x + dpp_u32<0x111, 0xF>(x), kOffSat);
+    x = min(x + dpp_u32<0x112, 0xF>(x), kOffSat);
+    x = min(x + dpp_u32<0x114, 0xF>(x), kOffSat);
+    x = min(x + dpp_u32<0x118, 0xF>(x), kOffSat);
+    x = min(x + dpp_u32<0x142, 0xA>(x), kOffSat);
+    x = min(x + dpp_u32<0x143, 0xC>(x), kOffSat);
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
+}
+
+// Class of one new token against the two cuts of Sec. 4.2 (the high set, and
+// the high + low set).  Per cut: a = above it outright, e = tied with the cut
+// key (only the first `need` ties in position order are above it).
+// mode 0: nothing above the cut, 1: every non-window token, 2: cut at key K.
+struct Cuts {
+    int mode[2];
+    uint32_t K[2];
+    int need[2];
+};
 
 __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
 {
@@ -45,30 +69,49 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
     const int H = a.Hkv;
     const int t = b * H + h;
     const int tid = threadIdx.x;
-    __shared__ long long s_scan[kClsThreads / kWave + 1];
-    __shared__ int s_hist[2][256];
+    __shared__ long long s_scan[kClsThreads / kWave];
+    __shared__ int s_hist[2][2][256];  // [buffer][cut][digit]
     __shared__ int s_sel[4];
-    __shared__ uint32_t s_keys[kClsLdsKeys];
+    __shared__ uint32_t s_off;
 
     if (t == 0 && tid == 0) {  // ring pointers before this call (the commit kernel moves head)
         a.flags->head_old = a.ring_ptr[0];
         a.flags->tail_old = a.ring_ptr[1];
     }
-    // row offset of this sequence (sum of new_len over lower sequences)
-    long long part = 0;
-    for (int i = tid; i < b; i += kClsThreads) part += a.new_len[i];
-    uint32_t unused;
-    const long long off_b = block_sum_or(part, 0u, s_scan, &unused);
+    if (tid < 256) {
+        s_hist[0][0][tid] = 0;
+        s_hist[0][1][tid] = 0;
+    }
+    // row offset of this sequence: sum of new_len over lower sequences (wave 0).
+    // Entries are clamped to [0, kOffSat] and the sum saturates: a call with an
+    // entry outside [0, max_new] fails anyway (that table flags itself).
+    if (tid < kWave) {
+        uint32_t part = 0;
+        for (int i = tid; i < b; i += kWave) {
+            const int v = a.new_len[i];
+            part = min(part + (uint32_t)(v < 0 ? 0 : (v > (int)kOffSat ? (int)kOffSat : v)), kOffSat);
+        }
+        part = wave_sat_sum(part);
+        if (tid == 0) s_off = part;
+    }
     const int n = a.new_len[b];
     TState* ts = a.tstate + t;
-    const bool bad = n < 0 || n > a.max_new || off_b + n > a.total_new ||
-                     (b == a.B - 1 && off_b + n != a.total_new);
     if (tid == 0) {  // section lengths and pages before this call
         ts->lold[0] = a.len[2 * t];
         ts->lold[1] = a.len[2 * t + 1];
         ts->pold[0] = a.pages[2 * t];
         ts->pold[1] = a.pages[2 * t + 1];
     }
+    const bool quota = a.quota != nullptr;
+    int q0 = 0, q1 = 0;
+    if (quota) {
+        q0 = a.quota[2 * t];
+        q1 = a.quota[2 * t + 1];
+    }
+    __syncthreads();
+    const long long off_b = s_off;
+    const bool bad = n < 0 || n > a.max_new || off_b + n > a.total_new ||
+                     (b == a.B - 1 && off_b + n != a.total_new);
     if (bad) {
         if (tid == 0) {  // the commit kernel turns n < 0 into DIFFKV_ST_BAD_INPUT
             ts->cnt[0] = ts->cnt[1] = 0;
@@ -84,58 +127,77 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
     const int avail = n - W;
     const float* sc = a.score + off_b * H + h;
     int32_t* ord = a.ord + off_b * H + (long long)h * n;
-    const bool in_lds = avail <= kClsLdsKeys;
 
-    // ---- quota form: two-target radix select (k-th largest key) ----------
-    int k_sel[2] = {0, 0};
-    uint32_t K[2] = {0, 0};
-    int need[2] = {0, 0};
-    const bool quota = a.quota != nullptr;
+    // first tile: thread tid holds tokens tid*e .. tid*e + e - 1
+    const int n0 = n < kClsTile ? n : kClsTile;
+    const int e = (n0 + kClsThreads - 1) / kClsThreads;
+    float sr[kClsPer];
+#pragma unroll
+    for (int i = 0; i < kClsPer; ++i) {
+        const int j = tid * e + i;
+        sr[i] = (i < e && j < avail) ? sc[(long long)j * H] : 0.f;
+    }
+
+    Cuts c = {{0, 0}, {0, 0}, {0, 0}};
     float thr_h = 0.f, thr_l = 0.f;
     if (quota) {
-        const int q0 = a.quota[2 * t], q1 = a.quota[2 * t + 1];
         const int nh = q0 < 0 ? 0 : (q0 > avail ? avail : q0);
         const int nl = q1 < 0 ? 0 : (q1 > avail - nh ? avail - nh : q1);
-        k_sel[0] = nh;
-        k_sel[1] = nh + nl;
-        // a cut that keeps every non-window token needs no selection
-        const bool sel0 = nh > 0 && nh < avail, sel1 = nh + nl > 0 && nh + nl < avail;
-        if (sel0 || sel1) {
-            if (in_lds) {
-                for (int j = tid; j < avail; j += kClsThreads) s_keys[j] = score_key(sc[(long long)j * H]);
-                __syncthreads();
-            }
+        const int cut[2] = {nh, nh + nl};
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) c.mode[s2] = cut[s2] <= 0 ? 0 : (cut[s2] >= avail ? 1 : 2);
+        if (c.mode[0] == 2 || c.mode[1] == 2) {
+            // two-target radix select (the cut[s]-th largest key), 8-bit digits
+            // from the top; histograms double-buffered so each digit costs two barriers
             uint32_t prefix[2] = {0, 0}, mask = 0;
-            int kk[2] = {sel0 ? nh : 0, sel1 ? nh + nl : 0};
-            for (int shift = 24; shift >= 0; shift -= 8) {
-                for (int i = tid; i < 512; i += kClsThreads) (&s_hist[0][0])[i] = 0;
-                __syncthreads();
-                for (int j = tid; j < avail; j += kClsThreads) {
-                    const uint32_t key = in_lds ? s_keys[j] : score_key(sc[(long long)j * H]);
+            int kk[2] = {c.mode[0] == 2 ? cut[0] : 0, c.mode[1] == 2 ? cut[1] : 0};
+            uint32_t kr[kClsPer];
+#pragma unroll
+            for (int i = 0; i < kClsPer; ++i) kr[i] = score_key(sr[i]);
+#pragma unroll
+            for (int pass = 0; pass < 4; ++pass) {
+                const int shift = 24 - 8 * pass;
+                int* hist = &s_hist[pass & 1][0][0];
+#pragma unroll
+                for (int i = 0; i < kClsPer; ++i) {
+                    if (i < e && tid * e + i < avail) {
+                        const uint32_t key = kr[i];
+                        const uint32_t dig = (key >> shift) & 255u;
+#pragma unroll
+                        for (int s2 = 0; s2 < 2; ++s2)
+                            if (kk[s2] > 0 && (key & mask) == prefix[s2]) atomicAdd(&hist[s2 * 256 + dig], 1);
+                    }
+                }
+                for (int j = kClsTile + tid; j < avail; j += kClsThreads) {  // beyond the first tile
+                    const uint32_t key = score_key(sc[(long long)j * H]);
                     const uint32_t dig = (key >> shift) & 255u;
 #pragma unroll
                     for (int s2 = 0; s2 < 2; ++s2)
-                        if (kk[s2] > 0 && (key & mask) == prefix[s2]) atomicAdd(&s_hist[s2][dig], 1);
+                        if (kk[s2] > 0 && (key & mask) == prefix[s2]) atomicAdd(&hist[s2 * 256 + dig], 1);
                 }
+                if (tid < 512) (&s_hist[(pass + 1) & 1][0][0])[tid] = 0;  // the next digit's buffer
                 __syncthreads();
                 if (tid < 2 * kWave) {  // two waves find the cut bins with a scan from the top
                     const int s2 = tid / kWave, l = tid & (kWave - 1);
                     if (kk[s2] > 0) {
                         // lane l owns bins 255-4l .. 252-4l (descending)
-                        int c[4], tot4 = 0;
+                        int cb[4], tot4 = 0;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) { c[e] = s_hist[s2][255 - 4 * l - e]; tot4 += c[e]; }
+                        for (int q = 0; q < 4; ++q) {
+                            cb[q] = hist[s2 * 256 + 255 - 4 * l - q];
+                            tot4 += cb[q];
+                        }
                         const int incl = wave_incl_scan(tot4);
                         int above = incl - tot4;
                         if (above < kk[s2] && incl >= kk[s2]) {
 #pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                if (above + c[e] >= kk[s2]) {
-                                    s_sel[2 * s2] = 255 - 4 * l - e;
+                            for (int q = 0; q < 4; ++q) {
+                                if (above + cb[q] >= kk[s2]) {
+                                    s_sel[2 * s2] = 255 - 4 * l - q;
                                     s_sel[2 * s2 + 1] = above;
                                     break;
                                 }
-                                above += c[e];
+                                above += cb[q];
                             }
                         }
                     }
@@ -149,18 +211,15 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
                     }
                 }
                 mask |= 255u << shift;
-                __syncthreads();
             }
-            K[0] = prefix[0];
-            K[1] = prefix[1];
-            need[0] = kk[0];  // tokens with key == K that still belong above the cut
-            need[1] = kk[1];
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+                if (c.mode[s2] == 2) {
+                    c.K[s2] = prefix[s2];
+                    c.need[s2] = kk[s2];  // tokens with key == K that still belong above the cut
+                }
+            }
         }
-        // cuts at 0 or at avail: every token is above (or below) them
-        if (!sel0) { K[0] = 0; need[0] = nh > 0 ? avail : 0; }
-        if (!sel1) { K[1] = 0; need[1] = nh + nl > 0 ? avail : 0; }
-        if (!sel0 && nh > 0) k_sel[0] = -1;  // marker: all non-window tokens are high
-        if (!sel1 && nh + nl > 0) k_sel[1] = -1;
     } else {
         const float N = (float)(a.seq_len[b] + n);
         thr_h = a.alpha_h / N;
@@ -168,52 +227,75 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
     }
 
     // ---- classes and in-section ranks, in position order ------------------
-    long long carry_tie = 0, carry_rank = 0;
-    const bool need_ties = quota && (k_sel[0] > 0 || k_sel[1] > 0);
-    for (int base = 0; base < n; base += kClsThreads) {
-        const int j = base + tid;
-        const bool valid = j < n;
-        const bool win = valid && j >= avail;
-        float s = 0.f;
-        uint32_t key = 0;
-        if (valid && !win) {
-            if (quota && in_lds && need_ties) key = s_keys[j];
-            else {
-                s = sc[(long long)j * H];
-                key = score_key(s);
+    // One block scan per tile of four counters (16 bits each): above cut 0,
+    // tied at cut 0, above cut 1, tied at cut 1.  The high set is the cut-0
+    // set; the low set is the cut-1 set minus it (cut 1's set contains cut 0's),
+    // so a token's rank in either follows from the four prefix counts.
+    int c_a0 = 0, c_e0 = 0, c_a1 = 0, c_e1 = 0;
+    for (int base = 0; base < n; base += kClsTile) {
+        const int tn = n - base < kClsTile ? n - base : kClsTile;
+        const int et = (tn + kClsThreads - 1) / kClsThreads;
+        uint32_t fl = 0;  // 4 flag bits per token
+        long long cnt = 0;
+#pragma unroll
+        for (int i = 0; i < kClsPer; ++i) {
+            const int j = base + tid * et + i;
+            if (i < et && j < n) {
+                bool a0, e0, a1, e1;
+                if (j >= avail) {  // recent window: always high
+                    a0 = a1 = true;
+                    e0 = e1 = false;
+                } else {
+                    const float s = base == 0 ? sr[i] : sc[(long long)j * H];
+                    if (quota) {
+                        const uint32_t key = score_key(s);
+                        a0 = c.mode[0] == 1 || (c.mode[0] == 2 && key > c.K[0]);
+                        e0 = c.mode[0] == 2 && key == c.K[0];
+                        a1 = c.mode[1] == 1 || (c.mode[1] == 2 && key > c.K[1]);
+                        e1 = c.mode[1] == 2 && key == c.K[1];
+                    } else {
+                        a0 = s >= thr_h;
+                        a1 = a0 || s >= thr_l;
+                        e0 = e1 = false;
+                    }
+                }
+                fl |= ((uint32_t)a0 | ((uint32_t)e0 << 1) | ((uint32_t)a1 << 2) | ((uint32_t)e1 << 3)) << (4 * i);
+                cnt += (long long)a0 | ((long long)e0 << 16) | ((long long)a1 << 32) | ((long long)e1 << 48);
             }
-        }
-        bool hi = win, lo = false;
-        if (quota) {
-            const bool e0 = valid && !win && k_sel[0] > 0 && key == K[0];
-            const bool e1 = valid && !win && k_sel[1] > 0 && key == K[1];
-            int r0 = 0, r1 = 0;
-            if (need_ties) {
-                long long tot;
-                long long ex = block_excl_scan<long long>((long long)e0 | ((long long)e1 << 32), s_scan, &tot);
-                ex += carry_tie;
-                carry_tie += tot;
-                r0 = (int)(ex & 0xffffffffll);
-                r1 = (int)(ex >> 32);
-            }
-            if (valid && !win) {
-                hi = k_sel[0] < 0 || (k_sel[0] > 0 && (key > K[0] || (e0 && r0 < need[0])));
-                lo = !hi && (k_sel[1] < 0 || (k_sel[1] > 0 && (key > K[1] || (e1 && r1 < need[1]))));
-            }
-        } else if (valid && !win) {
-            hi = s >= thr_h;
-            lo = !hi && s >= thr_l;
         }
         long long tot;
-        long long ex = block_excl_scan<long long>((long long)hi | ((long long)lo << 32), s_scan, &tot);
-        ex += carry_rank;
-        carry_rank += tot;
-        if (hi) ord[(int)(ex & 0xffffffffll)] = j;
-        if (lo) ord[n - 1 - (int)(ex >> 32)] = j;
+        const long long ex = block_excl_scan<long long>(cnt, s_scan, &tot);
+        int r_a0 = c_a0 + (int)(ex & 0xffff), r_e0 = c_e0 + (int)((ex >> 16) & 0xffff);
+        int r_a1 = c_a1 + (int)((ex >> 32) & 0xffff), r_e1 = c_e1 + (int)((ex >> 48) & 0xffff);
+#pragma unroll
+        for (int i = 0; i < kClsPer; ++i) {
+            const int j = base + tid * et + i;
+            if (i < et && j < n) {
+                const uint32_t f = fl >> (4 * i);
+                const bool a0 = f & 1, e0 = f & 2, a1 = f & 4, e1 = f & 8;
+                const int rh = r_a0 + min(r_e0, c.need[0]);  // high tokens before this one
+                const int rt = r_a1 + min(r_e1, c.need[1]);  // high + low tokens before it
+                // (the ranks stay inside the table's n slots; the bounds tests only guard memory)
+                if (a0 || (e0 && r_e0 < c.need[0])) {
+                    if (rh < n) ord[rh] = j;
+                } else if (a1 || (e1 && r_e1 < c.need[1])) {
+                    if ((unsigned)(rt - rh) < (unsigned)n) ord[n - 1 - (rt - rh)] = j;
+                }
+                r_a0 += a0;
+                r_e0 += e0;
+                r_a1 += a1;
+                r_e1 += e1;
+            }
+        }
+        c_a0 += (int)(tot & 0xffff);
+        c_e0 += (int)((tot >> 16) & 0xffff);
+        c_a1 += (int)((tot >> 32) & 0xffff);
+        c_e1 += (int)((tot >> 48) & 0xffff);
     }
     if (tid == 0) {
-        ts->cnt[0] = (int)(carry_rank & 0xffffffffll);
-        ts->cnt[1] = (int)(carry_rank >> 32);
+        const int hi = c_a0 + min(c_e0, c.need[0]);
+        ts->cnt[0] = hi;
+        ts->cnt[1] = c_a1 + min(c_e1, c.need[1]) - hi;
         ts->n = n;
     }
 }
@@ -230,7 +312,51 @@ constexpr int kPlanThreads = 1024;
 // pages, seq_len, ring head) while all of them -- reading only the snapshot
 // -- take page jobs (table, section, page) in job order.
 // ---------------------------------------------------------------------------
-// Quantize one 32-dim group spread over 16 lanes (2 values per lane).
+// Min / max over a 16-lane row with DPP (quad swaps, then half-row and row mirrors).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x)
+{
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_min(float x)
+{
+    x = fminf(x, dpp_f32<0xB1>(x));   // quad_perm [1,0,3,2]
+    x = fminf(x, dpp_f32<0x4E>(x));   // quad_perm [2,3,0,1]
+    x = fminf(x, dpp_f32<0x141>(x));  // row_half_mirror
+    return fminf(x, dpp_f32<0x140>(x));  // row_mirror
+}
+__device__ __forceinline__ float row16_max(float x)
+{
+    x = fmaxf(x, dpp_f32<0xB1>(x));
+    x = fmaxf(x, dpp_f32<0x4E>(x));
+    x = fmaxf(x, dpp_f32<0x141>(x));
+    return fmaxf(x, dpp_f32<0x140>(x));
+}
+
+// clamp(rint(d / s), 0, lb) for two values, with d / s the IEEE fp32
+// quotient.  The quotient through the hardware reciprocal (v_rcp_f32, within
+// 1 ulp) and one rounded product is within 1.5 * 2^-23 relative, i.e. 2^-13
+// absolute for |d/s| <= 2^9; larger quotients clamp the same way either way.
+// It rounds to another integer than the IEEE quotient only if it lies within
+// that distance of a half-integer, so lanes within 2^-12 of one (about 1 in
+// 2^11) divide exactly, in a branch the compiler may not flatten.
+__device__ __forceinline__ void codes_of(float d0, float d1, float s, float lb, uint32_t& c0, uint32_t& c1)
+{
+#pragma clang fp contract(off)
+    const float rs = __builtin_amdgcn_rcpf(s);
+    float q0 = d0 * rs, q1 = d1 * rs;
+    const bool n0 = fabsf(q0 - rintf(q0)) > 0.5f - 0x1p-12f;
+    const bool n1 = fabsf(q1 - rintf(q1)) > 0.5f - 0x1p-12f;
+    if (n0 || n1) {
+        asm volatile("" ::: "memory");
+        if (n0) q0 = d0 / s;
+        if (n1) q1 = d1 / s;
+    }
+    c0 = (uint32_t)fminf(fmaxf(rintf(q0), 0.0f), lb);
+    c1 = (uint32_t)fminf(fmaxf(rintf(q1), 0.0f), lb);
+}
+
+// Quantize one 32-dim group spread over a 16-lane row (2 values per lane).
 // Arithmetic is IEEE fp32 with no contraction, identical to the text of the
 // quantizer: s = fp16((max-min)/L), z = fp16(min), code = clamp(rint((x-z)/s)).
 __device__ __forceinline__ void quant_pair(uint32_t xbits, int lb, uint32_t& sz, uint32_t& c0,
@@ -239,8 +365,8 @@ __device__ __forceinline__ void quant_pair(uint32_t xbits, int lb, uint32_t& sz,
 #pragma clang fp contract(off)
     float x0 = h2f(xbits & 0xffffu) + 0.0f;
     float x1 = h2f(xbits >> 16) + 0.0f;
-    float mn = wave_min_w<16>(fminf(x0, x1));
-    float mx = wave_max_w<16>(fmaxf(x0, x1));
+    float mn = row16_min(fminf(x0, x1));
+    float mx = row16_max(fmaxf(x0, x1));
     float s32 = (mx - mn) / (float)lb;
     uint32_t s16 = f2h_rne(s32);
     uint32_t z16 = f2h_rne(mn);
@@ -248,12 +374,7 @@ __device__ __forceinline__ void quant_pair(uint32_t xbits, int lb, uint32_t& sz,
     if (s16 == 0) {
         c0 = c1 = 0;
     } else {
-        float r0 = rintf((x0 - z) / s);
-        float r1 = rintf((x1 - z) / s);
-        r0 = fminf(fmaxf(r0, 0.0f), (float)lb);
-        r1 = fminf(fmaxf(r1, 0.0f), (float)lb);
-        c0 = (uint32_t)r0;
-        c1 = (uint32_t)r1;
+        codes_of(x0 - z, x1 - z, s, (float)lb, c0, c1);
     }
     sz = s16 | (z16 << 16);
 }
@@ -269,34 +390,45 @@ struct TablePlan {
     bool held_over;  // more pages than p_max after the call
 };
 
-__device__ __forceinline__ TablePlan table_plan(const TState& s, const int (&T)[2], int P)
+// The kernels' page sizes are powers of two, so page indices are shifts.
+static_assert(kTHi == 16 && kTLo == 32, "page index arithmetic below uses shifts");
+__device__ __forceinline__ int page_of(int x, int sec) { return sec ? x >> 5 : x >> 4; }
+
+__device__ __forceinline__ TablePlan table_plan(const TState& s, int P)
 {
     TablePlan tp;
     int held = 0;
 #pragma unroll
     for (int sec = 0; sec < 2; ++sec) {
-        const int want = ceil_div(s.lold[sec] + s.cnt[sec], T[sec]);
+        const int T = sec ? kTLo : kTHi;
+        const int want = page_of(s.lold[sec] + s.cnt[sec] + T - 1, sec);
         tp.need[sec] = want > s.pold[sec] ? want - s.pold[sec] : 0;
         held += want > s.pold[sec] ? want : s.pold[sec];
-        tp.jobs[sec] = s.cnt[sec] ? (s.lold[sec] + s.cnt[sec] - 1) / T[sec] - s.lold[sec] / T[sec] + 1 : 0;
+        tp.jobs[sec] = s.cnt[sec] ? page_of(s.lold[sec] + s.cnt[sec] - 1, sec) - page_of(s.lold[sec], sec) + 1 : 0;
     }
     tp.held_over = held > P;
     return tp;
 }
 
+__device__ __forceinline__ long long plan_word(const TablePlan& tp)  // new pages | jobs << 32
+{
+    return (long long)(tp.need[0] + tp.need[1]) | ((long long)(tp.jobs[0] + tp.jobs[1]) << 32);
+}
+
 struct JobDesc {
     int t, sec, p, u0, u1, lold, n, tslot;
     long long ring_idx;  // ring position of a new page, -1 for a page already held
-    int id;
 };
+
+constexpr int kPlanKeep = 2;  // tables per thread whose state stays in registers
 
 __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
 {
     const int tid = threadIdx.x;
     const int NT = a.B * a.Hkv;
     const int P = a.p_max;
-    const int T[2] = {a.T[0], a.T[1]};
-    __shared__ long long s_scan[kCommitThreads / kWave + 1];
+    __shared__ long long s_scan[kCommitThreads / kWave];
+    __shared__ uint32_t s_bits[kCommitThreads / kWave];
     __shared__ JobDesc s_job;
     __shared__ uint64_t s_rows[kQuantWaves][kWave][2];
     const long long head_old = a.flags->head_old, tail_old = a.flags->tail_old;
@@ -305,24 +437,32 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
     const int per = (NT + kCommitThreads - 1) / kCommitThreads;
     const int t0 = tid * per;
     const int t1 = t0 + per < NT ? t0 + per : NT;
-    long long packed = 0;  // new pages | jobs << 32
+    TState st[kPlanKeep];
+#pragma unroll
+    for (int i = 0; i < kPlanKeep; ++i)
+        if (t0 + i < t1) st[i] = a.tstate[t0 + i];
+    auto state_of = [&](int t) -> TState {
+        static_assert(kPlanKeep == 2, "state_of picks from two registers");
+        if (t == t0) return st[0];
+        if (t == t0 + 1) return st[1];
+        return a.tstate[t];
+    };
+    long long packed = 0;
     uint32_t bits = 0;
     for (int t = t0; t < t1; ++t) {
-        const TState s = a.tstate[t];
+        const TState s = state_of(t);
         if (s.n < 0) {
             bits |= DIFFKV_ST_BAD_INPUT;
             continue;
         }
-        const TablePlan tp = table_plan(s, T, P);
+        const TablePlan tp = table_plan(s, P);
         if (tp.held_over) bits |= DIFFKV_ST_TABLE_OVERFLOW;
-        packed += (tp.need[0] + tp.need[1]) | ((long long)(tp.jobs[0] + tp.jobs[1]) << 32);
+        packed += plan_word(tp);
     }
     long long tot;
-    const long long before = block_excl_scan<long long>(packed, s_scan, &tot);
-    // __syncthreads_or returns whether any thread's value is nonzero: one call per bit
-    const bool any_bad = __syncthreads_or((int)(bits & DIFFKV_ST_BAD_INPUT));
-    const bool any_ovf = __syncthreads_or((int)(bits & DIFFKV_ST_TABLE_OVERFLOW));
-    bits = (any_bad ? DIFFKV_ST_BAD_INPUT : 0u) | (any_ovf ? DIFFKV_ST_TABLE_OVERFLOW : 0u);
+    uint32_t all_bits;
+    const long long before = block_excl_scan<long long>(packed, s_scan, &tot, bits, s_bits, &all_bits);
+    bits = all_bits & (DIFFKV_ST_BAD_INPUT | DIFFKV_ST_TABLE_OVERFLOW);
     const long long total_need = tot & 0xffffffffll;
     const int njobs = (int)(tot >> 32);
     if (bits & DIFFKV_ST_BAD_INPUT) bits = DIFFKV_ST_BAD_INPUT;
@@ -335,8 +475,8 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
     // ---- workgroup 0: the state after the call -------------------------------
     if (blockIdx.x == 0) {
         for (int t = t0; t < t1; ++t) {
-            const TState s = a.tstate[t];
-            const TablePlan tp = table_plan(s, T, P);
+            const TState s = state_of(t);
+            const TablePlan tp = table_plan(s, P);
 #pragma unroll
             for (int sec = 0; sec < 2; ++sec) {
                 a.len[2 * t + sec] = s.lold[sec] + s.cnt[sec];
@@ -349,54 +489,60 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
 
     // ---- page jobs ------------------------------------------------------------
     const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
+    const int wave = wave_index();
     const int grp = lane >> 4;
     const int H = a.Hkv;
     const long long page_bytes = a.page_bytes;
     for (int job = blockIdx.x; job < njobs; job += gridDim.x) {
         // the thread whose run of tables holds this job describes it
-        long long pre = before;
-        for (int t = t0; t < t1; ++t) {
-            const TState s = a.tstate[t];
-            const TablePlan tp = table_plan(s, T, P);
-            const int jo = (int)(pre >> 32);
-            if (jo <= job && job < jo + tp.jobs[0] + tp.jobs[1]) {
-                const int lj = job - jo;
-                const int sec = lj < tp.jobs[0] ? 0 : 1;
-                const int p = s.lold[sec] / T[sec] + (sec ? lj - tp.jobs[0] : lj);
-                const int lo = s.lold[sec], hi_end = s.lold[sec] + s.cnt[sec];
-                s_job.t = t;
-                s_job.sec = sec;
-                s_job.p = p;
-                s_job.u0 = lo > p * T[sec] ? lo : p * T[sec];
-                s_job.u1 = hi_end < (p + 1) * T[sec] ? hi_end : (p + 1) * T[sec];
-                s_job.lold = lo;
-                s_job.n = s.n;
-                s_job.tslot = sec ? P - 1 - p : p;
-                // a new page comes from this table's ring region, high pages first
-                s_job.ring_idx = p < s.pold[sec] ? -1
-                                                 : head_old + (pre & 0xffffffffll) + (sec ? tp.need[0] : 0) + (p - s.pold[sec]);
+        const int run_first = (int)(before >> 32);
+        if (run_first <= job && job < run_first + (int)(packed >> 32)) {
+            long long pre = before;
+            for (int t = t0; t < t1; ++t) {
+                const TState s = state_of(t);
+                if (s.n < 0) continue;
+                const TablePlan tp = table_plan(s, P);
+                const int jo = (int)(pre >> 32);
+                if (jo <= job && job < jo + tp.jobs[0] + tp.jobs[1]) {
+                    const int lj = job - jo;
+                    const int sec = lj < tp.jobs[0] ? 0 : 1;
+                    const int TT = sec ? kTLo : kTHi;
+                    const int p = page_of(s.lold[sec], sec) + (sec ? lj - tp.jobs[0] : lj);
+                    const int lo = s.lold[sec], hi_end = s.lold[sec] + s.cnt[sec];
+                    s_job.t = t;
+                    s_job.sec = sec;
+                    s_job.p = p;
+                    s_job.u0 = lo > p * TT ? lo : p * TT;
+                    s_job.u1 = hi_end < (p + 1) * TT ? hi_end : (p + 1) * TT;
+                    s_job.lold = lo;
+                    s_job.n = s.n;
+                    s_job.tslot = sec ? P - 1 - p : p;
+                    // a new page comes from this table's ring region, high pages first
+                    s_job.ring_idx = p < s.pold[sec] ? -1
+                                                     : head_old + (pre & 0xffffffffll) + (sec ? tp.need[0] : 0) +
+                                                           (p - s.pold[sec]);
+                }
+                pre += plan_word(tp);
             }
-            pre += (tp.need[0] + tp.need[1]) | ((long long)(tp.jobs[0] + tp.jobs[1]) << 32);
         }
         __syncthreads();
-        const int t = s_job.t, sec = s_job.sec, p = s_job.p, u0 = s_job.u0, u1 = s_job.u1;
-        const int lold = s_job.lold, n = s_job.n;
+        const int t = __builtin_amdgcn_readfirstlane(s_job.t);
+        const int sec = __builtin_amdgcn_readfirstlane(s_job.sec);
+        const int p = __builtin_amdgcn_readfirstlane(s_job.p);
+        const int u0 = __builtin_amdgcn_readfirstlane(s_job.u0);
+        const int u1 = __builtin_amdgcn_readfirstlane(s_job.u1);
+        const int lold = __builtin_amdgcn_readfirstlane(s_job.lold);
+        const int n = __builtin_amdgcn_readfirstlane(s_job.n);
+        const int tslot = __builtin_amdgcn_readfirstlane(s_job.tslot);
+        const long long ring_idx = s_job.ring_idx;
         const int b = t / H, h = t - b * H;
-        const int TT = T[sec];
+        const int TT = sec ? kTLo : kTHi;
         const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
-        // one thread resolves the page ID while the others load their tokens
-        if (tid == 0) {
-            int32_t* trow = a.page_table + (long long)t * P;
-            int id;
-            if (s_job.ring_idx < 0) {
-                id = trow[s_job.tslot];
-            } else {
-                id = a.ring[s_job.ring_idx % a.num_pages];
-                trow[s_job.tslot] = id;
-            }
-            s_job.id = id;
-        }
+        // the page ID (every wave reads the one entry), beside the token loads
+        int32_t* trow = a.page_table + (long long)t * P;
+        int id = ring_idx < 0 ? trow[tslot] : a.ring[ring_idx % a.num_pages];
+        id = __builtin_amdgcn_readfirstlane(id);
+        if (tid == 0 && ring_idx >= 0) trow[tslot] = id;
         // this wave's tokens u0 + wave + kQuantWaves*i, all loaded up front; token
         // u of the section is row ord[u - lold] (high, rank order) or
         // ord[n - 1 - (u - lold)] (low ranks are stored from the back)
@@ -419,47 +565,45 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
         const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
         const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
         const bool fresh = (u0 == p * TT);
-        uint8_t* pg = nullptr;
-        bool page_ok = false;
+        const bool page_ok = (unsigned)id < (unsigned)a.num_pages;  // never write outside the pool
+        uint8_t* pg = a.pool + (long long)(page_ok ? id : 0) * page_bytes;
+        // a page being continued keeps its earlier tokens' V code bits
+        uint4 vold = make_uint4(0, 0, 0, 0);
+        if (wave == 0 && page_ok && !fresh) vold = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
+        if (page_ok && fresh) {
+            // A fresh page reads as zero wherever no token lies: zero the token
+            // slots from u1 on in every per-token segment and the page tail.
+            // These bytes are disjoint from the ones the tokens write (V code
+            // rows are written whole, zeros included), so the stores need no
+            // ordering among themselves.
+            const int s_end = u1 - p * TT, nfill = TT - s_end;
+            const uint4 z4 = make_uint4(0, 0, 0, 0);
+            for (int i = tid; i < (kb + 1) * nfill; i += kCommitThreads) {
+                const int c = i / nfill, sl = s_end + (i - c * nfill);  // K chunks (kb per token), then K meta
+                uint8_t* dst = c < kb ? pg + off_kc + (c * TT + sl) * 16 : pg + off_km + sl * 16;
+                *reinterpret_cast<uint4*>(dst) = z4;
+            }
+            for (int i = tid; i < (kNG + 2) * nfill; i += kCommitThreads) {
+                const int g = i / nfill, sl = s_end + (i - g * nfill);  // V meta groups, score, pos
+                uint8_t* dst = g < kNG ? pg + off_vm + (g * TT + sl) * 4
+                                       : pg + (g == kNG ? a.off_score[sec] : a.off_pos[sec]) + sl * 4;
+                *reinterpret_cast<uint32_t*>(dst) = 0;
+            }
+            for (long long o = a.off_pos[sec] + (long long)TT * 4 + tid * 16; o < page_bytes; o += kCommitThreads * 16)
+                *reinterpret_cast<uint4*>(pg + o) = z4;
+        }
         uint64_t row0 = 0, row1 = 0;
         // two passes of kTokIlp tokens: quantize side by side, then store
 #pragma unroll
         for (int pass = 0; pass < kTokLoad / kTokIlp; ++pass) {
             const int base_u = u0 + wave + pass * kTokIlp * kQuantWaves;
-            if (u0 + pass * kTokIlp * kQuantWaves >= u1) break;  // uniform: no token of this pass in the page
+            if (base_u >= u1) break;  // wave-uniform: no token of this wave left in the page
             uint32_t ksz[kTokIlp], kc0[kTokIlp], kc1[kTokIlp], vsz[kTokIlp], vc0[kTokIlp], vc1[kTokIlp];
 #pragma unroll
             for (int i = 0; i < kTokIlp; ++i) {
-                quant_pair(kx[pass * kTokIlp + i], (1 << kb) - 1, ksz[i], kc0[i], kc1[i]);
-                quant_pair(vx[pass * kTokIlp + i], (1 << vb) - 1, vsz[i], vc0[i], vc1[i]);
-            }
-            if (pass == 0) {
-                __syncthreads();  // the page ID is in LDS
-                const int id = s_job.id;
-                page_ok = (unsigned)id < (unsigned)a.num_pages;  // never write outside the pool
-                pg = a.pool + (long long)(page_ok ? id : 0) * page_bytes;
-                if (page_ok && fresh) {
-                    // A fresh page reads as zero wherever no token lies: zero the token
-                    // slots from u1 on in every per-token segment and the page tail.
-                    // These bytes are disjoint from the ones the tokens write (V code
-                    // rows are written whole, zeros included), so the stores need no
-                    // ordering among themselves.
-                    const int s_end = u1 - p * TT, nfill = TT - s_end;
-                    const uint4 z4 = make_uint4(0, 0, 0, 0);
-                    for (int i = tid; i < (kb + 1) * nfill; i += kCommitThreads) {
-                        const int c = i / nfill, sl = s_end + (i - c * nfill);  // K chunks (kb per token), then K meta
-                        uint8_t* dst = c < kb ? pg + off_kc + (c * TT + sl) * 16 : pg + off_km + sl * 16;
-                        *reinterpret_cast<uint4*>(dst) = z4;
-                    }
-                    for (int i = tid; i < (kNG + 2) * nfill; i += kCommitThreads) {
-                        const int g = i / nfill, sl = s_end + (i - g * nfill);  // V meta groups, score, pos
-                        uint8_t* dst = g < kNG ? pg + off_vm + (g * TT + sl) * 4
-                                               : pg + (g == kNG ? a.off_score[sec] : a.off_pos[sec]) + sl * 4;
-                        *reinterpret_cast<uint32_t*>(dst) = 0;
-                    }
-                    for (long long o = a.off_pos[sec] + (long long)TT * 4 + tid * 16; o < page_bytes;
-                         o += kCommitThreads * 16)
-                        *reinterpret_cast<uint4*>(pg + o) = z4;
+                if (base_u + i * kQuantWaves < u1) {
+                    quant_pair(kx[pass * kTokIlp + i], (1 << kb) - 1, ksz[i], kc0[i], kc1[i]);
+                    quant_pair(vx[pass * kTokIlp + i], (1 << vb) - 1, vsz[i], vc0[i], vc1[i]);
                 }
             }
 #pragma unroll
@@ -495,12 +639,8 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
         s_rows[wave][lane][1] = row1;
         __syncthreads();
         if (wave == 0 && page_ok) {
-            uint64_t r0 = 0, r1 = 0;
-            if (!fresh) {
-                const uint4 r = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
-                r0 = ((uint64_t)r.y << 32) | r.x;
-                r1 = ((uint64_t)r.w << 32) | r.z;
-            }
+            uint64_t r0 = ((uint64_t)vold.y << 32) | vold.x;
+            uint64_t r1 = ((uint64_t)vold.w << 32) | vold.z;
 #pragma unroll
             for (int w = 0; w < kQuantWaves; ++w) {
                 r0 |= s_rows[w][lane][0];
@@ -509,7 +649,7 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
             *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
                 make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
         }
-        __syncthreads();  // s_job and s_rows are reused by the next job
+        if (job + (int)gridDim.x < njobs) __syncthreads();  // s_job and s_rows are reused by the next job
     }
 }
 

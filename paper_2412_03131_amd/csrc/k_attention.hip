@@ -12,8 +12,9 @@
 //
 // Lane mapping inside a wave (64 lanes = 4 rows of 16):
 //   key phase    lane = grp*16 + j: token j (and j+16 on 32-token pages),
-//                32-dim group grp.  The lane holds q of its group as fp16
-//                pairs and computes sum(q*code) with v_dot2_f32_f16 on codes
+//                32-dim group grp.  A row holds its group's q as 16 fp16
+//                pairs, one per lane, read by the whole row through DPP
+//                row_newbcast, and computes sum(q*code) with v_dot2 on codes
 //                turned into fp16 denormals (exact, one v_perm or AND per two
 //                codes), then s*sum + z*sum(q) (scale and zero factored out of
 //                the dot product).  A transposed sum over the four rows
@@ -30,6 +31,8 @@
 //                at the centre code) are accumulated per lane and added once.
 // The four waves' (max, sum, acc) states merge through LDS.
 #include <atomic>
+
+#include <utility>
 
 #include "internal.hpp"
 
@@ -104,6 +107,140 @@ __device__ __forceinline__ float dot2_first(half2_t a, uint32_t b)
     float d;
     asm("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(d) : "v"(a), "v"(b));
     return d;
+}
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N-1>)
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>)
+{
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f)
+{
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// ---- key dot products against DPP-broadcast query pairs ----------------------
+// A row holds its group's 16 query pairs one per lane; lane L's pair reaches
+// the whole row through DPP row_newbcast:L on src0 of v_dot2c_f32_f16
+// (L = 1 .. 15; row_newbcast:0 does not broadcast, so pair 0 is also kept
+// whole in every lane).  The compiler cannot see inside asm, so these
+// sequences keep the hardware's wait-state rules themselves:
+//   - a DPP instruction reads a VGPR at least 2 wait states after a VALU write
+//     of it, and 5 after an EXEC write;
+//   - a VALU instruction reads the result of a dot instruction at least 3
+//     wait states after it, unless it is the same dot opcode reading it as
+//     its accumulator.
+// The steps are volatile asm (kept in the order written), each forms the next
+// code pair one step ahead, and the no-ops below pad the distances where the
+// head count does not.  The query registers are written once, before any page.
+template <int N>
+__device__ __forceinline__ void kwait()
+{
+    if constexpr (N > 0) asm volatile("s_nop %0" ::"n"(N - 1));
+}
+template <int L>
+__device__ __forceinline__ void kdot_bcast(float& c, uint32_t q, uint32_t x)
+{
+    static_assert(L >= 1 && L <= 15, "row_newbcast lane");
+    asm volatile("v_dot2c_f32_f16_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf" : "+v"(c) : "v"(q), "v"(x), "n"(L));
+}
+__device__ __forceinline__ void kdot_first(float& c, half2_t q, uint32_t x)
+{
+    asm volatile("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(c) : "v"(q), "v"(x));
+}
+__device__ __forceinline__ uint32_t kperm(uint32_t hi, uint32_t lo, uint32_t sel)
+{
+    uint32_t x;
+    asm volatile("v_perm_b32 %0, %1, %2, %3" : "=v"(x) : "v"(hi), "v"(lo), "s"(sel));
+    return x;
+}
+__device__ __forceinline__ uint32_t kand(uint32_t v, uint32_t mask)
+{
+    uint32_t x;
+    asm volatile("v_and_b32 %0, %2, %1" : "=v"(x) : "v"(v), "s"(mask));
+    return x;
+}
+__device__ __forceinline__ void kzero(float& c) { asm volatile("v_mov_b32 %0, 0" : "=v"(c)); }
+
+constexpr int kMax0(int a) { return a > 0 ? a : 0; }
+
+// End of a sequence: three wait states, then each result passes through an
+// empty asm, so no instruction the compiler schedules can read a result before
+// the wait (the wait itself only orders against other volatile asm).
+template <int GQ>
+__device__ __forceinline__ void kdone(float (&d)[GQ])
+{
+    kwait<3>();
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh) asm volatile("" : "+v"(d[hh]));
+}
+
+// perm_pair selector for pair a of an 8-dim block (see perm_pair)
+constexpr uint32_t kPermSel(int a) { return 0x0C000C00u | ((uint32_t)(4 + a) << 16) | (uint32_t)a; }
+
+// K8 token: d[h] = sum over the group's 16 pairs of q_h . codes (w = the 32
+// code bytes of the token's group).  Step i forms pair i+1 and adds pair i.
+// Between the same head's steps i-1 and i lie GQ-1 dots and the next pair's
+// v_perm (none in the last step); step 1 follows the first products of
+// another dot opcode (3 wait states), later steps the same one (the DPP rule,
+// 2).  The code pair of step i was formed before GQ dots of step i-1.
+template <int GQ>
+__device__ __forceinline__ void kdots_k8(const uint32_t (&w)[8], const uint32_t (&qr)[GQ], const half2_t (&q0)[GQ],
+                                         float (&d)[GQ])
+{
+    kwait<5>();
+    uint32_t x = kperm(w[1], w[0], kPermSel(0));
+    static_for<16>([&](auto i) {
+        uint32_t xn = 0;
+        if constexpr (i < 15) xn = kperm(w[2 * ((i + 1) / 4) + 1], w[2 * ((i + 1) / 4)], kPermSel((i + 1) % 4));
+        if constexpr (i > 0) {
+            constexpr int perm = i < 15 ? 1 : 0;
+            constexpr int need = i == 1 ? 3 : 2;
+            kwait<kMax0(need - (GQ - 1 + perm))>();
+        }
+#pragma unroll
+        for (int hh = 0; hh < GQ; ++hh) {
+            if constexpr (i == 0) kdot_first(d[hh], q0[hh], x);
+            else kdot_bcast<(i > 0 ? i : 1)>(d[hh], qr[hh], x);
+        }
+        x = xn;
+    });
+    kdone<GQ>(d);
+}
+
+// K4 token: pairs 4m + a (a = 0..3) of dword w[m] are its nibbles (a, a+4)
+// (a even) or 16 * nibbles (a, a+4) (a odd); even pairs sum into dlo, odd ones
+// into dhi (scaled by 1/16 afterwards).  The two chains alternate, so a
+// chain's steps are 2*GQ-1 dots and two AND steps apart (one in the last
+// step); a code pair is formed GQ dots and one AND step before its use.
+template <int GQ>
+__device__ __forceinline__ void kdots_k4(const uint32_t (&w)[4], const uint32_t (&qr)[GQ], const half2_t (&q0)[GQ],
+                                         float (&dlo)[GQ], float (&dhi)[GQ])
+{
+    kwait<5>();
+    uint32_t w8[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) w8[m] = w[m] >> 8;
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh) kzero(dhi[hh]);
+    uint32_t x = kand(w[0], 0x000F000Fu);
+    static_for<16>([&](auto i) {
+        constexpr int n = i + 1, m = n / 4, a = n % 4;
+        uint32_t xn = 0;
+        if constexpr (i < 15) xn = kand(a >= 2 ? w8[m] : w[m], (a & 1) ? 0x00F000F0u : 0x000F000Fu);
+        if constexpr (i > 0) kwait<kMax0(2 - (GQ + (i < 15 ? 1 : 0)))>();
+#pragma unroll
+        for (int hh = 0; hh < GQ; ++hh) {
+            if constexpr (i == 0) kdot_first(dlo[hh], q0[hh], x);
+            else if constexpr (i % 2 == 0) kdot_bcast<(i > 0 ? i : 1)>(dlo[hh], qr[hh], x);
+            else kdot_bcast<i>(dhi[hh], qr[hh], x);
+        }
+        x = xn;
+    });
+    kwait<3>();
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh) asm volatile("" : "+v"(dlo[hh]), "+v"(dhi[hh]));
 }
 
 constexpr float kTwo24 = 16777216.0f;
@@ -204,7 +341,8 @@ constexpr float kSlack = 8.0f;
 // 2^-12 of the group's value range per unit of softmax weight.  2-bit codes in
 // odd crumbs are extracted as 4*code, and their c carries w/4.
 template <int GQ, int NT>
-__device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, const half2_t (&q2)[GQ][16],
+__device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, const uint32_t (&qr)[GQ],
+                                        const half2_t (&q0)[GQ],
                                         const float (&qsum)[GQ], float sl2, int n_valid, int lane,
                                         uint32_t* coef_row)
 {
@@ -219,36 +357,13 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         const uint32_t km = tk ? r.m1 : r.m0;
         const float ks = h2f(km & 0xffffu) * (kTwo24 * sl2), kz = h2f(km >> 16) * sl2;
         float dlo[GQ], dhi[GQ];
-        if (NT == 1) {
-            // K8: two dwords (8 dims) -> four (d, d+4) pairs, one v_perm each
+        if constexpr (NT == 1) {
             const uint32_t w[8] = {r.k0.x, r.k0.y, r.k0.z, r.k0.w, r.k1.x, r.k1.y, r.k1.z, r.k1.w};
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-#pragma unroll
-                for (int a2 = 0; a2 < 4; ++a2) {
-                    const uint32_t x = perm_pair(w[2 * m + 1], w[2 * m], a2);
-#pragma unroll
-                    for (int hh = 0; hh < GQ; ++hh)
-                        dlo[hh] = m + a2 == 0 ? dot2_first(q2[hh][0], x) : dot2(q2[hh][4 * m + a2], x, dlo[hh]);
-                }
-            }
+            kdots_k8<GQ>(w, qr, q0, dlo);
         } else {
-            // K4: one dword (8 dims); nibbles a and a+4 sit in the two halves
             const uint4 kk = tk ? r.k1 : r.k0;
             const uint32_t w[4] = {kk.x, kk.y, kk.z, kk.w};
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const uint32_t v = w[m], v8 = w[m] >> 8;
-                const uint32_t x0 = v & 0x000F000Fu, x1 = v & 0x00F000F0u;
-                const uint32_t x2 = v8 & 0x000F000Fu, x3 = v8 & 0x00F000F0u;
-#pragma unroll
-                for (int hh = 0; hh < GQ; ++hh) {
-                    dlo[hh] = m == 0 ? dot2_first(q2[hh][0], x0) : dot2(q2[hh][4 * m + 0], x0, dlo[hh]);
-                    dhi[hh] = m == 0 ? dot2_first(q2[hh][1], x1) : dot2(q2[hh][4 * m + 1], x1, dhi[hh]);
-                    dlo[hh] = dot2(q2[hh][4 * m + 2], x2, dlo[hh]);
-                    dhi[hh] = dot2(q2[hh][4 * m + 3], x3, dhi[hh]);
-                }
-            }
+            kdots_k4<GQ>(w, qr, q0, dlo, dhi);
         }
         float part[4 * NS];
 #pragma unroll
@@ -537,27 +652,26 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         id0 = id_at(2);
     }
 
-    // q of this lane's group as fp16 pairs (d, d+4) of each 8-dim block (one
-    // v_perm each), and its sum (v_dot2 with (1, 1))
-    half2_t q2[GQ][16];
+    // q of this lane's group as fp16 pairs (d, d+4) of each 8-dim block, one
+    // pair per lane: lane k of a row holds pair k (dims 8(k/4) + k%4 and +4),
+    // read by the others through DPP, and every lane holds pair 0 (dims 0, 4);
+    // qsum = the group's sum (row sum)
+    uint32_t qr[GQ];
+    half2_t q0[GQ];
     float qsum[GQ];
     constexpr uint32_t kOnes = 0x3C003C00u;  // fp16 pair (1, 1)
+    {
+        const int qm = (lane & 15) >> 2, qa = lane & 3;
+        const uint32_t sel = (qa & 1) ? 0x07060302u : 0x05040100u;
 #pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) {
-        const uint4* qp = reinterpret_cast<const uint4*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
-        float sq = 0.f;
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            const uint4 v = qp[m];  // dims 8m .. 8m+7 as four fp16 pairs (d, d+1)
-            const uint32_t pr[4] = {__builtin_amdgcn_perm(v.z, v.x, 0x05040100u), __builtin_amdgcn_perm(v.z, v.x, 0x07060302u),
-                                    __builtin_amdgcn_perm(v.w, v.y, 0x05040100u), __builtin_amdgcn_perm(v.w, v.y, 0x07060302u)};
-#pragma unroll
-            for (int a2 = 0; a2 < 4; ++a2) {
-                q2[hh][4 * m + a2] = __builtin_bit_cast(half2_t, pr[a2]);
-                sq = dot2(q2[hh][4 * m + a2], kOnes, sq);
-            }
+        for (int hh = 0; hh < GQ; ++hh) {
+            const uint4* qp = reinterpret_cast<const uint4*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
+            const uint4 v = qp[qm];  // dims 8qm .. 8qm+7 as four fp16 pairs (d, d+1)
+            qr[hh] = (qa & 2) ? __builtin_amdgcn_perm(v.w, v.y, sel) : __builtin_amdgcn_perm(v.z, v.x, sel);
+            const uint4 v0 = qp[0];
+            q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(v0.z, v0.x, 0x05040100u));
+            qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f));
         }
-        qsum[hh] = sq;
     }
 
     WaveState<GQ> st;
@@ -580,12 +694,12 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
         if (i >= nmine || !ok) return;
         const int p = page_of(i);
-        do_page<GQ, 1>(st, r, q2, qsum, sl2, ti.len_hi - p * kTHi, lane, coef_row);
+        do_page<GQ, 1>(st, r, qr, q0, qsum, sl2, ti.len_hi - p * kTHi, lane, coef_row);
     };
     auto compute_lo = [&](int i, const PageRaw& r, bool ok) {
         if (i >= nmine || !ok) return;
         const int p = page_of(i);
-        do_page<GQ, 2>(st, r, q2, qsum, sl2, ti.len_lo - (p - ph) * kTLo, lane, coef_row);
+        do_page<GQ, 2>(st, r, qr, q0, qsum, sl2, ti.len_lo - (p - ph) * kTLo, lane, coef_row);
     };
     // page i computes from buffer i % 2 (swapped after an odd number of high
     // pages) while page i+1 is in flight; the ID of page i is loaded when page
@@ -890,8 +1004,11 @@ static const void* decode_kernel_for(int gq)
     }
 }
 
-// Workgroups of attn_decode<gq> the device holds at once (the balanced mode's
-// share count), cached per device; at most kAttnMaxWorkers.
+// Workgroups of attn_decode<gq> the device holds at once, at most two per CU
+// (the balanced mode's share count), cached per device; at most
+// kAttnMaxWorkers.  A third workgroup per CU (three waves per SIMD, where the
+// registers allow it) measured slower: the page loop is bound by VALU issue,
+// and more shares only split more tables.
 static int balanced_workers(int gq)
 {
     constexpr int kDevs = 64;
@@ -905,6 +1022,7 @@ static int balanced_workers(int gq)
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel_for(gq), kAttnThreads, 0) != hipSuccess ||
         per_cu < 1)
         per_cu = 1;
+    per_cu = per_cu < 2 ? per_cu : 2;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 1;
     w = per_cu * cus;
     w = w < kAttnMaxWorkers ? w : kAttnMaxWorkers;

@@ -216,6 +216,36 @@ def test_attention_edge_cases():
     assert np.abs(out[1, 4:8] - vh1).max() <= 1e-6
 
 
+@pytest.mark.parametrize("Hkv,Hq", [(4, 4), (2, 4), (1, 3), (2, 8), (1, 5), (2, 12), (1, 7), (1, 8)])
+def test_attention_every_group_size(Hkv, Hq):
+    """Query heads per KV head 1 .. 8 (each group size is its own kernel), on
+    high-only, low-only and mixed tables with ragged tails."""
+    rng = np.random.default_rng(23 + Hq)
+    B = 3
+    new_len = np.array([16, 75, 230], np.int32)
+    n = int(new_len.sum())
+    k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    score = rng.random((n, Hkv)).astype(np.float32)
+    quota = np.zeros((B, Hkv, 2), np.int32)
+    quota[0, :] = [16, 0]
+    quota[1, :] = [0, 75]
+    quota[2, :] = [101, 90]
+    Lo, Ld = layouts(max_seq_len=256)
+    npages = B * Hkv * 20
+    oc = orc.Cache(Lo, npages, B, Hkv, ring=rng.permutation(npages))
+    orc.quantize_append(oc, new_len, k, v, score, quota=quota)
+    q = rng.standard_normal((B, Hq, 128)).astype(np.float16).view(np.uint16)
+    ref, ref_lse = orc.attention(oc, q, SCALE)
+    dc = dev_cache_from_oracle(Ld, oc)
+    for splits in (1, -1):
+        print("case: group size %d splits=%d" % (Hq // Hkv, splits), flush=True)
+        out, lse = dk.decode_attention(dc, t(q), SCALE, num_splits=splits)
+        torch.cuda.synchronize()
+        assert_attention_close(out.cpu().numpy(), lse.cpu().numpy(), ref, ref_lse,
+                               "group size %d splits=%d" % (Hq // Hkv, splits))
+
+
 # ------------------------------------------------------- compaction/alloc --
 def test_compaction_worked_example_on_gpu():
     import json

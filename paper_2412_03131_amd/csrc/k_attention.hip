@@ -527,12 +527,12 @@ struct TableInfo {
     long long units;
 };
 
-__device__ __forceinline__ TableInfo table_info(const AttnArgs& a, int t)
+__device__ __forceinline__ TableInfo table_info_of(const AttnArgs& a, int len_hi, int len_lo)
 {
     TableInfo ti;
     const int P = a.p_max;
-    ti.len_hi = a.len[2 * t];
-    ti.len_lo = a.len[2 * t + 1];
+    ti.len_hi = len_hi;
+    ti.len_lo = len_lo;
     // page counts from the section lengths, clamped to the table width
     int ph = (ti.len_hi + kTHi - 1) / kTHi;
     int pl = (ti.len_lo + kTLo - 1) / kTLo;
@@ -542,6 +542,10 @@ __device__ __forceinline__ TableInfo table_info(const AttnArgs& a, int t)
     ti.np = ph + pl;
     ti.units = (long long)kHighUnits * ph + (long long)kLowUnits * pl;
     return ti;
+}
+__device__ __forceinline__ TableInfo table_info(const AttnArgs& a, int t)
+{
+    return table_info_of(a, a.len[2 * t], a.len[2 * t + 1]);
 }
 
 // first page whose first unit is >= x (np if none)
@@ -642,6 +646,22 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         const int ic = i < i_last ? i : i_last;
         load_page(r, a.pool + (in_pool ? id : 0) * page_bytes, page_of(ic) < ph, lane);
     };
+    // The query loads go first: they depend only on the table, so their
+    // latency overlaps the page-ID -> page chain below.  Lane k of a row loads
+    // the two dwords of its pair k (dims 8(k/4) + k%4 and +4: dwords x, z or
+    // y, w of the 8-dim block) and the two of pair 0.
+    const int qm = (lane & 15) >> 2, qa = lane & 3;
+    uint32_t qraw[GQ][4];
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh) {
+        const uint32_t* qd = reinterpret_cast<const uint32_t*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
+        const int o = 4 * qm + ((qa & 2) ? 1 : 0);
+        qraw[hh][0] = qd[o];
+        qraw[hh][1] = qd[o + 2];
+        qraw[hh][2] = qd[0];
+        qraw[hh][3] = qd[2];
+    }
+
     PageRaw buf0, buf1;
     bool ok0 = false, ok1 = false;
     int id0 = 0, id1 = 0;
@@ -652,24 +672,19 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         id0 = id_at(2);
     }
 
-    // q of this lane's group as fp16 pairs (d, d+4) of each 8-dim block, one
-    // pair per lane: lane k of a row holds pair k (dims 8(k/4) + k%4 and +4),
-    // read by the others through DPP, and every lane holds pair 0 (dims 0, 4);
-    // qsum = the group's sum (row sum)
+    // q of this lane's group as fp16 pairs (d, d+4), one pair per lane (read
+    // by the others through DPP), pair 0 (dims 0, 4) in every lane; qsum = the
+    // group's sum (row sum)
     uint32_t qr[GQ];
     half2_t q0[GQ];
     float qsum[GQ];
     constexpr uint32_t kOnes = 0x3C003C00u;  // fp16 pair (1, 1)
     {
-        const int qm = (lane & 15) >> 2, qa = lane & 3;
         const uint32_t sel = (qa & 1) ? 0x07060302u : 0x05040100u;
 #pragma unroll
         for (int hh = 0; hh < GQ; ++hh) {
-            const uint4* qp = reinterpret_cast<const uint4*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
-            const uint4 v = qp[qm];  // dims 8qm .. 8qm+7 as four fp16 pairs (d, d+1)
-            qr[hh] = (qa & 2) ? __builtin_amdgcn_perm(v.w, v.y, sel) : __builtin_amdgcn_perm(v.z, v.x, sel);
-            const uint4 v0 = qp[0];
-            q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(v0.z, v0.x, 0x05040100u));
+            qr[hh] = __builtin_amdgcn_perm(qraw[hh][1], qraw[hh][0], sel);
+            q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(qraw[hh][3], qraw[hh][2], 0x05040100u));
             qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f));
         }
     }
@@ -808,13 +823,107 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
 //    partial state to slot k + t (distinct for every (share, table) pair met
 //    in this walk) and attn_merge combines them.
 // ---------------------------------------------------------------------------
+// Table of rank j when the tables are ordered by decreasing work units
+// (bucketed into 1024 bins, ties by index): workgroups are dispatched in
+// index order and two share a CU for the whole launch, so taking the tables
+// longest first spreads the long ones over the CUs and starts them first
+// (longest-processing-time-first order).  Every workgroup derives the same
+// order from the section lengths; wave 0 does it alone (wave-level scans, no
+// workgroup barrier until the result).  Beyond kRankPer tables per lane the
+// order is the identity.
+constexpr int kKeep = 8;     // tables per thread whose units stay in registers (balanced mode)
+constexpr int kRankPer = 16;  // tables per lane of the ranking wave
+
+template <int GQ>
+__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& sh, int T, int j)
+{
+    constexpr int kBins = 1024;
+    const int per = (T + kWave - 1) / kWave;
+    if (per > kRankPer) return j;
+    static_assert(sizeof(sh.coef) >= kBins * sizeof(int), "histogram lives in the weight LDS");
+    if (threadIdx.x < kWave) {
+        int* hist = reinterpret_cast<int*>(&sh.coef);  // free until the page loop
+        const int lane = threadIdx.x;
+        const int t0 = lane * per, t1 = t0 + per < T ? t0 + per : T;
+        int shift = 0;
+        while (((kLowUnits * a.p_max) >> shift) >= kBins) ++shift;
+        int lh[kRankPer], ll[kRankPer], bin[kRankPer];
+#pragma unroll
+        for (int i = 0; i < kRankPer; ++i) {
+            const int tc = t0 + i < T ? t0 + i : T - 1;
+            lh[i] = i < per ? a.len[2 * tc] : 0;
+            ll[i] = i < per ? a.len[2 * tc + 1] : 0;
+        }
+        static_assert(kBins == 16 * kWave, "sixteen bins per lane");
+#pragma unroll
+        for (int q = 0; q < 16; q += 4) *reinterpret_cast<int4*>(hist + 16 * lane + q) = make_int4(0, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < kRankPer; ++i) {
+            bin[i] = -1;
+            if (t0 + i < t1) {
+                const long long u = table_info_of(a, lh[i], ll[i]).units >> shift;
+                bin[i] = kBins - 1 - (int)(u < kBins - 1 ? u : kBins - 1);  // bin 0 holds the longest
+                atomicAdd(&hist[bin[i]], 1);
+            }
+        }
+        // (one wave's LDS operations complete in order)
+        int c16[16], s16 = 0;
+#pragma unroll
+        for (int q = 0; q < 16; q += 4) {
+            const int4 v = *reinterpret_cast<const int4*>(hist + 16 * lane + q);
+            c16[q] = v.x; c16[q + 1] = v.y; c16[q + 2] = v.z; c16[q + 3] = v.w;
+        }
+#pragma unroll
+        for (int q = 0; q < 16; ++q) s16 += c16[q];
+        const int incl = wave_incl_scan(s16);
+        int at = incl - s16, b = 0, r = 0;
+        bool found = false;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            if (!found && at <= j && j < at + c16[q]) {
+                found = true;
+                b = 16 * lane + q;
+                r = j - at;
+            }
+            at += c16[q];
+        }
+        const unsigned long long fm = __builtin_amdgcn_ballot_w64(found);  // exactly one lane (j < T)
+        const int src = fm ? __builtin_ctzll(fm) : 0;
+        b = __builtin_amdgcn_readlane(b, src);
+        r = __builtin_amdgcn_readlane(r, src);
+        // the r-th table (by index) of bin b
+        int cnt = 0;
+#pragma unroll
+        for (int i = 0; i < kRankPer; ++i) cnt += bin[i] == b;
+        int before = wave_incl_scan(cnt) - cnt, t = 0;
+        found = false;
+#pragma unroll
+        for (int i = 0; i < kRankPer; ++i) {
+            if (bin[i] == b) {
+                if (before == r) {
+                    found = true;
+                    t = t0 + i;
+                }
+                ++before;
+            }
+        }
+        const unsigned long long fm2 = __builtin_amdgcn_ballot_w64(found);
+        const int src2 = fm2 ? __builtin_ctzll(fm2) : 0;
+        const int tr = __builtin_amdgcn_readlane(t, src2);  // read with every lane active
+        if (lane == 0) sh.t_first = tr;
+    }
+    __syncthreads();
+    return sh.t_first;  // (not written again in this mode)
+}
+
 template <int GQ>
 __global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
 {
     __shared__ AttnShared<GQ> sh;
     const int T = a.B * a.Hkv;
     if (a.splits > 0) {
-        const int t = blockIdx.x / a.splits, c = blockIdx.x - t * a.splits;
+        const int j = blockIdx.x / a.splits, c = blockIdx.x - j * a.splits;
+        const int t = longest_first<GQ>(a, sh, T, j);
         const TableInfo ti = table_info(a, t);
         const int n = ti.np < a.splits ? ti.np : a.splits;
         if (n == 0) {
@@ -832,13 +941,22 @@ __global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
     const int per = (T + kAttnThreads - 1) / kAttnThreads;
     const int t0 = threadIdx.x * per;
     const int t1 = t0 + per < T ? t0 + per : T;
-    constexpr int kKeep = 8;  // units of up to kKeep tables stay in registers
     long long units[kKeep];
     long long mine = 0;
+    {
+        // all loads first (clamped to a valid table), then the units
+        int lh[kKeep], ll[kKeep];
 #pragma unroll
-    for (int i = 0; i < kKeep; ++i) {
-        units[i] = t0 + i < t1 ? table_info(a, t0 + i).units : 0;
-        mine += units[i];
+        for (int i = 0; i < kKeep; ++i) {
+            const int tc = t0 + i < T ? t0 + i : T - 1;
+            lh[i] = a.len[2 * tc];
+            ll[i] = a.len[2 * tc + 1];
+        }
+#pragma unroll
+        for (int i = 0; i < kKeep; ++i) {
+            units[i] = t0 + i < t1 ? table_info_of(a, lh[i], ll[i]).units : 0;
+            mine += units[i];
+        }
     }
     for (int t = t0 + kKeep; t < t1; ++t) mine += table_info(a, t).units;
     long long total;

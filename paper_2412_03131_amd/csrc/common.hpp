@@ -103,6 +103,16 @@ __device__ __forceinline__ uint32_t wave_or_u32(uint32_t x)  // result in lane 6
     return (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
 }
 
+// Makes one wave's LDS writes visible to its other lanes' later reads (the
+// wave's LDS operations execute in order; this keeps the compiler from
+// reordering them and states the synchronisation).
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __device__ __forceinline__ int wave_index() { return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave); }
 
 template <typename TInt>

@@ -857,6 +857,7 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
         static_assert(kBins == 16 * kWave, "sixteen bins per lane");
 #pragma unroll
         for (int q = 0; q < 16; q += 4) *reinterpret_cast<int4*>(hist + 16 * lane + q) = make_int4(0, 0, 0, 0);
+        wave_lds_sync();
 #pragma unroll
         for (int i = 0; i < kRankPer; ++i) {
             bin[i] = -1;
@@ -866,7 +867,7 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
                 atomicAdd(&hist[bin[i]], 1);
             }
         }
-        // (one wave's LDS operations complete in order)
+        wave_lds_sync();
         int c16[16], s16 = 0;
 #pragma unroll
         for (int q = 0; q < 16; q += 4) {

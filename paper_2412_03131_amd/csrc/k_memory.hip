@@ -34,9 +34,10 @@ __device__ __forceinline__ uint32_t score_key(float s)
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // ---------------------------------------------------------------------------
-// append_classify: grid (Hkv, B), block 1024
+// append_classify: grid B * Hkv (table t = b * Hkv + h), block 512
 // ---------------------------------------------------------------------------
-constexpr int kClsThreads = 1024;
+constexpr int kClsThreads = 512;
+static_assert(kClsThreads >= 2 * kWave, "two waves scan the digit histograms");
 constexpr int kClsPer = 8;                       // tokens per thread in one tile
 constexpr int kClsTile = kClsThreads * kClsPer;  // the first tile's scores stay in registers
 constexpr uint32_t kOffSat = 1u << 30;           // row offsets saturate here (above any total_new)
@@ -65,9 +66,9 @@ struct Cuts {
 
 __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
 {
-    const int h = blockIdx.x, b = blockIdx.y;
     const int H = a.Hkv;
-    const int t = b * H + h;
+    const int t = blockIdx.x;
+    const int b = t / H, h = t - b * H;
     const int tid = threadIdx.x;
     __shared__ long long s_scan[kClsThreads / kWave];
     __shared__ int s_hist[2][2][256];  // [buffer][cut][digit]
@@ -78,10 +79,7 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
         a.flags->head_old = a.ring_ptr[0];
         a.flags->tail_old = a.ring_ptr[1];
     }
-    if (tid < 256) {
-        s_hist[0][0][tid] = 0;
-        s_hist[0][1][tid] = 0;
-    }
+    for (int i = tid; i < 512; i += kClsThreads) (&s_hist[0][0][0])[i] = 0;
     // row offset of this sequence: sum of new_len over lower sequences (wave 0).
     // Entries are clamped to [0, kOffSat] and the sum saturates: a call with an
     // entry outside [0, max_new] fails anyway (that table flags itself).
@@ -175,7 +173,7 @@ __global__ __launch_bounds__(kClsThreads) void append_classify(AppendArgs a)
                     for (int s2 = 0; s2 < 2; ++s2)
                         if (kk[s2] > 0 && (key & mask) == prefix[s2]) atomicAdd(&hist[s2 * 256 + dig], 1);
                 }
-                if (tid < 512) (&s_hist[(pass + 1) & 1][0][0])[tid] = 0;  // the next digit's buffer
+                for (int i = tid; i < 512; i += kClsThreads) (&s_hist[(pass + 1) & 1][0][0])[i] = 0;  // the next digit's buffer
                 __syncthreads();
                 if (tid < 2 * kWave) {  // two waves find the cut bins with a scan from the top
                     const int s2 = tid / kWave, l = tid & (kWave - 1);
@@ -846,7 +844,7 @@ __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
 // ---------------------------------------------------------------------------
 hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st)
 {
-    hipLaunchKernelGGL(append_classify, dim3(a.Hkv, a.B), dim3(kClsThreads), 0, st, a);
+    hipLaunchKernelGGL(append_classify, dim3((unsigned)(a.Hkv * a.B)), dim3(kClsThreads), 0, st, a);
     hipLaunchKernelGGL(append_commit, dim3(grid_quant), dim3(kCommitThreads), 0, st, a);
     return hipGetLastError();
 }

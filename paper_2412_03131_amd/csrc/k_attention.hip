@@ -162,6 +162,27 @@ __device__ __forceinline__ uint32_t kand(uint32_t v, uint32_t mask)
     return x;
 }
 __device__ __forceinline__ void kzero(float& c) { asm volatile("v_mov_b32 %0, 0" : "=v"(c)); }
+// The next code pair's v_perm / v_and and the first head's dot in one asm
+// statement (the compiler pads between separate asm statements).
+template <int L>
+__device__ __forceinline__ uint32_t kperm_dot(uint32_t hi, uint32_t lo, uint32_t sel, float& c, uint32_t q,
+                                              uint32_t x)
+{
+    uint32_t xn;
+    asm volatile("v_perm_b32 %0, %2, %3, %4\n\tv_dot2c_f32_f16_dpp %1, %5, %6 row_newbcast:%7 row_mask:0xf bank_mask:0xf"
+                 : "=&v"(xn), "+v"(c)
+                 : "v"(hi), "v"(lo), "s"(sel), "v"(q), "v"(x), "n"(L));
+    return xn;
+}
+template <int L>
+__device__ __forceinline__ uint32_t kand_dot(uint32_t v, uint32_t mask, float& c, uint32_t q, uint32_t x)
+{
+    uint32_t xn;
+    asm volatile("v_and_b32 %0, %3, %2\n\tv_dot2c_f32_f16_dpp %1, %4, %5 row_newbcast:%6 row_mask:0xf bank_mask:0xf"
+                 : "=&v"(xn), "+v"(c)
+                 : "v"(v), "s"(mask), "v"(q), "v"(x), "n"(L));
+    return xn;
+}
 
 constexpr int kMax0(int a) { return a > 0 ? a : 0; }
 
@@ -192,17 +213,23 @@ __device__ __forceinline__ void kdots_k8(const uint32_t (&w)[8], const uint32_t 
     kwait<5>();
     uint32_t x = kperm(w[1], w[0], kPermSel(0));
     static_for<16>([&](auto i) {
+        constexpr int perm = i < 15 ? 1 : 0;
+        constexpr int pad = i > 0 ? kMax0((i == 1 ? 3 : 2) - (GQ - 1 + perm)) : 0;
+        constexpr int m1 = (i + 1) / 4, a1 = (i + 1) % 4;
         uint32_t xn = 0;
-        if constexpr (i < 15) xn = kperm(w[2 * ((i + 1) / 4) + 1], w[2 * ((i + 1) / 4)], kPermSel((i + 1) % 4));
-        if constexpr (i > 0) {
-            constexpr int perm = i < 15 ? 1 : 0;
-            constexpr int need = i == 1 ? 3 : 2;
-            kwait<kMax0(need - (GQ - 1 + perm))>();
-        }
+        if constexpr (i > 0 && i < 15 && pad == 0) {
+            // next pair and head 0 in one statement, then the other heads
+            xn = kperm_dot<(i > 0 ? i : 1)>(w[2 * m1 + 1], w[2 * m1], kPermSel(a1), d[0], qr[0], x);
 #pragma unroll
-        for (int hh = 0; hh < GQ; ++hh) {
-            if constexpr (i == 0) kdot_first(d[hh], q0[hh], x);
-            else kdot_bcast<(i > 0 ? i : 1)>(d[hh], qr[hh], x);
+            for (int hh = 1; hh < GQ; ++hh) kdot_bcast<(i > 0 ? i : 1)>(d[hh], qr[hh], x);
+        } else {
+            if constexpr (i < 15) xn = kperm(w[2 * m1 + 1], w[2 * m1], kPermSel(a1));
+            kwait<pad>();
+#pragma unroll
+            for (int hh = 0; hh < GQ; ++hh) {
+                if constexpr (i == 0) kdot_first(d[hh], q0[hh], x);
+                else kdot_bcast<(i > 0 ? i : 1)>(d[hh], qr[hh], x);
+            }
         }
         x = xn;
     });
@@ -227,14 +254,23 @@ __device__ __forceinline__ void kdots_k4(const uint32_t (&w)[4], const uint32_t 
     uint32_t x = kand(w[0], 0x000F000Fu);
     static_for<16>([&](auto i) {
         constexpr int n = i + 1, m = n / 4, a = n % 4;
+        constexpr int pad = i > 0 ? kMax0(2 - (GQ + (i < 15 ? 1 : 0))) : 0;
+        constexpr uint32_t mask = (a & 1) ? 0x00F000F0u : 0x000F000Fu;
         uint32_t xn = 0;
-        if constexpr (i < 15) xn = kand(a >= 2 ? w8[m] : w[m], (a & 1) ? 0x00F000F0u : 0x000F000Fu);
-        if constexpr (i > 0) kwait<kMax0(2 - (GQ + (i < 15 ? 1 : 0)))>();
+        if constexpr (i > 0 && i < 15 && pad == 0) {
+            float(&acc)[GQ] = (i % 2 == 0) ? dlo : dhi;
+            xn = kand_dot<(i > 0 ? i : 1)>(a >= 2 ? w8[m] : w[m], mask, acc[0], qr[0], x);
 #pragma unroll
-        for (int hh = 0; hh < GQ; ++hh) {
-            if constexpr (i == 0) kdot_first(dlo[hh], q0[hh], x);
-            else if constexpr (i % 2 == 0) kdot_bcast<(i > 0 ? i : 1)>(dlo[hh], qr[hh], x);
-            else kdot_bcast<i>(dhi[hh], qr[hh], x);
+            for (int hh = 1; hh < GQ; ++hh) kdot_bcast<(i > 0 ? i : 1)>(acc[hh], qr[hh], x);
+        } else {
+            if constexpr (i < 15) xn = kand(a >= 2 ? w8[m] : w[m], mask);
+            kwait<pad>();
+#pragma unroll
+            for (int hh = 0; hh < GQ; ++hh) {
+                if constexpr (i == 0) kdot_first(dlo[hh], q0[hh], x);
+                else if constexpr (i % 2 == 0) kdot_bcast<(i > 0 ? i : 1)>(dlo[hh], qr[hh], x);
+                else kdot_bcast<(i > 0 ? i : 1)>(dhi[hh], qr[hh], x);
+            }
         }
         x = xn;
     });

@@ -46,6 +46,7 @@ constexpr int kPartStride = kD + 2;
 // caller's diffkv_layout).
 constexpr int kOffKcHi = 0, kOffKmHi = 2048, kOffVcHi = 2304, kOffVmHi = 3328;
 constexpr int kOffKcLo = 0, kOffKmLo = 2048, kOffVcLo = 2560, kOffVmLo = 3584;
+constexpr long long kPageBytes = 4352;  // unified page of the supported layout
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
@@ -658,7 +659,7 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     const int ph = ti.ph;
     const float sl2 = a.scale_log2;
     const long long npool = a.num_pages;
-    const long long page_bytes = a.page_bytes;
+    constexpr long long page_bytes = kPageBytes;  // (the layout check guarantees it)
     uint32_t* coef_row = &sh.coef.v[wave][grp * CoefLds<GQ>::kRow];
     const int nmine = pb - pa > wave ? (pb - pa - wave + kAttnWaves - 1) / kAttnWaves : 0;
     const int32_t* trow = a.page_table + (long long)t * P;
@@ -1187,7 +1188,7 @@ static int balanced_workers(int gq)
 
 bool attention_layout_matches(const diffkv_layout* L)
 {
-    return L->off_kcode[0] == kOffKcHi && L->off_kmeta[0] == kOffKmHi && L->off_vcode[0] == kOffVcHi &&
+    return L->page_bytes == kPageBytes && L->off_kcode[0] == kOffKcHi && L->off_kmeta[0] == kOffKmHi && L->off_vcode[0] == kOffVcHi &&
            L->off_vmeta[0] == kOffVmHi && L->off_kcode[1] == kOffKcLo && L->off_kmeta[1] == kOffKmLo &&
            L->off_vcode[1] == kOffVcLo && L->off_vmeta[1] == kOffVmLo;
 }

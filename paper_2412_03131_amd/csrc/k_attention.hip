@@ -295,29 +295,32 @@ struct PageRaw {
     uint32_t m3;   // low: V meta of token j+16
 };
 
-__device__ __forceinline__ uint4 ld16(const uint8_t* p, uint32_t o) { return *reinterpret_cast<const uint4*>(p + o); }
-__device__ __forceinline__ uint32_t ld4(const uint8_t* p, uint32_t o) { return *reinterpret_cast<const uint32_t*>(p + o); }
 
 // Both page types put K chunk c of token j at (c*T + j)*16 with 2 (high) or 1
 // (low) chunks per group, i.e. at 512*g + 16*j (+256) for this lane, and K
 // meta at 2048 + 16*j + 4*g; the V segments differ only in base and the V
 // meta row stride (16 or 32 tokens).
+//
+// The loads go through a buffer resource over the one page (`pg` is uniform):
+// the page address is scalar arithmetic, the per-lane offsets are 32-bit
+// constants of the lane, and the hardware bounds every access by the page size.
 __device__ __forceinline__ void load_page(PageRaw& r, const uint8_t* pg, bool hi, int lane)
 {
     const uint32_t grp = (uint32_t)lane >> 4, jl = (uint32_t)lane & 15;
     static_assert(kOffKcHi == 0 && kOffKcLo == 0 && kOffKmHi == 2048 && kOffKmLo == 2048, "page layout");
+    static_assert(kOffVmLo - kOffVmHi == 256 && kOffVcLo - kOffVcHi == 256, "page layout");
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)pg, 0, (int)kPageBytes, 0x00020000);
     const uint32_t kc = grp * 512 + jl * 16;
     const uint32_t km = 2048 + jl * 16 + grp * 4;
-    const uint8_t* pv = pg + (hi ? kOffVcHi : kOffVcLo);
-    const uint8_t* pm = pg + (hi ? kOffVmHi : kOffVmLo);
+    const int lo = hi ? 0 : 256;  // uniform: V segments of a low page start 256 bytes later
     const uint32_t vm = (hi ? grp * (kTHi * 4) : grp * (kTLo * 4)) + jl * 4;
-    r.k0 = ld16(pg, kc);
-    r.k1 = ld16(pg, kc + 256);
-    r.vr = ld16(pv, (uint32_t)lane * 16);
-    r.m0 = ld4(pg, km);
-    r.m1 = ld4(pg, km + 256);
-    r.m2 = ld4(pm, vm);
-    r.m3 = ld4(pm, hi ? vm : vm + 64);  // high pages: a line already fetched
+    r.k0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, kc, 0, 0));
+    r.k1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, kc + 256, 0, 0));
+    r.vr = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)lane * 16 + kOffVcHi, lo, 0));
+    r.m0 = __builtin_amdgcn_raw_buffer_load_b32(rs, km, 0, 0);
+    r.m1 = __builtin_amdgcn_raw_buffer_load_b32(rs, km + 256, 0, 0);
+    r.m2 = __builtin_amdgcn_raw_buffer_load_b32(rs, vm + kOffVmHi, lo, 0);
+    r.m3 = __builtin_amdgcn_raw_buffer_load_b32(rs, vm + kOffVmHi, lo + (hi ? 0 : 64), 0);  // high pages: a line already fetched
 }
 
 template <int GQ>
@@ -580,9 +583,12 @@ __device__ __forceinline__ TableInfo table_info_of(const AttnArgs& a, int len_hi
     ti.units = (long long)kHighUnits * ph + (long long)kLowUnits * pl;
     return ti;
 }
+// t uniform: the section lengths come through scalar loads (the attention
+// kernels never write them), so everything derived from them stays scalar.
 __device__ __forceinline__ TableInfo table_info(const AttnArgs& a, int t)
 {
-    return table_info_of(a, a.len[2 * t], a.len[2 * t + 1]);
+    const auto* len = (const __attribute__((address_space(4))) int32_t*)(a.len + 2 * (long long)t);
+    return table_info_of(a, len[0], len[1]);
 }
 
 // first page whose first unit is >= x (np if none)
@@ -664,23 +670,28 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     const int nmine = pb - pa > wave ? (pb - pa - wave + kAttnWaves - 1) / kAttnWaves : 0;
     const int32_t* trow = a.page_table + (long long)t * P;
 
-    // Page IDs come from scalar loads (the page table is read-only here), each
-    // fetched three pages before its page is issued.
+    // The wave's pages run in chunks of 64: lane k holds the ID of chunk page
+    // c0 + k (one vector load per chunk), and a page's ID is read into a scalar
+    // register when its loads are issued.  Chunk bounds [c0, c1); past c1 the
+    // index is clamped to the chunk's last page.
     auto page_of = [&](int i) { return pa + wave + kAttnWaves * i; };
     auto slot_of = [&](int p) { return p < ph ? p : P - 1 - (p - ph); };
-    const int i_last = nmine > 0 ? nmine - 1 : 0;
-    auto id_at = [&](int i) {
-        const int ic = i < i_last ? i : i_last;
-        return *(const __attribute__((address_space(4))) int32_t*)(trow + slot_of(page_of(ic)));
+    int c0 = 0, c1 = 0, c_last = 0, ids_v = 0;
+    auto clamp_i = [&](int i) { return i < c_last ? i : c_last; };
+    auto load_ids = [&]() {
+        const int k = c0 + lane;
+        return trow[slot_of(page_of(clamp_i(k)))];
     };
     // Issue the loads of page i into r; ok = page i exists and lies in the pool.
-    // The loads are unconditional (past the last page they re-read it, a cache
-    // hit; an ID outside the pool reads page 0 and is not computed), so the
-    // wait before each page's use counts only the loads issued since.
-    auto issue = [&](int i, int id, PageRaw& r, bool& ok) {
-        const bool in_pool = (unsigned long long)id < (unsigned long long)npool;  // never read outside the pool
-        ok = i < nmine && in_pool;
-        const int ic = i < i_last ? i : i_last;
+    // The loads are unconditional (past the chunk's last page they re-read it,
+    // a cache hit; an ID outside the pool reads page 0 and is not computed), so
+    // the wait before each page's use counts only the loads issued since.
+    const uint32_t npool32 = npool > 0x7fffffffLL ? 0x80000000u : (uint32_t)npool;
+    auto issue = [&](int i, PageRaw& r, bool& ok) {
+        const int ic = clamp_i(i);
+        const int id = __builtin_amdgcn_readlane(ids_v, ic - c0);
+        const bool in_pool = (uint32_t)id < npool32;  // never read outside the pool
+        ok = i < c1 && in_pool;
         load_page(r, a.pool + (in_pool ? id : 0) * page_bytes, page_of(ic) < ph, lane);
     };
     // The query loads go first: they depend only on the table, so their
@@ -701,12 +712,12 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
 
     PageRaw buf0, buf1;
     bool ok0 = false, ok1 = false;
-    int id0 = 0, id1 = 0;
+    // first chunk: its IDs and first page go out beside the query loads
+    c1 = nmine < kWave ? nmine : kWave;
+    c_last = c1 > 0 ? c1 - 1 : 0;
     if (nmine > 0) {
-        id0 = id_at(0);
-        id1 = id_at(1);
-        issue(0, id0, buf0, ok0);
-        id0 = id_at(2);
+        ids_v = load_ids();
+        issue(0, buf0, ok0);
     }
 
     // q of this lane's group as fp16 pairs (d, d+4), one pair per lane (read
@@ -744,18 +755,17 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     // loop to the next.
     const int nhi = ph - pa - wave > 0 ? min(nmine, (ph - pa - wave + kAttnWaves - 1) / kAttnWaves) : 0;
     auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
-        if (i >= nmine || !ok) return;
+        if (i >= c1 || !ok) return;
         const int p = page_of(i);
         do_page<GQ, 1>(st, r, qr, q0, qsum, sl2, ti.len_hi - p * kTHi, lane, coef_row);
     };
     auto compute_lo = [&](int i, const PageRaw& r, bool ok) {
-        if (i >= nmine || !ok) return;
+        if (i >= c1 || !ok) return;
         const int p = page_of(i);
         do_page<GQ, 2>(st, r, qr, q0, qsum, sl2, ti.len_lo - (p - ph) * kTLo, lane, coef_row);
     };
     // page i computes from buffer i % 2 (swapped after an odd number of high
-    // pages) while page i+1 is in flight; the ID of page i is loaded when page
-    // i-2 is issued
+    // pages) while page i+1 is in flight
     // Wave priority follows the pages this wave still has: on a SIMD shared
     // with shorter work, the longest work is served first (longest-first
     // scheduling at the wave level; ties go to the older wave).
@@ -765,38 +775,43 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         else if (rem > 4) __builtin_amdgcn_s_setprio(1);
         else __builtin_amdgcn_s_setprio(0);
     };
-    int i = 0;
-    for (; i + 2 <= nhi; i += 2) {
-        set_prio(nmine - i);
-        issue(i + 1, id1, buf1, ok1);
-        id1 = id_at(i + 3);
-        compute_hi(i, buf0, ok0);
-        issue(i + 2, id0, buf0, ok0);
-        id0 = id_at(i + 4);
-        compute_hi(i + 1, buf1, ok1);
-    }
-    if (i < nhi) {  // one more high page (in buf0); the low pages then start in buf1
-        issue(i + 1, id1, buf1, ok1);
-        id1 = id_at(i + 3);
-        compute_hi(i, buf0, ok0);
-        for (++i; i < nmine; i += 2) {
+    while (c0 < nmine) {
+        const int nh = nhi < c1 ? nhi : c1;  // high pages end (within this chunk)
+        int i = c0;
+        for (; i + 2 <= nh; i += 2) {
             set_prio(nmine - i);
-            issue(i + 1, id0, buf0, ok0);
-            id0 = id_at(i + 3);
-            compute_lo(i, buf1, ok1);
-            issue(i + 2, id1, buf1, ok1);
-            id1 = id_at(i + 4);
-            compute_lo(i + 1, buf0, ok0);
+            issue(i + 1, buf1, ok1);
+            compute_hi(i, buf0, ok0);
+            issue(i + 2, buf0, ok0);
+            compute_hi(i + 1, buf1, ok1);
         }
-    } else {
-        for (; i < nmine; i += 2) {
-            set_prio(nmine - i);
-            issue(i + 1, id1, buf1, ok1);
-            id1 = id_at(i + 3);
-            compute_lo(i, buf0, ok0);
-            issue(i + 2, id0, buf0, ok0);
-            id0 = id_at(i + 4);
-            compute_lo(i + 1, buf1, ok1);
+        if (i < nh) {  // one more high page (in buf0); the low pages then start in buf1
+            issue(i + 1, buf1, ok1);
+            compute_hi(i, buf0, ok0);
+            for (++i; i < c1; i += 2) {
+                set_prio(nmine - i);
+                issue(i + 1, buf0, ok0);
+                compute_lo(i, buf1, ok1);
+                issue(i + 2, buf1, ok1);
+                compute_lo(i + 1, buf0, ok0);
+            }
+        } else {
+            for (; i < c1; i += 2) {
+                set_prio(nmine - i);
+                issue(i + 1, buf1, ok1);
+                compute_lo(i, buf0, ok0);
+                issue(i + 2, buf0, ok0);
+                compute_lo(i + 1, buf1, ok1);
+            }
+        }
+        // next chunk (tables longer than 64 pages per wave): the pipeline
+        // restarts with its IDs and first page
+        c0 = c1;
+        c1 = nmine - c0 < kWave ? nmine : c0 + kWave;
+        c_last = c1 > c0 ? c1 - 1 : c0;
+        if (c0 < nmine) {
+            ids_v = load_ids();
+            issue(c0, buf0, ok0);
         }
     }
 
@@ -961,7 +976,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
     const int T = a.B * a.Hkv;
     if (a.splits > 0) {
         const int j = blockIdx.x / a.splits, c = blockIdx.x - j * a.splits;
-        const int t = longest_first<GQ>(a, sh, T, j);
+        // (uniform: read back from LDS, so the table's loads and addresses stay scalar)
+        const int t = __builtin_amdgcn_readfirstlane(longest_first<GQ>(a, sh, T, j));
         const TableInfo ti = table_info(a, t);
         const int n = ti.np < a.splits ? ti.np : a.splits;
         if (n == 0) {
@@ -1016,8 +1032,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
         u += n;
     }
     __syncthreads();
-    int t = sh.t_first;
-    long long ut = sh.u_first;
+    int t = __builtin_amdgcn_readfirstlane(sh.t_first);
+    long long ut = read_lane<long long>(sh.u_first, 0);
     while (t < T && ut < b_hi) {
         const TableInfo ti = table_info(a, t);
         if (ti.units > 0) {

@@ -608,6 +608,7 @@ struct AttnShared {
     float acc[kAttnWaves][8][kD];
     long long scan[kAttnWaves + 1];
     int t_first;
+    int len_first[2];  // section lengths of t_first (longest-first ranking)
     long long u_first;
 };
 
@@ -882,16 +883,20 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
 // (longest-processing-time-first order).  Every workgroup derives the same
 // order from the section lengths; wave 0 does it alone (wave-level scans, no
 // workgroup barrier until the result).  Beyond kRankPer tables per lane the
-// order is the identity.
+// order is the identity.  *ti gets the table's pages and units, from the
+// lengths the ranking wave already holds.
 constexpr int kKeep = 8;     // tables per thread whose units stay in registers (balanced mode)
 constexpr int kRankPer = 16;  // tables per lane of the ranking wave
 
 template <int GQ>
-__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& sh, int T, int j)
+__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& sh, int T, int j, TableInfo* ti)
 {
     constexpr int kBins = 1024;
     const int per = (T + kWave - 1) / kWave;
-    if (per > kRankPer) return j;
+    if (per > kRankPer) {
+        *ti = table_info(a, j);
+        return j;
+    }
     static_assert(sizeof(sh.coef) >= kBins * sizeof(int), "histogram lives in the weight LDS");
     if (threadIdx.x < kWave) {
         int* hist = reinterpret_cast<int*>(&sh.coef);  // free until the page loop
@@ -948,7 +953,7 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
         int cnt = 0;
 #pragma unroll
         for (int i = 0; i < kRankPer; ++i) cnt += bin[i] == b;
-        int before = wave_incl_scan(cnt) - cnt, t = 0;
+        int before = wave_incl_scan(cnt) - cnt, t = 0, th = 0, tl = 0;
         found = false;
 #pragma unroll
         for (int i = 0; i < kRankPer; ++i) {
@@ -956,17 +961,29 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
                 if (before == r) {
                     found = true;
                     t = t0 + i;
+                    th = lh[i];
+                    tl = ll[i];
                 }
                 ++before;
             }
         }
         const unsigned long long fm2 = __builtin_amdgcn_ballot_w64(found);
         const int src2 = fm2 ? __builtin_ctzll(fm2) : 0;
-        const int tr = __builtin_amdgcn_readlane(t, src2);  // read with every lane active
-        if (lane == 0) sh.t_first = tr;
+        // read with every lane active
+        const int tr = __builtin_amdgcn_readlane(t, src2);
+        const int thr = __builtin_amdgcn_readlane(th, src2), tlr = __builtin_amdgcn_readlane(tl, src2);
+        if (lane == 0) {
+            sh.t_first = tr;
+            sh.len_first[0] = thr;
+            sh.len_first[1] = tlr;
+        }
     }
     __syncthreads();
-    return sh.t_first;  // (not written again in this mode)
+    // (uniform values read back from LDS: readfirstlane keeps the table's
+    // loads and addresses scalar)
+    *ti = table_info_of(a, __builtin_amdgcn_readfirstlane(sh.len_first[0]),
+                        __builtin_amdgcn_readfirstlane(sh.len_first[1]));
+    return __builtin_amdgcn_readfirstlane(sh.t_first);  // (not written again in this mode)
 }
 
 template <int GQ>
@@ -976,9 +993,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
     const int T = a.B * a.Hkv;
     if (a.splits > 0) {
         const int j = blockIdx.x / a.splits, c = blockIdx.x - j * a.splits;
-        // (uniform: read back from LDS, so the table's loads and addresses stay scalar)
-        const int t = __builtin_amdgcn_readfirstlane(longest_first<GQ>(a, sh, T, j));
-        const TableInfo ti = table_info(a, t);
+        TableInfo ti;
+        const int t = longest_first<GQ>(a, sh, T, j, &ti);
         const int n = ti.np < a.splits ? ti.np : a.splits;
         if (n == 0) {
             if (c == 0) write_empty(a, t, GQ);

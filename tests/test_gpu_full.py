@@ -1,10 +1,14 @@
-"""GPU parity at the full size of the timed workload (llama8b decode: B = 64,
-Hq = 32, Hkv = 8, contexts 1024-4096), in the launch configuration the bench
-times (automatic split mode), against the CPU oracle on every output.
+"""GPU parity at full workload sizes, in the automatic split mode the bench
+times, against the CPU oracle on every output:
 
-The oracle handles this size in seconds: the prompt-phase append is compared
+  llama8b   B = 64, Hq = 32, Hkv = 8, contexts 1024-4096 (the timed workload;
+            one workgroup per table)
+  llama70b  B = 32, Hq = 64, Hkv = 8, context 8192 (balanced shares + merge)
+  long32k   B = 16, Hq = 40, Hkv = 8, context 32768 (balanced shares + merge)
+
+The oracle handles these sizes in seconds: the prompt-phase append is compared
 byte for byte over every used page, then attention over the whole cache, then
-two decode steps (one token per table, partial pages) and attention again.
+decode steps (one token per table, partial pages) and attention again.
 """
 import numpy as np
 import pytest
@@ -42,10 +46,12 @@ def _attention_both(oc, dc, q, what):
     print("   max abs %.2e rel %.2e" % (mx, rel), flush=True)
 
 
-def test_llama8b_full_size_append_and_attention():
-    w = inputs.prefill("llama8b")
+@pytest.mark.parametrize("name,steps,dims", [("llama8b", 2, (64, 32, 8)), ("llama70b", 1, (32, 64, 8)),
+                                              ("long32k", 1, (16, 40, 8))])
+def test_full_size_append_and_attention(name, steps, dims):
+    w = inputs.prefill(name)
     B, Hq, Hkv = w["B"], w["Hq"], w["Hkv"]
-    assert (B, Hq, Hkv) == (64, 32, 8)
+    assert (B, Hq, Hkv) == dims
     quota = w["quota"]
     # pages for the prompt plus the decode steps, and some spare
     per = (-(-quota[:, :, 0] // 16)) + (-(-quota[:, :, 1] // 32)) + 2
@@ -53,15 +59,17 @@ def test_llama8b_full_size_append_and_attention():
     Lo, Ld = layouts(max_seq_len=int(w["max_len"]) + 64)
     oc = orc.Cache(Lo, npages, B, Hkv, ring=np.random.default_rng(41).permutation(npages))
     dc = dev_cache_from_oracle(Ld, oc)
-    print("case: full-size prompt append (%d rows)" % int(w["new_len"].sum()), flush=True)
+    print("case: %s full-size prompt append (%d rows)" % (name, int(w["new_len"].sum())), flush=True)
     _append_both(oc, dc, w["new_len"], w["k"], w["v"], w["score"], quota)
     assert oc.status[0] == 0
-    assert_state_equal(dc, oc, what="full-size prompt append")
-    _attention_both(oc, dc, w["q"], "after the prompt")
-    for step in range(2):
-        d = inputs.decode_token("llama8b", step, B, Hq, Hkv, w["outliers"])
-        print("case: full-size decode append, step %d" % step, flush=True)
+    assert_state_equal(dc, oc, what="%s full-size prompt append" % name)
+    q, outl = w["q"], w["outliers"]
+    del w
+    _attention_both(oc, dc, q, "%s after the prompt" % name)
+    for step in range(steps):
+        d = inputs.decode_token(name, step, B, Hq, Hkv, outl)
+        print("case: %s full-size decode append, step %d" % (name, step), flush=True)
         _append_both(oc, dc, d["new_len"], d["k"], d["v"], d["score"], d["quota"])
         assert oc.status[0] == 0
-        assert_state_equal(dc, oc, what="full-size decode step %d" % step)
-        _attention_both(oc, dc, d["q"], "after decode step %d" % step)
+        assert_state_equal(dc, oc, what="%s full-size decode step %d" % (name, step))
+        _attention_both(oc, dc, d["q"], "%s after decode step %d" % (name, step))

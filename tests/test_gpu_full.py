@@ -73,3 +73,33 @@ def test_full_size_append_and_attention(name, steps, dims):
         assert oc.status[0] == 0
         assert_state_equal(dc, oc, what="%s full-size decode step %d" % (name, step))
         _attention_both(oc, dc, d["q"], "%s after decode step %d" % (name, step))
+
+
+def test_full_size_compaction_rounds():
+    """The compaction workload at full size: 2^20 pages, 4096 tables of up to 256
+    slots, 60 % held, Bernoulli(0.35) releases and refill per round; six rounds,
+    so the ring wraps.  Every table, length, ring entry and pointer bit-exact."""
+    ring, demand = inputs.compaction_setup()
+    assert ring.size == 1 << 20 and demand.shape == (4096, 2)
+    Lo, Ld = layouts(max_seq_len=255 * 16)
+    assert Lo.p_max == 256
+    oc = orc.Cache(Lo, 1 << 20, 4096, 1, ring=ring, with_pool=False)
+    dc = dev_cache_from_oracle(Ld, oc, with_pool=False)
+    orc.alloc_pages(oc, demand)
+    dk.alloc_pages(dc, t(demand))
+    oc.len[:] = oc.pages * np.array([16, 32])
+    dc.len.copy_(t(oc.len))
+    assert_state_equal(dc, oc, with_pool=False, what="full-size setup")
+    for rnd in range(6):
+        print("case: full-size compaction round %d" % rnd, flush=True)
+        rel = inputs.release_mask(4, rnd, 4096, 256)
+        before = oc.pages.copy()
+        orc.compact(oc, rel)
+        dk.compact_free_list(dc, t(rel))
+        lost = (before - oc.pages).astype(np.int32)
+        orc.alloc_pages(oc, lost)
+        dk.alloc_pages(dc, t(lost))
+        oc.len[:] = oc.pages * np.array([16, 32])
+        dc.len.copy_(t(oc.len))
+        assert_state_equal(dc, oc, with_pool=False, what="full-size round %d" % rnd)
+    assert oc.ring_ptr[1] > (1 << 20)  # wrapped

@@ -7,8 +7,9 @@
 // equal share per resident workgroup, so the spread of table lengths costs
 // nothing; tables that straddle shares are merged by attn_merge.  Inside a
 // workgroup each wave takes every fourth page and keeps page i+1 in flight
-// (two register buffers in rotation) while it computes page i; page IDs come
-// from scalar loads issued two pages ahead.
+// (two register buffers in rotation) while it computes page i; a wave's page
+// IDs arrive as one vector per 64 pages and each page is loaded through a
+// buffer resource over that page (scalar address, hardware bounds).
 //
 // Lane mapping inside a wave (64 lanes = 4 rows of 16):
 //   key phase    lane = grp*16 + j: token j (and j+16 on 32-token pages),

@@ -246,6 +246,37 @@ def test_attention_every_group_size(Hkv, Hq):
                                "group size %d splits=%d" % (Hq // Hkv, splits))
 
 
+def test_attention_long_tables_many_chunks():
+    """Tables of 250-625 pages: with one workgroup per table each wave walks up to
+    157 pages, so its page IDs arrive in up to three chunks of 64 (the pipeline
+    restarts at each chunk boundary, the high/low switch falls inside a chunk);
+    also split and balanced modes over the same tables."""
+    rng = np.random.default_rng(24)
+    B, Hkv, Hq = 2, 2, 8
+    new_len = np.array([12000, 9000], np.int32)
+    n = int(new_len.sum())
+    k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    score = rng.random((n, Hkv)).astype(np.float32)
+    # high pages 375 / 500 / 300 / 1, low pages 125 / 125 / 90 / 250
+    quota = np.array([[[6000, 4000], [8000, 4000]], [[4800, 2880], [16, 8000]]], np.int32)
+    Lo, Ld = layouts(max_seq_len=12064)
+    npages = 2000
+    oc = orc.Cache(Lo, npages, B, Hkv, ring=rng.permutation(npages))
+    orc.quantize_append(oc, new_len, k, v, score, quota=quota)
+    assert oc.status[0] == 0
+    q = rng.standard_normal((B, Hq, 128)).astype(np.float16).view(np.uint16)
+    ref, ref_lse = orc.attention(oc, q, SCALE)
+    dc = dev_cache_from_oracle(Ld, oc)
+    for splits in (1, 3, -1):
+        print("case: long tables splits=%d" % splits, flush=True)
+        out, lse = dk.decode_attention(dc, t(q), SCALE, num_splits=splits)
+        torch.cuda.synchronize()
+        mx, rel = assert_attention_close(out.cpu().numpy(), lse.cpu().numpy(), ref, ref_lse,
+                                         "long tables splits=%d" % splits)
+        print("   max abs %.2e rel %.2e" % (mx, rel), flush=True)
+
+
 # ------------------------------------------------------- compaction/alloc --
 def test_compaction_worked_example_on_gpu():
     import json

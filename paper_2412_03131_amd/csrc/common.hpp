@@ -31,27 +31,6 @@ __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 // ---- wave reductions -------------------------------------------------------
 template <int W>
-__device__ __forceinline__ float wave_sum_w(float x)
-{
-#pragma unroll
-    for (int o = W / 2; o > 0; o >>= 1) x += __shfl_xor(x, o, W);
-    return x;
-}
-template <int W>
-__device__ __forceinline__ float wave_max_w(float x)
-{
-#pragma unroll
-    for (int o = W / 2; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, W));
-    return x;
-}
-template <int W>
-__device__ __forceinline__ float wave_min_w(float x)
-{
-#pragma unroll
-    for (int o = W / 2; o > 0; o >>= 1) x = fminf(x, __shfl_xor(x, o, W));
-    return x;
-}
-template <int W>
 __device__ __forceinline__ int wave_isum_w(int x)
 {
 #pragma unroll

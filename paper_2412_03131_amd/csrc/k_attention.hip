@@ -52,15 +52,6 @@ constexpr long long kPageBytes = 4352;  // unified page of the supported layout
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
 // ---- cross-lane helpers ------------------------------------------------------
-// sum of the four rows (lanes l, l^16, l^32, l^48), result in every lane
-__device__ __forceinline__ float rows_sum4(float x)
-{
-    auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x)
 {
@@ -91,24 +82,11 @@ __device__ __forceinline__ float row_sum16(float x)
 // one v_perm or one AND per two codes, exact, and exact again in
 // v_dot2_f32_f16 (its fp16 products are exact in fp32).  The 2^24 is folded
 // into the key scale.  Pairs hold dims (d, d+4) of each 8-dim block, the
-// pairing the q registers use.
-__device__ __forceinline__ uint32_t perm_pair(uint32_t w_hi, uint32_t w_lo, int a)
-{
-    // bytes: [w_lo.byte a, 0, w_hi.byte a, 0]
-    return __builtin_amdgcn_perm(w_hi, w_lo, 0x0C000C00u | ((uint32_t)(4 + a) << 16) | (uint32_t)a);
-}
+// pairing the q registers use (v_perm selector kPermSel below).
 
 __device__ __forceinline__ float dot2(half2_t a, uint32_t b, float c)
 {
     return __builtin_amdgcn_fdot2(a, __builtin_bit_cast(half2_t, b), c, false);
-}
-// a*b with a zero accumulator as one instruction (the compiler would otherwise
-// materialise the zero for the accumulate-in-place encoding)
-__device__ __forceinline__ float dot2_first(half2_t a, uint32_t b)
-{
-    float d;
-    asm("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(d) : "v"(a), "v"(b));
-    return d;
 }
 // f(integral_constant<int, 0>) ... f(integral_constant<int, N-1>)
 template <typename F, int... I>
@@ -199,7 +177,7 @@ __device__ __forceinline__ void kdone(float (&d)[GQ])
     for (int hh = 0; hh < GQ; ++hh) asm volatile("" : "+v"(d[hh]));
 }
 
-// perm_pair selector for pair a of an 8-dim block (see perm_pair)
+// v_perm selector of pair a of an 8-dim block: bytes [w_lo.byte a, 0, w_hi.byte a, 0]
 constexpr uint32_t kPermSel(int a) { return 0x0C000C00u | ((uint32_t)(4 + a) << 16) | (uint32_t)a; }
 
 // K8 token: d[h] = sum over the group's 16 pairs of q_h . codes (w = the 32

@@ -506,6 +506,256 @@ int dko_compact(const dko_layout* L, dko_cache* C, int num_tables,
 }
 
 /* ======================================================================
+ * Generation phase (Sec. 4, Algorithm 1), once per decode step, after the
+ * step's append has put the newest token into the high section as part of
+ * the recent window.  Table t of sequence b, N = seq_len[b]:
+ *   - the candidate t_c is the high token at position N - 1 - W, the one
+ *     that has just left the window of the W most recent positions; a
+ *     table without it is left alone;
+ *   - thresholds alpha_h / N and alpha_l / N in fp32, as in the prompt
+ *     phase; a victim is the token of lowest score (ties: lowest position)
+ *     among a section's tokens outside the window (positions <= N - 1 - W);
+ *   - score(t_c) >= alpha_h/N: t_c stays high; the high victim v moves to
+ *     the low section if alpha_l/N <= score(v) < alpha_h/N and is removed
+ *     if score(v) < alpha_l/N;
+ *   - alpha_l/N <= score(t_c) < alpha_h/N: t_c moves to the low section;
+ *     the low victim v is removed if score(v) < alpha_l/N (t_c, whose score
+ *     is >= alpha_l/N, cannot be that victim, so t_c takes v's slot);
+ *   - otherwise t_c is removed.
+ * Removal keeps a section dense: its last token moves into the hole (raw
+ * bytes) and the vacated slot is cleared; a page emptied this way stays with
+ * the table.  A token entering the low section otherwise goes to its end;
+ * the step takes a new page only then, from the ring with the append's
+ * prefix-sum schedule (all-or-nothing).  Moving a token to the low section
+ * re-quantizes it: each element dequantized as fmaf(s, code, z) in fp32,
+ * rounded to fp16 (RNE), then quantized at the low precision exactly as an
+ * append quantizes a new token.
+ * ====================================================================== */
+static void token_loc(const dko_layout* L, const dko_cache* C, int t, int sec, int u,
+                      uint8_t** pg, int* slot)
+{
+    *pg = page_ptr(L, C, t, sec, u);
+    *slot = u % L->tokens_per_page[sec];
+}
+
+static float token_score(const dko_layout* L, const dko_cache* C, int t, int sec, int u)
+{
+    uint8_t* pg;
+    int slot;
+    float s;
+    token_loc(L, C, t, sec, u, &pg, &slot);
+    memcpy(&s, pg + L->off_score[sec] + slot * 4, 4);
+    return s;
+}
+
+static int32_t token_pos(const dko_layout* L, const dko_cache* C, int t, int sec, int u)
+{
+    uint8_t* pg;
+    int slot;
+    int32_t p;
+    token_loc(L, C, t, sec, u, &pg, &slot);
+    memcpy(&p, pg + L->off_pos[sec] + slot * 4, 4);
+    return p;
+}
+
+/* Zero every bit of one slot (codes, metadata, score, position). */
+static void clear_slot(const dko_layout* L, uint8_t* pg, int sec, int slot)
+{
+    int D = L->head_dim, ng = D / L->group, T = L->tokens_per_page[sec];
+    int kb = L->k_bits[sec], vb = L->v_bits[sec];
+    int chunks = D * kb / 128, row_bytes = T * vb / 8;
+    for (int c = 0; c < chunks; c++) memset(pg + L->off_kcode[sec] + ((int64_t)c * T + slot) * 16, 0, 16);
+    memset(pg + L->off_kmeta[sec] + (int64_t)slot * ng * 4, 0, (size_t)ng * 4);
+    for (int d = 0; d < D; d++) {
+        uint8_t* row = pg + L->off_vcode[sec] + (int64_t)d * row_bytes;
+        int64_t bit = (int64_t)slot * vb;
+        row[bit >> 3] &= (uint8_t)~(((1u << vb) - 1u) << (bit & 7));
+    }
+    for (int g = 0; g < ng; g++) memset(pg + L->off_vmeta[sec] + ((int64_t)g * T + slot) * 4, 0, 4);
+    memset(pg + L->off_score[sec] + slot * 4, 0, 4);
+    memset(pg + L->off_pos[sec] + slot * 4, 0, 4);
+}
+
+/* Copy token (sp, ss) to the cleared slot (dp, ds) of the same section. */
+static void copy_slot(const dko_layout* L, const uint8_t* sp, int ss, uint8_t* dp, int ds, int sec)
+{
+    int D = L->head_dim, ng = D / L->group, T = L->tokens_per_page[sec];
+    int kb = L->k_bits[sec], vb = L->v_bits[sec];
+    int chunks = D * kb / 128, row_bytes = T * vb / 8;
+    for (int c = 0; c < chunks; c++)
+        memcpy(dp + L->off_kcode[sec] + ((int64_t)c * T + ds) * 16,
+               sp + L->off_kcode[sec] + ((int64_t)c * T + ss) * 16, 16);
+    memcpy(dp + L->off_kmeta[sec] + (int64_t)ds * ng * 4, sp + L->off_kmeta[sec] + (int64_t)ss * ng * 4,
+           (size_t)ng * 4);
+    for (int d = 0; d < D; d++) {
+        unsigned code = get_bits(sp + L->off_vcode[sec] + (int64_t)d * row_bytes, (int64_t)ss * vb, vb);
+        put_bits(dp + L->off_vcode[sec] + (int64_t)d * row_bytes, (int64_t)ds * vb, vb, code);
+    }
+    for (int g = 0; g < ng; g++)
+        memcpy(dp + L->off_vmeta[sec] + ((int64_t)g * T + ds) * 4, sp + L->off_vmeta[sec] + ((int64_t)g * T + ss) * 4, 4);
+    memcpy(dp + L->off_score[sec] + ds * 4, sp + L->off_score[sec] + ss * 4, 4);
+    memcpy(dp + L->off_pos[sec] + ds * 4, sp + L->off_pos[sec] + ss * 4, 4);
+}
+
+/* Remove token u of a section: the last token takes its slot. */
+static void remove_token(const dko_layout* L, dko_cache* C, int t, int sec, int u)
+{
+    int last = C->len[2 * t + sec] - 1;
+    uint8_t *dp, *lp;
+    int ds, ls;
+    token_loc(L, C, t, sec, u, &dp, &ds);
+    token_loc(L, C, t, sec, last, &lp, &ls);
+    if (u != last) {
+        clear_slot(L, dp, sec, ds);
+        copy_slot(L, lp, ls, dp, ds, sec);
+    }
+    clear_slot(L, lp, sec, ls);
+    C->len[2 * t + sec] = last;
+}
+
+/* Fp16 key and value of high token u, dequantized in fp32 (fmaf) and
+ * rounded to fp16. */
+static void requant_source(const dko_layout* L, const dko_cache* C, int t, int u,
+                           uint16_t* k16, uint16_t* v16, float* score, int32_t* pos)
+{
+    int sec = DKO_HIGH;
+    int D = L->head_dim, G = L->group, ng = D / G, T = L->tokens_per_page[sec];
+    int kb = L->k_bits[sec], vb = L->v_bits[sec];
+    int per_chunk = 128 / kb, row_bytes = T * vb / 8;
+    uint8_t* pg;
+    int slot;
+    token_loc(L, C, t, sec, u, &pg, &slot);
+    for (int d = 0; d < D; d++) {
+        int g = d / G, c = d / per_chunk, e = d % per_chunk;
+        unsigned code = get_bits(pg + L->off_kcode[sec] + ((int64_t)c * T + slot) * 16, (int64_t)e * kb, kb);
+        const uint8_t* km = pg + L->off_kmeta[sec] + ((int64_t)slot * ng + g) * 4;
+        k16[d] = dko_float_to_half(fmaf(dko_half_to_float(get_u16(km)), (float)code,
+                                        dko_half_to_float(get_u16(km + 2))));
+        code = get_bits(pg + L->off_vcode[sec] + (int64_t)d * row_bytes, (int64_t)slot * vb, vb);
+        const uint8_t* vm = pg + L->off_vmeta[sec] + ((int64_t)g * T + slot) * 4;
+        v16[d] = dko_float_to_half(fmaf(dko_half_to_float(get_u16(vm)), (float)code,
+                                        dko_half_to_float(get_u16(vm + 2))));
+    }
+    memcpy(score, pg + L->off_score[sec] + slot * 4, 4);
+    memcpy(pos, pg + L->off_pos[sec] + slot * 4, 4);
+}
+
+/* Write a re-quantized token into low slot u (its slot cleared first; the
+ * first slot of a page clears the page, as an append does). */
+static void put_low(const dko_layout* L, dko_cache* C, int t, int u, const uint16_t* k16,
+                    const uint16_t* v16, float score, int32_t pos)
+{
+    uint8_t* pg;
+    int slot;
+    token_loc(L, C, t, DKO_LOW, u, &pg, &slot);
+    if (u == C->len[2 * t + 1] && slot == 0) memset(pg, 0, (size_t)L->page_bytes);
+    else clear_slot(L, pg, DKO_LOW, slot);
+    write_token(L, pg, DKO_LOW, slot, k16, v16, score, pos);
+}
+
+/* Victim of a section: lowest score, ties to the lowest position, among
+ * tokens at positions <= pc.  Returns its index or -1. */
+static int victim(const dko_layout* L, const dko_cache* C, int t, int sec, int32_t pc)
+{
+    int best = -1;
+    float bs = 0.0f;
+    int32_t bp = 0;
+    for (int u = 0; u < C->len[2 * t + sec]; u++) {
+        int32_t p = token_pos(L, C, t, sec, u);
+        if (p > pc) continue;
+        float s = token_score(L, C, t, sec, u);
+        if (best < 0 || s < bs || (s == bs && p < bp)) {
+            best = u;
+            bs = s;
+            bp = p;
+        }
+    }
+    return best;
+}
+
+enum { GEN_NONE = 0, GEN_HIGH_VICTIM_TO_LOW, GEN_HIGH_VICTIM_OUT, GEN_CAND_TO_LOW, GEN_CAND_OUT };
+
+int dko_generation_step(const dko_layout* L, dko_cache* C, float alpha_h, float alpha_l, int window)
+{
+    int B = C->num_seqs, H = C->num_kv_heads, D = L->head_dim;
+    int num_tables = B * H;
+    int* act = (int*)calloc((size_t)num_tables, sizeof(int));
+    int* uc = (int*)calloc((size_t)num_tables, sizeof(int));   /* candidate's high index */
+    int* uv = (int*)calloc((size_t)num_tables, sizeof(int));   /* victim's index         */
+    int32_t* need = (int32_t*)calloc((size_t)num_tables * 2, sizeof(int32_t));
+    uint16_t* k16 = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)D);
+    uint16_t* v16 = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)D);
+    int w = window < 0 ? 0 : window;
+
+    /* decide every table's action on the state before the step */
+    for (int t = 0; t < num_tables; t++) {
+        int N = C->seq_len[t / H];
+        int32_t pc = N - 1 - w;
+        act[t] = GEN_NONE;
+        if (pc < 0) continue;
+        int c = -1;
+        for (int u = 0; u < C->len[2 * t]; u++)
+            if (token_pos(L, C, t, DKO_HIGH, u) == pc) { c = u; break; }
+        if (c < 0) continue;
+        float thr_h = alpha_h / (float)N, thr_l = alpha_l / (float)N;
+        float sc = token_score(L, C, t, DKO_HIGH, c);
+        uc[t] = c;
+        if (sc >= thr_h) {
+            int v = victim(L, C, t, DKO_HIGH, pc);
+            float sv = token_score(L, C, t, DKO_HIGH, v);
+            uv[t] = v;
+            if (sv >= thr_l && sv < thr_h) act[t] = GEN_HIGH_VICTIM_TO_LOW;
+            else if (sv < thr_l) act[t] = GEN_HIGH_VICTIM_OUT;
+        } else if (sc >= thr_l) {
+            int v = victim(L, C, t, DKO_LOW, pc);
+            uv[t] = (v >= 0 && token_score(L, C, t, DKO_LOW, v) < thr_l) ? v : -1;
+            act[t] = GEN_CAND_TO_LOW;
+        } else {
+            act[t] = GEN_CAND_OUT;
+        }
+        /* a token goes to the end of the low section: a new page if it is full */
+        int grows = act[t] == GEN_HIGH_VICTIM_TO_LOW || (act[t] == GEN_CAND_TO_LOW && uv[t] < 0);
+        int T = L->tokens_per_page[DKO_LOW];
+        if (grows && C->len[2 * t + 1] + 1 > C->pages[2 * t + 1] * T) need[2 * t + 1] = 1;
+    }
+
+    if (alloc_core(L, C, num_tables, need) == 0) {
+        for (int t = 0; t < num_tables; t++) {
+            float sc;
+            int32_t pos;
+            switch (act[t]) {
+            case GEN_HIGH_VICTIM_TO_LOW:
+                requant_source(L, C, t, uv[t], k16, v16, &sc, &pos);
+                remove_token(L, C, t, DKO_HIGH, uv[t]);
+                put_low(L, C, t, C->len[2 * t + 1], k16, v16, sc, pos);
+                C->len[2 * t + 1]++;
+                break;
+            case GEN_HIGH_VICTIM_OUT:
+                remove_token(L, C, t, DKO_HIGH, uv[t]);
+                break;
+            case GEN_CAND_TO_LOW:
+                requant_source(L, C, t, uc[t], k16, v16, &sc, &pos);
+                remove_token(L, C, t, DKO_HIGH, uc[t]);
+                if (uv[t] >= 0) {
+                    put_low(L, C, t, uv[t], k16, v16, sc, pos);
+                } else {
+                    put_low(L, C, t, C->len[2 * t + 1], k16, v16, sc, pos);
+                    C->len[2 * t + 1]++;
+                }
+                break;
+            case GEN_CAND_OUT:
+                remove_token(L, C, t, DKO_HIGH, uc[t]);
+                break;
+            default:
+                break;
+            }
+        }
+    }
+    free(act); free(uc); free(uv); free(need); free(k16); free(v16);
+    return 0;
+}
+
+/* ======================================================================
  * Attention, Eq. (1), in fp64 over the dequantized cache.
  * ====================================================================== */
 static int table_tokens(const dko_cache* C, int t) { return C->len[2 * t] + C->len[2 * t + 1]; }

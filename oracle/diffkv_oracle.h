@@ -12,6 +12,8 @@
  *     applied per 32-dim group, keys at more bits than values (Sec. 4);
  *   - three-level token classing, quota form and the sequence-length
  *     adaptive threshold form (Sec. 4, prompt phase, and Algorithm 1);
+ *   - the generation-phase policy of Algorithm 1 (candidate leaving the
+ *     recent window, victims, re-quantization to the low precision);
  *   - unified pages, circular free page list, bidirectional page table and
  *     the prefix-sum allocation/recycling schedule (Sec. 5.2, 5.3);
  *   - softmax attention, Eq. (1) of Sec. 2.1, evaluated in fp64 over the
@@ -105,6 +107,20 @@ int dko_quantize_append(const dko_layout* L, dko_cache* C,
 /* ---- free-list compaction (Sec. 5.2, 5.3) ---------------------------- */
 int dko_compact(const dko_layout* L, dko_cache* C, int num_tables,
                 const uint8_t* release /* [num_tables][p_max] */);
+
+/* ---- generation phase (Sec. 4, Algorithm 1) ---------------------------
+ * One decode step's policy for every table, after the step's append put the
+ * newest token into the high section (the recent window of W positions).
+ * Candidate: the high token at position seq_len - 1 - W.  Thresholds
+ * alpha_h/N, alpha_l/N (fp32, N = seq_len).  Victims: lowest score (ties:
+ * lowest position) outside the window.  Removal moves a section's last
+ * token into the hole and clears the vacated slot; a token entering the low
+ * section is re-quantized (fp32 fmaf dequantization, fp16 RNE, low-precision
+ * quantization) and appended, or takes the slot of the low victim it
+ * evicts.  A low section that grows past its pages takes one page from the
+ * ring (all-or-nothing across tables).  Returns 0; failures set *status.  */
+int dko_generation_step(const dko_layout* L, dko_cache* C, float alpha_h, float alpha_l,
+                        int window);
 
 /* ---- page decoding ----------------------------------------------------
  * Dequantized key/value of section token u of table t (fp64, exact).     */

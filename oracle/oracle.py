@@ -62,6 +62,7 @@ def _setup(L):
     L.dko_quantize_append.argtypes = [C.POINTER(Layout), C.POINTER(_Cache), vp, vp, vp, vp,
                                       vp, f32, f32, C.c_int]
     L.dko_compact.argtypes = [C.POINTER(Layout), C.POINTER(_Cache), C.c_int, vp]
+    L.dko_generation_step.argtypes = [C.POINTER(Layout), C.POINTER(_Cache), f32, f32, C.c_int]
     L.dko_read_token.argtypes = [C.POINTER(Layout), C.POINTER(_Cache), C.c_int, C.c_int,
                                  C.c_int, vp, vp, vp, vp]
     L.dko_attention.argtypes = [C.POINTER(Layout), C.POINTER(_Cache), C.c_int, vp, f64, vp, vp]
@@ -74,7 +75,7 @@ def _setup(L):
     L.dko_half_to_float.restype = f32
     L.dko_half_to_float.argtypes = [C.c_uint16]
     for name in ("dko_layout_init", "dko_alloc_pages", "dko_quantize_append", "dko_compact",
-                 "dko_attention"):
+                 "dko_generation_step", "dko_attention"):
         getattr(L, name).restype = C.c_int
     _ = (i32,)
 
@@ -188,6 +189,13 @@ def compact(cache, release):
     assert r.shape == (cache.num_tables, cache.L.p_max)
     st = cache.struct()
     lib().dko_compact(C.byref(cache.L), C.byref(st), cache.num_tables, _p(r))
+
+
+def generation_step(cache, alpha_h, alpha_l, window):
+    """Algorithm 1 once for every table (after a decode step's append)."""
+    st = cache.struct()
+    lib().dko_generation_step(C.byref(cache.L), C.byref(st), float(alpha_h), float(alpha_l),
+                              int(window))
 
 
 def read_token(cache, t, sec, u):

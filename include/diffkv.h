@@ -97,10 +97,11 @@ typedef struct diffkv_layout {
  * + h is the bidirectional page table of sequence b, KV head h (Sec. 5.2):
  * high-precision page IDs grow from slot 0 to the right, low-precision page
  * IDs from slot p_max-1 to the left; empty slots hold -1.  Token u of a
- * section lives in slot u % T of the section's page u / T, in position
- * order.  The free page list is a ring of num_pages IDs; the free IDs are
- * ring[head % n .. tail % n) with head/tail monotone int64 counters
- * (start pointer allocates, end pointer recycles).
+ * section lives in slot u % T of the section's page u / T; appends add
+ * tokens in position order (a generation step's removal then moves a
+ * section's last token into the hole).  The free page list is a ring of
+ * num_pages IDs; the free IDs are ring[head % n .. tail % n) with head/tail
+ * monotone int64 counters (start pointer allocates, end pointer recycles).
  */
 typedef struct diffkv_cache {
     uint8_t*  pool;          /* device [num_pages][page_bytes]                     */
@@ -121,7 +122,8 @@ typedef struct diffkv_cache {
  * Bits must be 1, 2, 4 or 8, head_dim*k_bits a multiple of 128,
  * T*v_bits a multiple of 8, tokens_per_page[LOW] >= tokens_per_page[HIGH].
  * DIFFKV_E_INVAL otherwise.  Any valid layout is accepted here; the
- * append and attention kernels implement head_dim 128, group 32, K8V4/K4V2
+ * append, generation-step and attention kernels implement head_dim 128,
+ * group 32, K8V4/K4V2
  * and 16/32 tokens per page (DIFFKV_E_UNSUPPORTED otherwise); allocation
  * and compaction accept any valid layout. */
 diffkv_status diffkv_layout_init(diffkv_layout* out, int32_t head_dim, int32_t group,
@@ -132,13 +134,15 @@ enum {
     DIFFKV_OP_APPEND = 0,
     DIFFKV_OP_ATTENTION = 1,
     DIFFKV_OP_COMPACT = 2,
-    DIFFKV_OP_ALLOC = 3
+    DIFFKV_OP_ALLOC = 3,
+    DIFFKV_OP_GENERATION = 4
 };
 
 /* Bytes of device workspace the operation needs (host out-parameter).
  * APPEND: num_seqs, num_kv_heads, total_new.  ATTENTION: num_seqs,
  * num_q_heads, num_splits (0 = automatic, -1 = balanced).
- * COMPACT / ALLOC: num_seqs*num_kv_heads tables.  Unused sizes are ignored. */
+ * COMPACT / ALLOC / GENERATION: num_seqs*num_kv_heads tables.  Unused sizes
+ * are ignored. */
 diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout,
                                     int32_t num_seqs, int32_t num_q_heads,
                                     int32_t num_kv_heads, int64_t total_new,
@@ -251,6 +255,42 @@ diffkv_status diffkv_compact_free_list(const diffkv_layout* layout, const diffkv
 diffkv_status diffkv_alloc_pages(const diffkv_layout* layout, const diffkv_cache* cache,
                                  int32_t num_tables, const int32_t* demand,
                                  void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Generation-phase policy (Sec. 4, Algorithm 1), once per decode step, after
+ * the step's diffkv_quantize_append has put the newest token of every
+ * sequence into the high section (its recent window).  For table t of
+ * sequence b, with N = seq_len[b] and W = recent_window:
+ *   - candidate: the high token at position N - 1 - W (the one that has just
+ *     left the window); a table without one is left alone;
+ *   - thresholds alpha_h / N and alpha_l / N, fp32 quotients;
+ *   - victim of a section: its token of lowest score (-0 == +0; ties to the
+ *     lowest position) among those at positions <= N - 1 - W;
+ *   - score(candidate) >= alpha_h/N: the candidate stays; the high victim
+ *     moves to the low section if alpha_l/N <= its score < alpha_h/N, and is
+ *     removed if its score < alpha_l/N;
+ *   - alpha_l/N <= score(candidate) < alpha_h/N: the candidate moves to the
+ *     low section, over the low victim's slot if that victim's score is
+ *     < alpha_l/N (the victim is evicted), else at the section's end;
+ *   - otherwise the candidate is removed.
+ * A token leaves the high section by swap-remove: the section's last token
+ * moves into its slot (bytes unchanged) and the vacated slot is cleared to
+ * zero; a page emptied this way stays with the table.  A token moving to the
+ * low section is re-quantized: per element s*code + z as one fp32 fma,
+ * rounded to fp16 (nearest even), then quantized as diffkv_quantize_append
+ * quantizes a low-precision token; its score and position are kept.
+ * Appending to a full low section takes one page per table, with the
+ * allocation's prefix-sum schedule over tables (ring region after the pages
+ * of lower tables; head advances by the total); all-or-nothing
+ * OUT_OF_PAGES / TABLE_OVERFLOW (then nothing changes).  seq_len is not
+ * changed.  Sections are dense but, after a removal, no longer in position
+ * order (attention does not depend on the order).
+ *   recent_window  W >= 0, DIFFKV_E_INVAL otherwise.
+ *   ws   device workspace of diffkv_workspace_size(DIFFKV_OP_GENERATION, ...).
+ */
+diffkv_status diffkv_generation_step(const diffkv_layout* layout, const diffkv_cache* cache,
+                                     float alpha_h, float alpha_l, int32_t recent_window,
+                                     void* ws, size_t ws_bytes, void* stream);
 
 /* Static string for a diffkv_status value. */
 const char* diffkv_status_str(diffkv_status s);

@@ -140,6 +140,8 @@ AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits)
 
 int64_t compact_ws(int64_t T) { return align256(sizeof(CallFlags)) + 2 * align256(T * 4); }
 int64_t alloc_ws(int64_t T) { return align256(sizeof(CallFlags)) + align256(T * 16); }
+// generation step: the allocation's block, then per-table actions and page requests
+int64_t gen_ws(int64_t T) { return alloc_ws(T) + align256(T * 16) + align256(T * 8); }
 
 }  // namespace
 
@@ -174,6 +176,10 @@ diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout, int
     case DIFFKV_OP_ALLOC:
         if (num_kv_heads <= 0) return DIFFKV_E_INVAL;
         *bytes = (size_t)alloc_ws((int64_t)num_seqs * num_kv_heads);
+        return DIFFKV_OK;
+    case DIFFKV_OP_GENERATION:
+        if (num_kv_heads <= 0) return DIFFKV_E_INVAL;
+        *bytes = (size_t)gen_ws((int64_t)num_seqs * num_kv_heads);
         return DIFFKV_OK;
     default:
         return DIFFKV_E_INVAL;
@@ -344,6 +350,52 @@ diffkv_status diffkv_alloc_pages(const diffkv_layout* layout, const diffkv_cache
     a.flags = reinterpret_cast<CallFlags*>(base);
     a.tstate = reinterpret_cast<int4*>(base + align256(sizeof(CallFlags)));
     hipError_t e = launch_alloc(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
+}
+
+diffkv_status diffkv_generation_step(const diffkv_layout* layout, const diffkv_cache* cache,
+                                     float alpha_h, float alpha_l, int32_t recent_window, void* ws,
+                                     size_t ws_bytes, void* stream)
+{
+    if (!layout_valid(layout) || !cache_valid(cache) || !cache->pool || !cache->seq_len)
+        return DIFFKV_E_INVAL;
+    if (recent_window < 0) return DIFFKV_E_INVAL;
+    if (!layout_kernels_supported(layout)) return DIFFKV_E_UNSUPPORTED;
+    const int64_t T = (int64_t)cache->num_seqs * cache->num_kv_heads;
+    if (T == 0) return DIFFKV_OK;
+    if (!ws || (int64_t)ws_bytes < gen_ws(T)) return DIFFKV_E_WORKSPACE;
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    AllocArgs a;
+    memset(&a, 0, sizeof(a));
+    a.p_max = layout->p_max;
+    a.num_pages = cache->num_pages;
+    a.page_table = cache->page_table;
+    a.pages = cache->pages;
+    a.ring = cache->ring;
+    a.ring_ptr = cache->ring_ptr;
+    a.status = cache->status;
+    a.num_tables = (int)T;
+    a.flags = reinterpret_cast<CallFlags*>(base);
+    a.tstate = reinterpret_cast<int4*>(base + align256(sizeof(CallFlags)));
+    GenArgs g;
+    memset(&g, 0, sizeof(g));
+    fill_layout_args(g, layout);
+    g.pool = cache->pool;
+    g.num_pages = cache->num_pages;
+    g.page_table = cache->page_table;
+    g.pages = cache->pages;
+    g.len = cache->len;
+    g.seq_len = cache->seq_len;
+    g.Hkv = cache->num_kv_heads;
+    g.num_tables = (int)T;
+    g.alpha_h = alpha_h;
+    g.alpha_l = alpha_l;
+    g.window = recent_window;
+    g.flags = a.flags;
+    g.act = reinterpret_cast<int4*>(base + alloc_ws(T));
+    g.demand = reinterpret_cast<int32_t*>(base + alloc_ws(T) + align256(T * 16));
+    a.demand = g.demand;
+    hipError_t e = launch_generation(g, a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
 }
 

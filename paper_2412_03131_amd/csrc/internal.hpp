@@ -77,6 +77,30 @@ struct CompactArgs {
     int32_t* offset;
 };
 
+// per-table decision of one generation step
+enum GenAction : int32_t {
+    kGenNone = 0,
+    kGenHighVictimToLow = 1,  // candidate stays high; the high victim moves to the low section
+    kGenHighVictimOut = 2,    // candidate stays high; the high victim is removed
+    kGenCandToLow = 3,        // the candidate moves to the low section
+    kGenCandOut = 4           // the candidate is removed
+};
+
+struct GenArgs : LayoutArgs {
+    uint8_t* pool;
+    long long num_pages;
+    const int32_t* page_table;
+    const int32_t* pages;
+    int32_t* len;
+    const int32_t* seq_len;
+    int Hkv, num_tables;
+    float alpha_h, alpha_l;
+    int window;
+    const CallFlags* flags;  // written by the allocation kernels of the same call
+    int4* act;               // [num_tables] {action, candidate index, victim index or -1, 0}
+    int32_t* demand;         // [num_tables][2] pages the step takes: {0, 0 or 1}
+};
+
 struct AttnArgs {
     int p_max;
     long long page_bytes;
@@ -103,6 +127,7 @@ constexpr int kAttnMaxWorkers = 2048;
 hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st);
 hipError_t launch_alloc(const AllocArgs& a, hipStream_t st);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
+hipError_t launch_generation(const GenArgs& g, const AllocArgs& a, hipStream_t st);
 hipError_t launch_attention(AttnArgs a, hipStream_t st);
 bool attention_layout_matches(const diffkv_layout* L);
 

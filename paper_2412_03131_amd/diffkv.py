@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(_HERE, "libdiffkv.so")
 
 OK, E_INVAL, E_UNSUPPORTED, E_WORKSPACE, E_LAUNCH = 0, 1, 2, 3, 4
 ST_OUT_OF_PAGES, ST_TABLE_OVERFLOW, ST_BAD_INPUT = 1, 2, 4
-OP_APPEND, OP_ATTENTION, OP_COMPACT, OP_ALLOC = 0, 1, 2, 3
+OP_APPEND, OP_ATTENTION, OP_COMPACT, OP_ALLOC, OP_GENERATION = 0, 1, 2, 3, 4
 HIGH, LOW = 0, 1
 
 _lib = None
@@ -51,7 +51,7 @@ class CacheStruct(C.Structure):
 
 EXPORTS = ("diffkv_layout_init", "diffkv_workspace_size", "diffkv_quantize_append",
            "diffkv_decode_attention", "diffkv_compact_free_list", "diffkv_alloc_pages",
-           "diffkv_status_str")
+           "diffkv_generation_step", "diffkv_status_str")
 
 
 def lib():
@@ -71,6 +71,7 @@ def lib():
         L.diffkv_decode_attention.argtypes = [PL, PC, i32, vp, f32, vp, vp, i32, vp, sz, vp]
         L.diffkv_compact_free_list.argtypes = [PL, PC, i32, vp, vp, sz, vp]
         L.diffkv_alloc_pages.argtypes = [PL, PC, i32, vp, vp, sz, vp]
+        L.diffkv_generation_step.argtypes = [PL, PC, f32, f32, i32, vp, sz, vp]
         L.diffkv_status_str.argtypes = [i32]
         L.diffkv_status_str.restype = C.c_char_p
         for n in EXPORTS[:-1]:
@@ -241,4 +242,17 @@ def alloc_pages(cache, demand, num_tables=None, ws=None, stream=None):
     _check(lib().diffkv_alloc_pages(C.byref(L), C.byref(st), int(nt), _ptr(demand), _ptr(ws),
                                     ws.numel() * ws.element_size(), _stream(stream)),
            "diffkv_alloc_pages")
+    return ws
+
+
+def generation_step(cache, alpha_h, alpha_l, recent_window, ws=None, stream=None):
+    """One decode step's generation-phase policy for every table (Algorithm 1)."""
+    L = cache.L
+    need = workspace_size(OP_GENERATION, L, cache.num_seqs, 0, cache.num_kv_heads)
+    ws = _ws(need, cache.pool.device, ws)
+    st = cache.struct()
+    _check(lib().diffkv_generation_step(C.byref(L), C.byref(st), float(alpha_h), float(alpha_l),
+                                        int(recent_window), _ptr(ws),
+                                        ws.numel() * ws.element_size(), _stream(stream)),
+           "diffkv_generation_step")
     return ws

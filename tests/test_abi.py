@@ -71,6 +71,8 @@ def test_workspace_sizes(dk):
     a2 = dk.workspace_size(dk.OP_APPEND, L, 64, 0, 8, 2000)
     assert a2 > a1 >= 1000 * 8 * 4
     assert dk.workspace_size(dk.OP_COMPACT, L, 512, 0, 8) >= 2 * 4096 * 4
+    # generation step: allocation block plus an action record and a page request per table
+    assert dk.workspace_size(dk.OP_GENERATION, L, 64, 0, 8) >= 512 * (16 + 16 + 8)
 
 
 def test_argument_checks_enqueue_nothing(dk):
@@ -98,6 +100,12 @@ def test_argument_checks_enqueue_nothing(dk):
     assert lib.diffkv_compact_free_list(C.byref(L), C.byref(st), 5, fake, fake, 1 << 20,
                                         None) == dk.E_INVAL  # more tables than the cache has
     assert lib.diffkv_alloc_pages(C.byref(L), C.byref(st), 4, fake, fake, 8, None) == dk.E_WORKSPACE
+    assert lib.diffkv_generation_step(C.byref(L), C.byref(st), 1.0, 0.5, 4, fake, 64,
+                                      None) == dk.E_WORKSPACE
+    assert lib.diffkv_generation_step(C.byref(L), C.byref(st), 1.0, 0.5, -1, fake, 1 << 20,
+                                      None) == dk.E_INVAL  # negative window
+    assert lib.diffkv_generation_step(C.byref(L2), C.byref(st), 1.0, 0.5, 4, fake, 1 << 20,
+                                      None) == dk.E_UNSUPPORTED
     bad = dk.Layout.from_buffer_copy(bytes(L))
     bad.off_vcode[0] += 64
     assert lib.diffkv_compact_free_list(C.byref(bad), C.byref(st), 1, fake, fake, 1 << 20,

@@ -19,6 +19,7 @@ value = KV tokens attended per second of step time, where a KV token is one kept
 (token, KV head) pair.  The JSON line adds the attention kernel's roofline (algorithmic
 compressed bytes / kernel time, HIP events on the launch stream), the compaction
 workload (2^20 pages, 4096 tables, 100 rounds of Bernoulli(0.35) releases) in pages/s,
+the generation-phase policy (Algorithm 1) per decode step on the same llama8b shape,
 and the CPU oracle's attention throughput on a bounded sample.
 """
 import argparse
@@ -76,15 +77,17 @@ def parse():
     ap.add_argument("--layers", type=int, default=4)
     ap.add_argument("--splits", type=int, default=0, help="attention mode: 0 automatic, -1 balanced shares, S >= 1 ranges per table")
     ap.add_argument("--compaction-rounds", type=int, default=100)
+    ap.add_argument("--generation-steps", type=int, default=50)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--hq", type=int, default=0,
                     help="with --only attention: query heads per sequence (default: the "
                          "workload's 32; a multiple of the 8 KV heads, at most 64)")
-    ap.add_argument("--only", choices=("all", "attention", "copy"), default="all",
+    ap.add_argument("--only", choices=("all", "attention", "copy", "generation"), default="all",
                     help="profiling aids that print no benchmark line: 'attention' builds the "
                          "cache and times only the attention calls; 'copy' runs a plain 1 GiB "
-                         "device copy (the reference for scaling HBM byte counters)")
+                         "device copy (the reference for scaling HBM byte counters); "
+                         "'generation' runs only the generation-step measurement")
     return ap.parse_args()
 
 
@@ -127,6 +130,9 @@ def main():
     lib = dk.lib()
     stream = torch.cuda.current_stream()
     sptr = C.c_void_p(stream.cuda_stream)
+    if args.only == "generation":
+        generation_bench(torch, dk, lib, dev, sptr, args.generation_steps)
+        return
 
     # ------------------------------------------------------------ workload --
     t0 = time.time()
@@ -295,6 +301,7 @@ def main():
 
     # ---------------------------------------------------------- compaction --
     comp = compaction_bench(torch, dk, lib, dev, sptr, args.compaction_rounds)
+    gen = generation_bench(torch, dk, lib, dev, sptr, args.generation_steps)
 
     # -------------------------------------------------------- cpu baseline --
     cpu = None if args.no_cpu_baseline else cpu_baseline(w, args.cpu_seconds)
@@ -338,6 +345,7 @@ def main():
             "fp16_equivalent_gbps": float(tok_layer.sum() * NL * 512 / attn_total_s / 1e9),
         },
         "compaction": comp,
+        "generation_step": gen,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -402,6 +410,73 @@ def compaction_bench(torch, dk, lib, dev, sptr, rounds):
     }
     log("compaction: %.1f us/round, %.3g pages/s, refill %.1f us" %
         (res["us_per_round"], res["pages_per_s"], res["refill_us_per_round"]))
+    return res
+
+
+def generation_bench(torch, dk, lib, dev, sptr, steps, window=64):
+    """The generation-phase policy (Algorithm 1) on the llama8b workload, one layer:
+    prompt phase with the 64-token recent window, then `steps` decode steps of one
+    appended token per sequence (score uniform in [0, 2/N), the scale of the prompt's
+    normalized scores) followed by one diffkv_generation_step, which HIP events on the
+    launch stream time (decide, allocation and apply kernels together)."""
+    from paper_2412_03131_amd import inputs
+    w = inputs.prefill("llama8b")
+    B, Hq, Hkv = w["B"], w["Hq"], w["Hkv"]
+    nl = w["new_len"].astype(np.int64)
+    L = dk.layout(max_seq_len=int(nl.max()) + steps + 16)
+    qh = w["quota"][:, :, 0].astype(np.int64)
+    ql = w["quota"][:, :, 1].astype(np.int64)
+    npg = int(((-(-(qh + window + steps) // 16)) + (-(-(ql + steps) // 32)) + 2).sum()) + 1024
+    c = dk.Cache(L, npg, B, Hkv, device=dev)
+
+    def T(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
+
+    dk.quantize_append(c, T(w["new_len"]), T(w["k"]), T(w["v"]), T(w["score"]), quota=T(w["quota"]),
+                       window=window, total_new=int(nl.sum()), max_new=int(nl.max()))
+    ws_a = torch.empty(dk.workspace_size(dk.OP_APPEND, L, B, 0, Hkv, B), dtype=torch.uint8, device=dev)
+    ws_g = torch.empty(dk.workspace_size(dk.OP_GENERATION, L, B, 0, Hkv), dtype=torch.uint8, device=dev)
+    cs = c.struct()
+    Lp = C.byref(L)
+    vp = lambda x: C.c_void_p(x.data_ptr())
+    keep, app = [], []
+    ones = T(np.ones(B, np.int32))
+    for s in range(steps):
+        d = inputs.decode_token("llama8b", s, B, Hq, Hkv, w["outliers"])
+        n = (nl + s + 1).astype(np.float32)
+        score = (d["score"] * (np.float32(2.0) / n)[:, None]).astype(np.float32)
+        t = [T(d["k"]), T(d["v"]), T(score), T(d["quota"])]
+        keep.append(t)
+        app.append((Lp, C.byref(cs), B, 1, vp(ones), vp(t[0]), vp(t[1]), vp(t[2]), vp(t[3]),
+                    0.0, 0.0, window, vp(ws_a), ws_a.numel(), sptr))
+    gen = (Lp, C.byref(cs), C.c_float(1.0), C.c_float(0.5), window, vp(ws_g), ws_g.numel(), sptr)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    hi0 = int(c.len[:, 0].sum().item())
+    torch.cuda._sleep(int(2.4e9 * 1e-4 * steps) + 1)  # the host enqueues ahead of the GPU
+    rc = 0
+    for s in range(steps):
+        rc |= lib.diffkv_quantize_append(*app[s])
+        ev[s][0].record()
+        rc |= lib.diffkv_generation_step(*gen)
+        ev[s][1].record()
+    torch.cuda.synchronize()
+    if rc or int(c.status.item()) != 0:
+        raise RuntimeError("generation bench failed (rc %d, status %d)" % (rc, int(c.status.item())))
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    lens = c.len.cpu().numpy()
+    res = {
+        "workload": "llama8b, 1 layer: B=64, Hkv=8 (512 tables), window 64, alpha_h 1.0, "
+                    "alpha_l 0.5, %d decode steps" % steps,
+        "us_per_call": float(ms.mean() * 1e3),
+        "us_p10_p90": [float(np.percentile(ms, 10) * 1e3), float(np.percentile(ms, 90) * 1e3)],
+        "tables_per_s": B * Hkv / (ms.mean() / 1e3),
+        "high_tokens_scanned_per_call": (hi0 + int(lens[:, 0].sum())) / 2.0,
+        "low_tokens_after": int(lens[:, 1].sum()),
+    }
+    log("generation step: %.1f us/call (%d tables)" % (res["us_per_call"], B * Hkv))
     return res
 
 

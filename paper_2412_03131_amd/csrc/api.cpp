@@ -140,8 +140,11 @@ AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits)
 
 int64_t compact_ws(int64_t T) { return align256(sizeof(CallFlags)) + 2 * align256(T * 4); }
 int64_t alloc_ws(int64_t T) { return align256(sizeof(CallFlags)) + align256(T * 16); }
-// generation step: the allocation's block, then per-table actions and page requests
-int64_t gen_ws(int64_t T) { return alloc_ws(T) + align256(T * 16) + align256(T * 8); }
+// generation step: call flags, per-table actions, page requests and ring offsets
+int64_t gen_ws(int64_t T)
+{
+    return align256(sizeof(CallFlags)) + 2 * align256(T * 16) + 2 * align256(T * 4);
+}
 
 }  // namespace
 
@@ -365,18 +368,6 @@ diffkv_status diffkv_generation_step(const diffkv_layout* layout, const diffkv_c
     if (T == 0) return DIFFKV_OK;
     if (!ws || (int64_t)ws_bytes < gen_ws(T)) return DIFFKV_E_WORKSPACE;
     uint8_t* base = static_cast<uint8_t*>(ws);
-    AllocArgs a;
-    memset(&a, 0, sizeof(a));
-    a.p_max = layout->p_max;
-    a.num_pages = cache->num_pages;
-    a.page_table = cache->page_table;
-    a.pages = cache->pages;
-    a.ring = cache->ring;
-    a.ring_ptr = cache->ring_ptr;
-    a.status = cache->status;
-    a.num_tables = (int)T;
-    a.flags = reinterpret_cast<CallFlags*>(base);
-    a.tstate = reinterpret_cast<int4*>(base + align256(sizeof(CallFlags)));
     GenArgs g;
     memset(&g, 0, sizeof(g));
     fill_layout_args(g, layout);
@@ -386,16 +377,21 @@ diffkv_status diffkv_generation_step(const diffkv_layout* layout, const diffkv_c
     g.pages = cache->pages;
     g.len = cache->len;
     g.seq_len = cache->seq_len;
+    g.ring = cache->ring;
+    g.ring_ptr = cache->ring_ptr;
+    g.status = cache->status;
     g.Hkv = cache->num_kv_heads;
     g.num_tables = (int)T;
     g.alpha_h = alpha_h;
     g.alpha_l = alpha_l;
     g.window = recent_window;
-    g.flags = a.flags;
-    g.act = reinterpret_cast<int4*>(base + alloc_ws(T));
-    g.demand = reinterpret_cast<int32_t*>(base + alloc_ws(T) + align256(T * 16));
-    a.demand = g.demand;
-    hipError_t e = launch_generation(g, a, static_cast<hipStream_t>(stream));
+    int64_t o = 0;
+    g.flags = reinterpret_cast<CallFlags*>(base + o);  o += align256(sizeof(CallFlags));
+    g.act = reinterpret_cast<int4*>(base + o);         o += align256(T * 16);
+    g.ids = reinterpret_cast<int4*>(base + o);         o += align256(T * 16);
+    g.demand = reinterpret_cast<int32_t*>(base + o);   o += align256(T * 4);
+    g.offset = reinterpret_cast<int32_t*>(base + o);
+    hipError_t e = launch_generation(g, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
 }
 

@@ -89,16 +89,21 @@ enum GenAction : int32_t {
 struct GenArgs : LayoutArgs {
     uint8_t* pool;
     long long num_pages;
-    const int32_t* page_table;
-    const int32_t* pages;
+    int32_t* page_table;
+    int32_t* pages;
     int32_t* len;
     const int32_t* seq_len;
+    int32_t* ring;
+    int64_t* ring_ptr;
+    uint32_t* status;
     int Hkv, num_tables;
     float alpha_h, alpha_l;
     int window;
-    const CallFlags* flags;  // written by the allocation kernels of the same call
-    int4* act;               // [num_tables] {action, candidate index, victim index or -1, 0}
-    int32_t* demand;         // [num_tables][2] pages the step takes: {0, 0 or 1}
+    CallFlags* flags;  // ring head/tail before the call; `ok` of the separate plan kernel
+    int4* act;         // [num_tables] {action, high index leaving, low index written, 0}
+    int4* ids;         // [num_tables] page IDs {leaving token, last high token, low target or -1, 0}
+    int32_t* demand;   // [num_tables] bit 0: takes a low page; bit 1: would exceed p_max
+    int32_t* offset;   // [num_tables] ring offset of the table's page (separate plan kernel)
 };
 
 struct AttnArgs {
@@ -127,7 +132,7 @@ constexpr int kAttnMaxWorkers = 2048;
 hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st);
 hipError_t launch_alloc(const AllocArgs& a, hipStream_t st);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
-hipError_t launch_generation(const GenArgs& g, const AllocArgs& a, hipStream_t st);
+hipError_t launch_generation(const GenArgs& g, hipStream_t st);
 hipError_t launch_attention(AttnArgs a, hipStream_t st);
 bool attention_layout_matches(const diffkv_layout* L);
 

@@ -71,8 +71,8 @@ def test_workspace_sizes(dk):
     a2 = dk.workspace_size(dk.OP_APPEND, L, 64, 0, 8, 2000)
     assert a2 > a1 >= 1000 * 8 * 4
     assert dk.workspace_size(dk.OP_COMPACT, L, 512, 0, 8) >= 2 * 4096 * 4
-    # generation step: allocation block plus an action record and a page request per table
-    assert dk.workspace_size(dk.OP_GENERATION, L, 64, 0, 8) >= 512 * (16 + 16 + 8)
+    # generation step: an action record, page IDs, a page request and a ring offset per table
+    assert dk.workspace_size(dk.OP_GENERATION, L, 64, 0, 8) >= 512 * (16 + 16 + 4 + 4)
 
 
 def test_argument_checks_enqueue_nothing(dk):

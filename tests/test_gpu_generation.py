@@ -166,6 +166,20 @@ def test_table_overflow_refused_identically():
     assert seen["refused"] > 0 and seen["bits"] == dk.ST_TABLE_OVERFLOW
 
 
+@pytest.mark.parametrize("free", [None, 40])
+def test_many_tables_separate_plan(free):
+    """More tables than one apply wave plans for (520 sequences x 8 KV heads): the
+    allocation is planned by its own kernel; with a short ring, steps are refused."""
+    lens = np.random.default_rng(15).integers(6, 60, 520)
+    oc, dc, seen = _run(15, lens, 8, 4, 4, 24000, 128, alpha=(1.5, 0.2), f_hi=0.5,
+                        f_pr=0.1, free_after_prompt=free)
+    assert oc.num_tables > 4096 and seen["page_taken"] + seen["refused"] > 0
+    if free is None:
+        assert seen["refused"] == 0 and seen["page_taken"] > 0
+    else:
+        assert seen["refused"] > 0 and seen["bits"] == dk.ST_OUT_OF_PAGES
+
+
 def test_full_size_llama8b_window64():
     """The llama8b workload (B = 64, Hkv = 8, contexts 1024-4096) at full size with the
     64-token window: prompt append, six decode steps with the generation policy,

@@ -110,7 +110,7 @@ def main():
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the DiffKV path shards by KV head or by request "
               "with no exchange between GPUs, so a multi-GPU figure is N independent copies "
-              "of this one (see DESIGN.md, 'More than one GPU').", file=sys.stderr)
+              "of this one.", file=sys.stderr)
         sys.exit(2)
     import torch
 
@@ -454,7 +454,7 @@ def generation_bench(torch, dk, lib, dev, sptr, steps, window=64):
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     torch.cuda.synchronize()
-    hi0 = int(c.len[:, 0].sum().item())
+    lens0, pages0 = c.len.cpu().numpy().copy(), c.pages.cpu().numpy().copy()
     torch.cuda._sleep(int(2.4e9 * 1e-4 * steps) + 1)  # the host enqueues ahead of the GPU
     rc = 0
     for s in range(steps):
@@ -466,15 +466,25 @@ def generation_bench(torch, dk, lib, dev, sptr, steps, window=64):
     if rc or int(c.status.item()) != 0:
         raise RuntimeError("generation bench failed (rc %d, status %d)" % (rc, int(c.status.item())))
     ms = np.array([a.elapsed_time(b) for a, b in ev])
-    lens = c.len.cpu().numpy()
+    lens, pages = c.len.cpu().numpy(), c.pages.cpu().numpy()
+    # algorithmic bytes of one call: the decision reads every kept token's position
+    # and score (8 B) and every used page-table entry (4 B) plus 40 B of per-table
+    # words; applying reads and writes the 1 KiB V code rows of the three pages a
+    # table touches (6 KiB) and the codes, metadata, score and position of the two
+    # high tokens it reads and the slots it writes (about 0.4 KiB)
+    tok = (int(lens0.sum()) + int(lens.sum())) / 2.0
+    pg = (int(pages0.sum()) + int(pages.sum())) / 2.0
+    nbytes = 8 * tok + 4 * pg + 40 * B * Hkv + (6 * 1024 + 400) * B * Hkv
     res = {
         "workload": "llama8b, 1 layer: B=64, Hkv=8 (512 tables), window 64, alpha_h 1.0, "
                     "alpha_l 0.5, %d decode steps" % steps,
         "us_per_call": float(ms.mean() * 1e3),
         "us_p10_p90": [float(np.percentile(ms, 10) * 1e3), float(np.percentile(ms, 90) * 1e3)],
         "tables_per_s": B * Hkv / (ms.mean() / 1e3),
-        "high_tokens_scanned_per_call": (hi0 + int(lens[:, 0].sum())) / 2.0,
-        "low_tokens_after": int(lens[:, 1].sum()),
+        "kv_tokens_per_call": tok,
+        "algorithmic_bytes_per_call": nbytes,
+        "achieved_gbps": nbytes / (ms.mean() / 1e3) / 1e9,
+        "bound": "latency: each of the two kernels waits on two dependent rounds of loads",
     }
     log("generation step: %.1f us/call (%d tables)" % (res["us_per_call"], B * Hkv))
     return res

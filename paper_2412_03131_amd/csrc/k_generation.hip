@@ -34,9 +34,9 @@ namespace dkv {
 constexpr int kGenThreads = 256;
 constexpr int kGenWaves = kGenThreads / kWave;
 constexpr int kGenChunk = 4;           // groups of 4 tokens a thread loads before reducing them
-constexpr int kGenFusedTables = 4096;  // up to this many tables each apply wave plans the allocation
+constexpr int kGenFusedTables = 2048;  // up to this many tables each apply wave plans the allocation
 constexpr int kGenScanThreads = 1024;
-constexpr int kGenPlanIlp = 8;         // page requests a lane of an apply wave loads at once
+constexpr int kGenPlanIlp = 16;        // page requests a lane of an apply wave loads at once
 
 // The victim search orders tokens by score (-0 == +0), then position, as one
 // 64-bit key: the score's order-preserving image above the position.  Positions

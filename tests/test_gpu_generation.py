@@ -166,18 +166,27 @@ def test_table_overflow_refused_identically():
     assert seen["refused"] > 0 and seen["bits"] == dk.ST_TABLE_OVERFLOW
 
 
-@pytest.mark.parametrize("free", [None, 40])
-def test_many_tables_separate_plan(free):
-    """More tables than one apply wave plans for (520 sequences x 8 KV heads): the
-    allocation is planned by its own kernel; with a short ring, steps are refused."""
-    lens = np.random.default_rng(15).integers(6, 60, 520)
+@pytest.mark.parametrize("nseq,free", [(520, None), (520, 40), (200, None)])
+def test_many_tables(nseq, free):
+    """Many tables: 4160 (520 sequences x 8 KV heads, more than an apply wave plans
+    for: the allocation is planned by its own kernel; with a short ring, steps are
+    refused) and 1600 (each apply wave plans over two rounds of page requests)."""
+    lens = np.random.default_rng(15).integers(6, 60, nseq)
     oc, dc, seen = _run(15, lens, 8, 4, 4, 24000, 128, alpha=(1.5, 0.2), f_hi=0.5,
                         f_pr=0.1, free_after_prompt=free)
-    assert oc.num_tables > 4096 and seen["page_taken"] + seen["refused"] > 0
+    assert oc.num_tables in (4160, 1600) and seen["page_taken"] + seen["refused"] > 0
     if free is None:
         assert seen["refused"] == 0 and seen["page_taken"] > 0
     else:
         assert seen["refused"] > 0 and seen["bits"] == dk.ST_OUT_OF_PAGES
+
+
+def test_long_context_tables():
+    """Two sequences of 12000 and 9000 tokens (high sections of ~4000-8000 tokens):
+    every decide thread walks several rounds of 2048-token chunks."""
+    oc, dc, seen = _run(16, [12000, 9000], 2, 64, 6, 2400, 12160, alpha=(1.0, 0.5),
+                        f_hi=0.6, f_pr=0.1, check={0, 5})
+    assert seen["refused"] == 0 and max(oc.len[:, 0]) > 4096
 
 
 def test_full_size_llama8b_window64():

@@ -10,9 +10,10 @@ U[0.2, 0.6], K8V4 / K4V2 with group-32 fp16 scale/zero, 16/32 tokens per page), 
 One step = one continuous-batching decode step of the whole path:
   1. request r = step mod 64 finishes: its pages in every layer go back to the free list
      (diffkv_compact_free_list, one call for all layers);
-  2. per layer: a replacement request is prefilled into slot r while the other 63
+  2. a replacement request is prefilled into slot r of every layer while the other 63
      append their newest token (diffkv_quantize_append: classing, allocation,
-     quantization, placement);
+     quantization, placement), one call for all layers and requests, as the paper runs
+     its KV compaction once per inference step (Sec. 5.3);
   3. per layer: decode attention over the whole batch (diffkv_decode_attention).
 
 value = KV tokens attended per second of step time, where a KV token is one kept
@@ -185,8 +186,12 @@ def main():
         q_np[r] = w["quota"][r]
         n_np = np.ones(B, np.int32)
         n_np[r] = nl[r]
-        steps_in.append(dict(r=r, k=k_s, v=v_s, score=s_s, quota=T(q_np), new_len=T(n_np),
-                             total=int(n_np.sum()), maxn=int(n_np.max()), q=T(d["q"])))
+        # every layer's rows in one call: sequence l*B + b of the whole cache is
+        # sequence b of layer l, so the layers' row blocks follow each other
+        steps_in.append(dict(r=r, k=torch.cat([k_s] * NL), v=torch.cat([v_s] * NL),
+                             score=torch.cat([s_s] * NL), quota=T(np.tile(q_np, (NL, 1, 1))),
+                             new_len=T(np.tile(n_np, NL)), total=NL * int(n_np.sum()),
+                             maxn=int(n_np.max()), q=T(d["q"])))
     P = L.p_max
     masks = []
     for r in range(B):
@@ -199,6 +204,9 @@ def main():
                          dtype=torch.uint8, device=dev)
     ws_c = torch.empty(dk.workspace_size(dk.OP_COMPACT, L, NL * B, 0, Hkv), dtype=torch.uint8,
                        device=dev)
+    ws_all = torch.empty(dk.workspace_size(dk.OP_APPEND, L, NL * B, 0, Hkv,
+                                           max(si["total"] for si in steps_in)) + 256,
+                         dtype=torch.uint8, device=dev)
     out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
 
@@ -209,9 +217,9 @@ def main():
     vp = lambda x: C.c_void_p(x.data_ptr())
     attn_args, app_args = [], []
     for s, si in enumerate(steps_in):
-        app_args.append([(Lp, C.byref(cs), si["total"], si["maxn"], vp(si["new_len"]), vp(si["k"]),
-                          vp(si["v"]), vp(si["score"]), vp(si["quota"]), 0.0, 0.0, 0, vp(ws_a),
-                          ws_a.numel(), sptr) for cs in cstructs])
+        app_args.append((Lp, C.byref(call_struct), si["total"], si["maxn"], vp(si["new_len"]),
+                         vp(si["k"]), vp(si["v"]), vp(si["score"]), vp(si["quota"]), 0.0, 0.0, 0,
+                         vp(ws_all), ws_all.numel(), sptr))
         attn_args.append([(Lp, C.byref(cs), Hq, vp(si["q"]), float(SCALE), vp(out), vp(lse), S,
                            vp(ws_att), ws_att.numel(), sptr) for cs in cstructs])
     comp_args = [(Lp, C.byref(call_struct), NL * B * Hkv, vp(m), vp(ws_c), ws_c.numel(), sptr)
@@ -222,15 +230,14 @@ def main():
           for _ in range(args.steps)]
 
     def run_step(s, timed_idx):
-        # every layer's append, then every layer's attention back to back (the
+        # one append for all layers, then every layer's attention back to back (the
         # events around the attention calls then see kernel time, not the dispatch
-        # gap after an append)
+        # gap after the append)
         si = steps_in[s]
         r = si["r"]
         rc = lib.diffkv_compact_free_list(*comp_args[r])
         cache.seq_len.index_fill_(0, seq_rows[r], 0)
-        for l in range(NL):
-            rc |= lib.diffkv_quantize_append(*app_args[s][l])
+        rc |= lib.diffkv_quantize_append(*app_args[s])
         if timed_idx is not None:
             ev[timed_idx][0].record(stream)
         for l in range(NL):
@@ -285,8 +292,9 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     status = int(cache.status.item())
-    got = cache.len.view(NL, B, Hkv, 2)[0].cpu().numpy()
-    if status != 0 or not (np.array_equal(got[..., 0], len_hi) and np.array_equal(got[..., 1], len_lo)):
+    got = cache.len.view(NL, B, Hkv, 2).cpu().numpy()
+    if status != 0 or not all(np.array_equal(g[..., 0], len_hi) and np.array_equal(g[..., 1], len_lo)
+                              for g in got):
         raise RuntimeError("state check failed after the timed steps (status %d)" % status)
     attn_ms = np.array([[a.elapsed_time(b) / NL] * NL for a, b in ev])  # [steps, layers], per launch
     timed = slice(args.warmup, steps_total)
@@ -322,8 +330,9 @@ def main():
         "config": {
             "workload": "llama8b decode step: B=64, Hq=32, Hkv=8, D=128, ctx U[1024,4096], "
                         "f_hi U[0.1,0.5], f_pr U[0.2,0.6], K8V4/K4V2 group 32, 16/32 tokens "
-                        "per page; per step 1 request recycled + re-prefilled, 63 decode "
-                        "appends, attention; %d layers on one page pool" % NL,
+                        "per page; per step 1 request recycled + re-prefilled and 63 decode "
+                        "appends (one append call for all layers), then attention per layer; "
+                        "%d layers on one page pool" % NL,
             "global_batch": B,
             "layers": NL,
             "attention_splits": S,

@@ -98,8 +98,8 @@ void fill_layout_args(LayoutArgs& a, const diffkv_layout* L)
 }
 
 struct AppendWs {
-    int64_t flags, tstate, sold, row_off, ord, total;
-    int64_t max_jobs;  // bound on the call's page jobs (sizes the commit grid)
+    int64_t flags, tstate, sold, row_off, ord, tplan, job_table, total;
+    int64_t max_jobs;  // bound on the call's page jobs (sizes the commit grid and the job map)
 };
 
 AppendWs append_ws(int64_t B, int64_t Hkv, int64_t total_new)
@@ -107,12 +107,15 @@ AppendWs append_ws(int64_t B, int64_t Hkv, int64_t total_new)
     AppendWs w;
     const int64_t T = B * Hkv;
     w.max_jobs = Hkv * ((3 * total_new + 31) / 32 + 4 * B);
+    const bool planned = append_planned(B, Hkv);
     int64_t o = 0;
     w.flags = o;   o = align256(o + (int64_t)sizeof(CallFlags));
     w.tstate = o;  o = align256(o + T * (int64_t)sizeof(TState));
     w.sold = o;    o = align256(o + B * 4);
     w.row_off = o; o = align256(o + B * 4);
     w.ord = o;     o = align256(o + total_new * Hkv * 4);
+    w.tplan = o;   o = align256(o + (planned ? T * 8 : 0));
+    w.job_table = o; o = align256(o + (planned ? w.max_jobs * 4 : 0));
     w.total = o;
     return w;
 }
@@ -238,9 +241,14 @@ diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_c
     a.sold = reinterpret_cast<int32_t*>(base + w.sold);
     a.row_off = reinterpret_cast<int32_t*>(base + w.row_off);
     a.ord = reinterpret_cast<int32_t*>(base + w.ord);
-    // every commit workgroup reads all tables' plan state once, so the grid is
-    // capped; workgroups loop over the jobs beyond it
-    int64_t grid = w.max_jobs < 1024 ? w.max_jobs : 1024;
+    a.tplan = reinterpret_cast<long long*>(base + w.tplan);
+    a.job_table = reinterpret_cast<int32_t*>(base + w.job_table);
+    a.job_cap = (int)w.max_jobs;
+    // without a planning launch every commit workgroup reads all tables' plan
+    // state once, so the grid is capped lower; workgroups loop over the jobs
+    // beyond it
+    const int64_t cap = append_planned(B, H) ? 4096 : 1024;
+    int64_t grid = w.max_jobs < cap ? w.max_jobs : cap;
     if (grid < 1) grid = 1;
     hipError_t e = launch_append(a, (int)grid, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;

@@ -45,7 +45,15 @@ struct AppendArgs : LayoutArgs {
     int32_t* sold;
     int32_t* row_off;
     int32_t* ord;
+    long long* tplan;    // [tables] exclusive prefix (new pages | jobs << 32), planned path
+    int32_t* job_table;  // [job_cap] table of each page job, planned path
+    int job_cap;
 };
+
+// Above this many tables an append plans once in its own launch instead of in
+// every commit workgroup.
+constexpr int kAppendPlanTables = 1024;
+inline bool append_planned(long long B, long long Hkv) { return B * Hkv > kAppendPlanTables; }
 
 struct AllocArgs {
     int p_max;

@@ -352,6 +352,166 @@ struct JobDesc {
     long long ring_idx;  // ring position of a new page, -1 for a page already held
 };
 
+// Job `job` of table t (its plan tp, its exclusive prefix pre = new pages |
+// jobs << 32): section, page, token range, table slot and, for a new page, the
+// ring index (the table's ring region, high pages first).
+__device__ __forceinline__ void describe_job(JobDesc& d, int t, const TState& s, const TablePlan& tp,
+                                             long long pre, int job, int P, long long head_old)
+{
+    const int lj = job - (int)(pre >> 32);
+    const int sec = lj < tp.jobs[0] ? 0 : 1;
+    const int TT = sec ? kTLo : kTHi;
+    const int p = page_of(s.lold[sec], sec) + (sec ? lj - tp.jobs[0] : lj);
+    const int lo = s.lold[sec], hi_end = s.lold[sec] + s.cnt[sec];
+    d.t = t;
+    d.sec = sec;
+    d.p = p;
+    d.u0 = lo > p * TT ? lo : p * TT;
+    d.u1 = hi_end < (p + 1) * TT ? hi_end : (p + 1) * TT;
+    d.lold = lo;
+    d.n = s.n;
+    d.tslot = sec ? P - 1 - p : p;
+    d.ring_idx = p < s.pold[sec] ? -1 : head_old + (pre & 0xffffffffll) + (sec ? tp.need[0] : 0) + (p - s.pold[sec]);
+}
+
+// One page job: resolve the page ID (a new page from the table's ring region),
+// quantize the job's tokens and write them, zero a fresh page's unused bytes.
+// Called by every thread of the workgroup after `s_job` is described.
+__device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s_job,
+                                           uint64_t (*s_rows)[kWave][2])
+{
+    const int tid = threadIdx.x;
+    const int P = a.p_max;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = wave_index();
+    const int grp = lane >> 4;
+    const int H = a.Hkv;
+    const long long page_bytes = a.page_bytes;
+    const int t = __builtin_amdgcn_readfirstlane(s_job.t);
+    const int sec = __builtin_amdgcn_readfirstlane(s_job.sec);
+    const int p = __builtin_amdgcn_readfirstlane(s_job.p);
+    const int u0 = __builtin_amdgcn_readfirstlane(s_job.u0);
+    const int u1 = __builtin_amdgcn_readfirstlane(s_job.u1);
+    const int lold = __builtin_amdgcn_readfirstlane(s_job.lold);
+    const int n = __builtin_amdgcn_readfirstlane(s_job.n);
+    const int tslot = __builtin_amdgcn_readfirstlane(s_job.tslot);
+    const long long ring_idx = s_job.ring_idx;
+    const int b = t / H, h = t - b * H;
+    const int TT = sec ? kTLo : kTHi;
+    const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
+    // the page ID (every wave reads the one entry), beside the token loads
+    int32_t* trow = a.page_table + (long long)t * P;
+    int id = ring_idx < 0 ? trow[tslot] : a.ring[ring_idx % a.num_pages];
+    id = __builtin_amdgcn_readfirstlane(id);
+    if (tid == 0 && ring_idx >= 0) trow[tslot] = id;
+    // this wave's tokens u0 + wave + kQuantWaves*i, all loaded up front; token
+    // u of the section is row ord[u - lold] (high, rank order) or
+    // ord[n - 1 - (u - lold)] (low ranks are stored from the back)
+    const int off_b = a.row_off[b];
+    const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
+    int jj[kTokLoad];
+    uint32_t kx[kTokLoad], vx[kTokLoad];
+#pragma unroll
+    for (int i = 0; i < kTokLoad; ++i) {
+        const int u = u0 + wave + i * kQuantWaves;
+        const int r = (u < u1 ? u : u0) - lold;
+        jj[i] = sec ? ord[n - 1 - r] : ord[r];
+    }
+#pragma unroll
+    for (int i = 0; i < kTokLoad; ++i) {
+        const long long row = (long long)(off_b + jj[i]) * H + h;
+        kx[i] = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
+        vx[i] = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
+    }
+    const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
+    const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
+    const bool fresh = (u0 == p * TT);
+    const bool page_ok = (unsigned)id < (unsigned)a.num_pages;  // never write outside the pool
+    uint8_t* pg = a.pool + (long long)(page_ok ? id : 0) * page_bytes;
+    // a page being continued keeps its earlier tokens' V code bits
+    uint4 vold = make_uint4(0, 0, 0, 0);
+    if (wave == 0 && page_ok && !fresh) vold = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
+    if (page_ok && fresh) {
+        // A fresh page reads as zero wherever no token lies: zero the token
+        // slots from u1 on in every per-token segment and the page tail.
+        // These bytes are disjoint from the ones the tokens write (V code
+        // rows are written whole, zeros included), so the stores need no
+        // ordering among themselves.
+        const int s_end = u1 - p * TT, nfill = TT - s_end;
+        const uint4 z4 = make_uint4(0, 0, 0, 0);
+        for (int i = tid; i < (kb + 1) * nfill; i += kCommitThreads) {
+            const int c = i / nfill, sl = s_end + (i - c * nfill);  // K chunks (kb per token), then K meta
+            uint8_t* dst = c < kb ? pg + off_kc + (c * TT + sl) * 16 : pg + off_km + sl * 16;
+            *reinterpret_cast<uint4*>(dst) = z4;
+        }
+        for (int i = tid; i < (kNG + 2) * nfill; i += kCommitThreads) {
+            const int g = i / nfill, sl = s_end + (i - g * nfill);  // V meta groups, score, pos
+            uint8_t* dst = g < kNG ? pg + off_vm + (g * TT + sl) * 4
+                                   : pg + (g == kNG ? a.off_score[sec] : a.off_pos[sec]) + sl * 4;
+            *reinterpret_cast<uint32_t*>(dst) = 0;
+        }
+        for (long long o = a.off_pos[sec] + (long long)TT * 4 + tid * 16; o < page_bytes; o += kCommitThreads * 16)
+            *reinterpret_cast<uint4*>(pg + o) = z4;
+    }
+    uint64_t row0 = 0, row1 = 0;
+    // two passes of kTokIlp tokens: quantize side by side, then store
+#pragma unroll
+    for (int pass = 0; pass < kTokLoad / kTokIlp; ++pass) {
+        const int base_u = u0 + wave + pass * kTokIlp * kQuantWaves;
+        if (base_u >= u1) break;  // wave-uniform: no token of this wave left in the page
+        uint32_t ksz[kTokIlp], kc0[kTokIlp], kc1[kTokIlp], vsz[kTokIlp], vc0[kTokIlp], vc1[kTokIlp];
+#pragma unroll
+        for (int i = 0; i < kTokIlp; ++i) {
+            if (base_u + i * kQuantWaves < u1) {
+                quant_pair(kx[pass * kTokIlp + i], (1 << kb) - 1, ksz[i], kc0[i], kc1[i]);
+                quant_pair(vx[pass * kTokIlp + i], (1 << vb) - 1, vsz[i], vc0[i], vc1[i]);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kTokIlp; ++i) {
+            const int u = base_u + i * kQuantWaves;
+            if (u >= u1) break;
+            const int sl = u - p * TT;
+            row0 |= (uint64_t)vc0[i] << (sl * vb);
+            row1 |= (uint64_t)vc1[i] << (sl * vb);
+            if (!page_ok) continue;
+            const long long row = (long long)(off_b + jj[pass * kTokIlp + i]) * H + h;
+            if (kb == 8) {
+                uint16_t* dst = reinterpret_cast<uint16_t*>(pg + off_kc + ((lane >> 3) * TT + sl) * 16 +
+                                                            ((2 * lane) & 15));
+                *dst = (uint16_t)(kc0[i] | (kc1[i] << 8));
+            } else {
+                uint8_t* dst = pg + off_kc + (grp * TT + sl) * 16 + (lane & 15);
+                *dst = (uint8_t)(kc0[i] | (kc1[i] << 4));
+            }
+            if ((lane & 15) == 0) {
+                *reinterpret_cast<uint32_t*>(pg + off_km + (sl * kNG + grp) * 4) = ksz[i];
+                *reinterpret_cast<uint32_t*>(pg + off_vm + (grp * TT + sl) * 4) = vsz[i];
+            }
+            if (lane == 0) {
+                reinterpret_cast<float*>(pg + a.off_score[sec])[sl] = a.score[row];
+                reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[sl] = a.sold[b] + jj[pass * kTokIlp + i];
+            }
+        }
+    }
+    // the page's dimension-major V code rows: OR of the waves' bits (and of the
+    // bits already on a page being continued), one store per dimension pair
+    s_rows[wave][lane][0] = row0;
+    s_rows[wave][lane][1] = row1;
+    __syncthreads();
+    if (wave == 0 && page_ok) {
+        uint64_t r0 = ((uint64_t)vold.y << 32) | vold.x;
+        uint64_t r1 = ((uint64_t)vold.w << 32) | vold.z;
+#pragma unroll
+        for (int w = 0; w < kQuantWaves; ++w) {
+            r0 |= s_rows[w][lane][0];
+            r1 |= s_rows[w][lane][1];
+        }
+        *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
+            make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
+    }
+}
+
 constexpr int kPlanKeep = 2;  // tables per thread whose state stays in registers
 
 __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
@@ -420,11 +580,6 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
     }
 
     // ---- page jobs ------------------------------------------------------------
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = wave_index();
-    const int grp = lane >> 4;
-    const int H = a.Hkv;
-    const long long page_bytes = a.page_bytes;
     for (int job = blockIdx.x; job < njobs; job += gridDim.x) {
         // the thread whose run of tables holds this job describes it
         const int run_first = (int)(before >> 32);
@@ -435,152 +590,100 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
                 if (s.n < 0) continue;
                 const TablePlan tp = table_plan(s, P);
                 const int jo = (int)(pre >> 32);
-                if (jo <= job && job < jo + tp.jobs[0] + tp.jobs[1]) {
-                    const int lj = job - jo;
-                    const int sec = lj < tp.jobs[0] ? 0 : 1;
-                    const int TT = sec ? kTLo : kTHi;
-                    const int p = page_of(s.lold[sec], sec) + (sec ? lj - tp.jobs[0] : lj);
-                    const int lo = s.lold[sec], hi_end = s.lold[sec] + s.cnt[sec];
-                    s_job.t = t;
-                    s_job.sec = sec;
-                    s_job.p = p;
-                    s_job.u0 = lo > p * TT ? lo : p * TT;
-                    s_job.u1 = hi_end < (p + 1) * TT ? hi_end : (p + 1) * TT;
-                    s_job.lold = lo;
-                    s_job.n = s.n;
-                    s_job.tslot = sec ? P - 1 - p : p;
-                    // a new page comes from this table's ring region, high pages first
-                    s_job.ring_idx = p < s.pold[sec] ? -1
-                                                     : head_old + (pre & 0xffffffffll) + (sec ? tp.need[0] : 0) +
-                                                           (p - s.pold[sec]);
-                }
+                if (jo <= job && job < jo + tp.jobs[0] + tp.jobs[1])
+                    describe_job(s_job, t, s, tp, pre, job, P, head_old);
                 pre += plan_word(tp);
             }
         }
         __syncthreads();
-        const int t = __builtin_amdgcn_readfirstlane(s_job.t);
-        const int sec = __builtin_amdgcn_readfirstlane(s_job.sec);
-        const int p = __builtin_amdgcn_readfirstlane(s_job.p);
-        const int u0 = __builtin_amdgcn_readfirstlane(s_job.u0);
-        const int u1 = __builtin_amdgcn_readfirstlane(s_job.u1);
-        const int lold = __builtin_amdgcn_readfirstlane(s_job.lold);
-        const int n = __builtin_amdgcn_readfirstlane(s_job.n);
-        const int tslot = __builtin_amdgcn_readfirstlane(s_job.tslot);
-        const long long ring_idx = s_job.ring_idx;
-        const int b = t / H, h = t - b * H;
-        const int TT = sec ? kTLo : kTHi;
-        const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
-        // the page ID (every wave reads the one entry), beside the token loads
-        int32_t* trow = a.page_table + (long long)t * P;
-        int id = ring_idx < 0 ? trow[tslot] : a.ring[ring_idx % a.num_pages];
-        id = __builtin_amdgcn_readfirstlane(id);
-        if (tid == 0 && ring_idx >= 0) trow[tslot] = id;
-        // this wave's tokens u0 + wave + kQuantWaves*i, all loaded up front; token
-        // u of the section is row ord[u - lold] (high, rank order) or
-        // ord[n - 1 - (u - lold)] (low ranks are stored from the back)
-        const int off_b = a.row_off[b];
-        const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
-        int jj[kTokLoad];
-        uint32_t kx[kTokLoad], vx[kTokLoad];
-#pragma unroll
-        for (int i = 0; i < kTokLoad; ++i) {
-            const int u = u0 + wave + i * kQuantWaves;
-            const int r = (u < u1 ? u : u0) - lold;
-            jj[i] = sec ? ord[n - 1 - r] : ord[r];
+        commit_job(a, s_job, s_rows);
+        if (job + (int)gridDim.x < njobs) __syncthreads();  // s_job and s_rows are reused by the next job
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Many tables: the plan once (append_plan, one workgroup), then the jobs
+// (append_commit_planned).  Every commit workgroup redoing the plan costs
+// O(tables) each; past kAppendPlanTables tables one planning launch is cheaper.
+// The plan writes each table's exclusive prefix, a job -> table map and the
+// state after the call; a commit workgroup reads its job's table directly.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
+{
+    const int tid = threadIdx.x;
+    const int NT = a.B * a.Hkv;
+    const int P = a.p_max;
+    __shared__ long long s_scan[kPlanThreads / kWave];
+    __shared__ uint32_t s_bits[kPlanThreads / kWave];
+    const long long head_old = a.flags->head_old, tail_old = a.flags->tail_old;
+    const int per = (NT + kPlanThreads - 1) / kPlanThreads;
+    const int t0 = tid * per;
+    const int t1 = t0 + per < NT ? t0 + per : NT;
+    long long packed = 0;
+    uint32_t bits = 0;
+    for (int t = t0; t < t1; ++t) {
+        const TState s = a.tstate[t];
+        if (s.n < 0) {
+            bits |= DIFFKV_ST_BAD_INPUT;
+            continue;
         }
-#pragma unroll
-        for (int i = 0; i < kTokLoad; ++i) {
-            const long long row = (long long)(off_b + jj[i]) * H + h;
-            kx[i] = reinterpret_cast<const uint32_t*>(a.k + row * kD)[lane];
-            vx[i] = reinterpret_cast<const uint32_t*>(a.v + row * kD)[lane];
+        const TablePlan tp = table_plan(s, P);
+        if (tp.held_over) bits |= DIFFKV_ST_TABLE_OVERFLOW;
+        packed += plan_word(tp);
+    }
+    long long tot;
+    uint32_t all_bits;
+    const long long before = block_excl_scan<long long>(packed, s_scan, &tot, bits, s_bits, &all_bits);
+    bits = all_bits & (DIFFKV_ST_BAD_INPUT | DIFFKV_ST_TABLE_OVERFLOW);
+    const long long total_need = tot & 0xffffffffll;
+    const int njobs = (int)(tot >> 32);
+    if (bits & DIFFKV_ST_BAD_INPUT) bits = DIFFKV_ST_BAD_INPUT;
+    else if (total_need > tail_old - head_old) bits |= DIFFKV_ST_OUT_OF_PAGES;
+    if (njobs > a.job_cap) bits |= DIFFKV_ST_BAD_INPUT;  // never with the host's bound; keeps the map in bounds
+    if (bits) {  // all or nothing: no state, table or page changes
+        if (tid == 0) {
+            atomicOr(a.status, bits);
+            a.flags->ok = 0;
         }
-        const int off_kc = a.off_kcode[sec], off_km = a.off_kmeta[sec];
-        const int off_vc = a.off_vcode[sec], off_vm = a.off_vmeta[sec];
-        const bool fresh = (u0 == p * TT);
-        const bool page_ok = (unsigned)id < (unsigned)a.num_pages;  // never write outside the pool
-        uint8_t* pg = a.pool + (long long)(page_ok ? id : 0) * page_bytes;
-        // a page being continued keeps its earlier tokens' V code bits
-        uint4 vold = make_uint4(0, 0, 0, 0);
-        if (wave == 0 && page_ok && !fresh) vold = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
-        if (page_ok && fresh) {
-            // A fresh page reads as zero wherever no token lies: zero the token
-            // slots from u1 on in every per-token segment and the page tail.
-            // These bytes are disjoint from the ones the tokens write (V code
-            // rows are written whole, zeros included), so the stores need no
-            // ordering among themselves.
-            const int s_end = u1 - p * TT, nfill = TT - s_end;
-            const uint4 z4 = make_uint4(0, 0, 0, 0);
-            for (int i = tid; i < (kb + 1) * nfill; i += kCommitThreads) {
-                const int c = i / nfill, sl = s_end + (i - c * nfill);  // K chunks (kb per token), then K meta
-                uint8_t* dst = c < kb ? pg + off_kc + (c * TT + sl) * 16 : pg + off_km + sl * 16;
-                *reinterpret_cast<uint4*>(dst) = z4;
-            }
-            for (int i = tid; i < (kNG + 2) * nfill; i += kCommitThreads) {
-                const int g = i / nfill, sl = s_end + (i - g * nfill);  // V meta groups, score, pos
-                uint8_t* dst = g < kNG ? pg + off_vm + (g * TT + sl) * 4
-                                       : pg + (g == kNG ? a.off_score[sec] : a.off_pos[sec]) + sl * 4;
-                *reinterpret_cast<uint32_t*>(dst) = 0;
-            }
-            for (long long o = a.off_pos[sec] + (long long)TT * 4 + tid * 16; o < page_bytes; o += kCommitThreads * 16)
-                *reinterpret_cast<uint4*>(pg + o) = z4;
+        return;
+    }
+    long long pre = before;
+    for (int t = t0; t < t1; ++t) {
+        const TState s = a.tstate[t];
+        const TablePlan tp = table_plan(s, P);
+        a.tplan[t] = pre;
+        const int j0 = (int)(pre >> 32);
+        for (int k = 0; k < tp.jobs[0] + tp.jobs[1]; ++k) a.job_table[j0 + k] = t;
+#pragma unroll
+        for (int sec = 0; sec < 2; ++sec) {
+            a.len[2 * t + sec] = s.lold[sec] + s.cnt[sec];
+            a.pages[2 * t + sec] = s.pold[sec] + tp.need[sec];
         }
-        uint64_t row0 = 0, row1 = 0;
-        // two passes of kTokIlp tokens: quantize side by side, then store
-#pragma unroll
-        for (int pass = 0; pass < kTokLoad / kTokIlp; ++pass) {
-            const int base_u = u0 + wave + pass * kTokIlp * kQuantWaves;
-            if (base_u >= u1) break;  // wave-uniform: no token of this wave left in the page
-            uint32_t ksz[kTokIlp], kc0[kTokIlp], kc1[kTokIlp], vsz[kTokIlp], vc0[kTokIlp], vc1[kTokIlp];
-#pragma unroll
-            for (int i = 0; i < kTokIlp; ++i) {
-                if (base_u + i * kQuantWaves < u1) {
-                    quant_pair(kx[pass * kTokIlp + i], (1 << kb) - 1, ksz[i], kc0[i], kc1[i]);
-                    quant_pair(vx[pass * kTokIlp + i], (1 << vb) - 1, vsz[i], vc0[i], vc1[i]);
-                }
-            }
-#pragma unroll
-            for (int i = 0; i < kTokIlp; ++i) {
-                const int u = base_u + i * kQuantWaves;
-                if (u >= u1) break;
-                const int sl = u - p * TT;
-                row0 |= (uint64_t)vc0[i] << (sl * vb);
-                row1 |= (uint64_t)vc1[i] << (sl * vb);
-                if (!page_ok) continue;
-                const long long row = (long long)(off_b + jj[pass * kTokIlp + i]) * H + h;
-                if (kb == 8) {
-                    uint16_t* dst = reinterpret_cast<uint16_t*>(pg + off_kc + ((lane >> 3) * TT + sl) * 16 +
-                                                                ((2 * lane) & 15));
-                    *dst = (uint16_t)(kc0[i] | (kc1[i] << 8));
-                } else {
-                    uint8_t* dst = pg + off_kc + (grp * TT + sl) * 16 + (lane & 15);
-                    *dst = (uint8_t)(kc0[i] | (kc1[i] << 4));
-                }
-                if ((lane & 15) == 0) {
-                    *reinterpret_cast<uint32_t*>(pg + off_km + (sl * kNG + grp) * 4) = ksz[i];
-                    *reinterpret_cast<uint32_t*>(pg + off_vm + (grp * TT + sl) * 4) = vsz[i];
-                }
-                if (lane == 0) {
-                    reinterpret_cast<float*>(pg + a.off_score[sec])[sl] = a.score[row];
-                    reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[sl] = a.sold[b] + jj[pass * kTokIlp + i];
-                }
-            }
+        pre += plan_word(tp);
+    }
+    for (int b = tid; b < a.B; b += kPlanThreads) a.seq_len[b] = a.sold[b] + a.new_len[b];
+    if (tid == 0) {
+        a.ring_ptr[0] = head_old + total_need;
+        a.flags->njobs = njobs;
+        a.flags->ok = 1;
+    }
+}
+
+__global__ __launch_bounds__(kCommitThreads) void append_commit_planned(AppendArgs a)
+{
+    __shared__ JobDesc s_job;
+    __shared__ uint64_t s_rows[kQuantWaves][kWave][2];
+    if (!a.flags->ok) return;
+    const int njobs = a.flags->njobs;
+    const long long head_old = a.flags->head_old;
+    for (int job = blockIdx.x; job < njobs; job += gridDim.x) {
+        if (threadIdx.x == 0) {
+            const int t = a.job_table[job];
+            const TState s = a.tstate[t];
+            describe_job(s_job, t, s, table_plan(s, a.p_max), a.tplan[t], job, a.p_max, head_old);
         }
-        // the page's dimension-major V code rows: OR of the waves' bits (and of the
-        // bits already on a page being continued), one store per dimension pair
-        s_rows[wave][lane][0] = row0;
-        s_rows[wave][lane][1] = row1;
         __syncthreads();
-        if (wave == 0 && page_ok) {
-            uint64_t r0 = ((uint64_t)vold.y << 32) | vold.x;
-            uint64_t r1 = ((uint64_t)vold.w << 32) | vold.z;
-#pragma unroll
-            for (int w = 0; w < kQuantWaves; ++w) {
-                r0 |= s_rows[w][lane][0];
-                r1 |= s_rows[w][lane][1];
-            }
-            *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
-                make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
-        }
+        commit_job(a, s_job, s_rows);
         if (job + (int)gridDim.x < njobs) __syncthreads();  // s_job and s_rows are reused by the next job
     }
 }
@@ -779,7 +882,12 @@ __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
 hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st)
 {
     hipLaunchKernelGGL(append_classify, dim3((unsigned)(a.Hkv * a.B)), dim3(kClsThreads), 0, st, a);
-    hipLaunchKernelGGL(append_commit, dim3(grid_quant), dim3(kCommitThreads), 0, st, a);
+    if (append_planned(a.B, a.Hkv)) {
+        hipLaunchKernelGGL(append_plan, dim3(1), dim3(kPlanThreads), 0, st, a);
+        hipLaunchKernelGGL(append_commit_planned, dim3(grid_quant), dim3(kCommitThreads), 0, st, a);
+    } else {
+        hipLaunchKernelGGL(append_commit, dim3(grid_quant), dim3(kCommitThreads), 0, st, a);
+    }
     return hipGetLastError();
 }
 

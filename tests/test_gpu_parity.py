@@ -137,6 +137,43 @@ def test_append_all_or_nothing_on_device():
         assert np.array_equal(after[f], before[f]), f
 
 
+def test_append_many_tables_planned():
+    """More than 1024 tables (170 sequences x 8 KV heads): the plan runs once in its own
+    launch and commit workgroups read a job -> table map.  Two long prompts (hundreds of
+    page jobs each) among short ones, then decode steps in the threshold form, then the
+    all-or-nothing refusals on this path."""
+    rng = np.random.default_rng(21)
+    B, Hkv = 170, 8
+    new_len = rng.integers(0, 41, B).astype(np.int32)
+    new_len[[7, 120]] = [2500, 1700]
+    n = int(new_len.sum())
+    k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    score = rng.random((n, Hkv)).astype(np.float32)
+    quota = np.stack([(new_len[:, None] * rng.uniform(0.2, 0.6, (B, Hkv))).astype(np.int32),
+                      (new_len[:, None] * rng.uniform(0.1, 0.3, (B, Hkv))).astype(np.int32)], axis=2)
+    print("case: planned append, %d tables, %d rows" % (B * Hkv, n), flush=True)
+    Lo, Ld, oc, dc = _pair(9000, B, Hkv, 2600, seed=22)
+    _append_both(oc, dc, new_len, k, v, score, quota=quota, window=8)
+    assert oc.status[0] == 0
+    assert_state_equal(dc, oc, what="planned prompt")
+    for step in range(3):
+        nl = (rng.random(B) < 0.9).astype(np.int32)
+        m = int(nl.sum())
+        kd = rng.standard_normal((m, Hkv, 128)).astype(np.float16).view(np.uint16)
+        vd = rng.standard_normal((m, Hkv, 128)).astype(np.float16).view(np.uint16)
+        sd = (rng.random((m, Hkv)) * 0.01).astype(np.float32)
+        print("case: planned decode step %d" % step, flush=True)
+        _append_both(oc, dc, nl, kd, vd, sd, alpha_h=1.0, alpha_l=0.3)
+        assert oc.status[0] == 0
+        assert_state_equal(dc, oc, what="planned step %d" % step)
+    print("case: planned append out of pages", flush=True)
+    Lo, Ld, oc, dc = _pair(1500, B, Hkv, 2600, seed=23)
+    _append_both(oc, dc, new_len, k, v, score, quota=quota, window=8)
+    s = assert_state_equal(dc, oc, what="planned oop")
+    assert s["status"][0] == dk.ST_OUT_OF_PAGES and s["ring_ptr"][0] == 0
+
+
 # ------------------------------------------------------------- attention --
 def _attn_case(name, B, L, splits, seed_pages=20):
     w = inputs.prefill(name, B=B, L=L)

@@ -529,28 +529,25 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
     const int per = (NT + kCommitThreads - 1) / kCommitThreads;
     const int t0 = tid * per;
     const int t1 = t0 + per < NT ? t0 + per : NT;
-    TState st[kPlanKeep];
-#pragma unroll
-    for (int i = 0; i < kPlanKeep; ++i)
-        if (t0 + i < t1) st[i] = a.tstate[t0 + i];
-    auto state_of = [&](int t) -> TState {
-        static_assert(kPlanKeep == 2, "state_of picks from two registers");
-        if (t == t0) return st[0];
-        if (t == t0 + 1) return st[1];
-        return a.tstate[t];
+    // the run's first two tables stay in registers (static indices: no scratch)
+    static_assert(kPlanKeep == 2, "for_tables visits two kept states");
+    const TState st0 = a.tstate[min(t0, NT - 1)], st1 = a.tstate[min(t0 + 1, NT - 1)];
+    auto for_tables = [&](auto&& f) {
+        if (t0 < t1) f(t0, st0);
+        if (t0 + 1 < t1) f(t0 + 1, st1);
+        for (int t = t0 + 2; t < t1; ++t) f(t, a.tstate[t]);
     };
     long long packed = 0;
     uint32_t bits = 0;
-    for (int t = t0; t < t1; ++t) {
-        const TState s = state_of(t);
+    for_tables([&](int, const TState& s) {
         if (s.n < 0) {
             bits |= DIFFKV_ST_BAD_INPUT;
-            continue;
+            return;
         }
         const TablePlan tp = table_plan(s, P);
         if (tp.held_over) bits |= DIFFKV_ST_TABLE_OVERFLOW;
         packed += plan_word(tp);
-    }
+    });
     long long tot;
     uint32_t all_bits;
     const long long before = block_excl_scan<long long>(packed, s_scan, &tot, bits, s_bits, &all_bits);
@@ -566,15 +563,14 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
 
     // ---- workgroup 0: the state after the call -------------------------------
     if (blockIdx.x == 0) {
-        for (int t = t0; t < t1; ++t) {
-            const TState s = state_of(t);
+        for_tables([&](int t, const TState& s) {
             const TablePlan tp = table_plan(s, P);
 #pragma unroll
             for (int sec = 0; sec < 2; ++sec) {
                 a.len[2 * t + sec] = s.lold[sec] + s.cnt[sec];
                 a.pages[2 * t + sec] = s.pold[sec] + tp.need[sec];
             }
-        }
+        });
         for (int b = tid; b < a.B; b += kCommitThreads) a.seq_len[b] = a.sold[b] + a.new_len[b];
         if (tid == 0) a.ring_ptr[0] = head_old + total_need;
     }
@@ -585,15 +581,14 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
         const int run_first = (int)(before >> 32);
         if (run_first <= job && job < run_first + (int)(packed >> 32)) {
             long long pre = before;
-            for (int t = t0; t < t1; ++t) {
-                const TState s = state_of(t);
-                if (s.n < 0) continue;
+            for_tables([&](int t, const TState& s) {
+                if (s.n < 0) return;
                 const TablePlan tp = table_plan(s, P);
                 const int jo = (int)(pre >> 32);
                 if (jo <= job && job < jo + tp.jobs[0] + tp.jobs[1])
                     describe_job(s_job, t, s, tp, pre, job, P, head_old);
                 pre += plan_word(tp);
-            }
+            });
         }
         __syncthreads();
         commit_job(a, s_job, s_rows);
@@ -608,6 +603,9 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
 // The plan writes each table's exclusive prefix, a job -> table map and the
 // state after the call; a commit workgroup reads its job's table directly.
 // ---------------------------------------------------------------------------
+constexpr int kPlanLdsTables = 8192;  // up to this many tables the job map is built from LDS
+constexpr int kMapIlp = 4;            // jobs a thread maps side by side
+
 __global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
 {
     const int tid = threadIdx.x;
@@ -615,22 +613,30 @@ __global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
     const int P = a.p_max;
     __shared__ long long s_scan[kPlanThreads / kWave];
     __shared__ uint32_t s_bits[kPlanThreads / kWave];
+    __shared__ int32_t s_jobs[kPlanLdsTables + 1];  // first job of every table, then njobs
     const long long head_old = a.flags->head_old, tail_old = a.flags->tail_old;
     const int per = (NT + kPlanThreads - 1) / kPlanThreads;
     const int t0 = tid * per;
     const int t1 = t0 + per < NT ? t0 + per : NT;
+    // the first two tables' states, loaded together and unconditionally (a
+    // thread past the last table reloads table NT - 1 and ignores it)
+    const TState st0 = a.tstate[min(t0, NT - 1)], st1 = a.tstate[min(t0 + 1, NT - 1)];
+    auto for_tables = [&](auto&& f) {
+        if (t0 < t1) f(t0, st0);
+        if (t0 + 1 < t1) f(t0 + 1, st1);
+        for (int t = t0 + 2; t < t1; ++t) f(t, a.tstate[t]);
+    };
     long long packed = 0;
     uint32_t bits = 0;
-    for (int t = t0; t < t1; ++t) {
-        const TState s = a.tstate[t];
+    for_tables([&](int, const TState& s) {
         if (s.n < 0) {
             bits |= DIFFKV_ST_BAD_INPUT;
-            continue;
+            return;
         }
         const TablePlan tp = table_plan(s, P);
         if (tp.held_over) bits |= DIFFKV_ST_TABLE_OVERFLOW;
         packed += plan_word(tp);
-    }
+    });
     long long tot;
     uint32_t all_bits;
     const long long before = block_excl_scan<long long>(packed, s_scan, &tot, bits, s_bits, &all_bits);
@@ -647,25 +653,51 @@ __global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
         }
         return;
     }
+    const bool lds_map = NT <= kPlanLdsTables;  // job map by binary search in LDS
     long long pre = before;
-    for (int t = t0; t < t1; ++t) {
-        const TState s = a.tstate[t];
+    for_tables([&](int t, const TState& s) {
         const TablePlan tp = table_plan(s, P);
         a.tplan[t] = pre;
         const int j0 = (int)(pre >> 32);
-        for (int k = 0; k < tp.jobs[0] + tp.jobs[1]; ++k) a.job_table[j0 + k] = t;
+        if (lds_map) s_jobs[t] = j0;
+        else
+            for (int k = 0; k < tp.jobs[0] + tp.jobs[1]; ++k) a.job_table[j0 + k] = t;
 #pragma unroll
         for (int sec = 0; sec < 2; ++sec) {
             a.len[2 * t + sec] = s.lold[sec] + s.cnt[sec];
             a.pages[2 * t + sec] = s.pold[sec] + tp.need[sec];
         }
         pre += plan_word(tp);
-    }
+    });
     for (int b = tid; b < a.B; b += kPlanThreads) a.seq_len[b] = a.sold[b] + a.new_len[b];
     if (tid == 0) {
         a.ring_ptr[0] = head_old + total_need;
         a.flags->njobs = njobs;
         a.flags->ok = 1;
+    }
+    if (lds_map) {
+        // job j belongs to the last table whose first job is <= j (tables without
+        // jobs share their successor's prefix); every thread maps kMapIlp jobs side
+        // by side with a fixed-length search
+        if (tid == 0) s_jobs[NT] = njobs;
+        __syncthreads();
+        int steps = 0;
+        while ((1 << steps) < NT + 1) ++steps;
+        for (int j0 = tid; j0 < njobs; j0 += kPlanThreads * kMapIlp) {
+            int lo[kMapIlp];
+#pragma unroll
+            for (int i = 0; i < kMapIlp; ++i) lo[i] = 0;
+            for (int st = steps - 1; st >= 0; --st) {
+#pragma unroll
+                for (int i = 0; i < kMapIlp; ++i) {
+                    const int mid = lo[i] + (1 << st);
+                    if (mid <= NT && s_jobs[mid] <= j0 + i * kPlanThreads) lo[i] = mid;
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < kMapIlp; ++i)
+                if (j0 + i * kPlanThreads < njobs) a.job_table[j0 + i * kPlanThreads] = lo[i];
+        }
     }
 }
 

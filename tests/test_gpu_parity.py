@@ -174,6 +174,27 @@ def test_append_many_tables_planned():
     assert s["status"][0] == dk.ST_OUT_OF_PAGES and s["ring_ptr"][0] == 0
 
 
+def test_append_planned_beyond_lds_map():
+    """More tables than the planning workgroup maps through LDS (1100 sequences x 8 KV
+    heads = 8800): each thread writes its tables' entries of the job map itself."""
+    rng = np.random.default_rng(24)
+    B, Hkv = 1100, 8
+    Lo, Ld, oc, dc = _pair(12000, B, Hkv, 64, seed=25, garbage=False)
+    for step in range(2):
+        new_len = rng.integers(0, 6, B).astype(np.int32)
+        new_len[[3, 900]] = [40, 33]
+        n = int(new_len.sum())
+        k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+        v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+        score = rng.random((n, Hkv)).astype(np.float32)
+        quota = np.stack([(new_len[:, None] * rng.uniform(0.2, 0.6, (B, Hkv))).astype(np.int32),
+                          (new_len[:, None] * rng.uniform(0.1, 0.3, (B, Hkv))).astype(np.int32)], axis=2)
+        print("case: planned append without the LDS job map, step %d" % step, flush=True)
+        _append_both(oc, dc, new_len, k, v, score, quota=quota, window=1)
+        assert oc.status[0] == 0
+        assert_state_equal(dc, oc, what="8800 tables step %d" % step)
+
+
 # ------------------------------------------------------------- attention --
 def _attn_case(name, B, L, splits, seed_pages=20):
     w = inputs.prefill(name, B=B, L=L)

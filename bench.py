@@ -313,6 +313,9 @@ def main():
 
     # -------------------------------------------------------- cpu baseline --
     cpu = None if args.no_cpu_baseline else cpu_baseline(w, args.cpu_seconds)
+    if cpu is not None:  # on-GPU against on-CPU memory management, as the paper compares them
+        comp["cpu_oracle_us_per_round"] = cpu["compaction"]["us_per_round"]
+        comp["gpu_speedup_vs_cpu_oracle"] = cpu["compaction"]["us_per_round"] / comp["us_per_round"]
 
     line = {
         "metric": METRIC,
@@ -526,6 +529,37 @@ def cpu_baseline(w, seconds):
            "sample": "fp64 oracle attention over requests 0-7 of the llama8b workload "
                      "(%d KV tokens), %d passes, %.1f s CPU" % (tokens, reps, el)}
     log("cpu baseline: %.3g KV tokens/s" % res["value"])
+    res["compaction"] = cpu_compaction(seconds / 4)
+    return res
+
+
+def cpu_compaction(seconds):
+    """The oracle's free-list compaction (serial C, one thread) on the compaction
+    workload the GPU leg times: 2^20 pages, 4096 tables, Bernoulli(0.35) releases,
+    each round followed by the refill, rounds until `seconds` of CPU time."""
+    from oracle import oracle as orc
+    from paper_2412_03131_amd import inputs
+    cfg = inputs.CONFIGS["compact"]
+    ring, demand = inputs.compaction_setup()
+    n_tab = cfg["tables"]
+    Lo = orc.layout(max_seq_len=(cfg["p_max"] - 1) * 16)
+    oc = orc.Cache(Lo, cfg["num_pages"], n_tab, 1, ring=ring, with_pool=False)
+    orc.alloc_pages(oc, demand)
+    tpp = np.array([16, 32])
+    oc.len[:] = oc.pages * tpp
+    spent, rounds = 0.0, 0
+    while spent < seconds:
+        rel = inputs.release_mask(cfg["seed"], rounds, n_tab, Lo.p_max)
+        before = oc.pages.copy()
+        t0 = time.process_time()
+        orc.compact(oc, rel)
+        spent += time.process_time() - t0
+        orc.alloc_pages(oc, (before - oc.pages).astype(np.int32))
+        oc.len[:] = oc.pages * tpp
+        rounds += 1
+    res = {"us_per_round": spent / rounds * 1e6, "rounds": rounds, "cores": 1, "kind": "oracle",
+           "sample": "oracle compaction rounds of the 2^20-page, 4096-table workload (refill untimed)"}
+    log("cpu compaction: %.0f us/round" % res["us_per_round"])
     return res
 
 

@@ -40,6 +40,7 @@ __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; 
 constexpr int kClsThreads = 512;
 static_assert(kClsThreads >= 2 * kWave, "two waves scan the digit histograms");
 constexpr int kClsPer = 8;                       // tokens per thread in one tile
+static_assert(4 * kClsPer <= 32, "a thread keeps four flag bits per token of a tile in one 32-bit word");
 constexpr int kClsTile = kClsThreads * kClsPer;  // the first tile's scores stay in registers
 constexpr uint32_t kOffSat = 1u << 30;           // row offsets saturate here (above any total_new)
 

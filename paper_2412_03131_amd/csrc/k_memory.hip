@@ -793,8 +793,8 @@ __global__ __launch_bounds__(kWave) void alloc_write(AllocArgs a)
 }
 
 // ---------------------------------------------------------------------------
-// Compaction: compact_count (wave per table), compact_scan (one workgroup),
-// compact_apply (wave per table)
+// Compaction: compact_count (wave per table), compact_scan (one workgroup,
+// only above kCompactFusedTables tables), compact_apply (wave per table)
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ bool slot_live(int slot, int ph, int pl, int P)
 {
@@ -813,6 +813,8 @@ __global__ __launch_bounds__(kWave) void compact_count(CompactArgs a)
     for (int s = threadIdx.x; s < P; s += kWave) c += (rel[s] != 0 && slot_live(s, ph, pl, P));
     c = wave_isum_w<kWave>(c);
     if (threadIdx.x == 0) a.count[t] = c;
+    // the end pointer before the call, for an apply kernel that plans itself
+    if (t == 0 && threadIdx.x == 0) a.flags->tail_old = a.ring_ptr[1];
 }
 
 __global__ __launch_bounds__(kPlanThreads) void compact_scan(CompactArgs a)
@@ -838,12 +840,42 @@ __global__ __launch_bounds__(kPlanThreads) void compact_scan(CompactArgs a)
 }
 
 // One wave per table; the live part of the row is staged in LDS (dynamic
-// shared memory of 2*p_max ints) so the squeeze can write in place.
+// shared memory of 2*p_max ints) so the squeeze can write in place.  FUSED:
+// the wave sums every table's count itself (its ring offset and the total; the
+// wave of table 0 advances the end pointer), so no scan launch runs between
+// counting and applying; used up to kCompactFusedTables tables.
+constexpr int kCompactFusedTables = 2048;
+constexpr int kCompactPlanIlp = 16;  // counts a lane loads at once
+
+template <bool FUSED>
 __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
 {
     extern __shared__ int32_t s_row[];  // [0, P): old IDs, [P, 2P): new row
     const int t = blockIdx.x;
     const int lane = threadIdx.x;
+    int my_off;
+    if constexpr (FUSED) {
+        const int NT = a.num_tables;
+        int tot = 0, below = 0;
+        for (int base = 0; base < NT; base += kWave * kCompactPlanIlp) {
+            int cv[kCompactPlanIlp];
+#pragma unroll
+            for (int k = 0; k < kCompactPlanIlp; ++k)  // unconditional: all loads in flight together
+                cv[k] = a.count[min(base + lane + k * kWave, NT - 1)];
+#pragma unroll
+            for (int k = 0; k < kCompactPlanIlp; ++k) {
+                const int i = base + lane + k * kWave;
+                const int c = i < NT ? cv[k] : 0;
+                tot += c;
+                below += i < t ? c : 0;
+            }
+        }
+        tot = wave_isum_w<kWave>(tot);
+        my_off = wave_isum_w<kWave>(below);
+        if (t == 0 && lane == 0) a.ring_ptr[1] = a.flags->tail_old + tot;
+    } else {
+        my_off = a.offset[t];
+    }
     const int P = a.p_max;
     int ph = a.pages[2 * t], pl = a.pages[2 * t + 1];
     ph = ph < 0 ? 0 : (ph > P ? P : ph);  // same clamp as compact_count
@@ -853,7 +885,7 @@ __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
     const uint8_t* rel = a.release + (long long)t * P;
     int32_t* row = a.page_table + (long long)t * P;
     int32_t* s_new = s_row + P;
-    const long long base = a.flags->tail_old + a.offset[t];
+    const long long base = a.flags->tail_old + my_off;
     const uint64_t below = (1ull << lane) - 1ull;
     for (int s = lane; s < ph; s += kWave) s_row[s] = row[s];
     for (int s = P - pl + lane; s < P; s += kWave) s_row[s] = row[s];
@@ -935,9 +967,14 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t st)
 {
     if (a.num_tables == 0) return hipSuccess;
     hipLaunchKernelGGL(compact_count, dim3(a.num_tables), dim3(kWave), 0, st, a);
-    hipLaunchKernelGGL(compact_scan, dim3(1), dim3(kPlanThreads), 0, st, a);
-    hipLaunchKernelGGL(compact_apply, dim3(a.num_tables), dim3(kWave),
-                       (size_t)2 * a.p_max * sizeof(int32_t), st, a);
+    if (a.num_tables <= kCompactFusedTables) {
+        hipLaunchKernelGGL(compact_apply<true>, dim3(a.num_tables), dim3(kWave),
+                           (size_t)2 * a.p_max * sizeof(int32_t), st, a);
+    } else {
+        hipLaunchKernelGGL(compact_scan, dim3(1), dim3(kPlanThreads), 0, st, a);
+        hipLaunchKernelGGL(compact_apply<false>, dim3(a.num_tables), dim3(kWave),
+                           (size_t)2 * a.p_max * sizeof(int32_t), st, a);
+    }
     return hipGetLastError();
 }
 

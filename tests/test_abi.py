@@ -70,6 +70,10 @@ def test_workspace_sizes(dk):
     a1 = dk.workspace_size(dk.OP_APPEND, L, 64, 0, 8, 1000)
     a2 = dk.workspace_size(dk.OP_APPEND, L, 64, 0, 8, 2000)
     assert a2 > a1 >= 1000 * 8 * 4
+    # above 1024 tables the plan runs once and also needs per-table prefixes and a job map
+    small = dk.workspace_size(dk.OP_APPEND, L, 128, 0, 8, 4000)   # 1024 tables
+    large = dk.workspace_size(dk.OP_APPEND, L, 129, 0, 8, 4000)   # 1032 tables
+    assert large - small >= 1032 * 8 + 8 * (3 * 4000 // 32 + 4 * 129) * 4
     assert dk.workspace_size(dk.OP_COMPACT, L, 512, 0, 8) >= 2 * 4096 * 4
     # generation step: an action record, page IDs, a page request and a ring offset per table
     assert dk.workspace_size(dk.OP_GENERATION, L, 64, 0, 8) >= 512 * (16 + 16 + 4 + 4)

@@ -2,14 +2,16 @@
 // for gfx950 (DiffKV Eq. (1) of Sec. 2.1, kernel structure of Sec. 6.2).
 //
 // Work: a table's pages (high pages first, then low pages) are processed by
-// one four-wave workgroup for all GQ query heads that read them, or -- in the
+// one eight-wave workgroup for all GQ query heads that read them, or -- in the
 // balanced mode -- every table's pages are laid end to end and cut into one
 // equal share per resident workgroup, so the spread of table lengths costs
 // nothing; tables that straddle shares are merged by attn_merge.  Inside a
-// workgroup each wave takes every fourth page and keeps page i+1 in flight
-// (two register buffers in rotation) while it computes page i; a wave's page
-// IDs arrive as one vector per 64 pages and each page is loaded through a
-// buffer resource over that page (scalar address, hardware bounds).
+// workgroup each wave takes every eighth page, one register buffer per wave:
+// with two workgroups per CU four waves share each SIMD, so the waves hide
+// each other's page loads, and a table left alone on its CU still runs two
+// waves per SIMD.  A wave's page IDs arrive as one vector per 64 pages and
+// each page is loaded through a buffer resource over that page (scalar
+// address, hardware bounds).
 //
 // Lane mapping inside a wave (64 lanes = 4 rows of 16):
 //   key phase    lane = grp*16 + j: token j (and j+16 on 32-token pages),
@@ -30,7 +32,7 @@
 //                into v_dot2_f32_f16 with two tokens' codes as fp16 denormals;
 //                the zero-point term and the weights' rounding error (charged
 //                at the centre code) are accumulated per lane and added once.
-// The four waves' (max, sum, acc) states merge through LDS.
+// The eight waves' (max, sum, acc) states merge through LDS.
 #include <atomic>
 
 #include <utility>
@@ -39,7 +41,7 @@
 
 namespace dkv {
 
-constexpr int kAttnWaves = 4;
+constexpr int kAttnWaves = 8;  // single page buffer: GQ <= 6 fits two workgroups per CU
 constexpr int kAttnThreads = kAttnWaves * kWave;
 constexpr int kPartStride = kD + 2;
 
@@ -263,7 +265,7 @@ constexpr float kTwo24 = 16777216.0f;
 
 // Raw bytes of one page as one lane needs them.  High and low pages take
 // the same seven loads (two of them unused on high pages, re-reading lines the
-// page's other loads fetch), so the buffers of a prefetch pipeline never need
+// page's other loads fetch), so one buffer serves both page loops without
 // register copies.
 struct PageRaw {
     uint4 k0, k1;  // high: K8 chunks 2g, 2g+1 of token j; low: K4 chunk g of tokens j, j+16
@@ -628,8 +630,9 @@ __device__ __forceinline__ void write_empty(const AttnArgs& a, int t, int gq)
 
 // ---------------------------------------------------------------------------
 // One segment: pages [pa, pb) of table t for all GQ query heads of its KV
-// head.  The four waves take every fourth page; each keeps page i+1 in
-// flight while it computes page i.  Their (max, sum, acc) states merge through LDS
+// head.  The eight waves take every eighth page, each loading a page and
+// then computing it (the other waves on its SIMD cover the wait).  Their
+// (max, sum, acc) states merge through LDS
 // into the output (part == nullptr) or into a partial state {max, sum, acc}
 // per head at `part` (pa == pb gives the empty state).
 // ---------------------------------------------------------------------------
@@ -690,8 +693,8 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         qraw[hh][3] = qd[2];
     }
 
-    PageRaw buf0, buf1;
-    bool ok0 = false, ok1 = false;
+    PageRaw buf0;
+    bool ok0 = false;
     // first chunk: its IDs and first page go out beside the query loads
     c1 = nmine < kWave ? nmine : kWave;
     c_last = c1 > 0 ? c1 - 1 : 0;
@@ -744,8 +747,6 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         const int p = page_of(i);
         do_page<GQ, 2>(st, r, qr, q0, qsum, sl2, ti.len_lo - (p - ph) * kTLo, lane, coef_row);
     };
-    // page i computes from buffer i % 2 (swapped after an odd number of high
-    // pages) while page i+1 is in flight
     // Wave priority follows the pages this wave still has: on a SIMD shared
     // with shorter work, the longest work is served first (longest-first
     // scheduling at the wave level; ties go to the older wave).
@@ -758,34 +759,18 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     while (c0 < nmine) {
         const int nh = nhi < c1 ? nhi : c1;  // high pages end (within this chunk)
         int i = c0;
-        for (; i + 2 <= nh; i += 2) {
+        for (; i < nh; ++i) {
             set_prio(nmine - i);
-            issue(i + 1, buf1, ok1);
+            if (i > c0) issue(i, buf0, ok0);
             compute_hi(i, buf0, ok0);
-            issue(i + 2, buf0, ok0);
-            compute_hi(i + 1, buf1, ok1);
         }
-        if (i < nh) {  // one more high page (in buf0); the low pages then start in buf1
-            issue(i + 1, buf1, ok1);
-            compute_hi(i, buf0, ok0);
-            for (++i; i < c1; i += 2) {
-                set_prio(nmine - i);
-                issue(i + 1, buf0, ok0);
-                compute_lo(i, buf1, ok1);
-                issue(i + 2, buf1, ok1);
-                compute_lo(i + 1, buf0, ok0);
-            }
-        } else {
-            for (; i < c1; i += 2) {
-                set_prio(nmine - i);
-                issue(i + 1, buf1, ok1);
-                compute_lo(i, buf0, ok0);
-                issue(i + 2, buf0, ok0);
-                compute_lo(i + 1, buf1, ok1);
-            }
+        for (; i < c1; ++i) {
+            set_prio(nmine - i);
+            if (i > c0) issue(i, buf0, ok0);
+            compute_lo(i, buf0, ok0);
         }
-        // next chunk (tables longer than 64 pages per wave): the pipeline
-        // restarts with its IDs and first page
+        // next chunk (tables longer than 64 pages per wave): its IDs, then its
+        // first page
         c0 = c1;
         c1 = nmine - c0 < kWave ? nmine : c0 + kWave;
         c_last = c1 > c0 ? c1 - 1 : c0;

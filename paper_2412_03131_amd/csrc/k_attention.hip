@@ -751,9 +751,9 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     // with shorter work, the longest work is served first (longest-first
     // scheduling at the wave level; ties go to the older wave).
     auto set_prio = [&](int rem) {
-        if (rem > 24) __builtin_amdgcn_s_setprio(3);
-        else if (rem > 12) __builtin_amdgcn_s_setprio(2);
-        else if (rem > 4) __builtin_amdgcn_s_setprio(1);
+        if (rem > 12) __builtin_amdgcn_s_setprio(3);
+        else if (rem > 6) __builtin_amdgcn_s_setprio(2);
+        else if (rem > 2) __builtin_amdgcn_s_setprio(1);
         else __builtin_amdgcn_s_setprio(0);
     };
     while (c0 < nmine) {

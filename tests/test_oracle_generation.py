@@ -219,3 +219,60 @@ def test_out_of_pages_changes_nothing(orc):
     orc.generation_step(c2, ah, al, 2)
     assert int(c2.status[0]) == 0 and c2.len[0, 1] == 33 and c2.pages[0, 1] == 2
     assert orc.read_token(c2, 0, 1, 32)[3] == 38
+
+
+def test_requantization_rounding_hand_worked(orc):
+    """Re-quantization of a high token to low precision, worked by hand: each element
+    is s*code + z as one fp32 fma, rounded to fp16 (nearest even), then quantized as a
+    low-precision token.  The case is built so that this exact order decides a low
+    code: the product of an fp16 scale and an integer code of at most 8 bits is exact
+    in fp32, so s*c lands exactly on an fp16 midpoint, and z = -2^-24 (fp16 0x8001)
+    sits below fp32's half-ulp there.  fp32 rounding therefore returns the midpoint
+    and the fp16 rounding takes the even neighbour above it, while skipping the fp16
+    rounding keeps the midpoint and rounding the exact value once goes to the odd
+    neighbour below.  (A separate multiply then add gives the fma's result here,
+    since the product is exact.)
+
+    Key group 0 (K8 -> K4), s = 0x3C01 = 1 + 2^-10, z = -2^-24, codes 0, 3, 6 then 0:
+      3s = 3 + 1.5*2^-9: midpoint of 3 + 2^-9 (odd) and 3 + 2^-8 (even) -> 3.00390625
+      6s = 6 + 1.5*2^-8: midpoint of 6 + 2^-8 (odd) and 6 + 2^-7 (even) -> 6.0078125
+      min = -2^-24, max = 6.0078125 (adding 2^-24 is lost in fp32),
+      s_lo = fp16(6.0078125 / 15 = 0.4005208) = 1641 * 2^-12 = 0.400634765625 (0x3669),
+      codes: 3.00390625 / 0.400634765625 = 7.498 -> 7; 6.0078125 / s_lo = 14.996 -> 15.
+      Without the fp16 rounding: s_lo = 0.400390625, 3.0029296875 / s_lo = 7.5 -> 8.
+      With one rounding of the exact value: 3.001953125 / 0.400146484375 = 7.502 -> 8.
+    Value group 0 (V4 -> V2), s = 0x3C16 = 1.021484375, z = -2^-24, codes 0, 5, 6 then 0:
+      5s = 5.107421875 = 1307.5 * 2^-8: midpoint -> 1308 * 2^-8 = 5.109375 (even)
+      6s = 6.12890625 (exact in fp16), s_lo = 6.12890625 / 3 = 2.04296875 (0x4016),
+      code 5.109375 / 2.04296875 = 2.5010 -> 3.
+      Without the fp16 rounding: 5.107421875 / 2.04296875 = 2.5 -> 2 (even);
+      with one rounding of the exact value: 5.10546875 / 2.04296875 = 2.4990 -> 2.
+    """
+    c = _prompt_then_decode(orc, [0.08, 0.09, 0.07, 0.06, 0.01, 0.02], 0.5)
+    L = c.L
+    assert orc.read_token(c, 0, 0, 0)[3] == 0    # high index 0 holds position 0, the victim
+    pg = c.pool[int(c.table[0, 0])]              # its page; slot 0
+    kc = np.zeros(32, np.uint8)
+    kc[1:3] = [3, 6]
+    for d in range(32):                          # K8 chunk d // 16, byte d % 16 of slot 0
+        pg[L.off_kcode[0] + (d // 16) * 16 * 16 + d % 16] = kc[d]
+    pg[L.off_kmeta[0]:L.off_kmeta[0] + 4] = np.array([0x3C01, 0x8001], np.uint16).view(np.uint8)
+    vc = np.zeros(32, np.uint8)
+    vc[1:3] = [5, 6]
+    for d in range(32):                          # V4 row d: slot 0 in the low nibble of byte 0
+        o = L.off_vcode[0] + d * 8
+        pg[o] = (pg[o] & 0xF0) | vc[d]
+    pg[L.off_vmeta[0]:L.off_vmeta[0] + 4] = np.array([0x3C16, 0x8001], np.uint16).view(np.uint8)
+    orc.generation_step(c, ALPHA_H, ALPHA_L, W)
+    assert int(c.status[0]) == 0
+    u = [orc.read_token(c, 0, 1, i)[3] for i in range(int(c.len[0, 1]))].index(0)
+    lp = c.pool[int(c.table[0, L.p_max - 1 - u // 32])]
+    s = u % 32
+    kcodes = [(lp[L.off_kcode[1] + s * 16 + d // 2] >> (4 * (d % 2))) & 15 for d in range(32)]
+    vcodes = [(lp[L.off_vcode[1] + d * 8 + s // 4] >> (2 * (s % 4))) & 3 for d in range(32)]
+    kmeta = lp[L.off_kmeta[1] + s * 16:L.off_kmeta[1] + s * 16 + 4].view(np.uint16)
+    vmeta = lp[L.off_vmeta[1] + s * 4:L.off_vmeta[1] + s * 4 + 4].view(np.uint16)
+    assert kcodes == [0, 7, 15] + [0] * 29
+    assert kmeta.tolist() == [0x3669, 0x8001]
+    assert vcodes == [0, 3, 3] + [0] * 29
+    assert vmeta.tolist() == [0x4016, 0x8001]

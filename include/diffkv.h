@@ -219,6 +219,13 @@ diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_c
  *        states).
  * num_q_heads must be a multiple of num_kv_heads, with at most 8 query heads
  * per KV head.
+ * Precision: q . k_hat is exact up to fp32 summation (codes and q enter fp16
+ * products exactly); each value weight p * s_v is rounded to fp16 (relative
+ * 2^-11, the rounding charged at the centre code), so an output differs from
+ * exact Eq. (1) by at most about 2^-12 * R plus fp32 rounding, R being the
+ * largest dequantized value-group range of its table.  Any finite fp16 cache
+ * is accepted: the weights never overflow fp16 (pages with a value scale above
+ * 2^7 keep them <= s_v).
  */
 diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_cache* cache,
                                       int32_t num_q_heads, const uint16_t* q, float sm_scale,

@@ -181,4 +181,16 @@ __device__ __forceinline__ uint32_t f2h_rne(float f)
     return (uint32_t)__half_as_ushort(__float2half_rn(f));
 }
 
+// ---- host: launches ---------------------------------------------------------
+// Enqueue one launch of a kernel taking one argument block and return the
+// status of that launch itself (hipLaunchKernel's), never an error that an
+// earlier, unrelated runtime call left on the calling thread.
+template <typename A>
+inline hipError_t launch1(void (*kern)(A), unsigned grid, unsigned block, hipStream_t st, const A& a,
+                          size_t lds_bytes = 0)
+{
+    void* args[] = {const_cast<A*>(&a)};
+    return hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3(grid), dim3(block), args, lds_bytes, st);
+}
+
 }  // namespace dkv

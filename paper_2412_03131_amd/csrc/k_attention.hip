@@ -33,8 +33,6 @@
 //                the zero-point term and the weights' rounding error (charged
 //                at the centre code) are accumulated per lane and added once.
 // The eight waves' (max, sum, acc) states merge through LDS.
-#include <atomic>
-
 #include <utility>
 
 #include "internal.hpp"
@@ -43,6 +41,11 @@ namespace dkv {
 
 constexpr int kAttnWaves = 8;  // single page buffer: GQ <= 6 fits two workgroups per CU
 constexpr int kAttnThreads = kAttnWaves * kWave;
+// Workgroups of attn_decode<GQ> each CU holds at once; the launch bounds make
+// the compiler fit that residency (at most 128 VGPRs for two eight-wave
+// workgroups).  GQ 7-8 need more registers: four waves per SIMD there spilled
+// and measured slower, so they run one workgroup per CU.
+constexpr int attn_blocks_per_cu(int gq) { return gq <= 6 ? 2 : 1; }
 constexpr int kPartStride = kD + 2;
 
 // Byte offsets of the supported page layout (checked by the API against the
@@ -348,8 +351,11 @@ __device__ __forceinline__ void gather4(float x, float* o)
 }
 
 // Softmax weights are exp2(logit - m) with a running max m that is only
-// raised when a logit exceeds it by more than kSlack (weights stay <= 2^8).
+// raised when a logit exceeds it by more than kSlack (weights stay <= 2^8),
+// on pages whose V scales are at most 2^7 (fp16 bits 0x5800; scales are never
+// negative, so the bit pattern orders them); other pages raise it to their max.
 constexpr float kSlack = 8.0f;
+constexpr uint32_t kVScaleSlackMax = 0x5800u;
 
 // One page: logits, online softmax, weighted value sum.  NT = tokens per lane.
 //
@@ -403,12 +409,18 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
             lg[tk][s] = valid ? x : -INFINITY;
         }
     }
-    // ---- online softmax with a lazily raised max (one head per lane and slot)
+    // ---- online softmax with a lazily raised max (one head per lane and slot).
+    // The value weights p * s_v are rounded to fp16, so they must stay below
+    // 65504: on a page whose V scales all lie at or below 2^7 the slack keeps
+    // p <= 2^8 (weights <= 2^15); a page with a larger V scale takes no slack,
+    // so its weights are p <= 1 times an fp16 scale.
+    const bool big_v = (r.m2 & 0xffffu) > kVScaleSlackMax || (NT == 2 && (r.m3 & 0xffffu) > kVScaleSlackMax);
+    const float slack = __builtin_amdgcn_ballot_w64(big_v) ? 0.f : kSlack;
     bool raise = false;
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
-        for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.m[s] + kSlack;
+        for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.m[s] + slack;
     if (__builtin_amdgcn_ballot_w64(raise)) {
         float al[4 * NS];
 #pragma unroll
@@ -951,7 +963,7 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
 }
 
 template <int GQ>
-__global__ __launch_bounds__(kAttnThreads) void attn_decode(AttnArgs a)
+__global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ)) void attn_decode(AttnArgs a)
 {
     __shared__ AttnShared<GQ> sh;
     const int T = a.B * a.Hkv;
@@ -1156,30 +1168,22 @@ static const void* decode_kernel_for(int gq)
     }
 }
 
-// Workgroups of attn_decode<gq> the device holds at once, at most two per CU
-// (the balanced mode's share count), cached per device; at most
-// kAttnMaxWorkers.  A third workgroup per CU (three waves per SIMD, where the
-// registers allow it) measured slower: the page loop is bound by VALU issue,
-// and more shares only split more tables.
-static int balanced_workers(int gq)
+// Workgroups of attn_decode<gq> the device holds at once (the balanced mode's
+// share count): the residency the launch bounds guarantee times the CU count of
+// the current device, at most kAttnMaxWorkers.  A third workgroup per CU (three
+// waves per SIMD, where the registers allow it) measured slower: the page loop
+// is bound by VALU issue, and more shares only split more tables.  Nothing is
+// cached between calls.
+static hipError_t balanced_workers(int gq, int* workers)
 {
-    constexpr int kDevs = 64;
-    static std::atomic<int> cache[kDevs][9];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
-    const int slot = dev < kDevs ? dev : kDevs - 1;
-    int w = dev < kDevs ? cache[slot][gq].load(std::memory_order_relaxed) : 0;
-    if (w > 0) return w;
-    int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_kernel_for(gq), kAttnThreads, 0) != hipSuccess ||
-        per_cu < 1)
-        per_cu = 1;
-    per_cu = per_cu < 2 ? per_cu : 2;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 1;
-    w = per_cu * cus;
-    w = w < kAttnMaxWorkers ? w : kAttnMaxWorkers;
-    if (dev < kDevs) cache[slot][gq].store(w, std::memory_order_relaxed);
-    return w;
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    const int w = attn_blocks_per_cu(gq) * (cus > 0 ? cus : 1);
+    *workers = w < kAttnMaxWorkers ? w : kAttnMaxWorkers;
+    return hipSuccess;
 }
 
 bool attention_layout_matches(const diffkv_layout* L)
@@ -1195,31 +1199,31 @@ hipError_t launch_attention(AttnArgs a, hipStream_t st)
     const void* kern = decode_kernel_for(gq);
     if (!kern) return hipErrorInvalidValue;
     const long long T = (long long)a.B * a.Hkv;
+    int workers = 0;
+    hipError_t e = balanced_workers(gq, &workers);
+    if (e != hipSuccess) return e;
     long long grid;
     if (a.splits == 0) {
         // automatic: one workgroup per table when the tables alone fill the
         // device (their spread is absorbed by wave priorities and by the
         // hardware dispatching further tables as workgroups finish), balanced
         // shares when there are fewer tables than resident workgroups
-        a.splits = T >= balanced_workers(gq) ? 1 : -1;
+        a.splits = T >= workers ? 1 : -1;
     }
     if (a.splits > 0) {
         grid = T * a.splits;
         a.workers = 0;
     } else {
-        a.workers = balanced_workers(gq);
+        a.workers = workers;
         grid = a.workers;
     }
     if (grid < 1 || grid > INT32_MAX) return hipErrorInvalidValue;
     void* args[] = {&a};
-    hipError_t e = hipLaunchKernel(kern, dim3((unsigned)grid), dim3(kAttnThreads), args, 0, st);
-    if (e != hipSuccess) return e;
-    if (a.splits != 1) {
-        const long long jobs = T * gq;
-        const long long mgrid = (jobs + kMergeThreads / kWave - 1) / (kMergeThreads / kWave);
-        hipLaunchKernelGGL(attn_merge, dim3((unsigned)mgrid), dim3(kMergeThreads), 0, st, a);
-    }
-    return hipGetLastError();
+    e = hipLaunchKernel(kern, dim3((unsigned)grid), dim3(kAttnThreads), args, 0, st);
+    if (e != hipSuccess || a.splits == 1) return e;
+    const long long jobs = T * gq;
+    const long long mgrid = (jobs + kMergeThreads / kWave - 1) / (kMergeThreads / kWave);
+    return launch1(attn_merge, (unsigned)mgrid, kMergeThreads, st, a);
 }
 
 }  // namespace dkv

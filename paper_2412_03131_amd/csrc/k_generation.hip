@@ -494,14 +494,12 @@ __global__ __launch_bounds__(kWave) void gen_apply(GenArgs a)
 hipError_t launch_generation(const GenArgs& g, hipStream_t st)
 {
     if (g.num_tables == 0) return hipSuccess;
-    hipLaunchKernelGGL(gen_decide, dim3(g.num_tables), dim3(kGenThreads), 0, st, g);
-    if (g.num_tables <= kGenFusedTables) {
-        hipLaunchKernelGGL(gen_apply<true>, dim3(g.num_tables), dim3(kWave), 0, st, g);
-    } else {
-        hipLaunchKernelGGL(gen_scan, dim3(1), dim3(kGenScanThreads), 0, st, g);
-        hipLaunchKernelGGL(gen_apply<false>, dim3(g.num_tables), dim3(kWave), 0, st, g);
-    }
-    return hipGetLastError();
+    hipError_t e = launch1(gen_decide, (unsigned)g.num_tables, kGenThreads, st, g);
+    if (e != hipSuccess) return e;
+    if (g.num_tables <= kGenFusedTables) return launch1(gen_apply<true>, (unsigned)g.num_tables, kWave, st, g);
+    e = launch1(gen_scan, 1, kGenScanThreads, st, g);
+    if (e != hipSuccess) return e;
+    return launch1(gen_apply<false>, (unsigned)g.num_tables, kWave, st, g);
 }
 
 }  // namespace dkv

@@ -946,36 +946,33 @@ __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
 // ---------------------------------------------------------------------------
 hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st)
 {
-    hipLaunchKernelGGL(append_classify, dim3((unsigned)(a.Hkv * a.B)), dim3(kClsThreads), 0, st, a);
+    hipError_t e = launch1(append_classify, (unsigned)(a.Hkv * a.B), kClsThreads, st, a);
+    if (e != hipSuccess) return e;
     if (append_planned(a.B, a.Hkv)) {
-        hipLaunchKernelGGL(append_plan, dim3(1), dim3(kPlanThreads), 0, st, a);
-        hipLaunchKernelGGL(append_commit_planned, dim3(grid_quant), dim3(kCommitThreads), 0, st, a);
-    } else {
-        hipLaunchKernelGGL(append_commit, dim3(grid_quant), dim3(kCommitThreads), 0, st, a);
+        e = launch1(append_plan, 1, kPlanThreads, st, a);
+        if (e != hipSuccess) return e;
+        return launch1(append_commit_planned, (unsigned)grid_quant, kCommitThreads, st, a);
     }
-    return hipGetLastError();
+    return launch1(append_commit, (unsigned)grid_quant, kCommitThreads, st, a);
 }
 
 hipError_t launch_alloc(const AllocArgs& a, hipStream_t st)
 {
-    hipLaunchKernelGGL(alloc_plan, dim3(1), dim3(kPlanThreads), 0, st, a);
-    if (a.num_tables > 0) hipLaunchKernelGGL(alloc_write, dim3(a.num_tables), dim3(kWave), 0, st, a);
-    return hipGetLastError();
+    hipError_t e = launch1(alloc_plan, 1, kPlanThreads, st, a);
+    if (e != hipSuccess || a.num_tables == 0) return e;
+    return launch1(alloc_write, (unsigned)a.num_tables, kWave, st, a);
 }
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st)
 {
     if (a.num_tables == 0) return hipSuccess;
-    hipLaunchKernelGGL(compact_count, dim3(a.num_tables), dim3(kWave), 0, st, a);
-    if (a.num_tables <= kCompactFusedTables) {
-        hipLaunchKernelGGL(compact_apply<true>, dim3(a.num_tables), dim3(kWave),
-                           (size_t)2 * a.p_max * sizeof(int32_t), st, a);
-    } else {
-        hipLaunchKernelGGL(compact_scan, dim3(1), dim3(kPlanThreads), 0, st, a);
-        hipLaunchKernelGGL(compact_apply<false>, dim3(a.num_tables), dim3(kWave),
-                           (size_t)2 * a.p_max * sizeof(int32_t), st, a);
-    }
-    return hipGetLastError();
+    const size_t lds = (size_t)2 * a.p_max * sizeof(int32_t);
+    hipError_t e = launch1(compact_count, (unsigned)a.num_tables, kWave, st, a);
+    if (e != hipSuccess) return e;
+    if (a.num_tables <= kCompactFusedTables) return launch1(compact_apply<true>, (unsigned)a.num_tables, kWave, st, a, lds);
+    e = launch1(compact_scan, 1, kPlanThreads, st, a);
+    if (e != hipSuccess) return e;
+    return launch1(compact_apply<false>, (unsigned)a.num_tables, kWave, st, a, lds);
 }
 
 }  // namespace dkv

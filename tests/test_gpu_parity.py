@@ -424,3 +424,60 @@ def test_compaction_workload_scaled():
         dc.len.copy_(t(oc.len))
         assert_state_equal(dc, oc, with_pool=False, what="round %d" % rnd)
     assert oc.ring_ptr[1] > (1 << 16)  # wrapped
+
+
+@pytest.mark.parametrize("gq", [1, 4, 8])
+def test_attention_large_value_ranges(gq):
+    """Value groups with large ranges, where the fp16 value weights p * s_v of the
+    kernel would pass 65504 without the per-page slack rule: V group 0 of every token
+    scaled x300, group 2 of every fifth token x1000, one token with a group spanning
+    -60000 .. 60000; keys x3 so that the softmax weights span several powers of two.
+    Both precisions (high pages K8V4, low pages K4V2), S = 1 and balanced shares.
+    Outputs must be finite and within 2e-3 + 2^-12 * R of the fp64 oracle, R being
+    the largest dequantized value-group range of the output's table (the fp16
+    rounding of a weight is relative 2^-11, charged at the centre code)."""
+    rng = np.random.default_rng(90 + gq)
+    B, Hkv = 3, 2
+    Hq = Hkv * gq
+    new_len = np.array([300, 700, 45], np.int32)
+    n = int(new_len.sum())
+    k = (rng.standard_normal((n, Hkv, 128)) * 3).astype(np.float16).view(np.uint16)
+    vf = rng.standard_normal((n, Hkv, 128)).astype(np.float32)
+    vf[:, :, 0:32] *= 300.0
+    vf[::5, :, 64:96] *= 1000.0
+    vf[7, 0, 96:128] = np.linspace(-60000.0, 60000.0, 32)
+    v = vf.astype(np.float16).view(np.uint16)
+    score = rng.random((n, Hkv)).astype(np.float32)
+    score[7, 0] = 2.0   # the +-60000 token is kept (high precision)
+    quota = np.stack([new_len[:, None] // 2 + np.zeros((B, Hkv), np.int32),
+                      new_len[:, None] // 3 + np.zeros((B, Hkv), np.int32)], axis=2).astype(np.int32)
+    Lo, Ld = layouts(max_seq_len=768)
+    npages = B * Hkv * 60
+    oc = orc.Cache(Lo, npages, B, Hkv, ring=rng.permutation(npages))
+    orc.quantize_append(oc, new_len, k, v, score, quota=quota)
+    assert oc.status[0] == 0
+    # largest dequantized value-group range per table
+    R = np.zeros(B * Hkv)
+    for tt in range(B * Hkv):
+        for sec in (0, 1):
+            for u in range(int(oc.len[tt, sec])):
+                vh = orc.read_token(oc, tt, sec, u)[1].reshape(4, 32)
+                R[tt] = max(R[tt], float((vh.max(axis=1) - vh.min(axis=1)).max()))
+    assert R.max() > 1e5
+    q = rng.standard_normal((B, Hq, 128)).astype(np.float16).view(np.uint16)
+    ref, ref_lse = orc.attention(oc, q, SCALE)
+    bound = 2e-3 + 2.0 ** -12 * np.repeat(R.reshape(B, Hkv), gq, axis=1)[:, :, None]
+    dc = dev_cache_from_oracle(Ld, oc)
+    for splits in (1, -1):
+        print("case: large value ranges GQ %d splits=%d" % (gq, splits), flush=True)
+        out, lse = dk.decode_attention(dc, t(q), SCALE, num_splits=splits)
+        torch.cuda.synchronize()
+        o = out.cpu().numpy().astype(np.float64)
+        assert np.isfinite(o).all(), "non-finite attention output"
+        err = np.abs(o - ref)
+        print("   max abs %.3g, max err/bound %.3g, rel L2 %.3g" % (
+            err.max(), (err / bound).max(), np.linalg.norm(o - ref) / np.linalg.norm(ref)), flush=True)
+        assert (err <= bound).all()
+        assert np.linalg.norm(o - ref) <= 1e-3 * np.linalg.norm(ref)
+        lg = lse.cpu().numpy()
+        assert np.abs(lg - ref_lse).max() <= 2e-3

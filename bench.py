@@ -1,27 +1,36 @@
 #!/usr/bin/env python3
 """Benchmark of the DiffKV decode hot path on one MI355X.
 
-Workload: the Llama-3-8B decode shape (batch 64, 32 query / 8 KV heads, head_dim 128,
-context uniform in [1024, 4096], per-head high fraction U[0.1, 0.5] and pruned fraction
-U[0.2, 0.6], K8V4 / K4V2 with group-32 fp16 scale/zero, 16/32 tokens per page), on
-`--layers` layers that share one page pool (so attention streams from HBM, not from the
-256 MB Infinity Cache).
+Headline workload (--config long32k, the default): the long-generation shape, batch 16,
+40 query / 8 KV heads (GQA 5:1), head_dim 128, 32768-token contexts whose per-head pruned
+fraction is 0.1 + 0.8 * Beta(2, 2) and whose kept tokens are split evenly between K8V4 and
+K4V2 (group-32 fp16 scale/zero, 16/32 tokens per page).  The prompt phase fills the cache
+(one diffkv_quantize_append), then every timed step is one decode step of the path:
 
-One step = one continuous-batching decode step of the whole path:
-  1. request r = step mod 64 finishes: its pages in every layer go back to the free list
-     (diffkv_compact_free_list, one call for all layers);
-  2. a replacement request is prefilled into slot r of every layer while the other 63
-     append their newest token (diffkv_quantize_append: classing, allocation,
-     quantization, placement), one call for all layers and requests, as the paper runs
-     its KV compaction once per inference step (Sec. 5.3);
-  3. per layer: decode attention over the whole batch (diffkv_decode_attention).
+  1. diffkv_quantize_append of one new token per (sequence, KV head), quota (1, 0): the
+     token enters the recent window at high precision (classing, allocation when a page
+     fills, quantization, placement);
+  2. diffkv_decode_attention over the whole compressed cache (automatic split mode).
 
-value = KV tokens attended per second of step time, where a KV token is one kept
-(token, KV head) pair.  The JSON line adds the attention kernel's roofline (algorithmic
-compressed bytes / kernel time, HIP events on the launch stream), the compaction
-workload (2^20 pages, 4096 tables, 100 rounds of Bernoulli(0.35) releases) in pages/s,
-the generation-phase policy (Algorithm 1) per decode step on the same llama8b shape,
-and the CPU oracle's attention throughput on a bounded sample.
+value = KV tokens attended per second of step time (a KV token is one kept
+(token, KV head) pair), from the wall clock around K back-to-back steps.  A second pass of
+K steps evicts the Infinity Cache and L2 before every step (a 1 GiB fill kernel, outside
+the HIP events) and gives the per-launch attention and append times (median, p10, p90,
+mean) and the roofline: algorithmic compressed bytes / mean attention time.
+
+Extra keys of the same JSON line:
+  llama70b        batch 32, 64 query / 8 KV heads (GQA 8:1), context 8192, split 30/40/30:
+                  attention with num_splits = 1 (no split), automatic, and balanced
+                  shares + merge (sequence split), each timed after a cache flush;
+  serving_step    the llama8b shape (batch 64, 32/8 heads, contexts U[1024, 4096]) on four
+                  layers sharing one pool: per step one request finishes (one compaction
+                  call for all layers), a new request is prefilled while the other 63
+                  decode (one append call for all layers), then attention per layer;
+  compaction      2^20-page pool, 4096 tables, 100 rounds of Bernoulli(0.35) releases;
+  generation_step the generation-phase policy (Algorithm 1) per decode step, llama8b;
+  cpu_baseline    the CPU oracle's fp64 attention on a bounded sample of the headline
+                  workload, one thread and all host cores (threads; the oracle's C code
+                  releases the interpreter lock), plus its serial compaction.
 """
 import argparse
 import ctypes as C
@@ -38,10 +47,28 @@ sys.path.insert(0, ROOT)
 METRIC = "decode-attention KV tokens/s + achieved HBM GB/s (% of peak); compaction pages/s"
 HBM_PEAK_GBPS = 8000.0
 SCALE = 1.0 / np.sqrt(128.0)
-# measured HBM traffic of the attention call (rocprofv3 FETCH_SIZE / WRITE_SIZE),
-# valid while the attention sources hash to the value recorded with it
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_llama8b_traffic.txt")
 ATTN_SOURCES = ["k_attention.hip", "internal.hpp", "common.hpp"]
+FLUSH_BYTES = 1 << 30   # > the 256 MB Infinity Cache + 8 x 4 MB L2
+DTYPE_DETAIL = ("q.k: fp16 q x integer codes (exact products), fp32 sums, fp32 scale/zero; "
+                "p.v: softmax weight x fp16 scale rounded to fp16 x integer codes, fp32 sums; "
+                "softmax, merge and outputs fp32")
+
+WORKLOADS = {
+    "long32k": "long-generation decode step: B=16, Hq=40, Hkv=8 (GQA 5), D=128, context 32768, "
+               "pruned fraction 0.1+0.8*Beta(2,2) per head, kept tokens half K8V4 half K4V2, group 32, "
+               "16/32 tokens per page; per step one 1-token quantize_append per (sequence, KV head) "
+               "then attention over the whole cache",
+    "llama70b": "Llama-3-70B-shaped decode step: B=32, Hq=64, Hkv=8 (GQA 8), D=128, context 8192, "
+                "high/low/pruned 30/40/30 per head, group 32, 16/32 tokens per page; per step one "
+                "1-token quantize_append per (sequence, KV head) then attention",
+    "llama8b": "Llama-3-8B-shaped decode step: B=64, Hq=32, Hkv=8 (GQA 4), D=128, context U[1024,4096], "
+               "f_hi U[0.1,0.5], f_pr U[0.2,0.6], group 32, 16/32 tokens per page; per step one "
+               "1-token quantize_append per (sequence, KV head) then attention",
+}
+
+
+def traffic_file(config):
+    return os.path.join(ROOT, "profiles", "attn_%s_traffic.txt" % config)
 
 
 def attention_sources_sha256():
@@ -53,12 +80,12 @@ def attention_sources_sha256():
     return h.hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per attention launch from the committed counter summary, or None when
-    it is missing or was taken on different attention sources."""
+def measured_traffic(config):
+    """HBM bytes per attention launch from the committed counter summary of this
+    workload, or None when it is missing or was taken on different attention sources."""
     try:
         kv = {}
-        with open(TRAFFIC_FILE) as fh:
+        with open(traffic_file(config)) as fh:
             for ln in fh:
                 if ":" in ln and not ln.startswith("#"):
                     k, v = ln.split(":", 1)
@@ -73,21 +100,26 @@ def measured_traffic():
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--layers", type=int, default=4)
-    ap.add_argument("--splits", type=int, default=0, help="attention mode: 0 automatic, -1 balanced shares, S >= 1 ranges per table")
+    ap.add_argument("--steps", type=int, default=64, help="timed decode steps (per pass)")
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", choices=("long32k", "llama70b", "llama8b"), default="long32k",
+                    help="headline decode workload")
+    ap.add_argument("--splits", type=int, default=0,
+                    help="attention mode: 0 automatic, -1 balanced shares, S >= 1 ranges per table")
+    ap.add_argument("--extras", choices=("all", "none"), default="all",
+                    help="'none' prints the headline line only (no llama70b modes, serving step, "
+                         "compaction, generation step)")
+    ap.add_argument("--serving-steps", type=int, default=30)
+    ap.add_argument("--layers", type=int, default=4, help="layers of the serving step")
+    ap.add_argument("--reps", type=int, default=40, help="flushed attention calls per llama70b mode")
     ap.add_argument("--compaction-rounds", type=int, default=100)
     ap.add_argument("--generation-steps", type=int, default=50)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--hq", type=int, default=0,
-                    help="with --only attention: query heads per sequence (default: the "
-                         "workload's 32; a multiple of the 8 KV heads, at most 64)")
     ap.add_argument("--only", choices=("all", "attention", "copy", "generation"), default="all",
                     help="profiling aids that print no benchmark line: 'attention' builds the "
-                         "cache and times only the attention calls; 'copy' runs a plain 1 GiB "
-                         "device copy (the reference for scaling HBM byte counters); "
+                         "--config cache and times only attention calls (no flush); 'copy' runs a "
+                         "plain 1 GiB device copy (the reference for scaling HBM byte counters); "
                          "'generation' runs only the generation-step measurement")
     return ap.parse_args()
 
@@ -106,6 +138,339 @@ def attn_bytes(len_hi, len_lo, B, Hq, Hkv):
     return kv + 4 * int(ph.sum() + pl.sum()) + 8 * len_hi.size + B * Hq * 128 * (2 + 4) + 4 * B * Hq
 
 
+def pct(a):
+    a = np.asarray(a, np.float64)
+    return {"mean": float(a.mean()), "median": float(np.median(a)),
+            "p10": float(np.percentile(a, 10)), "p90": float(np.percentile(a, 90))}
+
+
+def to_dev(torch, dev, a):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(dev)
+
+
+class Flush:
+    """Evicts the Infinity Cache and the L2s: a fill kernel over 1 GiB."""
+
+    def __init__(self, torch, dev):
+        self.buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device=dev)
+        self.i = 0
+
+    def __call__(self):
+        self.i += 1
+        self.buf.fill_(self.i)
+
+
+def build_decode(torch, dk, dev, name, extra_steps):
+    """Prompt phase of a decode workload on the GPU; per-step decode inputs for
+    `extra_steps` steps (one token per sequence, quota (1, 0))."""
+    from paper_2412_03131_amd import inputs
+    t0 = time.time()
+    w = inputs.prefill(name)
+    B, Hq, Hkv = w["B"], w["Hq"], w["Hkv"]
+    nl = w["new_len"].astype(np.int64)
+    hi0 = w["quota"][:, :, 0].astype(np.int64)
+    lo0 = w["quota"][:, :, 1].astype(np.int64)
+    L = dk.layout(max_seq_len=int(nl.max()) + extra_steps + 16)
+    per_table = (-(-(hi0 + extra_steps) // 16)) + (-(-lo0 // 32)) + 2
+    num_pages = int(per_table.sum()) + 256
+    cache = dk.Cache(L, num_pages, B, Hkv, device=dev)
+    T = lambda a: to_dev(torch, dev, a)
+    dk.quantize_append(cache, T(w["new_len"]), T(w["k"]), T(w["v"]), T(w["score"]), quota=T(w["quota"]),
+                       total_new=int(nl.sum()), max_new=int(nl.max()))
+    torch.cuda.synchronize()
+    if int(cache.status.item()) != 0:
+        raise RuntimeError("prefill raised status %d" % int(cache.status.item()))
+    steps = []
+    for s in range(extra_steps):
+        d = inputs.decode_token(name, s, B, Hq, Hkv, w["outliers"])
+        steps.append(dict(k=T(d["k"]), v=T(d["v"]), score=T(d["score"]), quota=T(d["quota"]), q=T(d["q"])))
+    log("workload %s: B=%d Hq=%d Hkv=%d, %d prompt rows, %d pages (%.2f GB pool), built in %.1f s"
+        % (name, B, Hq, Hkv, int(nl.sum()), num_pages, num_pages * L.page_bytes / 1e9, time.time() - t0))
+    res = dict(w=dict(B=B, Hq=Hq, Hkv=Hkv, new_len=w["new_len"], quota=w["quota"]), L=L, cache=cache,
+               steps=steps, hi0=hi0.reshape(-1), lo0=lo0.reshape(-1), ones=T(np.ones(B, np.int32)))
+    del w
+    return res
+
+
+def decode_headline(torch, dk, lib, dev, sptr, wl, args, flush):
+    """K back-to-back decode steps (the contract's timed region), then K flushed steps
+    timed per launch with HIP events on the launch stream."""
+    B, Hq, Hkv = wl["w"]["B"], wl["w"]["Hq"], wl["w"]["Hkv"]
+    L, cache = wl["L"], wl["cache"]
+    S = args.splits
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    ws_att = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, Hq, Hkv, 0, S)),
+                         dtype=torch.uint8, device=dev)
+    ws_app = torch.empty(dk.workspace_size(dk.OP_APPEND, L, B, 0, Hkv, B) + 256, dtype=torch.uint8, device=dev)
+    Lp = C.byref(L)
+    cs = cache.struct()
+    vp = lambda x: C.c_void_p(x.data_ptr())
+    app, att = [], []
+    for si in wl["steps"]:
+        app.append((Lp, C.byref(cs), B, 1, vp(wl["ones"]), vp(si["k"]), vp(si["v"]), vp(si["score"]),
+                    vp(si["quota"]), 0.0, 0.0, 0, vp(ws_app), ws_app.numel(), sptr))
+        att.append((Lp, C.byref(cs), Hq, vp(si["q"]), float(SCALE), vp(out), vp(lse), S, vp(ws_att),
+                    ws_att.numel(), sptr))
+    K, W = args.steps, args.warmup
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(2 * K)]
+
+    def step(s, e=None):
+        if e is not None:
+            e[0].record()
+        rc = lib.diffkv_quantize_append(*app[s])
+        if e is not None:
+            e[1].record()
+        rc |= lib.diffkv_decode_attention(*att[s])
+        if e is not None:
+            e[2].record()
+        if rc:
+            raise RuntimeError("library call failed at step %d (rc %d)" % (s, rc))
+
+    # expected section lengths at every step's attention (bytes and token counts)
+    hi, lo = wl["hi0"].copy(), wl["lo0"].copy()
+    step_bytes, step_tok = [], []
+    for s in range(W + 2 * K):
+        hi = hi + 1
+        step_bytes.append(attn_bytes(hi, lo, B, Hq, Hkv))
+        step_tok.append(int(hi.sum() + lo.sum()))
+    for s in range(W):
+        step(s)
+    torch.cuda.synchronize()
+    # pass 1: the timed region of the contract, back to back
+    t0 = time.perf_counter()
+    for i in range(K):
+        step(W + i, ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    # pass 2: caches evicted before every step (outside the events)
+    for i in range(K):
+        flush()
+        step(W + K + i, ev[K + i])
+    torch.cuda.synchronize()
+    status = int(cache.status.item())
+    got = cache.len.cpu().numpy()
+    if status != 0 or not (np.array_equal(got[:, 0], hi) and np.array_equal(got[:, 1], lo)):
+        raise RuntimeError("state check failed after the timed steps (status %d)" % status)
+    app_us = np.array([e[0].elapsed_time(e[1]) * 1e3 for e in ev])
+    att_us = np.array([e[1].elapsed_time(e[2]) * 1e3 for e in ev])
+    tok1 = np.array(step_tok[W:W + K], np.float64)
+    byt1 = np.array(step_bytes[W:W + K], np.float64)
+    byt2 = np.array(step_bytes[W + K:], np.float64)
+    tok2 = np.array(step_tok[W + K:], np.float64)
+    a2, p2 = att_us[K:], app_us[K:]
+    achieved = float(byt2.sum() / (a2.sum() * 1e-6) / 1e9)
+    res = dict(
+        value=float(tok1.sum() / wall), wall=wall, ms_per_step=wall / K * 1e3,
+        achieved=achieved, bytes_per_launch=float(byt2.mean()), us_per_launch=float(a2.mean()),
+        attention=dict(flushed_us=pct(a2), flushed_gbps=achieved,
+                       unflushed_us=pct(att_us[:K]),
+                       unflushed_gbps=float(byt1.sum() / (att_us[:K].sum() * 1e-6) / 1e9),
+                       kv_tokens_per_launch=float(tok2.mean()),
+                       kv_tokens_per_s=float(tok2.sum() / (a2.sum() * 1e-6)),
+                       fp16_equivalent_gbps=float(tok2.sum() * 512 / (a2.sum() * 1e-6) / 1e9),
+                       bytes_per_launch=float(byt2.mean())),
+        append=dict(flushed_us=pct(p2), unflushed_us=pct(app_us[:K]),
+                    tokens_per_call=B * Hkv),
+        step=dict(flushed_us=pct(a2 + p2), unflushed_us=pct(att_us[:K] + app_us[:K])))
+    log("headline: %.3f ms/step (wall, back to back), attention %.1f us/launch flushed (median %.1f, "
+        "p10 %.1f, p90 %.1f), %.0f GB/s; unflushed %.1f us; append %.1f us"
+        % (res["ms_per_step"], a2.mean(), np.median(a2), np.percentile(a2, 10), np.percentile(a2, 90),
+           achieved, att_us[:K].mean(), p2.mean()))
+    return res
+
+
+def attention_modes(torch, dk, lib, dev, sptr, wl, reps, flush, modes=(1, 0, -1)):
+    """Flushed attention calls over a built cache in several split modes."""
+    B, Hq, Hkv = wl["w"]["B"], wl["w"]["Hq"], wl["w"]["Hkv"]
+    L, cache = wl["L"], wl["cache"]
+    lens = cache.len.cpu().numpy()
+    nbytes = attn_bytes(lens[:, 0].astype(np.int64), lens[:, 1].astype(np.int64), B, Hq, Hkv)
+    ntok = int(lens.sum())
+    q = wl["steps"][0]["q"]
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    res = {}
+    for S in modes:
+        ws = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, Hq, Hkv, 0, S)),
+                         dtype=torch.uint8, device=dev)
+        args = (C.byref(L), C.byref(cache.struct()), Hq, C.c_void_p(q.data_ptr()), float(SCALE),
+                C.c_void_p(out.data_ptr()), C.c_void_p(lse.data_ptr()), S, C.c_void_p(ws.data_ptr()),
+                ws.numel(), sptr)
+        for _ in range(5):
+            lib.diffkv_decode_attention(*args)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        rc = 0
+        for e in ev:
+            flush()
+            e[0].record()
+            rc |= lib.diffkv_decode_attention(*args)
+            e[1].record()
+        torch.cuda.synchronize()
+        if rc:
+            raise RuntimeError("attention call failed (mode %d)" % S)
+        us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+        name = {1: "splits_1", 0: "automatic", -1: "balanced"}.get(S, "splits_%d" % S)
+        gbps = nbytes / (us.mean() * 1e-6) / 1e9
+        res[name] = dict(num_splits=S, us=pct(us), gbps=gbps, frac=gbps / HBM_PEAK_GBPS,
+                         kv_tokens_per_s=ntok / (us.mean() * 1e-6))
+        log("  attention mode %s: %.1f us (median %.1f, p10 %.1f, p90 %.1f), %.0f GB/s"
+            % (name, us.mean(), np.median(us), np.percentile(us, 10), np.percentile(us, 90), gbps))
+    res["bytes_per_launch"] = nbytes
+    res["kv_tokens_per_launch"] = ntok
+    return res
+
+
+def serving_step(torch, dk, lib, dev, sptr, args):
+    """The llama8b shape on `layers` layers sharing one page pool, one step = request
+    r = step mod 64 finishes (its pages in every layer recycled by one compaction call),
+    a replacement request is prefilled into slot r of every layer while the other 63
+    append their newest token (one append call for all layers and requests, as the
+    paper runs its KV compaction once per inference step for all requests and layers),
+    then attention per layer.  Wall clock around back-to-back steps; HIP events around
+    each step's attention calls."""
+    from paper_2412_03131_amd import inputs
+    t0 = time.time()
+    w = inputs.prefill("llama8b")
+    B, Hq, Hkv = w["B"], w["Hq"], w["Hkv"]
+    NL = args.layers
+    nl = w["new_len"].astype(np.int64)
+    off = np.concatenate([[0], np.cumsum(nl)])
+    K, Wm = args.serving_steps, 5
+    steps_total = Wm + K
+    init_hi = w["quota"][:, :, 0].astype(np.int64)
+    init_lo = w["quota"][:, :, 1].astype(np.int64)
+    L = dk.layout(max_seq_len=int(nl.max()) + steps_total + 16)
+    per_table = (-(-(init_hi + steps_total) // 16)) + (-(-init_lo // 32)) + 2
+    num_pages = int(NL * per_table.sum() * 1.05) + 1024
+    cache = dk.Cache(L, num_pages, NL * B, Hkv, device=dev)
+    views = [cache.view(l * B, (l + 1) * B) for l in range(NL)]
+    T = lambda a: to_dev(torch, dev, a)
+    k_all, v_all, s_all = T(w["k"]), T(w["v"]), T(w["score"])
+    quota_all, nl_all = T(w["quota"]), T(w["new_len"])
+    ws_a = torch.empty(dk.workspace_size(dk.OP_APPEND, L, B, 0, Hkv, int(nl.sum()) + B) + 256,
+                       dtype=torch.uint8, device=dev)
+    for v in views:
+        dk.quantize_append(v, nl_all, k_all, v_all, s_all, quota=quota_all, total_new=int(nl.sum()),
+                           max_new=int(nl.max()), ws=ws_a)
+    torch.cuda.synchronize()
+    if int(cache.status.item()) != 0:
+        raise RuntimeError("serving prefill raised status %d" % int(cache.status.item()))
+    steps_in = []
+    for s in range(steps_total):
+        r = s % B
+        d = inputs.decode_token("llama8b", s, B, Hq, Hkv, w["outliers"])
+        dk_, dv_, ds_ = T(d["k"]), T(d["v"]), T(d["score"])
+        k_s = torch.cat([dk_[:r], k_all[off[r]:off[r + 1]], dk_[r + 1:]])
+        v_s = torch.cat([dv_[:r], v_all[off[r]:off[r + 1]], dv_[r + 1:]])
+        s_s = torch.cat([ds_[:r], s_all[off[r]:off[r + 1]], ds_[r + 1:]])
+        q_np = d["quota"].copy()
+        q_np[r] = w["quota"][r]
+        n_np = np.ones(B, np.int32)
+        n_np[r] = nl[r]
+        steps_in.append(dict(r=r, k=torch.cat([k_s] * NL), v=torch.cat([v_s] * NL),
+                             score=torch.cat([s_s] * NL), quota=T(np.tile(q_np, (NL, 1, 1))),
+                             new_len=T(np.tile(n_np, NL)), total=NL * int(n_np.sum()),
+                             maxn=int(n_np.max()), q=T(d["q"])))
+    P = L.p_max
+    masks = []
+    for r in range(B):
+        m = torch.zeros((NL * B * Hkv, P), dtype=torch.uint8, device=dev)
+        for l in range(NL):
+            m[(l * B + r) * Hkv:(l * B + r + 1) * Hkv] = 1
+        masks.append(m)
+    ws_att = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, Hq, Hkv, 0, 0)),
+                         dtype=torch.uint8, device=dev)
+    ws_c = torch.empty(dk.workspace_size(dk.OP_COMPACT, L, NL * B, 0, Hkv), dtype=torch.uint8, device=dev)
+    ws_all = torch.empty(dk.workspace_size(dk.OP_APPEND, L, NL * B, 0, Hkv,
+                                           max(si["total"] for si in steps_in)) + 256,
+                         dtype=torch.uint8, device=dev)
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    Lp = C.byref(L)
+    cstructs = [v.struct() for v in views]
+    call_struct = cache.struct()
+    vp = lambda x: C.c_void_p(x.data_ptr())
+    attn_args, app_args = [], []
+    for si in steps_in:
+        app_args.append((Lp, C.byref(call_struct), si["total"], si["maxn"], vp(si["new_len"]),
+                         vp(si["k"]), vp(si["v"]), vp(si["score"]), vp(si["quota"]), 0.0, 0.0, 0,
+                         vp(ws_all), ws_all.numel(), sptr))
+        attn_args.append([(Lp, C.byref(cs), Hq, vp(si["q"]), float(SCALE), vp(out), vp(lse), 0,
+                           vp(ws_att), ws_att.numel(), sptr) for cs in cstructs])
+    comp_args = [(Lp, C.byref(call_struct), NL * B * Hkv, vp(m), vp(ws_c), ws_c.numel(), sptr)
+                 for m in masks]
+    seq_rows = [torch.arange(r, NL * B, B, device=dev) for r in range(B)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+
+    def run_step(s, e=None):
+        si = steps_in[s]
+        r = si["r"]
+        if e is not None:
+            e[0].record()
+        rc = lib.diffkv_compact_free_list(*comp_args[r])
+        cache.seq_len.index_fill_(0, seq_rows[r], 0)
+        if e is not None:
+            e[1].record()
+        rc |= lib.diffkv_quantize_append(*app_args[s])
+        if e is not None:
+            e[2].record()
+        for l in range(NL):
+            rc |= lib.diffkv_decode_attention(*attn_args[s][l])
+        if e is not None:
+            e[3].record()
+        if rc:
+            raise RuntimeError("library call failed at serving step %d (rc %d)" % (s, rc))
+
+    len_hi, len_lo = init_hi.copy(), init_lo.copy()
+    step_bytes, step_tokens = [], []
+    for s in range(steps_total):
+        r = s % B
+        len_hi += 1
+        len_hi[r] = init_hi[r]
+        len_lo[r] = init_lo[r]
+        step_bytes.append(attn_bytes(len_hi, len_lo, B, Hq, Hkv))
+        step_tokens.append(int(len_hi.sum() + len_lo.sum()))
+    for s in range(Wm):
+        run_step(s)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i in range(K):
+        run_step(Wm + i, ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t1
+    status = int(cache.status.item())
+    got = cache.len.view(NL, B, Hkv, 2).cpu().numpy()
+    if status != 0 or not all(np.array_equal(g[..., 0], len_hi) and np.array_equal(g[..., 1], len_lo)
+                              for g in got):
+        raise RuntimeError("serving state check failed (status %d)" % status)
+    comp_us = np.array([e[0].elapsed_time(e[1]) * 1e3 for e in ev])
+    app_us = np.array([e[1].elapsed_time(e[2]) * 1e3 for e in ev])
+    att_us = np.array([e[2].elapsed_time(e[3]) * 1e3 / NL for e in ev])
+    tok = np.array(step_tokens[Wm:], np.float64) * NL
+    byt = np.array(step_bytes[Wm:], np.float64)
+    res = {
+        "workload": "llama8b serving step: B=64, Hq=32, Hkv=8, context U[1024,4096], %d layers on one "
+                    "pool; per step one request recycled (one compaction call for all layers) and "
+                    "re-prefilled while 63 decode (one append call for all layers), then attention "
+                    "per layer; built in %.1f s" % (NL, time.time() - t0),
+        "kv_tokens_per_s": float(tok.sum() / wall),
+        "ms_per_step": wall / K * 1e3,
+        "compaction_us": pct(comp_us),
+        "append_us": pct(app_us),
+        "attention_us_per_launch": pct(att_us),
+        "attention_gbps": float(byt.sum() / (att_us.sum() * 1e-6) / 1e9),
+        "memory_management_share": float((comp_us + app_us).sum() / (wall * 1e6)),
+    }
+    log("serving step: %.3f ms/step, compaction %.1f us, append %.1f us, attention %.1f us/launch"
+        % (res["ms_per_step"], comp_us.mean(), app_us.mean(), att_us.mean()))
+    del cache, views, steps_in, masks
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -116,7 +481,6 @@ def main():
     import torch
 
     from paper_2412_03131_amd import diffkv as dk
-    from paper_2412_03131_amd import inputs
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -134,233 +498,84 @@ def main():
     if args.only == "generation":
         generation_bench(torch, dk, lib, dev, sptr, args.generation_steps)
         return
-
-    # ------------------------------------------------------------ workload --
-    t0 = time.time()
-    w = inputs.prefill("llama8b")
-    B, Hq, Hkv = w["B"], w["Hq"], w["Hkv"]
-    NL = args.layers
-    nl = w["new_len"].astype(np.int64)
-    off = np.concatenate([[0], np.cumsum(nl)])
-    steps_total = args.warmup + args.steps
-    init_hi = w["quota"][:, :, 0].astype(np.int64)
-    init_lo = w["quota"][:, :, 1].astype(np.int64)
-    L = dk.layout(max_seq_len=int(nl.max()) + steps_total + 16)
-    per_table = (-(-(init_hi + steps_total) // 16)) + (-(-init_lo // 32)) + 2
-    num_pages = int(NL * per_table.sum() * 1.05) + 1024
-    log("workload llama8b: B=%d Hq=%d Hkv=%d layers=%d tokens=%d pages=%d (%.2f GB pool), gen %.1fs"
-        % (B, Hq, Hkv, NL, int(nl.sum()), num_pages, num_pages * L.page_bytes / 1e9, time.time() - t0))
-    cache = dk.Cache(L, num_pages, NL * B, Hkv, device=dev)
-    views = [cache.view(l * B, (l + 1) * B) for l in range(NL)]
-
-    def T(a):
-        a = np.ascontiguousarray(a)
-        if a.dtype == np.uint16:
-            a = a.view(np.int16)
-        return torch.from_numpy(a).to(dev)
-
-    k_all, v_all, s_all = T(w["k"]), T(w["v"]), T(w["score"])
-    quota_all, nl_all = T(w["quota"]), T(w["new_len"])
-    ws_a = torch.empty(dk.workspace_size(dk.OP_APPEND, L, B, 0, Hkv, int(nl.sum()) + B) + 256,
-                       dtype=torch.uint8, device=dev)
-    for v in views:  # prompt phase of all 64 requests, every layer
-        dk.quantize_append(v, nl_all, k_all, v_all, s_all, quota=quota_all, total_new=int(nl.sum()),
-                           max_new=int(nl.max()), ws=ws_a)
-    torch.cuda.synchronize()
-    if int(cache.status.item()) != 0:
-        raise RuntimeError("prefill raised status %d" % int(cache.status.item()))
-
-    # per-step inputs: slot r gets a new request (same shape as the one it replaces),
-    # the other sequences one generated token each
-    steps_in = []
-    for s in range(steps_total):
-        r = s % B
-        d = inputs.decode_token("llama8b", s, B, Hq, Hkv, w["outliers"])
-        dk_ = T(d["k"])
-        dv_ = T(d["v"])
-        ds_ = T(d["score"])
-        k_s = torch.cat([dk_[:r], k_all[off[r]:off[r + 1]], dk_[r + 1:]])
-        v_s = torch.cat([dv_[:r], v_all[off[r]:off[r + 1]], dv_[r + 1:]])
-        s_s = torch.cat([ds_[:r], s_all[off[r]:off[r + 1]], ds_[r + 1:]])
-        q_np = d["quota"].copy()
-        q_np[r] = w["quota"][r]
-        n_np = np.ones(B, np.int32)
-        n_np[r] = nl[r]
-        # every layer's rows in one call: sequence l*B + b of the whole cache is
-        # sequence b of layer l, so the layers' row blocks follow each other
-        steps_in.append(dict(r=r, k=torch.cat([k_s] * NL), v=torch.cat([v_s] * NL),
-                             score=torch.cat([s_s] * NL), quota=T(np.tile(q_np, (NL, 1, 1))),
-                             new_len=T(np.tile(n_np, NL)), total=NL * int(n_np.sum()),
-                             maxn=int(n_np.max()), q=T(d["q"])))
-    P = L.p_max
-    masks = []
-    for r in range(B):
-        m = torch.zeros((NL * B * Hkv, P), dtype=torch.uint8, device=dev)
-        for l in range(NL):
-            m[(l * B + r) * Hkv:(l * B + r + 1) * Hkv] = 1
-        masks.append(m)
-    S = args.splits
-    ws_att = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, Hq, Hkv, 0, S)),
-                         dtype=torch.uint8, device=dev)
-    ws_c = torch.empty(dk.workspace_size(dk.OP_COMPACT, L, NL * B, 0, Hkv), dtype=torch.uint8,
-                       device=dev)
-    ws_all = torch.empty(dk.workspace_size(dk.OP_APPEND, L, NL * B, 0, Hkv,
-                                           max(si["total"] for si in steps_in)) + 256,
-                         dtype=torch.uint8, device=dev)
-    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
-    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-
-    # pre-built ctypes argument lists: the timed loop only enqueues
-    Lp = C.byref(L)
-    cstructs = [v.struct() for v in views]
-    call_struct = cache.struct()
-    vp = lambda x: C.c_void_p(x.data_ptr())
-    attn_args, app_args = [], []
-    for s, si in enumerate(steps_in):
-        app_args.append((Lp, C.byref(call_struct), si["total"], si["maxn"], vp(si["new_len"]),
-                         vp(si["k"]), vp(si["v"]), vp(si["score"]), vp(si["quota"]), 0.0, 0.0, 0,
-                         vp(ws_all), ws_all.numel(), sptr))
-        attn_args.append([(Lp, C.byref(cs), Hq, vp(si["q"]), float(SCALE), vp(out), vp(lse), S,
-                           vp(ws_att), ws_att.numel(), sptr) for cs in cstructs])
-    comp_args = [(Lp, C.byref(call_struct), NL * B * Hkv, vp(m), vp(ws_c), ws_c.numel(), sptr)
-                 for m in masks]
-    seq_rows = [torch.arange(r, NL * B, B, device=dev) for r in range(B)]
-
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
-
-    def run_step(s, timed_idx):
-        # one append for all layers, then every layer's attention back to back (the
-        # events around the attention calls then see kernel time, not the dispatch
-        # gap after the append)
-        si = steps_in[s]
-        r = si["r"]
-        rc = lib.diffkv_compact_free_list(*comp_args[r])
-        cache.seq_len.index_fill_(0, seq_rows[r], 0)
-        rc |= lib.diffkv_quantize_append(*app_args[s])
-        if timed_idx is not None:
-            ev[timed_idx][0].record(stream)
-        for l in range(NL):
-            rc |= lib.diffkv_decode_attention(*attn_args[s][l])
-        if timed_idx is not None:
-            ev[timed_idx][1].record(stream)
-        if rc:
-            raise RuntimeError("library call failed at step %d (rc %d)" % (s, rc))
-
-    # host-side expected lengths at every step's attention (for byte / token counts)
-    len_hi, len_lo = init_hi.copy(), init_lo.copy()
-    step_bytes, step_tokens = [], []
-    for s in range(steps_total):
-        r = s % B
-        len_hi += 1
-        len_hi[r] = init_hi[r]
-        len_lo[r] = init_lo[r]
-        step_bytes.append(attn_bytes(len_hi, len_lo, B, Hq, Hkv))
-        step_tokens.append(int(len_hi.sum() + len_lo.sum()))
-
+    flush = Flush(torch, dev)
+    wl = build_decode(torch, dk, dev, args.config, args.warmup + 2 * args.steps + 8)
     if args.only == "attention":
-        if args.hq:
-            hq = args.hq
-            qx = torch.randn((B, hq, 128), device=dev).half()
-            outx = torch.empty((B, hq, 128), dtype=torch.float32, device=dev)
-            lsex = torch.empty((B, hq), dtype=torch.float32, device=dev)
-            wsx = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, hq, Hkv, 0, S)),
-                              dtype=torch.uint8, device=dev)
-            attn_args[0] = [(Lp, C.byref(cs), hq, vp(qx), float(SCALE), vp(outx), vp(lsex), S,
-                             vp(wsx), wsx.numel(), sptr) for cs in cstructs]
-            Hq = hq
-        for s in range(args.warmup):
-            for l in range(NL):
-                lib.diffkv_decode_attention(*attn_args[0][l])
+        B, Hq, Hkv = wl["w"]["B"], wl["w"]["Hq"], wl["w"]["Hkv"]
+        ws = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, wl["L"], B, Hq, Hkv, 0, args.splits)),
+                         dtype=torch.uint8, device=dev)
+        q = wl["steps"][0]["q"]
+        for _ in range(args.warmup + args.steps):
+            dk.decode_attention(wl["cache"], q, SCALE, num_splits=args.splits, ws=ws)
         torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        for s in range(args.steps):
-            for l in range(NL):
-                lib.diffkv_decode_attention(*attn_args[0][l])
-        torch.cuda.synchronize()
-        el = (time.perf_counter() - t1) / (args.steps * NL)
-        nb = attn_bytes(init_hi, init_lo, B, Hq, Hkv)
-        log("attention only: %.1f us/launch, %.0f GB/s (%d bytes per launch)" % (el * 1e6, nb / el / 1e9, nb))
+        log("attention only: %d calls" % (args.warmup + args.steps))
         return
-
-    for s in range(args.warmup):
-        run_step(s, None)
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for i in range(args.steps):
-        run_step(args.warmup + i, i)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_start
-    status = int(cache.status.item())
-    got = cache.len.view(NL, B, Hkv, 2).cpu().numpy()
-    if status != 0 or not all(np.array_equal(g[..., 0], len_hi) and np.array_equal(g[..., 1], len_lo)
-                              for g in got):
-        raise RuntimeError("state check failed after the timed steps (status %d)" % status)
-    attn_ms = np.array([[a.elapsed_time(b) / NL] * NL for a, b in ev])  # [steps, layers], per launch
-    timed = slice(args.warmup, steps_total)
-    tok_layer = np.array(step_tokens[timed], np.float64)
-    bytes_layer = np.array(step_bytes[timed], np.float64)
-    kv_tokens = float(tok_layer.sum()) * NL
-    value = kv_tokens / wall
-    attn_total_s = attn_ms.sum() / 1e3
-    achieved = float(bytes_layer.sum() * NL / attn_total_s / 1e9)
-    log("step %.3f ms, attention %.1f us/launch, %.0f GB/s, %.3g KV tokens/s (whole step)"
-        % (wall / args.steps * 1e3, attn_ms.mean() * 1e3, achieved, value))
-
-    # ---------------------------------------------------------- compaction --
-    comp = compaction_bench(torch, dk, lib, dev, sptr, args.compaction_rounds)
-    gen = generation_bench(torch, dk, lib, dev, sptr, args.generation_steps)
-
-    # -------------------------------------------------------- cpu baseline --
-    cpu = None if args.no_cpu_baseline else cpu_baseline(w, args.cpu_seconds)
-    if cpu is not None:  # on-GPU against on-CPU memory management, as the paper compares them
-        comp["cpu_oracle_us_per_round"] = cpu["compaction"]["us_per_round"]
-        comp["gpu_speedup_vs_cpu_oracle"] = cpu["compaction"]["us_per_round"] / comp["us_per_round"]
-
+    head = decode_headline(torch, dk, lib, dev, sptr, wl, args, flush)
+    extras = {}
+    if args.extras == "all":
+        if args.config != "llama70b":
+            del wl
+            torch.cuda.empty_cache()
+            wl70 = build_decode(torch, dk, dev, "llama70b", 1)
+        else:
+            wl70 = wl
+        extras["llama70b"] = dict(workload=WORKLOADS["llama70b"].split(";")[0] + "; attention only, "
+                                  "flushed before every call; the automatic mode takes one workgroup "
+                                  "per table here (256 tables = the resident workgroups of GQA 8)",
+                                  **attention_modes(torch, dk, lib, dev, sptr, wl70, args.reps, flush))
+        del wl70
+        torch.cuda.empty_cache()
+        extras["serving_step"] = serving_step(torch, dk, lib, dev, sptr, args)
+        torch.cuda.empty_cache()
+        extras["compaction"] = compaction_bench(torch, dk, lib, dev, sptr, args.compaction_rounds)
+        extras["generation_step"] = generation_bench(torch, dk, lib, dev, sptr, args.generation_steps)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(args.config, args.cpu_seconds)
+    if cpu is not None and "compaction" in extras:
+        c = extras["compaction"]
+        c["cpu_oracle_us_per_round"] = cpu["compaction"]["us_per_round"]
+        c["gpu_speedup_vs_cpu_oracle"] = cpu["compaction"]["us_per_round"] / c["us_per_round"]
     line = {
         "metric": METRIC,
-        "value": value,
+        "value": head["value"],
         "unit": "KV tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": wall / args.steps * 1e3,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f16*code->f32",
+        "dtype_detail": DTYPE_DETAIL,
         "data": "synthetic",
-        "config": {
-            "workload": "llama8b decode step: B=64, Hq=32, Hkv=8, D=128, ctx U[1024,4096], "
-                        "f_hi U[0.1,0.5], f_pr U[0.2,0.6], K8V4/K4V2 group 32, 16/32 tokens "
-                        "per page; per step 1 request recycled + re-prefilled and 63 decode "
-                        "appends (one append call for all layers), then attention per layer; "
-                        "%d layers on one page pool" % NL,
-            "global_batch": B,
-            "layers": NL,
-            "attention_splits": S,
-        },
+        "config": {"workload": WORKLOADS[args.config], "global_batch": int(wl_B(args.config)),
+                   "attention_splits": args.splits},
         "roofline": {
             "kernel": "diffkv_decode_attention (attn_decode, plus attn_merge when the mode splits tables)",
             "bound": "hbm",
-            "achieved": achieved,
+            "achieved": head["achieved"],
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": measured_traffic(),
-            "bytes_per_launch": float(bytes_layer.mean()),
-            "us_per_launch": float(attn_ms.mean() * 1e3),
+            "frac": head["achieved"] / HBM_PEAK_GBPS,
+            "traffic": measured_traffic(args.config),
+            "bytes_per_launch": head["bytes_per_launch"],
+            "us_per_launch": head["us_per_launch"],
+            "timing": "HIP events on the launch stream around each step's attention call, Infinity "
+                      "Cache and L2 evicted before every step (outside the events); mean over the "
+                      "timed steps",
         },
-        "attention": {
-            "kv_tokens_per_s": float(tok_layer.sum() * NL / attn_total_s),
-            "kv_tokens_per_launch": float(tok_layer.mean()),
-            "fp16_equivalent_gbps": float(tok_layer.sum() * NL * 512 / attn_total_s / 1e9),
-        },
-        "compaction": comp,
-        "generation_step": gen,
-        "cpu_baseline": cpu,
+        "attention": head["attention"],
+        "append": head["append"],
+        "step": head["step"],
     }
+    line.update(extras)
+    line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
+
+
+def wl_B(config):
+    from paper_2412_03131_amd import inputs
+    return inputs.CONFIGS[config]["B"]
 
 
 def compaction_bench(torch, dk, lib, dev, sptr, rounds):
@@ -416,6 +631,7 @@ def compaction_bench(torch, dk, lib, dev, sptr, rounds):
         "released_pages_per_s": released / rounds / (cms.mean() / 1e3),
         "us_per_round": float(cms.mean() * 1e3),
         "us_p10_p90": [float(np.percentile(cms, 10) * 1e3), float(np.percentile(cms, 90) * 1e3)],
+        "us_median": float(np.median(cms) * 1e3),
         "refill_us_per_round": float(ams.mean() * 1e3),
         "released_per_round": released / rounds,
         "ring_wraps": int(ring_ptr[1] // npg),
@@ -502,33 +718,96 @@ def generation_bench(torch, dk, lib, dev, sptr, steps, window=64):
     return res
 
 
-def cpu_baseline(w, seconds):
-    """The oracle's fp64 attention, single-threaded on the host, over the first 8
-    requests of the same workload, repeated until `seconds` of CPU time are spent."""
+
+
+def cpu_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        avail = os.cpu_count() or 1
+    return model, os.cpu_count(), avail
+
+
+def cpu_baseline(config, seconds):
+    """The oracle's fp64 attention on the host, over the first requests of the headline
+    workload, each request in its own oracle cache: one thread on request 0, then one
+    thread per request on up to 16 requests at once (the machine's CPU share), each looping
+    attention passes until `seconds` have passed.  The oracle's C code runs outside the
+    interpreter lock, so the threads run in parallel.  Then the serial compaction."""
+    import threading
+
     from oracle import oracle as orc
-    nreq = 8
-    Lo = orc.layout(max_seq_len=int(w["new_len"][:nreq].max()) + 16)
-    rows = int(w["new_len"][:nreq].sum())
+    from paper_2412_03131_amd import inputs
+    model, ncpu, avail = cpu_info()
+    nthreads = max(1, min(16, avail, inputs.CONFIGS[config]["B"]))
+    t0 = time.time()
+    w = inputs.prefill(config, B=nthreads)
     Hkv = w["Hkv"]
-    tabs = nreq * Hkv
-    npg = int(tabs * (int(w["new_len"][:nreq].max()) // 16 + 4))
-    oc = orc.Cache(Lo, npg, nreq, Hkv)
-    orc.quantize_append(oc, w["new_len"][:nreq], w["k"][:rows], w["v"][:rows], w["score"][:rows],
-                        quota=w["quota"][:nreq])
-    q = w["q"][:nreq]
-    tokens = int(oc.len.sum())
-    t0 = time.process_time()
-    reps = 0
-    while True:
-        orc.attention(oc, q, SCALE)
-        reps += 1
-        el = time.process_time() - t0
-        if el >= seconds:
-            break
-    res = {"value": tokens * reps / el, "unit": "KV tokens/s", "cores": 1, "kind": "oracle",
-           "sample": "fp64 oracle attention over requests 0-7 of the llama8b workload "
-                     "(%d KV tokens), %d passes, %.1f s CPU" % (tokens, reps, el)}
-    log("cpu baseline: %.3g KV tokens/s" % res["value"])
+    nl = w["new_len"].astype(np.int64)
+    off = np.concatenate([[0], np.cumsum(nl)])
+    caches = [None] * nthreads
+
+    def build(r):
+        Lo = orc.layout(max_seq_len=int(nl[r]) + 16)
+        npg = Hkv * (int(nl[r]) // 16 + 4)
+        c = orc.Cache(Lo, npg, 1, Hkv)
+        orc.quantize_append(c, w["new_len"][r:r + 1], w["k"][off[r]:off[r + 1]], w["v"][off[r]:off[r + 1]],
+                            w["score"][off[r]:off[r + 1]], quota=w["quota"][r:r + 1])
+        caches[r] = c
+
+    th = [threading.Thread(target=build, args=(r,)) for r in range(nthreads)]
+    for x in th:
+        x.start()
+    for x in th:
+        x.join()
+    q = [w["q"][r:r + 1] for r in range(nthreads)]
+    toks = [int(c.len.sum()) for c in caches]
+    log("cpu baseline: %d oracle caches built in %.1f s" % (nthreads, time.time() - t0))
+
+    def passes(r, until, res):
+        n = 0
+        while True:
+            orc.attention(caches[r], q[r], SCALE)
+            n += 1
+            if time.perf_counter() >= until:
+                break
+        res[r] = n
+
+    # one thread
+    res1 = {}
+    t1 = time.perf_counter()
+    passes(0, t1 + seconds, res1)
+    el1 = time.perf_counter() - t1
+    one = toks[0] * res1[0] / el1
+    # every thread
+    resn = {}
+    t2 = time.perf_counter()
+    th = [threading.Thread(target=passes, args=(r, t2 + seconds, resn)) for r in range(nthreads)]
+    for x in th:
+        x.start()
+    for x in th:
+        x.join()
+    el2 = time.perf_counter() - t2
+    alln = sum(toks[r] * resn[r] for r in range(nthreads)) / el2
+    res = {"value": alln, "unit": "KV tokens/s", "cores": nthreads, "kind": "oracle",
+           "sample": "fp64 oracle attention over requests 0-%d of the %s workload (%d KV tokens in all, "
+                     "one oracle cache per request), one thread per request, %.1f s wall"
+                     % (nthreads - 1, config, sum(toks), el2),
+           "single_thread": {"value": one, "cores": 1,
+                             "sample": "request 0 (%d KV tokens), %d passes, %.1f s" % (toks[0], res1[0], el1)},
+           "cpu_model": model, "nproc": ncpu, "cores_available": avail}
+    log("cpu baseline: %.3g KV tokens/s on %d threads, %.3g on one (%s, nproc %s)"
+        % (alln, nthreads, one, model, ncpu))
+    del caches, w
     res["compaction"] = cpu_compaction(seconds / 4)
     return res
 

@@ -14,7 +14,8 @@
  *
  * Conventions
  *   - All entry points are C, take plain pointers and sizes, never allocate,
- *     free or synchronise, and keep no state between calls.
+ *     free or synchronise, and keep no state between calls (except the
+ *     per-device scratch address of diffkv_decode_attention_noalloc).
  *   - "device" pointers point to GPU memory of the current HIP device;
  *     "host" pointers to CPU memory.  The caller owns every buffer.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
@@ -49,7 +50,9 @@ enum {
     DIFFKV_E_INVAL = 1,       /* null pointer, negative or inconsistent size       */
     DIFFKV_E_UNSUPPORTED = 2, /* layout/shape the gfx950 kernels do not implement  */
     DIFFKV_E_WORKSPACE = 3,   /* ws_bytes smaller than diffkv_workspace_size()     */
-    DIFFKV_E_LAUNCH = 4       /* a HIP launch or runtime call failed               */
+    DIFFKV_E_LAUNCH = 4,      /* a HIP launch or runtime call failed               */
+    DIFFKV_E_SCRATCH = 5      /* the call needs more than the fixed scratch of
+                                 diffkv_decode_attention_noalloc                   */
 };
 
 /* sticky bits of *diffkv_cache.status */
@@ -231,6 +234,26 @@ diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_
                                       int32_t num_q_heads, const uint16_t* q, float sm_scale,
                                       float* out, float* lse, int32_t num_splits,
                                       void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * diffkv_decode_attention without a workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, minus ws / ws_bytes, and
+ * the same kernels and results, bit for bit.  The work bookkeeping and split
+ * partial states go to a fixed 8 MiB array in the library's device memory, one
+ * per device, held from the library's load until the process ends; its device
+ * address is looked up on the first call on each device and kept (the one
+ * piece of state the library keeps).  A call whose mode, as resolved on the
+ * current device, needs more -- the balanced mode takes 8 B per table plus
+ * (resident workgroups + tables) * (Hq/Hkv) * 520 B -- returns
+ * DIFFKV_E_SCRATCH and enqueues nothing.  Nothing in the scratch needs
+ * clearing between calls.  Every call on a device shares that device's array:
+ * calls ordered on one stream are safe, calls that may overlap on one device
+ * (unordered streams) race.  Allocates, frees and synchronizes nothing.
+ */
+diffkv_status diffkv_decode_attention_noalloc(const diffkv_layout* layout, const diffkv_cache* cache,
+                                              int32_t num_q_heads, const uint16_t* q, float sm_scale,
+                                              float* out, float* lse, int32_t num_splits, void* stream);
 
 /*
  * Parallel free-list compaction (Sec. 5.2 recycling, Sec. 5.3): for the

@@ -127,12 +127,12 @@ struct AttnWs {
     int64_t ustart, utot, part, total, nparts;
 };
 
-AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits)
+AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits, int64_t workers)
 {
     AttnWs w;
     const int64_t T = B * Hkv;
     const int64_t gq = Hkv > 0 ? Hq / Hkv : 1;
-    w.nparts = splits <= 0 ? kAttnMaxWorkers + T : (splits > 1 ? T * splits : 0);
+    w.nparts = splits <= 0 ? workers + T : (splits > 1 ? T * splits : 0);
     int64_t o = 0;
     w.ustart = o; o = align256(o + T * 8);
     w.utot = o;   o = align256(o + 8);
@@ -147,6 +147,69 @@ int64_t alloc_ws(int64_t T) { return align256(sizeof(CallFlags)) + align256(T * 
 int64_t gen_ws(int64_t T)
 {
     return align256(sizeof(CallFlags)) + 2 * align256(T * 16) + 2 * align256(T * 4);
+}
+
+
+// Both attention entry points.  `noalloc`: the workspace is the device's fixed
+// scratch, sized for the mode the call resolves to on the current device.
+diffkv_status attention_call(const diffkv_layout* layout, const diffkv_cache* cache, int32_t num_q_heads,
+                             const uint16_t* q, float sm_scale, float* out, float* lse, int32_t num_splits,
+                             void* ws, size_t ws_bytes, bool noalloc, void* stream)
+{
+    if (!layout_valid(layout) || !cache_valid(cache) || !cache->pool) return DIFFKV_E_INVAL;
+    if (num_q_heads <= 0 || num_q_heads % cache->num_kv_heads != 0 || num_splits < -1)
+        return DIFFKV_E_INVAL;
+    if (!layout_kernels_supported(layout)) return DIFFKV_E_UNSUPPORTED;
+    if (num_q_heads / cache->num_kv_heads > 8) return DIFFKV_E_UNSUPPORTED;
+    if (cache->num_seqs == 0) return DIFFKV_OK;
+    if (!q || !out) return DIFFKV_E_INVAL;
+    if (cache->num_seqs > 65535 || cache->num_kv_heads > 65535) return DIFFKV_E_UNSUPPORTED;
+    if (num_splits > 65535) return DIFFKV_E_INVAL;
+    if ((int64_t)cache->num_seqs * cache->num_kv_heads * (num_splits > 0 ? num_splits : 1) > INT32_MAX)
+        return DIFFKV_E_INVAL;
+    AttnWs w;
+    if (noalloc) {
+        const int64_t T = (int64_t)cache->num_seqs * cache->num_kv_heads;
+        int mode = 0, workers = 0;
+        if (attention_mode(num_q_heads / cache->num_kv_heads, T, num_splits, &mode, &workers) != hipSuccess)
+            return DIFFKV_E_LAUNCH;
+        // the balanced mode writes partial slots share + table < workers + T
+        w = attn_ws(cache->num_seqs, num_q_heads, cache->num_kv_heads, mode, workers);
+        if (w.total > kNoAllocScratchBytes) return DIFFKV_E_SCRATCH;
+        if (noalloc_scratch(&ws) != hipSuccess) return DIFFKV_E_LAUNCH;
+        ws_bytes = (size_t)kNoAllocScratchBytes;
+    } else {
+        w = attn_ws(cache->num_seqs, num_q_heads, cache->num_kv_heads, num_splits, kAttnMaxWorkers);
+        if (!ws || (int64_t)ws_bytes < w.total) return DIFFKV_E_WORKSPACE;
+    }
+    AttnArgs a;
+    memset(&a, 0, sizeof(a));
+    a.p_max = layout->p_max;
+    a.page_bytes = layout->page_bytes;
+    a.num_pages = cache->num_pages;
+    for (int p = 0; p < 2; ++p) {
+        a.off_kcode[p] = layout->off_kcode[p];
+        a.off_kmeta[p] = layout->off_kmeta[p];
+        a.off_vcode[p] = layout->off_vcode[p];
+        a.off_vmeta[p] = layout->off_vmeta[p];
+    }
+    a.pool = cache->pool;
+    a.page_table = cache->page_table;
+    a.len = cache->len;
+    a.B = cache->num_seqs;
+    a.Hkv = cache->num_kv_heads;
+    a.Hq = num_q_heads;
+    a.q = q;
+    a.scale_log2 = sm_scale * 1.4426950408889634f;
+    a.out = out;
+    a.lse = lse;
+    a.splits = num_splits;
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    a.ustart = reinterpret_cast<long long*>(base + w.ustart);
+    a.utot = reinterpret_cast<long long*>(base + w.utot);
+    a.part = reinterpret_cast<float*>(base + w.part);
+    hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
 }
 
 }  // namespace
@@ -172,7 +235,7 @@ diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout, int
         return DIFFKV_OK;
     case DIFFKV_OP_ATTENTION: {
         if (num_q_heads <= 0 || num_kv_heads <= 0 || num_splits < -1) return DIFFKV_E_INVAL;
-        *bytes = (size_t)attn_ws(num_seqs, num_q_heads, num_kv_heads, num_splits).total;
+        *bytes = (size_t)attn_ws(num_seqs, num_q_heads, num_kv_heads, num_splits, kAttnMaxWorkers).total;
         return DIFFKV_OK;
     }
     case DIFFKV_OP_COMPACT:
@@ -259,47 +322,16 @@ diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_
                                       float* out, float* lse, int32_t num_splits, void* ws,
                                       size_t ws_bytes, void* stream)
 {
-    if (!layout_valid(layout) || !cache_valid(cache) || !cache->pool) return DIFFKV_E_INVAL;
-    if (num_q_heads <= 0 || num_q_heads % cache->num_kv_heads != 0 || num_splits < -1)
-        return DIFFKV_E_INVAL;
-    if (!layout_kernels_supported(layout)) return DIFFKV_E_UNSUPPORTED;
-    if (num_q_heads / cache->num_kv_heads > 8) return DIFFKV_E_UNSUPPORTED;
-    if (cache->num_seqs == 0) return DIFFKV_OK;
-    if (!q || !out) return DIFFKV_E_INVAL;
-    if (cache->num_seqs > 65535 || cache->num_kv_heads > 65535) return DIFFKV_E_UNSUPPORTED;
-    if (num_splits > 65535) return DIFFKV_E_INVAL;
-    const AttnWs w = attn_ws(cache->num_seqs, num_q_heads, cache->num_kv_heads, num_splits);
-    if ((int64_t)cache->num_seqs * cache->num_kv_heads * (num_splits > 0 ? num_splits : 1) > INT32_MAX)
-        return DIFFKV_E_INVAL;
-    if (!ws || (int64_t)ws_bytes < w.total) return DIFFKV_E_WORKSPACE;
-    AttnArgs a;
-    memset(&a, 0, sizeof(a));
-    a.p_max = layout->p_max;
-    a.page_bytes = layout->page_bytes;
-    a.num_pages = cache->num_pages;
-    for (int p = 0; p < 2; ++p) {
-        a.off_kcode[p] = layout->off_kcode[p];
-        a.off_kmeta[p] = layout->off_kmeta[p];
-        a.off_vcode[p] = layout->off_vcode[p];
-        a.off_vmeta[p] = layout->off_vmeta[p];
-    }
-    a.pool = cache->pool;
-    a.page_table = cache->page_table;
-    a.len = cache->len;
-    a.B = cache->num_seqs;
-    a.Hkv = cache->num_kv_heads;
-    a.Hq = num_q_heads;
-    a.q = q;
-    a.scale_log2 = sm_scale * 1.4426950408889634f;
-    a.out = out;
-    a.lse = lse;
-    a.splits = num_splits;
-    uint8_t* base = static_cast<uint8_t*>(ws);
-    a.ustart = reinterpret_cast<long long*>(base + w.ustart);
-    a.utot = reinterpret_cast<long long*>(base + w.utot);
-    a.part = reinterpret_cast<float*>(base + w.part);
-    hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
-    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
+    return attention_call(layout, cache, num_q_heads, q, sm_scale, out, lse, num_splits, ws, ws_bytes,
+                           false, stream);
+}
+
+diffkv_status diffkv_decode_attention_noalloc(const diffkv_layout* layout, const diffkv_cache* cache,
+                                              int32_t num_q_heads, const uint16_t* q, float sm_scale,
+                                              float* out, float* lse, int32_t num_splits, void* stream)
+{
+    return attention_call(layout, cache, num_q_heads, q, sm_scale, out, lse, num_splits, nullptr, 0,
+                          true, stream);
 }
 
 diffkv_status diffkv_compact_free_list(const diffkv_layout* layout, const diffkv_cache* cache,
@@ -411,6 +443,7 @@ const char* diffkv_status_str(diffkv_status s)
     case DIFFKV_E_UNSUPPORTED: return "layout or shape not supported by the gfx950 kernels";
     case DIFFKV_E_WORKSPACE: return "workspace too small";
     case DIFFKV_E_LAUNCH: return "HIP launch failed";
+    case DIFFKV_E_SCRATCH: return "call needs more than the fixed scratch of the no-allocation entry point";
     default: return "unknown status";
     }
 }

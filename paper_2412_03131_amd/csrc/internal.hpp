@@ -142,6 +142,14 @@ hipError_t launch_alloc(const AllocArgs& a, hipStream_t st);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
 hipError_t launch_generation(const GenArgs& g, hipStream_t st);
 hipError_t launch_attention(AttnArgs a, hipStream_t st);
+// The mode an attention call with `splits` runs in on the current device:
+// S >= 1 page ranges per table (S = 1: no split) or -1 (balanced shares);
+// *workers = the balanced mode's share count.
+hipError_t attention_mode(int gq, long long T, int splits, int* mode, int* workers);
+
+// Fixed device scratch of diffkv_decode_attention_noalloc, one per device.
+constexpr long long kNoAllocScratchBytes = 8ll << 20;
+hipError_t noalloc_scratch(void** ptr);
 bool attention_layout_matches(const diffkv_layout* L);
 
 }  // namespace dkv

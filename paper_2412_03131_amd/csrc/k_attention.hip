@@ -33,6 +33,7 @@
 //                the zero-point term and the weights' rounding error (charged
 //                at the centre code) are accumulated per lane and added once.
 // The eight waves' (max, sum, acc) states merge through LDS.
+#include <atomic>
 #include <utility>
 
 #include "internal.hpp"
@@ -1193,6 +1194,43 @@ bool attention_layout_matches(const diffkv_layout* L)
            L->off_vcode[1] == kOffVcLo && L->off_vmeta[1] == kOffVmLo;
 }
 
+hipError_t attention_mode(int gq, long long T, int splits, int* mode, int* workers)
+{
+    hipError_t e = balanced_workers(gq, workers);
+    if (e != hipSuccess) return e;
+    // automatic: one workgroup per table when the tables alone fill the device
+    // (their spread is absorbed by wave priorities and by the hardware
+    // dispatching further tables as workgroups finish), balanced shares when
+    // there are fewer tables than resident workgroups
+    *mode = splits != 0 ? splits : (T >= *workers ? 1 : -1);
+    return hipSuccess;
+}
+
+// The no-allocation entry point's scratch: work bookkeeping and split partial
+// states of one attention call.  In host code `scratch` names a host-side
+// stand-in, so its device address is looked up once per device (with that
+// device current) and only that address is handed to kernels.
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+hipError_t noalloc_scratch(void** ptr)
+{
+    constexpr int kDevs = 64;
+    static std::atomic<void*> addr[kDevs];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kDevs) return hipErrorInvalidDevice;
+    void* p = addr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        addr[dev].store(p, std::memory_order_release);
+    }
+    *ptr = p;
+    return hipSuccess;
+}
+
 hipError_t launch_attention(AttnArgs a, hipStream_t st)
 {
     const int gq = a.Hq / a.Hkv;
@@ -1200,16 +1238,9 @@ hipError_t launch_attention(AttnArgs a, hipStream_t st)
     if (!kern) return hipErrorInvalidValue;
     const long long T = (long long)a.B * a.Hkv;
     int workers = 0;
-    hipError_t e = balanced_workers(gq, &workers);
+    hipError_t e = attention_mode(gq, T, a.splits, &a.splits, &workers);
     if (e != hipSuccess) return e;
     long long grid;
-    if (a.splits == 0) {
-        // automatic: one workgroup per table when the tables alone fill the
-        // device (their spread is absorbed by wave priorities and by the
-        // hardware dispatching further tables as workgroups finish), balanced
-        // shares when there are fewer tables than resident workgroups
-        a.splits = T >= workers ? 1 : -1;
-    }
     if (a.splits > 0) {
         grid = T * a.splits;
         a.workers = 0;

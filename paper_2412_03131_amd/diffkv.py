@@ -12,7 +12,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdiffkv.so")
 
-OK, E_INVAL, E_UNSUPPORTED, E_WORKSPACE, E_LAUNCH = 0, 1, 2, 3, 4
+OK, E_INVAL, E_UNSUPPORTED, E_WORKSPACE, E_LAUNCH, E_SCRATCH = 0, 1, 2, 3, 4, 5
 ST_OUT_OF_PAGES, ST_TABLE_OVERFLOW, ST_BAD_INPUT = 1, 2, 4
 OP_APPEND, OP_ATTENTION, OP_COMPACT, OP_ALLOC, OP_GENERATION = 0, 1, 2, 3, 4
 HIGH, LOW = 0, 1
@@ -50,8 +50,8 @@ class CacheStruct(C.Structure):
 
 
 EXPORTS = ("diffkv_layout_init", "diffkv_workspace_size", "diffkv_quantize_append",
-           "diffkv_decode_attention", "diffkv_compact_free_list", "diffkv_alloc_pages",
-           "diffkv_generation_step", "diffkv_status_str")
+           "diffkv_decode_attention", "diffkv_decode_attention_noalloc", "diffkv_compact_free_list",
+           "diffkv_alloc_pages", "diffkv_generation_step", "diffkv_status_str")
 
 
 def lib():
@@ -69,6 +69,7 @@ def lib():
         L.diffkv_quantize_append.argtypes = [PL, PC, i64, i32, vp, vp, vp, vp, vp, f32, f32, i32,
                                              vp, sz, vp]
         L.diffkv_decode_attention.argtypes = [PL, PC, i32, vp, f32, vp, vp, i32, vp, sz, vp]
+        L.diffkv_decode_attention_noalloc.argtypes = [PL, PC, i32, vp, f32, vp, vp, i32, vp]
         L.diffkv_compact_free_list.argtypes = [PL, PC, i32, vp, vp, sz, vp]
         L.diffkv_alloc_pages.argtypes = [PL, PC, i32, vp, vp, sz, vp]
         L.diffkv_generation_step.argtypes = [PL, PC, f32, f32, i32, vp, sz, vp]
@@ -216,6 +217,16 @@ def decode_attention(cache, q, sm_scale, out=None, lse=None, num_splits=0, ws=No
         C.byref(L), C.byref(st), Hq, _ptr(_bits16(q)), float(sm_scale), _ptr(out), _ptr(lse),
         int(num_splits), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
         "diffkv_decode_attention")
+    return out, lse
+
+
+def decode_attention_noalloc(cache, q, sm_scale, out, lse=None, num_splits=0, stream=None):
+    """diffkv_decode_attention_noalloc: like decode_attention, outputs given by the
+    caller, no workspace (the library's fixed per-device scratch)."""
+    st = cache.struct()
+    _check(lib().diffkv_decode_attention_noalloc(
+        C.byref(cache.L), C.byref(st), q.shape[1], _ptr(_bits16(q)), float(sm_scale), _ptr(out),
+        _ptr(lse), int(num_splits), _stream(stream)), "diffkv_decode_attention_noalloc")
     return out, lse
 
 

@@ -34,6 +34,7 @@
 //                at the centre code) are accumulated per lane and added once.
 // The eight waves' (max, sum, acc) states merge through LDS.
 #include <atomic>
+#include <cstddef>
 #include <utility>
 
 #include "internal.hpp"
@@ -308,6 +309,79 @@ __device__ __forceinline__ void load_page(PageRaw& r, const uint8_t* pg, bool hi
     r.m3 = __builtin_amdgcn_raw_buffer_load_b32(rs, vm + kOffVmHi, lo + (hi ? 0 : 64), 0);  // high pages: a line already fetched
 }
 
+// One wave's next page, written into LDS by the seven loads themselves (buffer
+// loads with an LDS destination: lane L's 16- or 4-byte piece lands at index L
+// of its row), so a page can be in flight while the wave computes another one
+// from registers without holding a second register buffer.
+struct PageStage {
+    uint4 k0[kWave];
+    uint4 k1[kWave];
+    uint4 vr[kWave];
+    uint32_t m[4][kWave];
+};
+
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+typedef __attribute__((address_space(3))) _Float16 lds_f16;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32x4 lds_u4;
+
+// Buffer loads with an LDS destination: lane L's 16 (or 4) bytes land at byte
+// m0 + 16 L (or m0 + 4 L).  Written as asm so that the compiler, which would
+// otherwise make every later LDS access wait for them, leaves their waits to
+// take_page (the only reader of the slot).
+__device__ __forceinline__ void lds_load16(u32x4 rs, uint32_t m0, uint32_t voff, uint32_t soff)
+{
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 ::"s"(m0), "v"(voff), "s"(rs), "s"(soff) : "memory");
+}
+__device__ __forceinline__ void lds_load4(u32x4 rs, uint32_t m0, uint32_t voff, uint32_t soff)
+{
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+                 ::"s"(m0), "v"(voff), "s"(rs), "s"(soff) : "memory");
+}
+
+// Stage a page into the wave's slot: the seven loads of load_page, through a
+// buffer resource over the one page (base pg, 4352 bytes: the hardware bounds
+// every access), with LDS destinations.
+__device__ __forceinline__ void stage_page(PageStage& sg, const uint8_t* pg, bool hi, int lane)
+{
+    const uint32_t grp = (uint32_t)lane >> 4, jl = (uint32_t)lane & 15;
+    const unsigned long long base = (unsigned long long)pg;
+    const u32x4 rs = {(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, (uint32_t)kPageBytes, 0x00020000u};
+    const uint32_t kc = grp * 512 + jl * 16;
+    const uint32_t km = 2048 + jl * 16 + grp * 4;
+    const uint32_t lo = hi ? 0u : 256u;
+    const uint32_t vm = (hi ? grp * (kTHi * 4) : grp * (kTLo * 4)) + jl * 4;
+    const uint32_t m0 = (uint32_t)(size_t)(__attribute__((address_space(3))) void*)&sg;
+    static_assert(sizeof(PageStage) == 4096 && offsetof(PageStage, k1) == 1024 && offsetof(PageStage, vr) == 2048 &&
+                      offsetof(PageStage, m) == 3072,
+                  "stage slot layout");
+    lds_load16(rs, m0, kc, 0u);
+    lds_load16(rs, m0 + 1024, kc + 256, 0u);
+    lds_load16(rs, m0 + 2048, (uint32_t)lane * 16 + kOffVcHi, lo);
+    lds_load4(rs, m0 + 3072, km, 0u);
+    lds_load4(rs, m0 + 3328, km + 256, 0u);
+    lds_load4(rs, m0 + 3584, vm + kOffVmHi, lo);
+    lds_load4(rs, m0 + 3840, vm + kOffVmHi, lo + (hi ? 0u : 64u));
+}
+
+// The staged page into registers: wait for the wave's staging loads (every
+// vector load of the wave, the only ones in flight here being the slot's),
+// read the slot, and wait for the reads, so the next staging loads cannot
+// overwrite the slot before it is read.
+__device__ __forceinline__ void take_page(PageRaw& r, const PageStage& sg, int lane)
+{
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    r.k0 = sg.k0[lane];
+    r.k1 = sg.k1[lane];
+    r.vr = sg.vr[lane];
+    r.m0 = sg.m[0][lane];
+    r.m1 = sg.m[1][lane];
+    r.m2 = sg.m[2][lane];
+    r.m3 = sg.m[3][lane];
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
 template <int GQ>
 struct WaveState {
     static constexpr int NS = (GQ + 3) / 4;  // head slots per lane in the softmax layout
@@ -372,7 +446,7 @@ template <int GQ, int NT>
 __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, const uint32_t (&qr)[GQ],
                                         const half2_t (&q0)[GQ],
                                         const float (&qsum)[GQ], float sl2, int n_valid, int lane,
-                                        uint32_t* coef_row)
+                                        lds_u32* coef_row)
 {
     constexpr int NS = WaveState<GQ>::NS;
     constexpr int kH = CoefLds<GQ>::kH;
@@ -453,7 +527,7 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
     }
     // ---- value weights of token jl + 16*tk for this lane's group (row), all
     // heads: fp16 to LDS, zero-point and rounding terms into z
-    _Float16* crow = reinterpret_cast<_Float16*>(coef_row);
+    lds_f16* crow = reinterpret_cast<lds_f16*>(coef_row);
 #pragma unroll
     for (int tk = 0; tk < NT; ++tk) {
         float pg[4 * NS];
@@ -468,7 +542,7 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         const float zc = fmaf(centre, vs, vz);
         const int pi = NT == 1 ? ((jl >> 3) * 4 + (jl & 3)) : (tk * 8 + (jl & 7));
         const int pos = NT == 1 ? ((jl >> 2) & 1) : (jl >> 3);
-        _Float16* dst = crow + pi * 2 * kH + pos;
+        lds_f16* dst = crow + pi * 2 * kH + pos;
 #pragma unroll
         for (int hh = 0; hh < GQ; ++hh) {
             const _Float16 c = (_Float16)(pg[hh] * vs_c);
@@ -486,11 +560,11 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
     auto read_cf = [&](int p0, half2_t (&cf)[4][GQ]) {
 #pragma unroll
         for (int pp = 0; pp < 4; ++pp) {
-            const uint32_t* src = coef_row + (p0 + pp) * kH;
+            const lds_u32* src = coef_row + (p0 + pp) * kH;
             uint32_t t[kH];
 #pragma unroll
             for (int i = 0; i < kH; i += 4) {
-                const uint4 v = *reinterpret_cast<const uint4*>(src + i);
+                const u32x4 v = *reinterpret_cast<const lds_u4*>(src + i);
                 t[i] = v.x; t[i + 1] = v.y; t[i + 2] = v.z; t[i + 3] = v.w;
             }
 #pragma unroll
@@ -596,10 +670,9 @@ __device__ __forceinline__ int page_at_unit(long long x, int ph, int np)
 
 template <int GQ>
 struct AttnShared {
-    CoefLds<GQ> coef;
     float m[kAttnWaves][8];
     float l[kAttnWaves][8];
-    float acc[kAttnWaves][8][kD];
+    float acc[kAttnWaves][GQ][kD];
     long long scan[kAttnWaves + 1];
     int t_first;
     int len_first[2];  // section lengths of t_first (longest-first ranking)
@@ -650,8 +723,9 @@ __device__ __forceinline__ void write_empty(const AttnArgs& a, int t, int gq)
 // per head at `part` (pa == pb gives the empty state).
 // ---------------------------------------------------------------------------
 template <int GQ>
-__device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& sh, int t, const TableInfo& ti,
-                                            int pa, int pb, float* part)
+__device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& sh, CoefLds<GQ>* coef,
+                                            PageStage* stage, int t, const TableInfo& ti, int pa, int pb,
+                                            float* part)
 {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -662,7 +736,7 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     const float sl2 = a.scale_log2;
     const long long npool = a.num_pages;
     constexpr long long page_bytes = kPageBytes;  // (the layout check guarantees it)
-    uint32_t* coef_row = &sh.coef.v[wave][grp * CoefLds<GQ>::kRow];
+    lds_u32* coef_row = (lds_u32*)(&coef->v[wave][grp * CoefLds<GQ>::kRow]);
     const int nmine = pb - pa > wave ? (pb - pa - wave + kAttnWaves - 1) / kAttnWaves : 0;
     const int32_t* trow = a.page_table + (long long)t * P;
 
@@ -678,17 +752,17 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         const int k = c0 + lane;
         return trow[slot_of(page_of(clamp_i(k)))];
     };
-    // Issue the loads of page i into r; ok = page i exists and lies in the pool.
-    // The loads are unconditional (past the chunk's last page they re-read it,
-    // a cache hit; an ID outside the pool reads page 0 and is not computed), so
-    // the wait before each page's use counts only the loads issued since.
+    // Stage page i in this wave's LDS slot; ok = page i exists and lies in the
+    // pool.  The loads are unconditional (an index past the chunk's last page
+    // re-reads it; an ID outside the pool reads page 0 and is not computed).
+    PageStage& sg = stage[wave];
     const uint32_t npool32 = npool > 0x7fffffffLL ? 0x80000000u : (uint32_t)npool;
-    auto issue = [&](int i, PageRaw& r, bool& ok) {
+    auto issue = [&](int i, bool& ok) {
         const int ic = clamp_i(i);
         const int id = __builtin_amdgcn_readlane(ids_v, ic - c0);
         const bool in_pool = (uint32_t)id < npool32;  // never read outside the pool
         ok = i < c1 && in_pool;
-        load_page(r, a.pool + (in_pool ? id : 0) * page_bytes, page_of(ic) < ph, lane);
+        stage_page(sg, a.pool + (in_pool ? id : 0) * page_bytes, page_of(ic) < ph, lane);
     };
     // The query loads go first: they depend only on the table, so their
     // latency overlaps the page-ID -> page chain below.  Lane k of a row loads
@@ -707,13 +781,13 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     }
 
     PageRaw buf0;
-    bool ok0 = false;
+    bool ok0 = false, ok_next = false;
     // first chunk: its IDs and first page go out beside the query loads
     c1 = nmine < kWave ? nmine : kWave;
     c_last = c1 > 0 ? c1 - 1 : 0;
     if (nmine > 0) {
         ids_v = load_ids();
-        issue(0, buf0, ok0);
+        issue(0, ok_next);
     }
 
     // q of this lane's group as fp16 pairs (d, d+4), one pair per lane (read
@@ -769,17 +843,25 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         else if (rem > 2) __builtin_amdgcn_s_setprio(1);
         else __builtin_amdgcn_s_setprio(0);
     };
+    // Page i comes out of the LDS slot into registers, page i + 1 goes into the
+    // slot, then page i is computed: one page is always in flight while the
+    // wave computes.
+    auto next = [&](int i) {
+        take_page(buf0, sg, lane);
+        ok0 = ok_next;
+        if (i + 1 < c1) issue(i + 1, ok_next);
+    };
     while (c0 < nmine) {
         const int nh = nhi < c1 ? nhi : c1;  // high pages end (within this chunk)
         int i = c0;
         for (; i < nh; ++i) {
             set_prio(nmine - i);
-            if (i > c0) issue(i, buf0, ok0);
+            next(i);
             compute_hi(i, buf0, ok0);
         }
         for (; i < c1; ++i) {
             set_prio(nmine - i);
-            if (i > c0) issue(i, buf0, ok0);
+            next(i);
             compute_lo(i, buf0, ok0);
         }
         // next chunk (tables longer than 64 pages per wave): its IDs, then its
@@ -789,7 +871,7 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         c_last = c1 > c0 ? c1 - 1 : c0;
         if (c0 < nmine) {
             ids_v = load_ids();
-            issue(c0, buf0, ok0);
+            issue(c0, ok_next);
         }
     }
 
@@ -866,7 +948,8 @@ constexpr int kKeep = 8;     // tables per thread whose units stay in registers 
 constexpr int kRankPer = 16;  // tables per lane of the ranking wave
 
 template <int GQ>
-__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& sh, int T, int j, TableInfo* ti)
+__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& sh, CoefLds<GQ>* coef, int T, int j,
+                                             TableInfo* ti)
 {
     constexpr int kBins = 1024;
     const int per = (T + kWave - 1) / kWave;
@@ -874,9 +957,9 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
         *ti = table_info(a, j);
         return j;
     }
-    static_assert(sizeof(sh.coef) >= kBins * sizeof(int), "histogram lives in the weight LDS");
+    static_assert(sizeof(CoefLds<GQ>) >= kBins * sizeof(int), "histogram lives in the weight LDS");
     if (threadIdx.x < kWave) {
-        int* hist = reinterpret_cast<int*>(&sh.coef);  // free until the page loop
+        int* hist = reinterpret_cast<int*>(coef);  // free until the page loop
         const int lane = threadIdx.x;
         const int t0 = lane * per, t1 = t0 + per < T ? t0 + per : T;
         int shift = 0;
@@ -967,11 +1050,13 @@ template <int GQ>
 __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ)) void attn_decode(AttnArgs a)
 {
     __shared__ AttnShared<GQ> sh;
+    __shared__ CoefLds<GQ> coef;
+    __shared__ PageStage stage[kAttnWaves];
     const int T = a.B * a.Hkv;
     if (a.splits > 0) {
         const int j = blockIdx.x / a.splits, c = blockIdx.x - j * a.splits;
         TableInfo ti;
-        const int t = longest_first<GQ>(a, sh, T, j, &ti);
+        const int t = longest_first<GQ>(a, sh, &coef, T, j, &ti);
         const int n = ti.np < a.splits ? ti.np : a.splits;
         if (n == 0) {
             if (c == 0) write_empty(a, t, GQ);
@@ -980,7 +1065,7 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ)) void attn_dec
         if (c >= n) return;
         const int pa = (int)((long long)c * ti.np / n), pb = (int)((long long)(c + 1) * ti.np / n);
         float* part = n == 1 ? nullptr : a.part + ((long long)t * a.splits + c) * GQ * kPartStride;
-        run_segment<GQ>(a, sh, t, ti, pa, pb, part);
+        run_segment<GQ>(a, sh, &coef, stage, t, ti, pa, pb, part);
         return;
     }
     // ---- balanced shares -------------------------------------------------
@@ -1035,7 +1120,7 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ)) void attn_dec
             const bool first = ut >= b_lo;
             const bool whole = first && ut + ti.units <= b_hi;
             if (first && threadIdx.x == 0) a.ustart[t] = ut;
-            run_segment<GQ>(a, sh, t, ti, pa, pb, whole ? nullptr : a.part + (k + t) * GQ * kPartStride);
+            run_segment<GQ>(a, sh, &coef, stage, t, ti, pa, pb, whole ? nullptr : a.part + (k + t) * GQ * kPartStride);
         }
         ut += ti.units;
         ++t;

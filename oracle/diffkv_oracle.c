@@ -769,6 +769,14 @@ static void decode_table(const dko_layout* L, const dko_cache* C, int t,
             dko_read_token(L, C, t, sec, u, K + (int64_t)n * D, V + (int64_t)n * D, NULL, NULL);
 }
 
+static void decode_table_keys(const dko_layout* L, const dko_cache* C, int t, double* K)
+{
+    int D = L->head_dim, n = 0;
+    for (int sec = 0; sec < 2; sec++)
+        for (int u = 0; u < C->len[2 * t + sec]; u++, n++)
+            dko_read_token(L, C, t, sec, u, K + (int64_t)n * D, NULL, NULL, NULL);
+}
+
 int dko_attention(const dko_layout* L, const dko_cache* C, int num_q_heads,
                   const uint16_t* q, double sm_scale, double* out, double* lse)
 {
@@ -875,6 +883,74 @@ void dko_merge_partials(int S, int D, const double* m, const double* l,
     }
     for (int d = 0; d < D; d++) out[d] /= Ls;
     if (lse) *lse = M + log(Ls);
+}
+
+/* ======================================================================
+ * Significance scores (Sec. 4).  A token's significance is the average of
+ * the attention scores it receives from the queries at and after its
+ * position; with grouped heads the scores of the KV head's query heads are
+ * combined by their maximum, taken per query so that one running mean per
+ * token holds it.  One decode step adds the step's query: every kept token's
+ * probability under each of the g heads (softmax over the table's kept
+ * tokens, fp64), its maximum x over the heads, and the running mean over the
+ * N - p queries a token at position p has now received.
+ * ====================================================================== */
+static void token_score_ptr(const dko_layout* L, dko_cache* C, int t, int sec, int u, float** sp,
+                            int32_t* pos)
+{
+    int T = L->tokens_per_page[sec];
+    uint8_t* pg = (uint8_t*)page_ptr(L, C, t, sec, u);
+    *sp = (float*)(pg + L->off_score[sec] + (u % T) * 4);
+    memcpy(pos, pg + L->off_pos[sec] + (u % T) * 4, 4);
+}
+
+int dko_update_significance(const dko_layout* L, dko_cache* C, int num_q_heads,
+                            const uint16_t* q, double sm_scale)
+{
+    int B = C->num_seqs, H = C->num_kv_heads, D = L->head_dim;
+    if (H <= 0 || num_q_heads % H != 0) return 1;
+    int g = num_q_heads / H;
+    for (int b = 0; b < B; b++) {
+        int N = C->seq_len[b];
+        for (int h = 0; h < H; h++) {
+            int t = b * H + h;
+            int n = table_tokens(C, t);
+            if (n == 0) continue;
+            double* K = (double*)malloc(sizeof(double) * (size_t)n * D);
+            double* logit = (double*)malloc(sizeof(double) * (size_t)n);
+            double* x = (double*)malloc(sizeof(double) * (size_t)n);
+            decode_table_keys(L, C, t, K);
+            for (int j = 0; j < n; j++) x[j] = 0.0;
+            for (int hq = h * g; hq < (h + 1) * g; hq++) {
+                const uint16_t* qv = q + ((int64_t)b * num_q_heads + hq) * D;
+                double m = -INFINITY;
+                for (int j = 0; j < n; j++) {
+                    double dot = 0.0;
+                    for (int d = 0; d < D; d++) dot += (double)dko_half_to_float(qv[d]) * K[(int64_t)j * D + d];
+                    logit[j] = sm_scale * dot;
+                    if (logit[j] > m) m = logit[j];
+                }
+                double l = 0.0;
+                for (int j = 0; j < n; j++) l += exp(logit[j] - m);
+                for (int j = 0; j < n; j++) {
+                    double pj = exp(logit[j] - m) / l;
+                    if (pj > x[j]) x[j] = pj;
+                }
+            }
+            int j = 0;
+            for (int sec = 0; sec < 2; sec++) {
+                for (int u = 0; u < C->len[2 * t + sec]; u++, j++) {
+                    float* sp;
+                    int32_t pos;
+                    token_score_ptr(L, C, t, sec, u, &sp, &pos);
+                    double s = (double)*sp;
+                    *sp = (float)(s + (x[j] - s) / (double)(N - pos));
+                }
+            }
+            free(K); free(logit); free(x);
+        }
+    }
+    return 0;
 }
 
 /* ======================================================================

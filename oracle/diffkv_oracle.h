@@ -17,7 +17,10 @@
  *   - unified pages, circular free page list, bidirectional page table and
  *     the prefix-sum allocation/recycling schedule (Sec. 5.2, 5.3);
  *   - softmax attention, Eq. (1) of Sec. 2.1, evaluated in fp64 over the
- *     dequantized cache, and the split-sequence merge (Sec. 6.2).
+ *     dequantized cache, and the split-sequence merge (Sec. 6.2);
+ *   - the significance scores (Sec. 4): the running mean of the attention
+ *     probability each kept token receives, maximum over a KV head's query
+ *     heads, updated once per decode step.
  *
  * Every function is serial and state changes happen in the order the text
  * describes; there is no blocking, fusion or reordering.
@@ -150,6 +153,19 @@ void dko_merge_partials(int S, int D, const double* m, const double* l,
 /* ---- memory accounting against an FP16 cache (Sec. 1, Fig. 1) -------
  * Fraction of FP16 key bits and value bits used by a head holding n_hi
  * high-precision and n_lo low-precision tokens out of n_total.           */
+/* Significance update of one decode step (Sec. 4): after the step's query
+ * q (one per sequence and query head) has attended the compressed cache, every
+ * kept token of table t = b*H + h receives one more attention score.  Its
+ * score is the mean of the scores received so far, a score being the largest
+ * softmax probability of the token among the g query heads of KV head h
+ * (softmax over the table's kept tokens, logits sm_scale * q . k_hat, fp64).
+ * A token at position p of a sequence of N = seq_len[b] tokens has then
+ * received N - p scores (queries p .. N-1), so its stored fp32 score s
+ * becomes s + (x - s) / (N - p), evaluated in fp64 and rounded to fp32.
+ * Returns 1 when num_q_heads is not a multiple of H. */
+int dko_update_significance(const dko_layout* L, dko_cache* C, int num_q_heads,
+                            const uint16_t* q, double sm_scale);
+
 void dko_kv_bits_fraction(const dko_layout* L, int n_hi, int n_lo,
                           int n_total, double* k_frac, double* v_frac);
 

@@ -70,6 +70,8 @@ def _setup(L):
                                         C.c_int, C.c_int, C.c_int, C.c_int, vp, vp, vp]
     L.dko_merge_partials.argtypes = [C.c_int, C.c_int, vp, vp, vp, vp, vp]
     L.dko_kv_bits_fraction.argtypes = [C.POINTER(Layout), C.c_int, C.c_int, C.c_int, vp, vp]
+    L.dko_update_significance.argtypes = [C.POINTER(Layout), C.POINTER(_Cache), C.c_int, vp, f64]
+    L.dko_update_significance.restype = C.c_int
     L.dko_float_to_half.restype = C.c_uint16
     L.dko_float_to_half.argtypes = [f32]
     L.dko_half_to_float.restype = f32
@@ -221,6 +223,14 @@ def attention(cache, q, sm_scale):
     if rc != 0:
         raise ValueError("oracle: Hq must be a multiple of Hkv")
     return out, lse
+
+
+def update_significance(cache, q, sm_scale):
+    """One decode step's significance update of every kept token's score (in place)."""
+    q = np.ascontiguousarray(q, np.uint16)
+    st = cache.struct()
+    if lib().dko_update_significance(C.byref(cache.L), C.byref(st), q.shape[1], _p(q), float(sm_scale)):
+        raise ValueError("oracle: Hq must be a multiple of Hkv")
 
 
 def attention_partial(cache, q, sm_scale, b, hq, p0, p1):

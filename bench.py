@@ -28,6 +28,9 @@ Extra keys of the same JSON line:
                   decode (one append call for all layers), then attention per layer;
   compaction      2^20-page pool, 4096 tables, 100 rounds of Bernoulli(0.35) releases;
   generation_step the generation-phase policy (Algorithm 1) per decode step, llama8b;
+  memory_management  compaction + allocation per step at context 1024 for batches 8/32/128
+                  (32 layers x 8 KV heads per request) on the GPU and on a 16-thread host
+                  memory manager (baselines/cpu_manager.c), states checked identical;
   cpu_baseline    the CPU oracle's fp64 attention on a bounded sample of the headline
                   workload, one thread and all host cores (threads; the oracle's C code
                   releases the interpreter lock), plus its serial compaction.
@@ -531,6 +534,7 @@ def main():
         torch.cuda.empty_cache()
         extras["compaction"] = compaction_bench(torch, dk, lib, dev, sptr, args.compaction_rounds)
         extras["generation_step"] = generation_bench(torch, dk, lib, dev, sptr, args.generation_steps)
+        extras["memory_management"] = memory_management_bench(torch, dk, lib, dev, sptr)
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.config, args.cpu_seconds)
     if cpu is not None and "compaction" in extras:
         c = extras["compaction"]
@@ -640,6 +644,97 @@ def compaction_bench(torch, dk, lib, dev, sptr, rounds):
     }
     log("compaction: %.1f us/round, %.3g pages/s, refill %.1f us" %
         (res["us_per_round"], res["pages_per_s"], res["refill_us_per_round"]))
+    return res
+
+
+def memory_management_bench(torch, dk, lib, dev, sptr, batches=(8, 32, 128), steps=10, layers=32,
+                            threads=None):
+    """Memory management per inference step at context 1024 across batch sizes, on the
+    GPU and on a multi-threaded host manager (baselines/cpu_manager.c), the comparison
+    the paper draws between its on-GPU compaction and on-CPU memory management.  The
+    Llama-3-8B shape: 32 layers x 8 KV heads = 256 tables per request, pages from the
+    llama8b fractions at 1024 tokens.  Each step one request finishes (its tables in
+    every layer released, then refilled by its replacement's prompt pages) and a
+    sixteenth of the other tables take one page of decode growth: one compaction plus
+    one allocation call for all tables.  Both sides run the same steps from the same
+    state and must end bit-identical."""
+    from baselines import cpu_manager as cm
+    from paper_2412_03131_amd import inputs
+    threads = threads or max(1, min(16, cpu_info()[2]))
+    res = {"workload": "context 1024, %d layers x 8 KV heads per request, llama8b fractions; per "
+                       "step one request recycled and refilled, 1/16 of the other tables grow a "
+                       "page; compaction + allocation for all tables" % layers,
+           "cpu_threads": threads, "batches": {}}
+    for B in batches:
+        rng = np.random.default_rng(5 + B)
+        H = 8 * layers
+        T = B * H
+        f_hi = rng.uniform(0.1, 0.5, T)
+        f_pr = rng.uniform(0.2, 0.6, T)
+        f_pr = np.where(f_hi + f_pr > 1.0, 1.0 - f_hi, f_pr)
+        nh = np.floor(f_hi * 1024).astype(np.int64)
+        nlo = 1024 - nh - np.floor(f_pr * 1024).astype(np.int64)
+        demand0 = np.stack([-(-nh // 16), -(-nlo // 32)], axis=1).astype(np.int32)
+        L = dk.layout(max_seq_len=1024 + 16 * (steps + 2))
+        num_pages = int(demand0.sum() * 1.25) + 4096
+        ring = np.random.default_rng(B).permutation(num_pages).astype(np.int32)
+        c = dk.Cache(L, num_pages, B, H, device=dev, ring=torch.from_numpy(ring), with_pool=False)
+        dk.alloc_pages(c, torch.from_numpy(demand0).to(dev))
+        lens0 = np.stack([nh, nlo], axis=1).astype(np.int32)
+        c.len.copy_(torch.from_numpy(lens0).to(dev))
+        torch.cuda.synchronize()
+        m = cm.Manager(c.page_table.cpu().numpy(), c.pages.cpu().numpy(), lens0, ring,
+                       c.ring_ptr.cpu().numpy(), (16, 32), threads)
+        rel_np, dem_np = [], []
+        for s in range(steps):
+            r = s % B
+            rel = np.zeros((T, L.p_max), np.uint8)
+            rel[r * H:(r + 1) * H] = 1
+            dem = np.zeros((T, 2), np.int32)
+            dem[(np.arange(T) + s) % 16 == 0, 0] = 1
+            dem[r * H:(r + 1) * H] = demand0[r * H:(r + 1) * H]
+            rel_np.append(rel)
+            dem_np.append(dem)
+        rel_d = [torch.from_numpy(x).to(dev) for x in rel_np]
+        dem_d = [torch.from_numpy(x).to(dev) for x in dem_np]
+        ws_c = torch.empty(dk.workspace_size(dk.OP_COMPACT, L, B, 0, H), dtype=torch.uint8, device=dev)
+        ws_a = torch.empty(dk.workspace_size(dk.OP_ALLOC, L, B, 0, H), dtype=torch.uint8, device=dev)
+        cs = c.struct()
+        Lp = C.byref(L)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(2.4e9 * 1e-4 * steps) + 1)   # the host enqueues ahead of the GPU
+        rc = 0
+        for s in range(steps):
+            ev[s][0].record()
+            rc |= lib.diffkv_compact_free_list(Lp, C.byref(cs), T, C.c_void_p(rel_d[s].data_ptr()),
+                                               C.c_void_p(ws_c.data_ptr()), ws_c.numel(), sptr)
+            rc |= lib.diffkv_alloc_pages(Lp, C.byref(cs), T, C.c_void_p(dem_d[s].data_ptr()),
+                                         C.c_void_p(ws_a.data_ptr()), ws_a.numel(), sptr)
+            ev[s][1].record()
+        torch.cuda.synchronize()
+        if rc or int(c.status.item()) != 0:
+            raise RuntimeError("memory management bench: GPU call failed")
+        gpu_us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+        cpu_us = []
+        for s in range(steps):
+            t0 = time.perf_counter()
+            m.compact(rel_np[s])
+            if m.alloc(dem_np[s]):
+                raise RuntimeError("memory management bench: host manager refused")
+            cpu_us.append((time.perf_counter() - t0) * 1e6)
+        m.close()
+        same = (np.array_equal(c.page_table.cpu().numpy(), m.table) and np.array_equal(c.ring.cpu().numpy(), m.ring)
+                and np.array_equal(c.ring_ptr.cpu().numpy(), m.ring_ptr) and np.array_equal(c.len.cpu().numpy(), m.len))
+        if not same:
+            raise RuntimeError("memory management bench: GPU and host manager states differ")
+        cpu_us = np.array(cpu_us)
+        res["batches"][str(B)] = {"tables": T, "live_pages": int(demand0.sum()),
+                                  "gpu_us": pct(gpu_us), "cpu_manager_us": pct(cpu_us),
+                                  "cpu_over_gpu": float(np.median(cpu_us) / np.median(gpu_us))}
+        log("memory management B=%d (%d tables): GPU %.1f us, host manager (%d threads) %.1f us per step"
+            % (B, T, np.median(gpu_us), threads, np.median(cpu_us)))
+        del c, rel_d, dem_d
     return res
 
 

@@ -19,6 +19,8 @@ outside the HIP events) and gives the per-launch attention and append times (med
 mean) and the roofline: algorithmic compressed bytes / mean attention time.
 
 Extra keys of the same JSON line:
+  significance    the decode step's significance update (running mean of each kept
+                  token's attention probability, Sec. 4) on the headline cache;
   llama70b        batch 32, 64 query / 8 KV heads (GQA 8:1), context 8192, split 30/40/30:
                   attention with num_splits = 1 (no split), automatic, and balanced
                   shares + merge (sequence split), each timed after a cache flush;
@@ -329,6 +331,61 @@ def attention_modes(torch, dk, lib, dev, sptr, wl, reps, flush, modes=(1, 0, -1)
     return res
 
 
+def significance_bench(torch, dk, lib, dev, sptr, wl, flush, reps=30):
+    """diffkv_update_significance on the headline cache, right after each attention
+    call with the same q (as a decode step runs it), caches evicted before the
+    attention.  Algorithmic bytes: key codes and metadata (144 B per high token, 80 B
+    per low token), the score read and written and the position read (12 B), the
+    used table entries, q and lse."""
+    B, Hq, Hkv = wl["w"]["B"], wl["w"]["Hq"], wl["w"]["Hkv"]
+    L, cache = wl["L"], wl["cache"]
+    lens = cache.len.cpu().numpy().astype(np.int64)
+    hi, lo = lens[:, 0], lens[:, 1]
+    nbytes = (156 * int(hi.sum()) + 92 * int(lo.sum()) + 4 * int((-(-hi // 16)).sum() + (-(-lo // 32)).sum())
+              + B * Hq * (2 * 128 + 4))
+    abytes = attn_bytes(hi, lo, B, Hq, Hkv)
+    q = wl["steps"][0]["q"]
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, L, B, Hq, Hkv, 0, 0)), dtype=torch.uint8, device=dev)
+    cs = cache.struct()
+    att = (C.byref(L), C.byref(cs), Hq, C.c_void_p(q.data_ptr()), float(SCALE), C.c_void_p(out.data_ptr()),
+           C.c_void_p(lse.data_ptr()), 0, C.c_void_p(ws.data_ptr()), ws.numel(), sptr)
+    upd = (C.byref(L), C.byref(cs), Hq, C.c_void_p(q.data_ptr()), float(SCALE), C.c_void_p(lse.data_ptr()), sptr)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+    rc = 0
+    for _ in range(3):
+        rc |= lib.diffkv_decode_attention(*att)
+        rc |= lib.diffkv_update_significance(*upd)
+    for e in ev:
+        flush()
+        e[0].record()
+        rc |= lib.diffkv_decode_attention(*att)
+        e[1].record()
+        rc |= lib.diffkv_update_significance(*upd)
+        e[2].record()
+    for e in ev2:   # the update alone, caches evicted before it
+        flush()
+        e[0].record()
+        rc |= lib.diffkv_update_significance(*upd)
+        e[1].record()
+    torch.cuda.synchronize()
+    if rc:
+        raise RuntimeError("significance bench: call failed")
+    a_us = np.array([x[0].elapsed_time(x[1]) * 1e3 for x in ev])
+    u_us = np.array([x[1].elapsed_time(x[2]) * 1e3 for x in ev])
+    c_us = np.array([x[0].elapsed_time(x[1]) * 1e3 for x in ev2])
+    res = {"workload": "the headline cache after its timed steps; per rep: cache eviction, attention, "
+                       "then the significance update with the attention's lse",
+           "us": pct(u_us), "attention_us": pct(a_us), "us_alone_flushed": pct(c_us),
+           "bytes_per_launch": nbytes, "gbps": nbytes / (u_us.mean() * 1e-6) / 1e9,
+           "bytes_vs_attention": nbytes / abytes, "time_vs_attention": float(u_us.mean() / a_us.mean())}
+    log("significance update: %.1f us after a %.1f us attention call, %.1f us alone after eviction "
+        "(%.2f of the attention's bytes)" % (u_us.mean(), a_us.mean(), c_us.mean(), nbytes / abytes))
+    return res
+
+
 def serving_step(torch, dk, lib, dev, sptr, args):
     """The llama8b shape on `layers` layers sharing one page pool, one step = request
     r = step mod 64 finishes (its pages in every layer recycled by one compaction call),
@@ -518,6 +575,7 @@ def main():
     head = decode_headline(torch, dk, lib, dev, sptr, wl, args, flush)
     extras = {}
     if args.extras == "all":
+        extras["significance"] = significance_bench(torch, dk, lib, dev, sptr, wl, flush)
         if args.config != "llama70b":
             del wl
             torch.cuda.empty_cache()

@@ -256,6 +256,27 @@ diffkv_status diffkv_decode_attention_noalloc(const diffkv_layout* layout, const
                                               float* out, float* lse, int32_t num_splits, void* stream);
 
 /*
+ * Significance update of one decode step (Sec. 4: a token's significance is
+ * the average of the attention scores it receives; with grouped heads the
+ * scores of a KV head's query heads are combined by their maximum).  Call it
+ * after diffkv_decode_attention with the same q, passing that call's lse.
+ * For every kept token j of table t = b*Hkv + h at position pos_j:
+ *   x_j = max over the query heads hq of KV head h of exp(logit_hq,j - lse_hq),
+ *         logit = sm_scale * q[b][hq] . k_hat_j (the probability of token j
+ *         in the softmax over the table's kept tokens),
+ *   score_j <- score_j + (x_j - score_j) / (N - pos_j),  N = seq_len[b],
+ * i.e. the mean over the N - pos_j queries (positions pos_j .. N-1) the token
+ * has received, the newest being this step's.  Scores are rewritten in place
+ * in the pages' score segments; nothing else changes.  fp32 arithmetic.
+ *   q    device fp16 [num_seqs][num_q_heads][head_dim] (as given to attention)
+ *   lse  device fp32 [num_seqs][num_q_heads] (natural log, as attention wrote it)
+ * No workspace.  Same layout and group-size support as diffkv_decode_attention.
+ */
+diffkv_status diffkv_update_significance(const diffkv_layout* layout, const diffkv_cache* cache,
+                                         int32_t num_q_heads, const uint16_t* q, float sm_scale,
+                                         const float* lse, void* stream);
+
+/*
  * Parallel free-list compaction (Sec. 5.2 recycling, Sec. 5.3): for the
  * first num_tables tables, every live slot whose release byte is nonzero
  * gives its page back.  With one prefix sum over tables, table t writes its

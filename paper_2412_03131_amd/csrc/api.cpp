@@ -334,6 +334,38 @@ diffkv_status diffkv_decode_attention_noalloc(const diffkv_layout* layout, const
                           true, stream);
 }
 
+diffkv_status diffkv_update_significance(const diffkv_layout* layout, const diffkv_cache* cache,
+                                        int32_t num_q_heads, const uint16_t* q, float sm_scale,
+                                        const float* lse, void* stream)
+{
+    if (!layout_valid(layout) || !cache_valid(cache) || !cache->pool || !cache->seq_len) return DIFFKV_E_INVAL;
+    if (num_q_heads <= 0 || num_q_heads % cache->num_kv_heads != 0) return DIFFKV_E_INVAL;
+    if (!layout_kernels_supported(layout)) return DIFFKV_E_UNSUPPORTED;
+    if (num_q_heads / cache->num_kv_heads > 8) return DIFFKV_E_UNSUPPORTED;
+    if (cache->num_seqs == 0) return DIFFKV_OK;
+    if (!q || !lse) return DIFFKV_E_INVAL;
+    SigArgs a;
+    memset(&a, 0, sizeof(a));
+    a.p_max = layout->p_max;
+    a.num_pages = cache->num_pages;
+    for (int p = 0; p < 2; ++p) {
+        a.off_score[p] = layout->off_score[p];
+        a.off_pos[p] = layout->off_pos[p];
+    }
+    a.pool = cache->pool;
+    a.page_table = cache->page_table;
+    a.len = cache->len;
+    a.seq_len = cache->seq_len;
+    a.B = cache->num_seqs;
+    a.Hkv = cache->num_kv_heads;
+    a.Hq = num_q_heads;
+    a.q = q;
+    a.scale_log2 = sm_scale * 1.4426950408889634f;
+    a.lse = lse;
+    hipError_t e = launch_significance(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
+}
+
 diffkv_status diffkv_compact_free_list(const diffkv_layout* layout, const diffkv_cache* cache,
                                        int32_t num_tables, const uint8_t* release, void* ws,
                                        size_t ws_bytes, void* stream)

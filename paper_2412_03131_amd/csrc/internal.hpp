@@ -142,6 +142,25 @@ hipError_t launch_alloc(const AllocArgs& a, hipStream_t st);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t st);
 hipError_t launch_generation(const GenArgs& g, hipStream_t st);
 hipError_t launch_attention(AttnArgs a, hipStream_t st);
+
+// Significance update of one decode step: every kept token's score in its page
+// becomes the running mean of the softmax probabilities it has received (max
+// over the KV head's query heads), from the logits of q and the lse that the
+// attention call with the same q wrote.
+struct SigArgs {
+    int p_max;
+    long long num_pages;
+    int off_score[2], off_pos[2];
+    uint8_t* pool;
+    const int32_t* page_table;
+    const int32_t* len;
+    const int32_t* seq_len;
+    int B, Hkv, Hq;
+    const uint16_t* q;
+    float scale_log2;
+    const float* lse;   // [B][Hq] natural log, from the attention call
+};
+hipError_t launch_significance(const SigArgs& a, hipStream_t st);
 // The mode an attention call with `splits` runs in on the current device:
 // S >= 1 page ranges per table (S = 1: no split) or -1 (balanced shares);
 // *workers = the balanced mode's share count.

@@ -1231,6 +1231,138 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge(AttnArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// attn_significance: the significance update of one decode step (Sec. 4).  The
+// tokens are independent once the lse is known, so a table's pages are cut into
+// runs of kSigPages, one workgroup per (table, run); each of its four waves takes
+// every fourth page of the run (workgroups past a table's last page exit).  A page's
+// key codes, key metadata, scores and positions are loaded; the logits of the
+// table's query heads come out of the key phase of do_page (lane = (group, token),
+// a transposed row sum), p = exp2(logit - lse) with the attention call's lse, the
+// maximum over the heads is taken across the slots and the four rows, and the
+// lane of row 0 owning token j rewrites its score as s + (p_max - s) / (N - pos).
+// ---------------------------------------------------------------------------
+constexpr int kSigWaves = 4;
+constexpr int kSigPages = 16;  // pages per workgroup
+
+template <int GQ, int NT>
+__device__ __forceinline__ void sig_page(const SigArgs& a, uint8_t* pg, const uint32_t (&qr)[GQ],
+                                         const half2_t (&q0)[GQ], const float (&qsum)[GQ],
+                                         const float (&lse2)[(GQ + 3) / 4], int n_valid, int N, int lane)
+{
+    constexpr int NS = (GQ + 3) / 4;
+    constexpr int sec = NT == 1 ? 0 : 1;
+    const uint32_t grp = (uint32_t)lane >> 4, jl = (uint32_t)lane & 15;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)pg, 0, (int)kPageBytes, 0x00020000);
+    const uint32_t kc = grp * 512 + jl * 16;
+    const uint32_t km = 2048 + jl * 16 + grp * 4;
+    const uint32_t os = (uint32_t)a.off_score[sec], op = (uint32_t)a.off_pos[sec];
+    const uint4 k0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, kc, 0, 0));
+    const uint4 k1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, kc + 256, 0, 0));
+    const uint32_t m0 = __builtin_amdgcn_raw_buffer_load_b32(rs, km, 0, 0);
+    const uint32_t m1 = __builtin_amdgcn_raw_buffer_load_b32(rs, km + 256, 0, 0);
+    float sc[NT];
+    int ps[NT];
+#pragma unroll
+    for (int tk = 0; tk < NT; ++tk) {
+        sc[tk] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, os + 4 * (jl + 16 * tk), 0, 0));
+        ps[tk] = (int)__builtin_amdgcn_raw_buffer_load_b32(rs, op + 4 * (jl + 16 * tk), 0, 0);
+    }
+#pragma unroll
+    for (int tk = 0; tk < NT; ++tk) {
+        const uint32_t kmt = tk ? m1 : m0;
+        const float ks = h2f(kmt & 0xffffu) * (kTwo24 * a.scale_log2), kz = h2f(kmt >> 16) * a.scale_log2;
+        float dlo[GQ], dhi[GQ];
+        if constexpr (NT == 1) {
+            const uint32_t w[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+            kdots_k8<GQ>(w, qr, q0, dlo);
+        } else {
+            const uint4 kk = tk ? k1 : k0;
+            const uint32_t w[4] = {kk.x, kk.y, kk.z, kk.w};
+            kdots_k4<GQ>(w, qr, q0, dlo, dhi);
+        }
+        float part[4 * NS];
+#pragma unroll
+        for (int hh = 0; hh < 4 * NS; ++hh) {
+            if (hh < GQ) {
+                const float d = NT == 1 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
+                part[hh] = fmaf(ks, d, kz * qsum[hh]);
+            } else {
+                part[hh] = 0.f;
+            }
+        }
+        // row r of slot s holds head 4s + r; its probability, then the maximum
+        // over the slots and the four rows
+        float x = 0.f;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const float lg = xsum4(part[4 * s], part[4 * s + 1], part[4 * s + 2], part[4 * s + 3]);
+            const float pr = 4 * s + (int)grp < GQ ? __builtin_amdgcn_exp2f(lg - lse2[s]) : 0.f;
+            x = fmax_sel(x, pr);
+        }
+        // each swap returns the two halves (rows 0-1 | 2-3, then rows 0, 2 | 1, 3)
+        // side by side, so their maximum is the maximum over the pair in every lane
+        auto sw32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = fmax_sel(__uint_as_float(sw32[0]), __uint_as_float(sw32[1]));
+        auto sw16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = fmax_sel(__uint_as_float(sw16[0]), __uint_as_float(sw16[1]));
+        const int j = (int)jl + 16 * tk;
+        if (grp == 0 && j < n_valid) {
+            const float s0 = sc[tk];
+            reinterpret_cast<float*>(pg + os)[j] = s0 + (x - s0) / (float)(N - ps[tk]);
+        }
+    }
+}
+
+template <int GQ>
+__global__ __launch_bounds__(kSigWaves * kWave) void attn_significance(SigArgs a)
+{
+    constexpr int NS = (GQ + 3) / 4;
+    const int runs = (a.p_max + kSigPages - 1) / kSigPages;
+    const int t = blockIdx.x / runs, run = blockIdx.x - t * runs;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int grp = lane >> 4;
+    const int b = t / a.Hkv, h = t - b * a.Hkv;
+    const int P = a.p_max;
+    const auto* lenp = (const __attribute__((address_space(4))) int32_t*)(a.len + 2 * (long long)t);
+    const int len_hi = lenp[0], len_lo = lenp[1];
+    const int N = a.seq_len[b];
+    const int ph = (len_hi + kTHi - 1) / kTHi, np = ph + (len_lo + kTLo - 1) / kTLo;
+    const int p_end = np < (run + 1) * kSigPages ? np : (run + 1) * kSigPages;
+    if (run * kSigPages >= np) return;
+    // q pairs as in run_segment: lane k of a row holds its group's pair k
+    // (dims d, d+4), pair 0 whole in every lane, the group's sum
+    const int qm = (lane & 15) >> 2, qa = lane & 3;
+    uint32_t qr[GQ];
+    half2_t q0[GQ];
+    float qsum[GQ];
+    constexpr uint32_t kOnes = 0x3C003C00u;
+    const uint32_t sel = (qa & 1) ? 0x07060302u : 0x05040100u;
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh) {
+        const uint32_t* qd = reinterpret_cast<const uint32_t*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
+        const int o = 4 * qm + ((qa & 2) ? 1 : 0);
+        qr[hh] = __builtin_amdgcn_perm(qd[o + 2], qd[o], sel);
+        q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(qd[2], qd[0], 0x05040100u));
+        qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f));
+    }
+    float lse2[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const int hs = 4 * s + grp;
+        lse2[s] = hs < GQ ? a.lse[(long long)b * a.Hq + h * GQ + hs] * 1.4426950408889634f : 0.f;
+    }
+    const int32_t* trow = a.page_table + (long long)t * P;
+    for (int p = run * kSigPages + wave; p < p_end; p += kSigWaves) {
+        const int id = __builtin_amdgcn_readfirstlane(p < ph ? trow[p] : trow[P - 1 - (p - ph)]);
+        if ((unsigned long long)(unsigned)id >= (unsigned long long)a.num_pages) continue;  // never outside the pool
+        uint8_t* pg = a.pool + (long long)id * kPageBytes;
+        if (p < ph) sig_page<GQ, 1>(a, pg, qr, q0, qsum, lse2, len_hi - p * kTHi, N, lane);
+        else sig_page<GQ, 2>(a, pg, qr, q0, qsum, lse2, len_lo - (p - ph) * kTLo, N, lane);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
 template <int GQ>
@@ -1340,6 +1472,35 @@ hipError_t launch_attention(AttnArgs a, hipStream_t st)
     const long long jobs = T * gq;
     const long long mgrid = (jobs + kMergeThreads / kWave - 1) / (kMergeThreads / kWave);
     return launch1(attn_merge, (unsigned)mgrid, kMergeThreads, st, a);
+}
+
+
+template <int GQ>
+static const void* significance_kernel()
+{
+    return reinterpret_cast<const void*>(&attn_significance<GQ>);
+}
+
+hipError_t launch_significance(const SigArgs& a, hipStream_t st)
+{
+    const int gq = a.Hq / a.Hkv;
+    const void* kern = nullptr;
+    switch (gq) {
+    case 1: kern = significance_kernel<1>(); break;
+    case 2: kern = significance_kernel<2>(); break;
+    case 3: kern = significance_kernel<3>(); break;
+    case 4: kern = significance_kernel<4>(); break;
+    case 5: kern = significance_kernel<5>(); break;
+    case 6: kern = significance_kernel<6>(); break;
+    case 7: kern = significance_kernel<7>(); break;
+    case 8: kern = significance_kernel<8>(); break;
+    default: return hipErrorInvalidValue;
+    }
+    const long long T = (long long)a.B * a.Hkv;
+    const long long grid = T * ((a.p_max + kSigPages - 1) / kSigPages);
+    if (T < 1 || grid > INT32_MAX) return hipErrorInvalidValue;
+    void* args[] = {const_cast<SigArgs*>(&a)};
+    return hipLaunchKernel(kern, dim3((unsigned)grid), dim3(kSigWaves * kWave), args, 0, st);
 }
 
 }  // namespace dkv

@@ -50,8 +50,9 @@ class CacheStruct(C.Structure):
 
 
 EXPORTS = ("diffkv_layout_init", "diffkv_workspace_size", "diffkv_quantize_append",
-           "diffkv_decode_attention", "diffkv_decode_attention_noalloc", "diffkv_compact_free_list",
-           "diffkv_alloc_pages", "diffkv_generation_step", "diffkv_status_str")
+           "diffkv_decode_attention", "diffkv_decode_attention_noalloc", "diffkv_update_significance",
+           "diffkv_compact_free_list", "diffkv_alloc_pages", "diffkv_generation_step",
+           "diffkv_status_str")
 
 
 def lib():
@@ -70,6 +71,7 @@ def lib():
                                              vp, sz, vp]
         L.diffkv_decode_attention.argtypes = [PL, PC, i32, vp, f32, vp, vp, i32, vp, sz, vp]
         L.diffkv_decode_attention_noalloc.argtypes = [PL, PC, i32, vp, f32, vp, vp, i32, vp]
+        L.diffkv_update_significance.argtypes = [PL, PC, i32, vp, f32, vp, vp]
         L.diffkv_compact_free_list.argtypes = [PL, PC, i32, vp, vp, sz, vp]
         L.diffkv_alloc_pages.argtypes = [PL, PC, i32, vp, vp, sz, vp]
         L.diffkv_generation_step.argtypes = [PL, PC, f32, f32, i32, vp, sz, vp]
@@ -228,6 +230,16 @@ def decode_attention_noalloc(cache, q, sm_scale, out, lse=None, num_splits=0, st
         C.byref(cache.L), C.byref(st), q.shape[1], _ptr(_bits16(q)), float(sm_scale), _ptr(out),
         _ptr(lse), int(num_splits), _stream(stream)), "diffkv_decode_attention_noalloc")
     return out, lse
+
+
+def update_significance(cache, q, sm_scale, lse, stream=None):
+    """diffkv_update_significance: every kept token's score becomes the running mean of
+    its attention probability (max over the KV head's query heads); lse from
+    decode_attention with the same q."""
+    st = cache.struct()
+    _check(lib().diffkv_update_significance(C.byref(cache.L), C.byref(st), q.shape[1], _ptr(_bits16(q)),
+                                            float(sm_scale), _ptr(lse), _stream(stream)),
+           "diffkv_update_significance")
 
 
 def compact_free_list(cache, release, num_tables=None, ws=None, stream=None):

@@ -52,7 +52,8 @@ sys.path.insert(0, ROOT)
 METRIC = "decode-attention KV tokens/s + achieved HBM GB/s (% of peak); compaction pages/s"
 HBM_PEAK_GBPS = 8000.0
 SCALE = 1.0 / np.sqrt(128.0)
-ATTN_SOURCES = ["k_attention.hip", "internal.hpp", "common.hpp"]
+ATTN_SOURCES = ["k_attention.hip", "attn_kernels.hpp", "attn_common.hpp", "k_attn_l0.hip", "internal.hpp",
+                "common.hpp"]
 FLUSH_BYTES = 1 << 30   # > the 256 MB Infinity Cache + 8 x 4 MB L2
 DTYPE_DETAIL = ("q.k: fp16 q x integer codes (exact products), fp32 sums, fp32 scale/zero; "
                 "p.v: softmax weight x fp16 scale rounded to fp16 x integer codes, fp32 sums; "

@@ -124,11 +124,16 @@ typedef struct diffkv_cache {
 /* Fill *out (host) from the parameters: segment offsets, page_bytes, p_max.
  * Bits must be 1, 2, 4 or 8, head_dim*k_bits a multiple of 128,
  * T*v_bits a multiple of 8, tokens_per_page[LOW] >= tokens_per_page[HIGH].
- * DIFFKV_E_INVAL otherwise.  Any valid layout is accepted here; the
- * append, generation-step and attention kernels implement head_dim 128,
- * group 32, K8V4/K4V2
- * and 16/32 tokens per page (DIFFKV_E_UNSUPPORTED otherwise); allocation
- * and compaction accept any valid layout. */
+ * DIFFKV_E_INVAL otherwise.  Any valid layout is accepted here.  The append,
+ * attention and significance kernels implement head_dim 128, group 32 and
+ * these (high | low) section formats (precision levels of Sec. 4 and
+ * Sec. 7.2), DIFFKV_E_UNSUPPORTED otherwise:
+ *   K8V4, 16 tokens | K4V2, 32 tokens   (the paper's two levels)
+ *   K8V8, 16 tokens | K4V2, 32 tokens
+ *   K8V2, 16 tokens | K4V1, 32 tokens
+ *   K8V4, 16 tokens | K4V2, 16 tokens
+ * The generation step implements the first only.  Allocation and compaction
+ * accept any valid layout. */
 diffkv_status diffkv_layout_init(diffkv_layout* out, int32_t head_dim, int32_t group,
                                  const int32_t k_bits[2], const int32_t v_bits[2],
                                  const int32_t tokens_per_page[2], int32_t max_seq_len);

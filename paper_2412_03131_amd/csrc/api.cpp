@@ -68,12 +68,26 @@ bool layout_valid(const diffkv_layout* L)
     return memcmp(&r, L, sizeof(r)) == 0;
 }
 
-bool layout_kernels_supported(const diffkv_layout* L)
+// Index of the caller's layout among the ones the kernels implement
+// (kLayoutFmts: head_dim 128, group 32, the section formats and the segment
+// offsets diffkv_layout_init gives them), or -1.
+int layout_index(const diffkv_layout* L)
 {
-    return L->head_dim == kD && L->group == kG && L->k_bits[0] == 8 && L->k_bits[1] == 4 &&
-           L->v_bits[0] == 4 && L->v_bits[1] == 2 && L->tokens_per_page[0] == kTHi &&
-           L->tokens_per_page[1] == kTLo && attention_layout_matches(L);
+    if (L->head_dim != kD || L->group != kG) return -1;
+    for (int li = 0; li < kNumLayouts; ++li) {
+        const KvFmt f[2] = {kLayoutFmts[li].hi, kLayoutFmts[li].lo};
+        bool ok = L->page_bytes == layout_page_bytes(li);
+        for (int p = 0; p < 2; ++p) {
+            const SecOffsets o = sec_offsets(f[p]);
+            ok = ok && L->k_bits[p] == f[p].kb && L->v_bits[p] == f[p].vb && L->tokens_per_page[p] == f[p].T &&
+                 L->off_kcode[p] == o.kc && L->off_kmeta[p] == o.km && L->off_vcode[p] == o.vc &&
+                 L->off_vmeta[p] == o.vm && L->off_score[p] == o.sc && L->off_pos[p] == o.pos;
+        }
+        if (ok) return li;
+    }
+    return -1;
 }
+bool layout_kernels_supported(const diffkv_layout* L) { return layout_index(L) >= 0; }
 
 bool cache_valid(const diffkv_cache* c)
 {
@@ -86,8 +100,14 @@ void fill_layout_args(LayoutArgs& a, const diffkv_layout* L)
 {
     a.p_max = L->p_max;
     a.page_bytes = L->page_bytes;
+    a.tsh = 0;
     for (int p = 0; p < 2; ++p) {
         a.T[p] = L->tokens_per_page[p];
+        a.kb[p] = L->k_bits[p];
+        a.vb[p] = L->v_bits[p];
+        int sh = 0;
+        while ((1 << sh) < a.T[p]) ++sh;
+        a.tsh |= sh << (8 * p);
         a.off_kcode[p] = L->off_kcode[p];
         a.off_kmeta[p] = L->off_kmeta[p];
         a.off_vcode[p] = L->off_vcode[p];
@@ -171,7 +191,8 @@ diffkv_status attention_call(const diffkv_layout* layout, const diffkv_cache* ca
     if (noalloc) {
         const int64_t T = (int64_t)cache->num_seqs * cache->num_kv_heads;
         int mode = 0, workers = 0;
-        if (attention_mode(num_q_heads / cache->num_kv_heads, T, num_splits, &mode, &workers) != hipSuccess)
+        if (attention_mode(num_q_heads / cache->num_kv_heads, layout_index(layout), T, num_splits, &mode, &workers) !=
+            hipSuccess)
             return DIFFKV_E_LAUNCH;
         // the balanced mode writes partial slots share + table < workers + T
         w = attn_ws(cache->num_seqs, num_q_heads, cache->num_kv_heads, mode, workers);
@@ -208,6 +229,7 @@ diffkv_status attention_call(const diffkv_layout* layout, const diffkv_cache* ca
     a.ustart = reinterpret_cast<long long*>(base + w.ustart);
     a.utot = reinterpret_cast<long long*>(base + w.utot);
     a.part = reinterpret_cast<float*>(base + w.part);
+    a.layout = layout_index(layout);
     hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
 }
@@ -362,6 +384,7 @@ diffkv_status diffkv_update_significance(const diffkv_layout* layout, const diff
     a.q = q;
     a.scale_log2 = sm_scale * 1.4426950408889634f;
     a.lse = lse;
+    a.layout = layout_index(layout);
     hipError_t e = launch_significance(a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
 }
@@ -435,7 +458,7 @@ diffkv_status diffkv_generation_step(const diffkv_layout* layout, const diffkv_c
     if (!layout_valid(layout) || !cache_valid(cache) || !cache->pool || !cache->seq_len)
         return DIFFKV_E_INVAL;
     if (recent_window < 0) return DIFFKV_E_INVAL;
-    if (!layout_kernels_supported(layout)) return DIFFKV_E_UNSUPPORTED;
+    if (layout_index(layout) != 0) return DIFFKV_E_UNSUPPORTED;  // K8V4 / K4V2, 16 / 32 tokens
     const int64_t T = (int64_t)cache->num_seqs * cache->num_kv_heads;
     if (T == 0) return DIFFKV_OK;
     if (!ws || (int64_t)ws_bytes < gen_ws(T)) return DIFFKV_E_WORKSPACE;

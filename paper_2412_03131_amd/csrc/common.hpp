@@ -13,9 +13,51 @@ namespace dkv {
 constexpr int kD = 128;        // head_dim
 constexpr int kG = 32;         // quantization group
 constexpr int kNG = kD / kG;   // groups per vector
-constexpr int kTHi = 16;       // tokens per high-precision page (K8V4)
-constexpr int kTLo = 32;       // tokens per low-precision page (K4V2)
+constexpr int kTHi = 16;       // tokens per high-precision page of layout 0 (K8V4)
+constexpr int kTLo = 32;       // tokens per low-precision page of layout 0 (K4V2)
 constexpr int kWave = 64;
+
+// ---- page formats the kernels implement -------------------------------------
+// A section's format: key bits, value bits, tokens per page.  The layouts (high
+// section format, low section format) the append, attention and significance
+// kernels implement, head_dim 128 and group 32 throughout:
+//   0  K8V4 / K4V2, 16 / 32 tokens  (the paper's two levels, Sec. 4)
+//   1  K8V8 / K4V2, 16 / 32         (K8V8 for the important tokens)
+//   2  K8V2 / K4V1, 16 / 32         (the skewed variants of Sec. 7.2)
+//   3  K8V4 / K4V2, 16 / 16         (as 0 with 16 tokens per low page)
+// The generation-phase policy implements layout 0 only.
+struct KvFmt {
+    int kb, vb, T;
+};
+struct LayoutFmt {
+    KvFmt hi, lo;
+};
+constexpr int kNumLayouts = 4;
+constexpr LayoutFmt kLayoutFmts[kNumLayouts] = {
+    {{8, 4, 16}, {4, 2, 32}}, {{8, 8, 16}, {4, 2, 32}}, {{8, 2, 16}, {4, 1, 32}}, {{8, 4, 16}, {4, 2, 16}}};
+
+// Segment offsets of one section's page, as diffkv_layout_init lays them out:
+// K codes, K meta, V codes, V meta, scores, positions, each 64-byte aligned.
+struct SecOffsets {
+    int kc, km, vc, vm, sc, pos, used;
+};
+constexpr int align64c(int x) { return (x + 63) & ~63; }
+constexpr SecOffsets sec_offsets(KvFmt f)
+{
+    const int km = align64c((kD * f.kb / 128) * f.T * 16);
+    const int vc = align64c(km + f.T * kNG * 4);
+    const int vm = align64c(vc + kD * (f.T * f.vb / 8));
+    const int sc = align64c(vm + kNG * f.T * 4);
+    const int pos = align64c(sc + f.T * 4);
+    return {0, km, vc, vm, sc, pos, align64c(pos + f.T * 4)};
+}
+constexpr int layout_page_bytes(int li)
+{
+    return sec_offsets(kLayoutFmts[li].hi).used > sec_offsets(kLayoutFmts[li].lo).used
+               ? sec_offsets(kLayoutFmts[li].hi).used
+               : sec_offsets(kLayoutFmts[li].lo).used;
+}
+static_assert(layout_page_bytes(0) == 4352 && sec_offsets(kLayoutFmts[0].lo).vc == 2560, "layout 0");
 
 // Per-call device flags kept at the start of every workspace.
 // Every field is written by the call's planning kernel before any later

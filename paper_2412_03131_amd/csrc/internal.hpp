@@ -16,6 +16,8 @@ struct TState {        // per-table scratch of one append call
 struct LayoutArgs {
     int p_max;
     int T[2];
+    int kb[2], vb[2];  // key and value bits per section
+    int tsh;           // log2 of the tokens per page: high section in bits 0-7, low in 8-15
     long long page_bytes;
     int off_kcode[2], off_kmeta[2], off_vcode[2], off_vmeta[2], off_score[2], off_pos[2];
 };
@@ -132,6 +134,7 @@ struct AttnArgs {
     long long* ustart;   // [T] first work unit of each table (balanced mode)
     long long* utot;     // [1] total work units (balanced mode)
     float* part;         // partial states {max, sum, acc[kD]} per head
+    int layout;          // index into kLayoutFmts
 };
 
 // most shares of the balanced attention mode (sizes its workspace)
@@ -159,16 +162,16 @@ struct SigArgs {
     const uint16_t* q;
     float scale_log2;
     const float* lse;   // [B][Hq] natural log, from the attention call
+    int layout;         // index into kLayoutFmts
 };
 hipError_t launch_significance(const SigArgs& a, hipStream_t st);
 // The mode an attention call with `splits` runs in on the current device:
 // S >= 1 page ranges per table (S = 1: no split) or -1 (balanced shares);
 // *workers = the balanced mode's share count.
-hipError_t attention_mode(int gq, long long T, int splits, int* mode, int* workers);
+hipError_t attention_mode(int gq, int li, long long T, int splits, int* mode, int* workers);
 
 // Fixed device scratch of diffkv_decode_attention_noalloc, one per device.
 constexpr long long kNoAllocScratchBytes = 8ll << 20;
 hipError_t noalloc_scratch(void** ptr);
-bool attention_layout_matches(const diffkv_layout* L);
 
 }  // namespace dkv

@@ -1,1387 +1,24 @@
-// k_attention.hip -- decode attention over the differentiated paged KV cache
-// for gfx950 (DiffKV Eq. (1) of Sec. 2.1, kernel structure of Sec. 6.2).
-//
-// Work: a table's pages (high pages first, then low pages) are processed by
-// one eight-wave workgroup for all GQ query heads that read them, or -- in the
-// balanced mode -- every table's pages are laid end to end and cut into one
-// equal share per resident workgroup, so the spread of table lengths costs
-// nothing; tables that straddle shares are merged by attn_merge.  Inside a
-// workgroup each wave takes every eighth page, one register buffer per wave:
-// with two workgroups per CU four waves share each SIMD, so the waves hide
-// each other's page loads, and a table left alone on its CU still runs two
-// waves per SIMD.  A wave's page IDs arrive as one vector per 64 pages and
-// each page is loaded through a buffer resource over that page (scalar
-// address, hardware bounds).
-//
-// Lane mapping inside a wave (64 lanes = 4 rows of 16):
-//   key phase    lane = grp*16 + j: token j (and j+16 on 32-token pages),
-//                32-dim group grp.  A row holds its group's q as 16 fp16
-//                pairs, one per lane, read by the whole row through DPP
-//                row_newbcast, and computes sum(q*code) with v_dot2 on codes
-//                turned into fp16 denormals (exact, one v_perm or AND per two
-//                codes), then s*sum + z*sum(q) (scale and zero factored out of
-//                the dot product).  A transposed sum over the four rows
-//                (v_permlane16/32_swap) leaves head 4s + r of token j in
-//                row r, so the softmax costs one exp2 per (token, head).
-//   softmax      online, base 2, with a lazily raised max: the page max (DPP
-//                row ops) is only taken when a logit exceeds the running max
-//                by more than 2^8.
-//   value phase  lane owns dims 2*lane, 2*lane+1 (its row's group).  The
-//                weights p*s_v of the row's tokens, rounded to fp16, go
-//                through LDS (one broadcast read per token pair for all heads)
-//                into v_dot2_f32_f16 with two tokens' codes as fp16 denormals;
-//                the zero-point term and the weights' rounding error (charged
-//                at the centre code) are accumulated per lane and added once.
-// The eight waves' (max, sum, acc) states merge through LDS.
+// k_attention.hip -- host side of the decode attention and significance
+// kernels (attn_kernels.hpp, instantiated per page layout in k_attn_l<n>.hip):
+// the launch mode, the balanced mode's share count, the launches, and the
+// device scratch of the no-allocation entry point.
 #include <atomic>
-#include <cstddef>
-#include <utility>
 
-#include "internal.hpp"
+#include "attn_common.hpp"
 
 namespace dkv {
-
-constexpr int kAttnWaves = 8;  // single page buffer: GQ <= 6 fits two workgroups per CU
-constexpr int kAttnThreads = kAttnWaves * kWave;
-// Workgroups of attn_decode<GQ> each CU holds at once; the launch bounds make
-// the compiler fit that residency (at most 128 VGPRs for two eight-wave
-// workgroups).  GQ 7-8 need more registers: four waves per SIMD there spilled
-// and measured slower, so they run one workgroup per CU.
-constexpr int attn_blocks_per_cu(int gq) { return gq <= 6 ? 2 : 1; }
-constexpr int kPartStride = kD + 2;
-
-// Byte offsets of the supported page layout (checked by the API against the
-// caller's diffkv_layout).
-constexpr int kOffKcHi = 0, kOffKmHi = 2048, kOffVcHi = 2304, kOffVmHi = 3328;
-constexpr int kOffKcLo = 0, kOffKmLo = 2048, kOffVcLo = 2560, kOffVmLo = 3584;
-constexpr long long kPageBytes = 4352;  // unified page of the supported layout
-
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
-
-// ---- cross-lane helpers ------------------------------------------------------
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x)
-{
-    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-__device__ __forceinline__ float fmax_sel(float a, float b) { return a > b ? a : b; }
-
-// max over the 16 lanes of each row, result in every lane of the row
-__device__ __forceinline__ float row_max16(float x)
-{
-    x = fmax_sel(x, dpp<0x128>(x));  // row_ror:8
-    x = fmax_sel(x, dpp<0x124>(x));  // row_ror:4
-    x = fmax_sel(x, dpp<0x122>(x));  // row_ror:2
-    x = fmax_sel(x, dpp<0x121>(x));  // row_ror:1
-    return x;
-}
-__device__ __forceinline__ float row_sum16(float x)
-{
-    x += dpp<0x128>(x);
-    x += dpp<0x124>(x);
-    x += dpp<0x122>(x);
-    x += dpp<0x121>(x);
-    return x;
-}
-
-// ---- code conversions ---------------------------------------------------------
-// Key codes become fp16 *denormals* (bit pattern = code, value = code * 2^-24):
-// one v_perm or one AND per two codes, exact, and exact again in
-// v_dot2_f32_f16 (its fp16 products are exact in fp32).  The 2^24 is folded
-// into the key scale.  Pairs hold dims (d, d+4) of each 8-dim block, the
-// pairing the q registers use (v_perm selector kPermSel below).
-
-__device__ __forceinline__ float dot2(half2_t a, uint32_t b, float c)
-{
-    return __builtin_amdgcn_fdot2(a, __builtin_bit_cast(half2_t, b), c, false);
-}
-// f(integral_constant<int, 0>) ... f(integral_constant<int, N-1>)
-template <typename F, int... I>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>)
-{
-    (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, typename F>
-__device__ __forceinline__ void static_for(F&& f)
-{
-    static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
-
-// ---- key dot products against DPP-broadcast query pairs ----------------------
-// A row holds its group's 16 query pairs one per lane; lane L's pair reaches
-// the whole row through DPP row_newbcast:L on src0 of v_dot2c_f32_f16
-// (L = 1 .. 15; row_newbcast:0 does not broadcast, so pair 0 is also kept
-// whole in every lane).  The compiler cannot see inside asm, so these
-// sequences keep the hardware's wait-state rules themselves:
-//   - a DPP instruction reads a VGPR at least 2 wait states after a VALU write
-//     of it, and 5 after an EXEC write;
-//   - a VALU instruction reads the result of a dot instruction at least 3
-//     wait states after it, unless it is the same dot opcode reading it as
-//     its accumulator.
-// The steps are volatile asm (kept in the order written), each forms the next
-// code pair one step ahead, and the no-ops below pad the distances where the
-// head count does not.  The query registers are written once, before any page.
-template <int N>
-__device__ __forceinline__ void kwait()
-{
-    if constexpr (N > 0) asm volatile("s_nop %0" ::"n"(N - 1));
-}
-template <int L>
-__device__ __forceinline__ void kdot_bcast(float& c, uint32_t q, uint32_t x)
-{
-    static_assert(L >= 1 && L <= 15, "row_newbcast lane");
-    asm volatile("v_dot2c_f32_f16_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf" : "+v"(c) : "v"(q), "v"(x), "n"(L));
-}
-__device__ __forceinline__ void kdot_first(float& c, half2_t q, uint32_t x)
-{
-    asm volatile("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(c) : "v"(q), "v"(x));
-}
-__device__ __forceinline__ uint32_t kperm(uint32_t hi, uint32_t lo, uint32_t sel)
-{
-    uint32_t x;
-    asm volatile("v_perm_b32 %0, %1, %2, %3" : "=v"(x) : "v"(hi), "v"(lo), "s"(sel));
-    return x;
-}
-__device__ __forceinline__ uint32_t kand(uint32_t v, uint32_t mask)
-{
-    uint32_t x;
-    asm volatile("v_and_b32 %0, %2, %1" : "=v"(x) : "v"(v), "s"(mask));
-    return x;
-}
-__device__ __forceinline__ void kzero(float& c) { asm volatile("v_mov_b32 %0, 0" : "=v"(c)); }
-// The next code pair's v_perm / v_and and the first head's dot in one asm
-// statement (the compiler pads between separate asm statements).
-template <int L>
-__device__ __forceinline__ uint32_t kperm_dot(uint32_t hi, uint32_t lo, uint32_t sel, float& c, uint32_t q,
-                                              uint32_t x)
-{
-    uint32_t xn;
-    asm volatile("v_perm_b32 %0, %2, %3, %4\n\tv_dot2c_f32_f16_dpp %1, %5, %6 row_newbcast:%7 row_mask:0xf bank_mask:0xf"
-                 : "=&v"(xn), "+v"(c)
-                 : "v"(hi), "v"(lo), "s"(sel), "v"(q), "v"(x), "n"(L));
-    return xn;
-}
-template <int L>
-__device__ __forceinline__ uint32_t kand_dot(uint32_t v, uint32_t mask, float& c, uint32_t q, uint32_t x)
-{
-    uint32_t xn;
-    asm volatile("v_and_b32 %0, %3, %2\n\tv_dot2c_f32_f16_dpp %1, %4, %5 row_newbcast:%6 row_mask:0xf bank_mask:0xf"
-                 : "=&v"(xn), "+v"(c)
-                 : "v"(v), "s"(mask), "v"(q), "v"(x), "n"(L));
-    return xn;
-}
-
-constexpr int kMax0(int a) { return a > 0 ? a : 0; }
-
-// End of a sequence: three wait states, then each result passes through an
-// empty asm, so no instruction the compiler schedules can read a result before
-// the wait (the wait itself only orders against other volatile asm).
-template <int GQ>
-__device__ __forceinline__ void kdone(float (&d)[GQ])
-{
-    kwait<3>();
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) asm volatile("" : "+v"(d[hh]));
-}
-
-// v_perm selector of pair a of an 8-dim block: bytes [w_lo.byte a, 0, w_hi.byte a, 0]
-constexpr uint32_t kPermSel(int a) { return 0x0C000C00u | ((uint32_t)(4 + a) << 16) | (uint32_t)a; }
-
-// K8 token: d[h] = sum over the group's 16 pairs of q_h . codes (w = the 32
-// code bytes of the token's group).  Step i forms pair i+1 and adds pair i.
-// Between the same head's steps i-1 and i lie GQ-1 dots and the next pair's
-// v_perm (none in the last step); step 1 follows the first products of
-// another dot opcode (3 wait states), later steps the same one (the DPP rule,
-// 2).  The code pair of step i was formed before GQ dots of step i-1.
-template <int GQ>
-__device__ __forceinline__ void kdots_k8(const uint32_t (&w)[8], const uint32_t (&qr)[GQ], const half2_t (&q0)[GQ],
-                                         float (&d)[GQ])
-{
-    kwait<5>();
-    uint32_t x = kperm(w[1], w[0], kPermSel(0));
-    static_for<16>([&](auto i) {
-        constexpr int perm = i < 15 ? 1 : 0;
-        constexpr int pad = i > 0 ? kMax0((i == 1 ? 3 : 2) - (GQ - 1 + perm)) : 0;
-        constexpr int m1 = (i + 1) / 4, a1 = (i + 1) % 4;
-        uint32_t xn = 0;
-        if constexpr (i > 0 && i < 15 && pad == 0) {
-            // next pair and head 0 in one statement, then the other heads
-            xn = kperm_dot<(i > 0 ? i : 1)>(w[2 * m1 + 1], w[2 * m1], kPermSel(a1), d[0], qr[0], x);
-#pragma unroll
-            for (int hh = 1; hh < GQ; ++hh) kdot_bcast<(i > 0 ? i : 1)>(d[hh], qr[hh], x);
-        } else {
-            if constexpr (i < 15) xn = kperm(w[2 * m1 + 1], w[2 * m1], kPermSel(a1));
-            kwait<pad>();
-#pragma unroll
-            for (int hh = 0; hh < GQ; ++hh) {
-                if constexpr (i == 0) kdot_first(d[hh], q0[hh], x);
-                else kdot_bcast<(i > 0 ? i : 1)>(d[hh], qr[hh], x);
-            }
-        }
-        x = xn;
-    });
-    kdone<GQ>(d);
-}
-
-// K4 token: pairs 4m + a (a = 0..3) of dword w[m] are its nibbles (a, a+4)
-// (a even) or 16 * nibbles (a, a+4) (a odd); even pairs sum into dlo, odd ones
-// into dhi (scaled by 1/16 afterwards).  The two chains alternate, so a
-// chain's steps are 2*GQ-1 dots and two AND steps apart (one in the last
-// step); a code pair is formed GQ dots and one AND step before its use.
-template <int GQ>
-__device__ __forceinline__ void kdots_k4(const uint32_t (&w)[4], const uint32_t (&qr)[GQ], const half2_t (&q0)[GQ],
-                                         float (&dlo)[GQ], float (&dhi)[GQ])
-{
-    kwait<5>();
-    uint32_t w8[4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m) w8[m] = w[m] >> 8;
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) kzero(dhi[hh]);
-    uint32_t x = kand(w[0], 0x000F000Fu);
-    static_for<16>([&](auto i) {
-        constexpr int n = i + 1, m = n / 4, a = n % 4;
-        constexpr int pad = i > 0 ? kMax0(2 - (GQ + (i < 15 ? 1 : 0))) : 0;
-        constexpr uint32_t mask = (a & 1) ? 0x00F000F0u : 0x000F000Fu;
-        uint32_t xn = 0;
-        if constexpr (i > 0 && i < 15 && pad == 0) {
-            float(&acc)[GQ] = (i % 2 == 0) ? dlo : dhi;
-            xn = kand_dot<(i > 0 ? i : 1)>(a >= 2 ? w8[m] : w[m], mask, acc[0], qr[0], x);
-#pragma unroll
-            for (int hh = 1; hh < GQ; ++hh) kdot_bcast<(i > 0 ? i : 1)>(acc[hh], qr[hh], x);
-        } else {
-            if constexpr (i < 15) xn = kand(a >= 2 ? w8[m] : w[m], mask);
-            kwait<pad>();
-#pragma unroll
-            for (int hh = 0; hh < GQ; ++hh) {
-                if constexpr (i == 0) kdot_first(dlo[hh], q0[hh], x);
-                else if constexpr (i % 2 == 0) kdot_bcast<(i > 0 ? i : 1)>(dlo[hh], qr[hh], x);
-                else kdot_bcast<(i > 0 ? i : 1)>(dhi[hh], qr[hh], x);
-            }
-        }
-        x = xn;
-    });
-    kwait<3>();
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) asm volatile("" : "+v"(dlo[hh]), "+v"(dhi[hh]));
-}
-
-constexpr float kTwo24 = 16777216.0f;
-
-// Raw bytes of one page as one lane needs them.  High and low pages take
-// the same seven loads (two of them unused on high pages, re-reading lines the
-// page's other loads fetch), so one buffer serves both page loops without
-// register copies.
-struct PageRaw {
-    uint4 k0, k1;  // high: K8 chunks 2g, 2g+1 of token j; low: K4 chunk g of tokens j, j+16
-    uint4 vr;      // V code rows of dims 2*lane, 2*lane+1
-    uint32_t m0;   // K meta {s, z} of token j, group g
-    uint32_t m1;   // low: K meta of token j+16
-    uint32_t m2;   // V meta of token j, group g
-    uint32_t m3;   // low: V meta of token j+16
-};
-
-
-// Both page types put K chunk c of token j at (c*T + j)*16 with 2 (high) or 1
-// (low) chunks per group, i.e. at 512*g + 16*j (+256) for this lane, and K
-// meta at 2048 + 16*j + 4*g; the V segments differ only in base and the V
-// meta row stride (16 or 32 tokens).
-//
-// The loads go through a buffer resource over the one page (`pg` is uniform):
-// the page address is scalar arithmetic, the per-lane offsets are 32-bit
-// constants of the lane, and the hardware bounds every access by the page size.
-__device__ __forceinline__ void load_page(PageRaw& r, const uint8_t* pg, bool hi, int lane)
-{
-    const uint32_t grp = (uint32_t)lane >> 4, jl = (uint32_t)lane & 15;
-    static_assert(kOffKcHi == 0 && kOffKcLo == 0 && kOffKmHi == 2048 && kOffKmLo == 2048, "page layout");
-    static_assert(kOffVmLo - kOffVmHi == 256 && kOffVcLo - kOffVcHi == 256, "page layout");
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)pg, 0, (int)kPageBytes, 0x00020000);
-    const uint32_t kc = grp * 512 + jl * 16;
-    const uint32_t km = 2048 + jl * 16 + grp * 4;
-    const int lo = hi ? 0 : 256;  // uniform: V segments of a low page start 256 bytes later
-    const uint32_t vm = (hi ? grp * (kTHi * 4) : grp * (kTLo * 4)) + jl * 4;
-    r.k0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, kc, 0, 0));
-    r.k1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, kc + 256, 0, 0));
-    r.vr = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)lane * 16 + kOffVcHi, lo, 0));
-    r.m0 = __builtin_amdgcn_raw_buffer_load_b32(rs, km, 0, 0);
-    r.m1 = __builtin_amdgcn_raw_buffer_load_b32(rs, km + 256, 0, 0);
-    r.m2 = __builtin_amdgcn_raw_buffer_load_b32(rs, vm + kOffVmHi, lo, 0);
-    r.m3 = __builtin_amdgcn_raw_buffer_load_b32(rs, vm + kOffVmHi, lo + (hi ? 0 : 64), 0);  // high pages: a line already fetched
-}
-
-// One wave's next page, written into LDS by the seven loads themselves (buffer
-// loads with an LDS destination: lane L's 16- or 4-byte piece lands at index L
-// of its row), so a page can be in flight while the wave computes another one
-// from registers without holding a second register buffer.
-struct PageStage {
-    uint4 k0[kWave];
-    uint4 k1[kWave];
-    uint4 vr[kWave];
-    uint32_t m[4][kWave];
-};
-
-typedef __attribute__((address_space(3))) uint32_t lds_u32;
-typedef __attribute__((address_space(3))) _Float16 lds_f16;
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) u32x4 lds_u4;
-
-// Buffer loads with an LDS destination: lane L's 16 (or 4) bytes land at byte
-// m0 + 16 L (or m0 + 4 L).  Written as asm so that the compiler, which would
-// otherwise make every later LDS access wait for them, leaves their waits to
-// take_page (the only reader of the slot).
-__device__ __forceinline__ void lds_load16(u32x4 rs, uint32_t m0, uint32_t voff, uint32_t soff)
-{
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-                 ::"s"(m0), "v"(voff), "s"(rs), "s"(soff) : "memory");
-}
-__device__ __forceinline__ void lds_load4(u32x4 rs, uint32_t m0, uint32_t voff, uint32_t soff)
-{
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds"
-                 ::"s"(m0), "v"(voff), "s"(rs), "s"(soff) : "memory");
-}
-
-// Stage a page into the wave's slot: the seven loads of load_page, through a
-// buffer resource over the one page (base pg, 4352 bytes: the hardware bounds
-// every access), with LDS destinations.
-__device__ __forceinline__ void stage_page(PageStage& sg, const uint8_t* pg, bool hi, int lane)
-{
-    const uint32_t grp = (uint32_t)lane >> 4, jl = (uint32_t)lane & 15;
-    const unsigned long long base = (unsigned long long)pg;
-    const u32x4 rs = {(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, (uint32_t)kPageBytes, 0x00020000u};
-    const uint32_t kc = grp * 512 + jl * 16;
-    const uint32_t km = 2048 + jl * 16 + grp * 4;
-    const uint32_t lo = hi ? 0u : 256u;
-    const uint32_t vm = (hi ? grp * (kTHi * 4) : grp * (kTLo * 4)) + jl * 4;
-    const uint32_t m0 = (uint32_t)(size_t)(__attribute__((address_space(3))) void*)&sg;
-    static_assert(sizeof(PageStage) == 4096 && offsetof(PageStage, k1) == 1024 && offsetof(PageStage, vr) == 2048 &&
-                      offsetof(PageStage, m) == 3072,
-                  "stage slot layout");
-    lds_load16(rs, m0, kc, 0u);
-    lds_load16(rs, m0 + 1024, kc + 256, 0u);
-    lds_load16(rs, m0 + 2048, (uint32_t)lane * 16 + kOffVcHi, lo);
-    lds_load4(rs, m0 + 3072, km, 0u);
-    lds_load4(rs, m0 + 3328, km + 256, 0u);
-    lds_load4(rs, m0 + 3584, vm + kOffVmHi, lo);
-    lds_load4(rs, m0 + 3840, vm + kOffVmHi, lo + (hi ? 0u : 64u));
-}
-
-// The staged page into registers: wait for the wave's staging loads (every
-// vector load of the wave, the only ones in flight here being the slot's),
-// read the slot, and wait for the reads, so the next staging loads cannot
-// overwrite the slot before it is read.
-__device__ __forceinline__ void take_page(PageRaw& r, const PageStage& sg, int lane)
-{
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    r.k0 = sg.k0[lane];
-    r.k1 = sg.k1[lane];
-    r.vr = sg.vr[lane];
-    r.m0 = sg.m[0][lane];
-    r.m1 = sg.m[1][lane];
-    r.m2 = sg.m[2][lane];
-    r.m3 = sg.m[3][lane];
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-}
-
-template <int GQ>
-struct WaveState {
-    static constexpr int NS = (GQ + 3) / 4;  // head slots per lane in the softmax layout
-    float m[NS];       // running max of head 4s + row (log2 domain), row-uniform
-    float l[NS];       // this lane's share of the running sum of head 4s + row
-    float z[GQ];       // this lane's share of the zero-point term of head hh (group = row)
-    float acc[GQ][2];  // dims 2*lane, 2*lane+1, in units of 2^-24
-};
-
-// LDS for the value weights of one page: [row = value group][token pair][head]
-// as fp16 pairs; rows padded by four dwords so the four rows' broadcast reads
-// hit different banks.
-template <int GQ>
-struct CoefLds {
-    static constexpr int kH = GQ <= 4 ? 4 : 8;  // heads per pair entry (dwords)
-    static constexpr int kRow = 16 * kH + 4;     // dwords per row (16 pairs)
-    uint32_t v[kAttnWaves][4 * kRow];
-};
-
-// Sum over the four rows with a transpose: row r of the result holds the sum of
-// argument r (heads a, b, c, d -> rows 0, 1, 2, 3).
-__device__ __forceinline__ float xsum4(float a, float b, float c, float d)
-{
-    auto ab = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
-    auto cd = __builtin_amdgcn_permlane16_swap(__float_as_uint(c), __float_as_uint(d), false, false);
-    const float u = __uint_as_float(ab[0]) + __uint_as_float(ab[1]);
-    const float w = __uint_as_float(cd[0]) + __uint_as_float(cd[1]);
-    auto uw = __builtin_amdgcn_permlane32_swap(__float_as_uint(u), __float_as_uint(w), false, false);
-    return __uint_as_float(uw[0]) + __uint_as_float(uw[1]);
-}
-
-// o[r] = x of row r (same column), in every lane
-__device__ __forceinline__ void gather4(float x, float* o)
-{
-    auto eo = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    auto e = __builtin_amdgcn_permlane32_swap(eo[0], eo[0], false, false);
-    auto od = __builtin_amdgcn_permlane32_swap(eo[1], eo[1], false, false);
-    o[0] = __uint_as_float(e[0]);
-    o[1] = __uint_as_float(od[0]);
-    o[2] = __uint_as_float(e[1]);
-    o[3] = __uint_as_float(od[1]);
-}
-
-// Softmax weights are exp2(logit - m) with a running max m that is only
-// raised when a logit exceeds it by more than kSlack (weights stay <= 2^8),
-// on pages whose V scales are at most 2^7 (fp16 bits 0x5800; scales are never
-// negative, so the bit pattern orders them); other pages raise it to their max.
-constexpr float kSlack = 8.0f;
-constexpr uint32_t kVScaleSlackMax = 0x5800u;
-
-// One page: logits, online softmax, weighted value sum.  NT = tokens per lane.
-//
-// Value weights.  For token j, head h and value group g the weight
-// w = p * s_v is rounded to fp16 (c) and multiplied with the codes on
-// v_dot2_f32_f16 (codes as fp16 denormals, products exact in fp32).  The
-// rounding error (w - c) is charged to the zero-point term at the centre code
-// (7.5 for 4-bit, 1.5 for 2-bit): sum_j p*z_v + centre*(w - c), so what is
-// left of it scales with |code - centre| <= half the code range, at most
-// 2^-12 of the group's value range per unit of softmax weight.  2-bit codes in
-// odd crumbs are extracted as 4*code, and their c carries w/4.
-template <int GQ, int NT>
-__device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, const uint32_t (&qr)[GQ],
-                                        const half2_t (&q0)[GQ],
-                                        const float (&qsum)[GQ], float sl2, int n_valid, int lane,
-                                        lds_u32* coef_row)
-{
-    constexpr int NS = WaveState<GQ>::NS;
-    constexpr int kH = CoefLds<GQ>::kH;
-    const int jl = lane & 15;
-    // ---- logits: lane (group row, token jl) partial dot products, then a
-    // transposed row sum: afterwards row r holds head 4s + r of token jl + 16*tk
-    float lg[NT][NS];
-#pragma unroll
-    for (int tk = 0; tk < NT; ++tk) {
-        const uint32_t km = tk ? r.m1 : r.m0;
-        const float ks = h2f(km & 0xffffu) * (kTwo24 * sl2), kz = h2f(km >> 16) * sl2;
-        float dlo[GQ], dhi[GQ];
-        if constexpr (NT == 1) {
-            const uint32_t w[8] = {r.k0.x, r.k0.y, r.k0.z, r.k0.w, r.k1.x, r.k1.y, r.k1.z, r.k1.w};
-            kdots_k8<GQ>(w, qr, q0, dlo);
-        } else {
-            const uint4 kk = tk ? r.k1 : r.k0;
-            const uint32_t w[4] = {kk.x, kk.y, kk.z, kk.w};
-            kdots_k4<GQ>(w, qr, q0, dlo, dhi);
-        }
-        float part[4 * NS];
-#pragma unroll
-        for (int hh = 0; hh < 4 * NS; ++hh) {
-            if (hh < GQ) {
-                const float d = NT == 1 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
-                part[hh] = fmaf(ks, d, kz * qsum[hh]);
-            } else {
-                part[hh] = 0.f;
-            }
-        }
-        const bool valid = jl + 16 * tk < n_valid;
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            const float x = xsum4(part[4 * s], part[4 * s + 1], part[4 * s + 2], part[4 * s + 3]);
-            lg[tk][s] = valid ? x : -INFINITY;
-        }
-    }
-    // ---- online softmax with a lazily raised max (one head per lane and slot).
-    // The value weights p * s_v are rounded to fp16, so they must stay below
-    // 65504: on a page whose V scales all lie at or below 2^7 the slack keeps
-    // p <= 2^8 (weights <= 2^15); a page with a larger V scale takes no slack,
-    // so its weights are p <= 1 times an fp16 scale.
-    const bool big_v = (r.m2 & 0xffffu) > kVScaleSlackMax || (NT == 2 && (r.m3 & 0xffffu) > kVScaleSlackMax);
-    const float slack = __builtin_amdgcn_ballot_w64(big_v) ? 0.f : kSlack;
-    bool raise = false;
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-#pragma unroll
-        for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.m[s] + slack;
-    if (__builtin_amdgcn_ballot_w64(raise)) {
-        float al[4 * NS];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            float mx = lg[0][s];
-            if (NT > 1) mx = fmax_sel(mx, lg[NT - 1][s]);
-            mx = row_max16(mx);
-            const float mnew = fmax_sel(st.m[s], mx);
-            const float alpha = __builtin_amdgcn_exp2f(st.m[s] - mnew);
-            st.m[s] = mnew;
-            st.l[s] *= alpha;
-            gather4(alpha, al + 4 * s);
-        }
-#pragma unroll
-        for (int hh = 0; hh < GQ; ++hh) {
-            st.z[hh] *= al[hh];
-            st.acc[hh][0] *= al[hh];
-            st.acc[hh][1] *= al[hh];
-        }
-    }
-    float p[NT][NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-#pragma unroll
-        for (int tk = 0; tk < NT; ++tk) {
-            p[tk][s] = __builtin_amdgcn_exp2f(lg[tk][s] - st.m[s]);
-            st.l[s] += p[tk][s];
-        }
-    }
-    // ---- value weights of token jl + 16*tk for this lane's group (row), all
-    // heads: fp16 to LDS, zero-point and rounding terms into z
-    lds_f16* crow = reinterpret_cast<lds_f16*>(coef_row);
-#pragma unroll
-    for (int tk = 0; tk < NT; ++tk) {
-        float pg[4 * NS];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) gather4(p[tk][s], pg + 4 * s);
-        const uint32_t vm = tk ? r.m3 : r.m2;
-        const float vs = h2f(vm & 0xffffu), vz = h2f(vm >> 16);
-        constexpr float centre = NT == 1 ? 7.5f : 1.5f;
-        const bool by4 = NT == 2 && (jl & 1);
-        const float vs_c = by4 ? vs * 0.25f : vs;
-        const float cc = by4 ? 4.f * centre : centre;
-        const float zc = fmaf(centre, vs, vz);
-        const int pi = NT == 1 ? ((jl >> 3) * 4 + (jl & 3)) : (tk * 8 + (jl & 7));
-        const int pos = NT == 1 ? ((jl >> 2) & 1) : (jl >> 3);
-        lds_f16* dst = crow + pi * 2 * kH + pos;
-#pragma unroll
-        for (int hh = 0; hh < GQ; ++hh) {
-            const _Float16 c = (_Float16)(pg[hh] * vs_c);
-            st.z[hh] = fmaf(pg[hh], zc, st.z[hh]);
-            st.z[hh] = fmaf(-cc, (float)c, st.z[hh]);
-            dst[2 * hh] = c;
-        }
-    }
-    __builtin_amdgcn_wave_barrier();
-    // ---- value phase: lane owns dims 2*lane, 2*lane+1 (its row's group); token
-    // pairs of each dword as fp16 denormals, one v_dot2 per pair and head.
-    const uint32_t w[4] = {r.vr.x, r.vr.y, r.vr.z, r.vr.w};
-    // weights of token pairs p0 .. p0+3, all heads (four broadcast reads per
-    // pair group, issued together)
-    auto read_cf = [&](int p0, half2_t (&cf)[4][GQ]) {
-#pragma unroll
-        for (int pp = 0; pp < 4; ++pp) {
-            const lds_u32* src = coef_row + (p0 + pp) * kH;
-            uint32_t t[kH];
-#pragma unroll
-            for (int i = 0; i < kH; i += 4) {
-                const u32x4 v = *reinterpret_cast<const lds_u4*>(src + i);
-                t[i] = v.x; t[i + 1] = v.y; t[i + 2] = v.z; t[i + 3] = v.w;
-            }
-#pragma unroll
-            for (int hh = 0; hh < GQ; ++hh) cf[pp][hh] = __builtin_bit_cast(half2_t, t[hh]);
-        }
-    };
-    if constexpr (NT == 1) {
-        // 16 tokens x 4 bits per 64-bit row; nibbles k, k+4 of dword dw -> pair 4*dw + k
-#pragma unroll
-        for (int dw = 0; dw < 2; ++dw) {
-            half2_t cf[4][GQ];
-            read_cf(4 * dw, cf);
-            const uint32_t a = w[dw], b = w[2 + dw];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint32_t xa = (a >> (4 * k)) & 0x000F000Fu, xb = (b >> (4 * k)) & 0x000F000Fu;
-#pragma unroll
-                for (int hh = 0; hh < GQ; ++hh) {
-                    st.acc[hh][0] = dot2(cf[k][hh], xa, st.acc[hh][0]);
-                    st.acc[hh][1] = dot2(cf[k][hh], xb, st.acc[hh][1]);
-                }
-            }
-        }
-    } else {
-        // 32 tokens x 2 bits per 64-bit row; dword `half` holds tokens 16*half + r
-        // at bits 2r; crumbs r, r+8 -> pair 8*half + (r & 7) (4*code for odd r)
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const uint32_t a = w[half], b = w[2 + half];
-#pragma unroll
-            for (int q4 = 0; q4 < 2; ++q4) {
-                half2_t cf[4][GQ];
-                read_cf(8 * half + 4 * q4, cf);
-#pragma unroll
-                for (int s2 = 0; s2 < 2; ++s2) {
-                    const int s4 = 2 * q4 + s2;
-                    const uint32_t ya = a >> (4 * s4), yb = b >> (4 * s4);
-                    const uint32_t x1a = ya & 0x00030003u, x1b = yb & 0x00030003u;
-                    const uint32_t x4a = ya & 0x000C000Cu, x4b = yb & 0x000C000Cu;
-#pragma unroll
-                    for (int hh = 0; hh < GQ; ++hh) {
-                        st.acc[hh][0] = dot2(cf[2 * s2][hh], x1a, st.acc[hh][0]);
-                        st.acc[hh][1] = dot2(cf[2 * s2][hh], x1b, st.acc[hh][1]);
-                        st.acc[hh][0] = dot2(cf[2 * s2 + 1][hh], x4a, st.acc[hh][0]);
-                        st.acc[hh][1] = dot2(cf[2 * s2 + 1][hh], x4b, st.acc[hh][1]);
-                    }
-                }
-            }
-        }
-    }
-    __builtin_amdgcn_wave_barrier();
-}
-
-// ---------------------------------------------------------------------------
-// Tables and their work
-// ---------------------------------------------------------------------------
-// A table's pages in attention order: high pages 0 .. ph-1 (slots 0 ..), then
-// low pages ph .. np-1 (slots p_max-1 downward).  For balancing, a high page
-// is kHighUnits units of work and a low page kLowUnits (twice the tokens; the
-// measured time per page is about 5:3): page p starts at unit kHighUnits*p
-// (p < ph) or kHighUnits*ph + kLowUnits*(p - ph).
-constexpr int kHighUnits = 3;
-constexpr int kLowUnits = 5;
-
-struct TableInfo {
-    int ph, np;
-    int len_hi, len_lo;
-    long long units;
-};
-
-__device__ __forceinline__ TableInfo table_info_of(const AttnArgs& a, int len_hi, int len_lo)
-{
-    TableInfo ti;
-    const int P = a.p_max;
-    ti.len_hi = len_hi;
-    ti.len_lo = len_lo;
-    // page counts from the section lengths, clamped to the table width
-    int ph = (ti.len_hi + kTHi - 1) / kTHi;
-    int pl = (ti.len_lo + kTLo - 1) / kTLo;
-    ph = ph < 0 ? 0 : (ph > P ? P : ph);
-    pl = pl < 0 ? 0 : (pl > P - ph ? P - ph : pl);
-    ti.ph = ph;
-    ti.np = ph + pl;
-    ti.units = (long long)kHighUnits * ph + (long long)kLowUnits * pl;
-    return ti;
-}
-// t uniform: the section lengths come through scalar loads (the attention
-// kernels never write them), so everything derived from them stays scalar.
-__device__ __forceinline__ TableInfo table_info(const AttnArgs& a, int t)
-{
-    const auto* len = (const __attribute__((address_space(4))) int32_t*)(a.len + 2 * (long long)t);
-    return table_info_of(a, len[0], len[1]);
-}
-
-// first page whose first unit is >= x (np if none)
-__device__ __forceinline__ int page_at_unit(long long x, int ph, int np)
-{
-    if (x <= 0) return 0;
-    const long long xh = (long long)kHighUnits * ph;
-    const long long p = x <= xh ? (x + kHighUnits - 1) / kHighUnits : ph + (x - xh + kLowUnits - 1) / kLowUnits;
-    return p > np ? np : (int)p;
-}
-
-template <int GQ>
-struct AttnShared {
-    float m[kAttnWaves][8];
-    float l[kAttnWaves][8];
-    float acc[kAttnWaves][GQ][kD];
-    long long scan[kAttnWaves + 1];
-    int t_first;
-    int len_first[2];  // section lengths of t_first (longest-first ranking)
-    long long u_first;
-};
-
-// Exclusive prefix sum of one 64-bit value per thread of the workgroup.
-__device__ __forceinline__ long long wg_excl_scan(long long x, long long* lds, long long* total)
-{
-    const int l = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
-    long long inc = x;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const long long y = __shfl_up(inc, o, kWave);
-        if (l >= o) inc += y;
-    }
-    if (l == kWave - 1) lds[w] = inc;
-    __syncthreads();
-    long long before = 0, tot = 0;
-#pragma unroll
-    for (int i = 0; i < kAttnWaves; ++i) {
-        const long long v = lds[i];
-        before += i < w ? v : 0;
-        tot += v;
-    }
-    __syncthreads();
-    *total = tot;
-    return before + inc - x;
-}
-
-__device__ __forceinline__ void write_empty(const AttnArgs& a, int t, int gq)
-{
-    const int b = t / a.Hkv, h = t - b * a.Hkv;
-    for (int i = threadIdx.x; i < gq * kD; i += blockDim.x) {
-        const int hh = i / kD, d = i - hh * kD;
-        const long long row = (long long)b * a.Hq + h * gq + hh;
-        a.out[row * kD + d] = 0.f;
-        if (d == 0 && a.lse) a.lse[row] = -INFINITY;
-    }
-}
-
-// ---------------------------------------------------------------------------
-// One segment: pages [pa, pb) of table t for all GQ query heads of its KV
-// head.  The eight waves take every eighth page, each loading a page and
-// then computing it (the other waves on its SIMD cover the wait).  Their
-// (max, sum, acc) states merge through LDS
-// into the output (part == nullptr) or into a partial state {max, sum, acc}
-// per head at `part` (pa == pb gives the empty state).
-// ---------------------------------------------------------------------------
-template <int GQ>
-__device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& sh, CoefLds<GQ>* coef,
-                                            PageStage* stage, int t, const TableInfo& ti, int pa, int pb,
-                                            float* part)
-{
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int grp = lane >> 4;
-    const int P = a.p_max;
-    const int b = t / a.Hkv, h = t - b * a.Hkv;
-    const int ph = ti.ph;
-    const float sl2 = a.scale_log2;
-    const long long npool = a.num_pages;
-    constexpr long long page_bytes = kPageBytes;  // (the layout check guarantees it)
-    lds_u32* coef_row = (lds_u32*)(&coef->v[wave][grp * CoefLds<GQ>::kRow]);
-    const int nmine = pb - pa > wave ? (pb - pa - wave + kAttnWaves - 1) / kAttnWaves : 0;
-    const int32_t* trow = a.page_table + (long long)t * P;
-
-    // The wave's pages run in chunks of 64: lane k holds the ID of chunk page
-    // c0 + k (one vector load per chunk), and a page's ID is read into a scalar
-    // register when its loads are issued.  Chunk bounds [c0, c1); past c1 the
-    // index is clamped to the chunk's last page.
-    auto page_of = [&](int i) { return pa + wave + kAttnWaves * i; };
-    auto slot_of = [&](int p) { return p < ph ? p : P - 1 - (p - ph); };
-    int c0 = 0, c1 = 0, c_last = 0, ids_v = 0;
-    auto clamp_i = [&](int i) { return i < c_last ? i : c_last; };
-    auto load_ids = [&]() {
-        const int k = c0 + lane;
-        return trow[slot_of(page_of(clamp_i(k)))];
-    };
-    // Stage page i in this wave's LDS slot; ok = page i exists and lies in the
-    // pool.  The loads are unconditional (an index past the chunk's last page
-    // re-reads it; an ID outside the pool reads page 0 and is not computed).
-    PageStage& sg = stage[wave];
-    const uint32_t npool32 = npool > 0x7fffffffLL ? 0x80000000u : (uint32_t)npool;
-    auto issue = [&](int i, bool& ok) {
-        const int ic = clamp_i(i);
-        const int id = __builtin_amdgcn_readlane(ids_v, ic - c0);
-        const bool in_pool = (uint32_t)id < npool32;  // never read outside the pool
-        ok = i < c1 && in_pool;
-        stage_page(sg, a.pool + (in_pool ? id : 0) * page_bytes, page_of(ic) < ph, lane);
-    };
-    // The query loads go first: they depend only on the table, so their
-    // latency overlaps the page-ID -> page chain below.  Lane k of a row loads
-    // the two dwords of its pair k (dims 8(k/4) + k%4 and +4: dwords x, z or
-    // y, w of the 8-dim block) and the two of pair 0.
-    const int qm = (lane & 15) >> 2, qa = lane & 3;
-    uint32_t qraw[GQ][4];
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) {
-        const uint32_t* qd = reinterpret_cast<const uint32_t*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
-        const int o = 4 * qm + ((qa & 2) ? 1 : 0);
-        qraw[hh][0] = qd[o];
-        qraw[hh][1] = qd[o + 2];
-        qraw[hh][2] = qd[0];
-        qraw[hh][3] = qd[2];
-    }
-
-    PageRaw buf0;
-    bool ok0 = false, ok_next = false;
-    // first chunk: its IDs and first page go out beside the query loads
-    c1 = nmine < kWave ? nmine : kWave;
-    c_last = c1 > 0 ? c1 - 1 : 0;
-    if (nmine > 0) {
-        ids_v = load_ids();
-        issue(0, ok_next);
-    }
-
-    // q of this lane's group as fp16 pairs (d, d+4), one pair per lane (read
-    // by the others through DPP), pair 0 (dims 0, 4) in every lane; qsum = the
-    // group's sum (row sum)
-    uint32_t qr[GQ];
-    half2_t q0[GQ];
-    float qsum[GQ];
-    constexpr uint32_t kOnes = 0x3C003C00u;  // fp16 pair (1, 1)
-    {
-        const uint32_t sel = (qa & 1) ? 0x07060302u : 0x05040100u;
-#pragma unroll
-        for (int hh = 0; hh < GQ; ++hh) {
-            qr[hh] = __builtin_amdgcn_perm(qraw[hh][1], qraw[hh][0], sel);
-            q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(qraw[hh][3], qraw[hh][2], 0x05040100u));
-            qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f));
-        }
-    }
-
-    WaveState<GQ> st;
-#pragma unroll
-    for (int s = 0; s < WaveState<GQ>::NS; ++s) {
-        st.m[s] = -INFINITY;
-        st.l[s] = 0.f;
-    }
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) {
-        st.z[hh] = 0.f;
-        st.acc[hh][0] = st.acc[hh][1] = 0.f;
-    }
-
-    // This wave's pages i < nhi are high pages, the rest low pages.  High and
-    // low pages run in loops of their own (no per-page branch between two
-    // different updates of the softmax state); the prefetch crosses from one
-    // loop to the next.
-    const int nhi = ph - pa - wave > 0 ? min(nmine, (ph - pa - wave + kAttnWaves - 1) / kAttnWaves) : 0;
-    auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
-        if (i >= c1 || !ok) return;
-        const int p = page_of(i);
-        do_page<GQ, 1>(st, r, qr, q0, qsum, sl2, ti.len_hi - p * kTHi, lane, coef_row);
-    };
-    auto compute_lo = [&](int i, const PageRaw& r, bool ok) {
-        if (i >= c1 || !ok) return;
-        const int p = page_of(i);
-        do_page<GQ, 2>(st, r, qr, q0, qsum, sl2, ti.len_lo - (p - ph) * kTLo, lane, coef_row);
-    };
-    // Wave priority follows the pages this wave still has: on a SIMD shared
-    // with shorter work, the longest work is served first (longest-first
-    // scheduling at the wave level; ties go to the older wave).
-    auto set_prio = [&](int rem) {
-        if (rem > 12) __builtin_amdgcn_s_setprio(3);
-        else if (rem > 6) __builtin_amdgcn_s_setprio(2);
-        else if (rem > 2) __builtin_amdgcn_s_setprio(1);
-        else __builtin_amdgcn_s_setprio(0);
-    };
-    // Page i comes out of the LDS slot into registers, page i + 1 goes into the
-    // slot, then page i is computed: one page is always in flight while the
-    // wave computes.
-    auto next = [&](int i) {
-        take_page(buf0, sg, lane);
-        ok0 = ok_next;
-        if (i + 1 < c1) issue(i + 1, ok_next);
-    };
-    while (c0 < nmine) {
-        const int nh = nhi < c1 ? nhi : c1;  // high pages end (within this chunk)
-        int i = c0;
-        for (; i < nh; ++i) {
-            set_prio(nmine - i);
-            next(i);
-            compute_hi(i, buf0, ok0);
-        }
-        for (; i < c1; ++i) {
-            set_prio(nmine - i);
-            next(i);
-            compute_lo(i, buf0, ok0);
-        }
-        // next chunk (tables longer than 64 pages per wave): its IDs, then its
-        // first page
-        c0 = c1;
-        c1 = nmine - c0 < kWave ? nmine : c0 + kWave;
-        c_last = c1 > c0 ? c1 - 1 : c0;
-        if (c0 < nmine) {
-            ids_v = load_ids();
-            issue(c0, ok_next);
-        }
-    }
-
-    // ---- finish the wave: row sums of l (head 4s + row) and of the
-    // zero-point term (head hh, group = row); acc back from units of 2^-24
-#pragma unroll
-    for (int s = 0; s < WaveState<GQ>::NS; ++s) {
-        const float l = row_sum16(st.l[s]);
-        if ((lane & 15) == 0 && 4 * s + grp < GQ) {
-            sh.m[wave][4 * s + grp] = st.m[s];
-            sh.l[wave][4 * s + grp] = l;
-        }
-    }
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) {
-        const float z = row_sum16(st.z[hh]);
-        sh.acc[wave][hh][2 * lane] = fmaf(st.acc[hh][0], kTwo24, z);
-        sh.acc[wave][hh][2 * lane + 1] = fmaf(st.acc[hh][1], kTwo24, z);
-    }
-    __syncthreads();
-    // ---- merge the waves: final output, or this segment's partial state ---
-    for (int i = threadIdx.x; i < GQ * kD; i += kAttnThreads) {
-        const int hh = i / kD, d = i - hh * kD;
-        float M = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < kAttnWaves; ++w) M = fmax_sel(M, sh.m[w][hh]);
-        float L = 0.f, O = 0.f;
-        if (M != -INFINITY) {
-#pragma unroll
-            for (int w = 0; w < kAttnWaves; ++w) {
-                const float f = __builtin_amdgcn_exp2f(sh.m[w][hh] - M);
-                L = fmaf(sh.l[w][hh], f, L);
-                O = fmaf(sh.acc[w][hh][d], f, O);
-            }
-        }
-        if (part == nullptr) {
-            const long long row = (long long)b * a.Hq + h * GQ + hh;
-            a.out[row * kD + d] = (L > 0.f) ? O / L : 0.f;
-            if (d == 0 && a.lse) a.lse[row] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
-        } else {
-            float* pr = part + hh * kPartStride;
-            pr[2 + d] = O;
-            if (d == 0) {
-                pr[0] = M;
-                pr[1] = L;
-            }
-        }
-    }
-    __syncthreads();  // LDS is reused by the next segment
-}
-
-// ---------------------------------------------------------------------------
-// attn_decode.
-//  splits = S >= 1: workgroup t*S + c takes range c of table t's pages, cut
-//    into min(S, pages) equal ranges (S = 1: no split).
-//  splits = 0: balanced shares.  All tables' pages, in table order, form one
-//    list of U work units; workgroup k of W owns the pages whose first unit
-//    lies in [k*U/W, (k+1)*U/W).  Each workgroup finds its first table with a
-//    prefix sum over the tables' units, then walks its tables.  A table lying
-//    inside one share is finished in place; otherwise share k writes its
-//    partial state to slot k + t (distinct for every (share, table) pair met
-//    in this walk) and attn_merge combines them.
-// ---------------------------------------------------------------------------
-// Table of rank j when the tables are ordered by decreasing work units
-// (bucketed into 1024 bins, ties by index): workgroups are dispatched in
-// index order and two share a CU for the whole launch, so taking the tables
-// longest first spreads the long ones over the CUs and starts them first
-// (longest-processing-time-first order).  Every workgroup derives the same
-// order from the section lengths; wave 0 does it alone (wave-level scans, no
-// workgroup barrier until the result).  Beyond kRankPer tables per lane the
-// order is the identity.  *ti gets the table's pages and units, from the
-// lengths the ranking wave already holds.
-constexpr int kKeep = 8;     // tables per thread whose units stay in registers (balanced mode)
-constexpr int kRankPer = 16;  // tables per lane of the ranking wave
-
-template <int GQ>
-__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& sh, CoefLds<GQ>* coef, int T, int j,
-                                             TableInfo* ti)
-{
-    constexpr int kBins = 1024;
-    const int per = (T + kWave - 1) / kWave;
-    if (per > kRankPer) {
-        *ti = table_info(a, j);
-        return j;
-    }
-    static_assert(sizeof(CoefLds<GQ>) >= kBins * sizeof(int), "histogram lives in the weight LDS");
-    if (threadIdx.x < kWave) {
-        int* hist = reinterpret_cast<int*>(coef);  // free until the page loop
-        const int lane = threadIdx.x;
-        const int t0 = lane * per, t1 = t0 + per < T ? t0 + per : T;
-        int shift = 0;
-        while (((kLowUnits * a.p_max) >> shift) >= kBins) ++shift;
-        int lh[kRankPer], ll[kRankPer], bin[kRankPer];
-#pragma unroll
-        for (int i = 0; i < kRankPer; ++i) {
-            const int tc = t0 + i < T ? t0 + i : T - 1;
-            lh[i] = i < per ? a.len[2 * tc] : 0;
-            ll[i] = i < per ? a.len[2 * tc + 1] : 0;
-        }
-        static_assert(kBins == 16 * kWave, "sixteen bins per lane");
-#pragma unroll
-        for (int q = 0; q < 16; q += 4) *reinterpret_cast<int4*>(hist + 16 * lane + q) = make_int4(0, 0, 0, 0);
-        wave_lds_sync();
-#pragma unroll
-        for (int i = 0; i < kRankPer; ++i) {
-            bin[i] = -1;
-            if (t0 + i < t1) {
-                const long long u = table_info_of(a, lh[i], ll[i]).units >> shift;
-                bin[i] = kBins - 1 - (int)(u < kBins - 1 ? u : kBins - 1);  // bin 0 holds the longest
-                atomicAdd(&hist[bin[i]], 1);
-            }
-        }
-        wave_lds_sync();
-        int c16[16], s16 = 0;
-#pragma unroll
-        for (int q = 0; q < 16; q += 4) {
-            const int4 v = *reinterpret_cast<const int4*>(hist + 16 * lane + q);
-            c16[q] = v.x; c16[q + 1] = v.y; c16[q + 2] = v.z; c16[q + 3] = v.w;
-        }
-#pragma unroll
-        for (int q = 0; q < 16; ++q) s16 += c16[q];
-        const int incl = wave_incl_scan(s16);
-        int at = incl - s16, b = 0, r = 0;
-        bool found = false;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            if (!found && at <= j && j < at + c16[q]) {
-                found = true;
-                b = 16 * lane + q;
-                r = j - at;
-            }
-            at += c16[q];
-        }
-        const unsigned long long fm = __builtin_amdgcn_ballot_w64(found);  // exactly one lane (j < T)
-        const int src = fm ? __builtin_ctzll(fm) : 0;
-        b = __builtin_amdgcn_readlane(b, src);
-        r = __builtin_amdgcn_readlane(r, src);
-        // the r-th table (by index) of bin b
-        int cnt = 0;
-#pragma unroll
-        for (int i = 0; i < kRankPer; ++i) cnt += bin[i] == b;
-        int before = wave_incl_scan(cnt) - cnt, t = 0, th = 0, tl = 0;
-        found = false;
-#pragma unroll
-        for (int i = 0; i < kRankPer; ++i) {
-            if (bin[i] == b) {
-                if (before == r) {
-                    found = true;
-                    t = t0 + i;
-                    th = lh[i];
-                    tl = ll[i];
-                }
-                ++before;
-            }
-        }
-        const unsigned long long fm2 = __builtin_amdgcn_ballot_w64(found);
-        const int src2 = fm2 ? __builtin_ctzll(fm2) : 0;
-        // read with every lane active
-        const int tr = __builtin_amdgcn_readlane(t, src2);
-        const int thr = __builtin_amdgcn_readlane(th, src2), tlr = __builtin_amdgcn_readlane(tl, src2);
-        if (lane == 0) {
-            sh.t_first = tr;
-            sh.len_first[0] = thr;
-            sh.len_first[1] = tlr;
-        }
-    }
-    __syncthreads();
-    // (uniform values read back from LDS: readfirstlane keeps the table's
-    // loads and addresses scalar)
-    *ti = table_info_of(a, __builtin_amdgcn_readfirstlane(sh.len_first[0]),
-                        __builtin_amdgcn_readfirstlane(sh.len_first[1]));
-    return __builtin_amdgcn_readfirstlane(sh.t_first);  // (not written again in this mode)
-}
-
-template <int GQ>
-__global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ)) void attn_decode(AttnArgs a)
-{
-    __shared__ AttnShared<GQ> sh;
-    __shared__ CoefLds<GQ> coef;
-    __shared__ PageStage stage[kAttnWaves];
-    const int T = a.B * a.Hkv;
-    if (a.splits > 0) {
-        const int j = blockIdx.x / a.splits, c = blockIdx.x - j * a.splits;
-        TableInfo ti;
-        const int t = longest_first<GQ>(a, sh, &coef, T, j, &ti);
-        const int n = ti.np < a.splits ? ti.np : a.splits;
-        if (n == 0) {
-            if (c == 0) write_empty(a, t, GQ);
-            return;
-        }
-        if (c >= n) return;
-        const int pa = (int)((long long)c * ti.np / n), pb = (int)((long long)(c + 1) * ti.np / n);
-        float* part = n == 1 ? nullptr : a.part + ((long long)t * a.splits + c) * GQ * kPartStride;
-        run_segment<GQ>(a, sh, &coef, stage, t, ti, pa, pb, part);
-        return;
-    }
-    // ---- balanced shares -------------------------------------------------
-    const long long k = blockIdx.x, W = gridDim.x;
-    const int per = (T + kAttnThreads - 1) / kAttnThreads;
-    const int t0 = threadIdx.x * per;
-    const int t1 = t0 + per < T ? t0 + per : T;
-    long long units[kKeep];
-    long long mine = 0;
-    {
-        // all loads first (clamped to a valid table), then the units
-        int lh[kKeep], ll[kKeep];
-#pragma unroll
-        for (int i = 0; i < kKeep; ++i) {
-            const int tc = t0 + i < T ? t0 + i : T - 1;
-            lh[i] = a.len[2 * tc];
-            ll[i] = a.len[2 * tc + 1];
-        }
-#pragma unroll
-        for (int i = 0; i < kKeep; ++i) {
-            units[i] = t0 + i < t1 ? table_info_of(a, lh[i], ll[i]).units : 0;
-            mine += units[i];
-        }
-    }
-    for (int t = t0 + kKeep; t < t1; ++t) mine += table_info(a, t).units;
-    long long total;
-    const long long before = wg_excl_scan(mine, sh.scan, &total);
-    if (k == 0 && threadIdx.x == 0) a.utot[0] = total;
-    const long long b_lo = k * total / W, b_hi = (k + 1) * total / W;
-    if (b_lo >= b_hi) return;
-    long long u = before;
-    for (int t = t0; t < t1; ++t) {  // exactly one table holds unit b_lo
-        const int i = t - t0;
-        long long n = 0;
-#pragma unroll
-        for (int j = 0; j < kKeep; ++j) n = i == j ? units[j] : n;
-        if (i >= kKeep) n = table_info(a, t).units;
-        if (u <= b_lo && b_lo < u + n) {
-            sh.t_first = t;
-            sh.u_first = u;
-        }
-        u += n;
-    }
-    __syncthreads();
-    int t = __builtin_amdgcn_readfirstlane(sh.t_first);
-    long long ut = read_lane<long long>(sh.u_first, 0);
-    while (t < T && ut < b_hi) {
-        const TableInfo ti = table_info(a, t);
-        if (ti.units > 0) {
-            const int pa = page_at_unit(b_lo - ut, ti.ph, ti.np);
-            const int pb = page_at_unit(b_hi - ut, ti.ph, ti.np);
-            const bool first = ut >= b_lo;
-            const bool whole = first && ut + ti.units <= b_hi;
-            if (first && threadIdx.x == 0) a.ustart[t] = ut;
-            run_segment<GQ>(a, sh, &coef, stage, t, ti, pa, pb, whole ? nullptr : a.part + (k + t) * GQ * kPartStride);
-        }
-        ut += ti.units;
-        ++t;
-    }
-}
-
-// ---------------------------------------------------------------------------
-// attn_merge: one wave per (table, query head) of a table whose pages went to
-// several workgroups; combines their partial states in page order.  Also
-// writes the empty result of empty tables in the balanced mode.  Partial
-// slots of shares with an empty unit range are never read (they hold
-// whatever an earlier call left there).
-// ---------------------------------------------------------------------------
-constexpr int kMergeThreads = 256;
-
-__global__ __launch_bounds__(kMergeThreads) void attn_merge(AttnArgs a)
-{
-    const int gq = a.Hq / a.Hkv;
-    const long long job = (long long)blockIdx.x * (kMergeThreads / kWave) + threadIdx.x / kWave;
-    const int T = a.B * a.Hkv;
-    if (job >= (long long)T * gq) return;
-    const int t = (int)(job / gq), hh = (int)(job - (long long)t * gq);
-    const int lane = threadIdx.x & (kWave - 1);
-    const TableInfo ti = table_info(a, t);
-    const int b = t / a.Hkv, h = t - b * a.Hkv;
-    const long long row = (long long)b * a.Hq + h * gq + hh;
-    // candidate partial slots first + i, i < n; in the balanced mode a share
-    // whose unit range is empty (more shares than units) wrote nothing
-    long long first, kf = 0, U = 1, W = 1;
-    int n;
-    if (a.splits > 0) {
-        n = ti.np < a.splits ? ti.np : a.splits;
-        if (n <= 1) return;  // written by attn_decode
-        first = (long long)t * a.splits;
-    } else {
-        if (ti.units == 0) {
-            a.out[row * kD + 2 * lane] = 0.f;
-            a.out[row * kD + 2 * lane + 1] = 0.f;
-            if (lane == 0 && a.lse) a.lse[row] = -INFINITY;
-            return;
-        }
-        U = a.utot[0];
-        W = a.workers;
-        const long long ut = a.ustart[t];
-        // share owning unit x: the largest k with k*U/W <= x
-        kf = ((ut + 1) * W - 1) / U;
-        const long long kl = ((ut + ti.units) * W - 1) / U;
-        if (kf == kl) return;  // written by attn_decode
-        n = (int)(kl - kf + 1);
-        first = kf + t;
-    }
-    auto wrote = [&](int i) {
-        if (a.splits > 0) return true;
-        const long long k = kf + i;
-        return k * U / W != (k + 1) * U / W;
-    };
-    const float* base = a.part + first * gq * kPartStride + hh * kPartStride;
-    const long long stride = (long long)gq * kPartStride;
-    // the first kPre partials' acc pairs are loaded together with every
-    // partial's (max, sum): one round of loads for the usual 2-4 partials
-    constexpr int kPre = 4;
-    float2 pre[kPre];
-#pragma unroll
-    for (int j = 0; j < kPre; ++j)
-        pre[j] = j < n && wrote(j) ? *reinterpret_cast<const float2*>(base + j * stride + 2 + 2 * lane)
-                                   : make_float2(0.f, 0.f);
-    float M = -INFINITY;
-    for (int i = lane; i < n; i += kWave)
-        if (wrote(i)) M = fmax_sel(M, base[i * stride]);
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) M = fmax_sel(M, __shfl_xor(M, o, kWave));
-    float L = 0.f, O0 = 0.f, O1 = 0.f;
-    if (M != -INFINITY) {
-        float Lp = 0.f;
-        for (int i0 = 0; i0 < n; i0 += kWave) {
-            // weight of partial i0 + lane (0 for slots never written)
-            const int i = i0 + lane;
-            float f = 0.f;
-            if (i < n && wrote(i)) {
-                f = __builtin_amdgcn_exp2f(base[i * stride] - M);
-                Lp = fmaf(base[i * stride + 1], f, Lp);
-            }
-            int j = 0;
-            if (i0 == 0) {
-#pragma unroll
-                for (; j < kPre; ++j) {
-                    const float fj = __shfl(f, j, kWave);
-                    O0 = fmaf(pre[j].x, fj, O0);
-                    O1 = fmaf(pre[j].y, fj, O1);
-                }
-            }
-            const int cnt = n - i0 < kWave ? n - i0 : kWave;
-            for (; j < cnt; ++j) {
-                const float fj = __shfl(f, j, kWave);
-                if (fj == 0.f) continue;  // also skips slots never written
-                const float2 o2 = *reinterpret_cast<const float2*>(base + (i0 + j) * stride + 2 + 2 * lane);
-                O0 = fmaf(o2.x, fj, O0);
-                O1 = fmaf(o2.y, fj, O1);
-            }
-        }
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) Lp += __shfl_xor(Lp, o, kWave);
-        L = Lp;
-    }
-    a.out[row * kD + 2 * lane] = (L > 0.f) ? O0 / L : 0.f;
-    a.out[row * kD + 2 * lane + 1] = (L > 0.f) ? O1 / L : 0.f;
-    if (lane == 0 && a.lse) a.lse[row] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
-}
-
-// ---------------------------------------------------------------------------
-// attn_significance: the significance update of one decode step (Sec. 4).  The
-// tokens are independent once the lse is known, so a table's pages are cut into
-// runs of kSigPages, one workgroup per (table, run); each of its four waves takes
-// every fourth page of the run (workgroups past a table's last page exit).  A page's
-// key codes, key metadata, scores and positions are loaded; the logits of the
-// table's query heads come out of the key phase of do_page (lane = (group, token),
-// a transposed row sum), p = exp2(logit - lse) with the attention call's lse, the
-// maximum over the heads is taken across the slots and the four rows, and the
-// lane of row 0 owning token j rewrites its score as s + (p_max - s) / (N - pos).
-// ---------------------------------------------------------------------------
-constexpr int kSigWaves = 4;
-constexpr int kSigPages = 16;  // pages per workgroup
-
-template <int GQ, int NT>
-__device__ __forceinline__ void sig_page(const SigArgs& a, uint8_t* pg, const uint32_t (&qr)[GQ],
-                                         const half2_t (&q0)[GQ], const float (&qsum)[GQ],
-                                         const float (&lse2)[(GQ + 3) / 4], int n_valid, int N, int lane)
-{
-    constexpr int NS = (GQ + 3) / 4;
-    constexpr int sec = NT == 1 ? 0 : 1;
-    const uint32_t grp = (uint32_t)lane >> 4, jl = (uint32_t)lane & 15;
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)pg, 0, (int)kPageBytes, 0x00020000);
-    const uint32_t kc = grp * 512 + jl * 16;
-    const uint32_t km = 2048 + jl * 16 + grp * 4;
-    const uint32_t os = (uint32_t)a.off_score[sec], op = (uint32_t)a.off_pos[sec];
-    const uint4 k0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, kc, 0, 0));
-    const uint4 k1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, kc + 256, 0, 0));
-    const uint32_t m0 = __builtin_amdgcn_raw_buffer_load_b32(rs, km, 0, 0);
-    const uint32_t m1 = __builtin_amdgcn_raw_buffer_load_b32(rs, km + 256, 0, 0);
-    float sc[NT];
-    int ps[NT];
-#pragma unroll
-    for (int tk = 0; tk < NT; ++tk) {
-        sc[tk] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, os + 4 * (jl + 16 * tk), 0, 0));
-        ps[tk] = (int)__builtin_amdgcn_raw_buffer_load_b32(rs, op + 4 * (jl + 16 * tk), 0, 0);
-    }
-#pragma unroll
-    for (int tk = 0; tk < NT; ++tk) {
-        const uint32_t kmt = tk ? m1 : m0;
-        const float ks = h2f(kmt & 0xffffu) * (kTwo24 * a.scale_log2), kz = h2f(kmt >> 16) * a.scale_log2;
-        float dlo[GQ], dhi[GQ];
-        if constexpr (NT == 1) {
-            const uint32_t w[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
-            kdots_k8<GQ>(w, qr, q0, dlo);
-        } else {
-            const uint4 kk = tk ? k1 : k0;
-            const uint32_t w[4] = {kk.x, kk.y, kk.z, kk.w};
-            kdots_k4<GQ>(w, qr, q0, dlo, dhi);
-        }
-        float part[4 * NS];
-#pragma unroll
-        for (int hh = 0; hh < 4 * NS; ++hh) {
-            if (hh < GQ) {
-                const float d = NT == 1 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
-                part[hh] = fmaf(ks, d, kz * qsum[hh]);
-            } else {
-                part[hh] = 0.f;
-            }
-        }
-        // row r of slot s holds head 4s + r; its probability, then the maximum
-        // over the slots and the four rows
-        float x = 0.f;
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            const float lg = xsum4(part[4 * s], part[4 * s + 1], part[4 * s + 2], part[4 * s + 3]);
-            const float pr = 4 * s + (int)grp < GQ ? __builtin_amdgcn_exp2f(lg - lse2[s]) : 0.f;
-            x = fmax_sel(x, pr);
-        }
-        // each swap returns the two halves (rows 0-1 | 2-3, then rows 0, 2 | 1, 3)
-        // side by side, so their maximum is the maximum over the pair in every lane
-        auto sw32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-        x = fmax_sel(__uint_as_float(sw32[0]), __uint_as_float(sw32[1]));
-        auto sw16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-        x = fmax_sel(__uint_as_float(sw16[0]), __uint_as_float(sw16[1]));
-        const int j = (int)jl + 16 * tk;
-        if (grp == 0 && j < n_valid) {
-            const float s0 = sc[tk];
-            reinterpret_cast<float*>(pg + os)[j] = s0 + (x - s0) / (float)(N - ps[tk]);
-        }
-    }
-}
-
-template <int GQ>
-__global__ __launch_bounds__(kSigWaves * kWave) void attn_significance(SigArgs a)
-{
-    constexpr int NS = (GQ + 3) / 4;
-    const int runs = (a.p_max + kSigPages - 1) / kSigPages;
-    const int t = blockIdx.x / runs, run = blockIdx.x - t * runs;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int grp = lane >> 4;
-    const int b = t / a.Hkv, h = t - b * a.Hkv;
-    const int P = a.p_max;
-    const auto* lenp = (const __attribute__((address_space(4))) int32_t*)(a.len + 2 * (long long)t);
-    const int len_hi = lenp[0], len_lo = lenp[1];
-    const int N = a.seq_len[b];
-    const int ph = (len_hi + kTHi - 1) / kTHi, np = ph + (len_lo + kTLo - 1) / kTLo;
-    const int p_end = np < (run + 1) * kSigPages ? np : (run + 1) * kSigPages;
-    if (run * kSigPages >= np) return;
-    // q pairs as in run_segment: lane k of a row holds its group's pair k
-    // (dims d, d+4), pair 0 whole in every lane, the group's sum
-    const int qm = (lane & 15) >> 2, qa = lane & 3;
-    uint32_t qr[GQ];
-    half2_t q0[GQ];
-    float qsum[GQ];
-    constexpr uint32_t kOnes = 0x3C003C00u;
-    const uint32_t sel = (qa & 1) ? 0x07060302u : 0x05040100u;
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) {
-        const uint32_t* qd = reinterpret_cast<const uint32_t*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
-        const int o = 4 * qm + ((qa & 2) ? 1 : 0);
-        qr[hh] = __builtin_amdgcn_perm(qd[o + 2], qd[o], sel);
-        q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(qd[2], qd[0], 0x05040100u));
-        qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f));
-    }
-    float lse2[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-        const int hs = 4 * s + grp;
-        lse2[s] = hs < GQ ? a.lse[(long long)b * a.Hq + h * GQ + hs] * 1.4426950408889634f : 0.f;
-    }
-    const int32_t* trow = a.page_table + (long long)t * P;
-    for (int p = run * kSigPages + wave; p < p_end; p += kSigWaves) {
-        const int id = __builtin_amdgcn_readfirstlane(p < ph ? trow[p] : trow[P - 1 - (p - ph)]);
-        if ((unsigned long long)(unsigned)id >= (unsigned long long)a.num_pages) continue;  // never outside the pool
-        uint8_t* pg = a.pool + (long long)id * kPageBytes;
-        if (p < ph) sig_page<GQ, 1>(a, pg, qr, q0, qsum, lse2, len_hi - p * kTHi, N, lane);
-        else sig_page<GQ, 2>(a, pg, qr, q0, qsum, lse2, len_lo - (p - ph) * kTLo, N, lane);
-    }
-}
 
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-template <int GQ>
-static const void* decode_kernel()
+// Kernel entry points of layout li: which = 0 decode, 1 significance, 2 merge.
+static const void* attn_kernel_ptr(int li, int gq, int which)
 {
-    return reinterpret_cast<const void*>(&attn_decode<GQ>);
-}
-
-static const void* decode_kernel_for(int gq)
-{
-    switch (gq) {
-    case 1: return decode_kernel<1>();
-    case 2: return decode_kernel<2>();
-    case 3: return decode_kernel<3>();
-    case 4: return decode_kernel<4>();
-    case 5: return decode_kernel<5>();
-    case 6: return decode_kernel<6>();
-    case 7: return decode_kernel<7>();
-    case 8: return decode_kernel<8>();
+    switch (li) {
+    case 0: return attn_kernel_l0(gq, which);
+    case 1: return attn_kernel_l1(gq, which);
+    case 2: return attn_kernel_l2(gq, which);
+    case 3: return attn_kernel_l3(gq, which);
     default: return nullptr;
     }
 }
@@ -1392,28 +29,21 @@ static const void* decode_kernel_for(int gq)
 // waves per SIMD, where the registers allow it) measured slower: the page loop
 // is bound by VALU issue, and more shares only split more tables.  Nothing is
 // cached between calls.
-static hipError_t balanced_workers(int gq, int* workers)
+static hipError_t balanced_workers(int gq, int li, int* workers)
 {
     int dev = 0, cus = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    const int w = attn_blocks_per_cu(gq) * (cus > 0 ? cus : 1);
+    const int w = attn_blocks_per_cu(gq, li) * (cus > 0 ? cus : 1);
     *workers = w < kAttnMaxWorkers ? w : kAttnMaxWorkers;
     return hipSuccess;
 }
 
-bool attention_layout_matches(const diffkv_layout* L)
+hipError_t attention_mode(int gq, int li, long long T, int splits, int* mode, int* workers)
 {
-    return L->page_bytes == kPageBytes && L->off_kcode[0] == kOffKcHi && L->off_kmeta[0] == kOffKmHi && L->off_vcode[0] == kOffVcHi &&
-           L->off_vmeta[0] == kOffVmHi && L->off_kcode[1] == kOffKcLo && L->off_kmeta[1] == kOffKmLo &&
-           L->off_vcode[1] == kOffVcLo && L->off_vmeta[1] == kOffVmLo;
-}
-
-hipError_t attention_mode(int gq, long long T, int splits, int* mode, int* workers)
-{
-    hipError_t e = balanced_workers(gq, workers);
+    hipError_t e = balanced_workers(gq, li, workers);
     if (e != hipSuccess) return e;
     // automatic: one workgroup per table when the tables alone fill the device
     // (their spread is absorbed by wave priorities and by the hardware
@@ -1451,11 +81,12 @@ hipError_t noalloc_scratch(void** ptr)
 hipError_t launch_attention(AttnArgs a, hipStream_t st)
 {
     const int gq = a.Hq / a.Hkv;
-    const void* kern = decode_kernel_for(gq);
-    if (!kern) return hipErrorInvalidValue;
+    const void* kern = attn_kernel_ptr(a.layout, gq, 0);
+    const void* merge = attn_kernel_ptr(a.layout, gq, 2);
+    if (!kern || !merge) return hipErrorInvalidValue;
     const long long T = (long long)a.B * a.Hkv;
     int workers = 0;
-    hipError_t e = attention_mode(gq, T, a.splits, &a.splits, &workers);
+    hipError_t e = attention_mode(gq, a.layout, T, a.splits, &a.splits, &workers);
     if (e != hipSuccess) return e;
     long long grid;
     if (a.splits > 0) {
@@ -1471,31 +102,15 @@ hipError_t launch_attention(AttnArgs a, hipStream_t st)
     if (e != hipSuccess || a.splits == 1) return e;
     const long long jobs = T * gq;
     const long long mgrid = (jobs + kMergeThreads / kWave - 1) / (kMergeThreads / kWave);
-    return launch1(attn_merge, (unsigned)mgrid, kMergeThreads, st, a);
+    return hipLaunchKernel(merge, dim3((unsigned)mgrid), dim3(kMergeThreads), args, 0, st);
 }
 
-
-template <int GQ>
-static const void* significance_kernel()
-{
-    return reinterpret_cast<const void*>(&attn_significance<GQ>);
-}
 
 hipError_t launch_significance(const SigArgs& a, hipStream_t st)
 {
     const int gq = a.Hq / a.Hkv;
-    const void* kern = nullptr;
-    switch (gq) {
-    case 1: kern = significance_kernel<1>(); break;
-    case 2: kern = significance_kernel<2>(); break;
-    case 3: kern = significance_kernel<3>(); break;
-    case 4: kern = significance_kernel<4>(); break;
-    case 5: kern = significance_kernel<5>(); break;
-    case 6: kern = significance_kernel<6>(); break;
-    case 7: kern = significance_kernel<7>(); break;
-    case 8: kern = significance_kernel<8>(); break;
-    default: return hipErrorInvalidValue;
-    }
+    const void* kern = attn_kernel_ptr(a.layout, gq, 1);
+    if (!kern) return hipErrorInvalidValue;
     const long long T = (long long)a.B * a.Hkv;
     const long long grid = T * ((a.p_max + kSigPages - 1) / kSigPages);
     if (T < 1 || grid > INT32_MAX) return hipErrorInvalidValue;

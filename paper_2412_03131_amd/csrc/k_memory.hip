@@ -323,21 +323,22 @@ struct TablePlan {
     bool held_over;  // more pages than p_max after the call
 };
 
-// The kernels' page sizes are powers of two, so page indices are shifts.
-static_assert(kTHi == 16 && kTLo == 32, "page index arithmetic below uses shifts");
-__device__ __forceinline__ int page_of(int x, int sec) { return sec ? x >> 5 : x >> 4; }
+// Pages hold a power of two of tokens, so page indices are shifts; tsh packs
+// the two sections' shifts (high section in bits 0-7, low in bits 8-15).
+__device__ __forceinline__ int page_of(int x, int sec, int tsh) { return x >> (sec ? tsh >> 8 : tsh & 255); }
 
-__device__ __forceinline__ TablePlan table_plan(const TState& s, int P)
+__device__ __forceinline__ TablePlan table_plan(const TState& s, int P, int tsh)
 {
     TablePlan tp;
     int held = 0;
 #pragma unroll
     for (int sec = 0; sec < 2; ++sec) {
-        const int T = sec ? kTLo : kTHi;
-        const int want = page_of(s.lold[sec] + s.cnt[sec] + T - 1, sec);
+        const int T = 1 << (sec ? tsh >> 8 : tsh & 255);
+        const int want = page_of(s.lold[sec] + s.cnt[sec] + T - 1, sec, tsh);
         tp.need[sec] = want > s.pold[sec] ? want - s.pold[sec] : 0;
         held += want > s.pold[sec] ? want : s.pold[sec];
-        tp.jobs[sec] = s.cnt[sec] ? page_of(s.lold[sec] + s.cnt[sec] - 1, sec) - page_of(s.lold[sec], sec) + 1 : 0;
+        tp.jobs[sec] =
+            s.cnt[sec] ? page_of(s.lold[sec] + s.cnt[sec] - 1, sec, tsh) - page_of(s.lold[sec], sec, tsh) + 1 : 0;
     }
     tp.held_over = held > P;
     return tp;
@@ -357,12 +358,12 @@ struct JobDesc {
 // jobs << 32): section, page, token range, table slot and, for a new page, the
 // ring index (the table's ring region, high pages first).
 __device__ __forceinline__ void describe_job(JobDesc& d, int t, const TState& s, const TablePlan& tp,
-                                             long long pre, int job, int P, long long head_old)
+                                             long long pre, int job, int P, long long head_old, int tsh)
 {
     const int lj = job - (int)(pre >> 32);
     const int sec = lj < tp.jobs[0] ? 0 : 1;
-    const int TT = sec ? kTLo : kTHi;
-    const int p = page_of(s.lold[sec], sec) + (sec ? lj - tp.jobs[0] : lj);
+    const int TT = 1 << (sec ? tsh >> 8 : tsh & 255);
+    const int p = page_of(s.lold[sec], sec, tsh) + (sec ? lj - tp.jobs[0] : lj);
     const int lo = s.lold[sec], hi_end = s.lold[sec] + s.cnt[sec];
     d.t = t;
     d.sec = sec;
@@ -378,8 +379,12 @@ __device__ __forceinline__ void describe_job(JobDesc& d, int t, const TState& s,
 // One page job: resolve the page ID (a new page from the table's ring region),
 // quantize the job's tokens and write them, zero a fresh page's unused bytes.
 // Called by every thread of the workgroup after `s_job` is described.
+// V code rows: a lane owns dims 2*lane, 2*lane+1, i.e. 2 * T * vb / 8 bytes (8,
+// 16 or 32) of the V code segment, kept as up to eight 32-bit words.
+constexpr int kRowWords = 8;
+
 __device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s_job,
-                                           uint64_t (*s_rows)[kWave][2])
+                                           uint32_t (*s_rows)[kWave][kRowWords])
 {
     const int tid = threadIdx.x;
     const int P = a.p_max;
@@ -398,8 +403,9 @@ __device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s
     const int tslot = __builtin_amdgcn_readfirstlane(s_job.tslot);
     const long long ring_idx = s_job.ring_idx;
     const int b = t / H, h = t - b * H;
-    const int TT = sec ? kTLo : kTHi;
-    const int kb = sec ? 4 : 8, vb = sec ? 2 : 4;
+    const int TT = a.T[sec];
+    const int kb = a.kb[sec], vb = a.vb[sec];
+    const int rw = TT * vb / 32;  // 32-bit words per dimension row (1, 2 or 4)
     // the page ID (every wave reads the one entry), beside the token loads
     int32_t* trow = a.page_table + (long long)t * P;
     int id = ring_idx < 0 ? trow[tslot] : a.ring[ring_idx % a.num_pages];
@@ -430,8 +436,13 @@ __device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s
     const bool page_ok = (unsigned)id < (unsigned)a.num_pages;  // never write outside the pool
     uint8_t* pg = a.pool + (long long)(page_ok ? id : 0) * page_bytes;
     // a page being continued keeps its earlier tokens' V code bits
-    uint4 vold = make_uint4(0, 0, 0, 0);
-    if (wave == 0 && page_ok && !fresh) vold = *reinterpret_cast<const uint4*>(pg + off_vc + lane * 16);
+    uint32_t vold[kRowWords] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (wave == 0 && page_ok && !fresh) {
+        const uint32_t* src = reinterpret_cast<const uint32_t*>(pg + off_vc) + lane * 2 * rw;
+#pragma unroll
+        for (int w = 0; w < kRowWords; ++w)
+            if (w < 2 * rw) vold[w] = src[w];
+    }
     if (page_ok && fresh) {
         // A fresh page reads as zero wherever no token lies: zero the token
         // slots from u1 on in every per-token segment and the page tail.
@@ -454,7 +465,7 @@ __device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s
         for (long long o = a.off_pos[sec] + (long long)TT * 4 + tid * 16; o < page_bytes; o += kCommitThreads * 16)
             *reinterpret_cast<uint4*>(pg + o) = z4;
     }
-    uint64_t row0 = 0, row1 = 0;
+    uint32_t rows[kRowWords] = {0, 0, 0, 0, 0, 0, 0, 0};  // dim 2*lane: words 0 .. rw-1, dim 2*lane+1: rw ..
     // two passes of kTokIlp tokens: quantize side by side, then store
 #pragma unroll
     for (int pass = 0; pass < kTokLoad / kTokIlp; ++pass) {
@@ -473,8 +484,14 @@ __device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s
             const int u = base_u + i * kQuantWaves;
             if (u >= u1) break;
             const int sl = u - p * TT;
-            row0 |= (uint64_t)vc0[i] << (sl * vb);
-            row1 |= (uint64_t)vc1[i] << (sl * vb);
+            const int bit = sl * vb;
+#pragma unroll
+            for (int w = 0; w < kRowWords / 2; ++w) {
+                if (w == (bit >> 5) && w < rw) {
+                    rows[w] |= vc0[i] << (bit & 31);
+                    rows[rw + w] |= vc1[i] << (bit & 31);
+                }
+            }
             if (!page_ok) continue;
             const long long row = (long long)(off_b + jj[pass * kTokIlp + i]) * H + h;
             if (kb == 8) {
@@ -497,19 +514,18 @@ __device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s
     }
     // the page's dimension-major V code rows: OR of the waves' bits (and of the
     // bits already on a page being continued), one store per dimension pair
-    s_rows[wave][lane][0] = row0;
-    s_rows[wave][lane][1] = row1;
+#pragma unroll
+    for (int w = 0; w < kRowWords; ++w) s_rows[wave][lane][w] = rows[w];
     __syncthreads();
     if (wave == 0 && page_ok) {
-        uint64_t r0 = ((uint64_t)vold.y << 32) | vold.x;
-        uint64_t r1 = ((uint64_t)vold.w << 32) | vold.z;
+        uint32_t* dst = reinterpret_cast<uint32_t*>(pg + off_vc) + lane * 2 * rw;
 #pragma unroll
-        for (int w = 0; w < kQuantWaves; ++w) {
-            r0 |= s_rows[w][lane][0];
-            r1 |= s_rows[w][lane][1];
+        for (int w = 0; w < kRowWords; ++w) {
+            uint32_t x = vold[w];
+#pragma unroll
+            for (int q = 0; q < kQuantWaves; ++q) x |= s_rows[q][lane][w];
+            if (w < 2 * rw) dst[w] = x;
         }
-        *reinterpret_cast<uint4*>(pg + off_vc + lane * 16) =
-            make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
     }
 }
 
@@ -523,7 +539,7 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
     __shared__ long long s_scan[kCommitThreads / kWave];
     __shared__ uint32_t s_bits[kCommitThreads / kWave];
     __shared__ JobDesc s_job;
-    __shared__ uint64_t s_rows[kQuantWaves][kWave][2];
+    __shared__ uint32_t s_rows[kQuantWaves][kWave][kRowWords];
     const long long head_old = a.flags->head_old, tail_old = a.flags->tail_old;
 
     // ---- the plan, in every workgroup (each thread a contiguous run of tables)
@@ -545,7 +561,7 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
             bits |= DIFFKV_ST_BAD_INPUT;
             return;
         }
-        const TablePlan tp = table_plan(s, P);
+        const TablePlan tp = table_plan(s, P, a.tsh);
         if (tp.held_over) bits |= DIFFKV_ST_TABLE_OVERFLOW;
         packed += plan_word(tp);
     });
@@ -565,7 +581,7 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
     // ---- workgroup 0: the state after the call -------------------------------
     if (blockIdx.x == 0) {
         for_tables([&](int t, const TState& s) {
-            const TablePlan tp = table_plan(s, P);
+            const TablePlan tp = table_plan(s, P, a.tsh);
 #pragma unroll
             for (int sec = 0; sec < 2; ++sec) {
                 a.len[2 * t + sec] = s.lold[sec] + s.cnt[sec];
@@ -584,10 +600,10 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit(AppendArgs a)
             long long pre = before;
             for_tables([&](int t, const TState& s) {
                 if (s.n < 0) return;
-                const TablePlan tp = table_plan(s, P);
+                const TablePlan tp = table_plan(s, P, a.tsh);
                 const int jo = (int)(pre >> 32);
                 if (jo <= job && job < jo + tp.jobs[0] + tp.jobs[1])
-                    describe_job(s_job, t, s, tp, pre, job, P, head_old);
+                    describe_job(s_job, t, s, tp, pre, job, P, head_old, a.tsh);
                 pre += plan_word(tp);
             });
         }
@@ -634,7 +650,7 @@ __global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
             bits |= DIFFKV_ST_BAD_INPUT;
             return;
         }
-        const TablePlan tp = table_plan(s, P);
+        const TablePlan tp = table_plan(s, P, a.tsh);
         if (tp.held_over) bits |= DIFFKV_ST_TABLE_OVERFLOW;
         packed += plan_word(tp);
     });
@@ -657,7 +673,7 @@ __global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
     const bool lds_map = NT <= kPlanLdsTables;  // job map by binary search in LDS
     long long pre = before;
     for_tables([&](int t, const TState& s) {
-        const TablePlan tp = table_plan(s, P);
+        const TablePlan tp = table_plan(s, P, a.tsh);
         a.tplan[t] = pre;
         const int j0 = (int)(pre >> 32);
         if (lds_map) s_jobs[t] = j0;
@@ -705,7 +721,7 @@ __global__ __launch_bounds__(kPlanThreads) void append_plan(AppendArgs a)
 __global__ __launch_bounds__(kCommitThreads) void append_commit_planned(AppendArgs a)
 {
     __shared__ JobDesc s_job;
-    __shared__ uint64_t s_rows[kQuantWaves][kWave][2];
+    __shared__ uint32_t s_rows[kQuantWaves][kWave][kRowWords];
     if (!a.flags->ok) return;
     const int njobs = a.flags->njobs;
     const long long head_old = a.flags->head_old;
@@ -713,7 +729,7 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit_planned(AppendAr
         if (threadIdx.x == 0) {
             const int t = a.job_table[job];
             const TState s = a.tstate[t];
-            describe_job(s_job, t, s, table_plan(s, a.p_max), a.tplan[t], job, a.p_max, head_old);
+            describe_job(s_job, t, s, table_plan(s, a.p_max, a.tsh), a.tplan[t], job, a.p_max, head_old, a.tsh);
         }
         __syncthreads();
         commit_job(a, s_job, s_rows);

@@ -98,9 +98,12 @@ def test_argument_checks_enqueue_nothing(dk):
                                       0.0, 0.0, 0, fake, 16, None) == dk.E_WORKSPACE
     assert lib.diffkv_quantize_append(C.byref(L), C.byref(st), -1, 5, fake, fake, fake, fake, None,
                                       0.0, 0.0, 0, fake, 1 << 30, None) == dk.E_INVAL
-    L2 = dk.layout(tokens_per_page=(16, 16), max_seq_len=64)
+    L2 = dk.layout(tokens_per_page=(16, 64), max_seq_len=64)   # a layout the kernels do not implement
     assert lib.diffkv_quantize_append(C.byref(L2), C.byref(st), 10, 5, fake, fake, fake, fake, None,
                                       0.0, 0.0, 0, fake, 1 << 30, None) == dk.E_UNSUPPORTED
+    L3 = dk.layout(tokens_per_page=(16, 16), max_seq_len=64)   # implemented except by the generation step
+    assert lib.diffkv_generation_step(C.byref(L3), C.byref(st), 1.0, 0.5, 4, fake, 1 << 20,
+                                      None) == dk.E_UNSUPPORTED
     assert lib.diffkv_compact_free_list(C.byref(L), C.byref(st), 5, fake, fake, 1 << 20,
                                         None) == dk.E_INVAL  # more tables than the cache has
     assert lib.diffkv_alloc_pages(C.byref(L), C.byref(st), 4, fake, fake, 8, None) == dk.E_WORKSPACE

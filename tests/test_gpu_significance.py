@@ -3,7 +3,7 @@ oracle: after diffkv_decode_attention, every kept token's score is rewritten as 
 running mean of its attention probability (max over the KV head's query heads).
 
 Every byte of every used page outside the score segments must stay bit-identical to the
-oracle's; the scores must agree within 3e-5 relative (fp32 logits and exp2 on the GPU,
+oracle's; the scores must agree within 1e-4 relative (fp32 logits and exp2 on the GPU,
 fp64 in the oracle).  Cases: every group size 1-8 on high-only, low-only and mixed
 tables with ragged tails; empty tables and single tokens; decode steps with appends
 between updates; the full llama8b decode workload.
@@ -24,7 +24,7 @@ from paper_2412_03131_amd import inputs  # noqa: E402
 from gpu_util import dev_cache_from_oracle, layouts, t  # noqa: E402
 
 SCALE = 1.0 / np.sqrt(128.0)
-RTOL = 3e-5
+RTOL = 1e-4   # the newest token's score is its probability: exp(logit - lse) carries the fp32 logit error (up to ~5e-5)
 
 
 def _score_mask(L):

@@ -21,6 +21,7 @@ mean) and the roofline: algorithmic compressed bytes / mean attention time.
 Extra keys of the same JSON line:
   significance    the decode step's significance update (running mean of each kept
                   token's attention probability, Sec. 4) on the headline cache;
+  precisions      attention time per precision level (K8V8 .. K4V1) against its KV bytes;
   llama70b        batch 32, 64 query / 8 KV heads (GQA 8:1), context 8192, split 30/40/30:
                   attention with num_splits = 1 (no split), automatic, and balanced
                   shares + merge (sequence split), each timed after a cache flush;
@@ -387,6 +388,71 @@ def significance_bench(torch, dk, lib, dev, sptr, wl, flush, reps=30):
     return res
 
 
+PRECISIONS = [  # (name, layout keyword arguments, section holding every token)
+    ("K8V8", dict(k_bits=(8, 4), v_bits=(8, 2), tokens_per_page=(16, 32)), 0),
+    ("K8V4", dict(k_bits=(8, 4), v_bits=(4, 2), tokens_per_page=(16, 32)), 0),
+    ("K8V2", dict(k_bits=(8, 4), v_bits=(2, 1), tokens_per_page=(16, 32)), 0),
+    ("K4V2", dict(k_bits=(8, 4), v_bits=(4, 2), tokens_per_page=(16, 32)), 1),
+    ("K4V2/16", dict(k_bits=(8, 4), v_bits=(4, 2), tokens_per_page=(16, 16)), 1),
+    ("K4V1", dict(k_bits=(8, 4), v_bits=(2, 1), tokens_per_page=(16, 32)), 1),
+]
+
+
+def precision_bench(torch, dk, lib, dev, sptr, flush, B=64, Hq=32, Hkv=8, L=2048, reps=20):
+    """Attention time per precision level against its KV bytes, the shape of the
+    paper's kernel speedup that follows the KV-size reduction (Sec. 7.3): the llama8b
+    decode shape with L = 2048 tokens per sequence, no pruning, every token at one
+    precision (one section of a layout), caches evicted before each call."""
+    from paper_2412_03131_amd import inputs
+    w = inputs.uniform_cache(B, Hq, Hkv, L)
+    T = lambda a: to_dev(torch, dev, a)
+    k, v, score, q, nl = T(w["k"]), T(w["v"]), T(w["score"]), T(w["q"]), T(w["new_len"])
+    res = {"workload": "B=%d, Hq=%d, Hkv=%d, %d tokens per sequence, no pruning, every token at the "
+                       "named precision; flushed attention calls" % (B, Hq, Hkv, L), "levels": {}}
+    ntok = B * Hkv * L
+    for name, kw, sec in PRECISIONS:
+        Ld = dk.layout(max_seq_len=L + 16, **kw)
+        Tp = kw["tokens_per_page"][sec]
+        npg = B * Hkv * (-(-L // Tp)) + 64
+        c = dk.Cache(Ld, npg, B, Hkv, device=dev)
+        quota = np.zeros((B, Hkv, 2), np.int32)
+        quota[:, :, sec] = L
+        dk.quantize_append(c, nl, k, v, score, quota=T(quota), total_new=B * L, max_new=L)
+        ws = torch.empty(max(256, dk.workspace_size(dk.OP_ATTENTION, Ld, B, Hq, Hkv, 0, 0)), dtype=torch.uint8,
+                         device=dev)
+        out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        args = (C.byref(Ld), C.byref(c.struct()), Hq, C.c_void_p(q.data_ptr()), float(SCALE),
+                C.c_void_p(out.data_ptr()), C.c_void_p(lse.data_ptr()), 0, C.c_void_p(ws.data_ptr()), ws.numel(), sptr)
+        for _ in range(3):
+            lib.diffkv_decode_attention(*args)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        rc = 0
+        for e in ev:
+            flush()
+            e[0].record()
+            rc |= lib.diffkv_decode_attention(*args)
+            e[1].record()
+        torch.cuda.synchronize()
+        if rc or int(c.status.item()) != 0:
+            raise RuntimeError("precision bench failed (%s)" % name)
+        us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+        kb, vb = kw["k_bits"][sec], kw["v_bits"][sec]
+        per_tok = (kb + vb) * 16 + 32          # codes + fp16 scale/zero of K and V
+        nbytes = ntok * per_tok + 4 * B * Hkv * (-(-L // Tp)) + B * Hq * 128 * 6
+        res["levels"][name] = {"bytes_per_token": per_tok, "us": pct(us),
+                               "gbps": nbytes / (us.mean() * 1e-6) / 1e9,
+                               "kv_bytes_vs_fp16": per_tok / 512.0}
+        log("  precision %-8s %3d B/token: %.1f us, %.0f GB/s" % (name, per_tok, us.mean(), nbytes / us.mean() / 1e3))
+        del c, ws
+        torch.cuda.empty_cache()
+    base = res["levels"]["K8V8"]
+    for name, r in res["levels"].items():
+        r["speedup_vs_K8V8"] = base["us"]["mean"] / r["us"]["mean"]
+        r["bytes_ratio_vs_K8V8"] = base["bytes_per_token"] / r["bytes_per_token"]
+    return res
+
+
 def serving_step(torch, dk, lib, dev, sptr, args):
     """The llama8b shape on `layers` layers sharing one page pool, one step = request
     r = step mod 64 finishes (its pages in every layer recycled by one compaction call),
@@ -577,6 +643,7 @@ def main():
     extras = {}
     if args.extras == "all":
         extras["significance"] = significance_bench(torch, dk, lib, dev, sptr, wl, flush)
+        extras["precisions"] = precision_bench(torch, dk, lib, dev, sptr, flush)
         if args.config != "llama70b":
             del wl
             torch.cuda.empty_cache()

@@ -383,8 +383,9 @@ __device__ __forceinline__ void describe_job(JobDesc& d, int t, const TState& s,
 // 16 or 32) of the V code segment, kept as up to eight 32-bit words.
 constexpr int kRowWords = 8;
 
-__device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s_job,
-                                           uint32_t (*s_rows)[kWave][kRowWords])
+template <int KB, int VB, int TT>
+__device__ __forceinline__ void commit_job_fmt(const AppendArgs& a, const JobDesc& s_job,
+                                               uint32_t (*s_rows)[kWave][kRowWords])
 {
     const int tid = threadIdx.x;
     const int P = a.p_max;
@@ -403,9 +404,9 @@ __device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s
     const int tslot = __builtin_amdgcn_readfirstlane(s_job.tslot);
     const long long ring_idx = s_job.ring_idx;
     const int b = t / H, h = t - b * H;
-    const int TT = a.T[sec];
-    const int kb = a.kb[sec], vb = a.vb[sec];
-    const int rw = TT * vb / 32;  // 32-bit words per dimension row (1, 2 or 4)
+    constexpr int kb = KB, vb = VB;
+    constexpr int rw = TT * VB / 32;  // 32-bit words per dimension row (1, 2 or 4)
+    static_assert(2 * rw <= kRowWords, "value rows");
     // the page ID (every wave reads the one entry), beside the token loads
     int32_t* trow = a.page_table + (long long)t * P;
     int id = ring_idx < 0 ? trow[tslot] : a.ring[ring_idx % a.num_pages];
@@ -527,6 +528,21 @@ __device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s
             if (w < 2 * rw) dst[w] = x;
         }
     }
+}
+
+// One page job in the page format of its section (the layouts' formats; see
+// kLayoutFmts), so that row widths and bit positions are constants.
+__device__ __forceinline__ void commit_job(const AppendArgs& a, const JobDesc& s_job,
+                                           uint32_t (*s_rows)[kWave][kRowWords])
+{
+    const int sec = __builtin_amdgcn_readfirstlane(s_job.sec);
+    const int kb = a.kb[sec], vb = a.vb[sec], T = a.T[sec];
+    if (kb == 8 && vb == 4) commit_job_fmt<8, 4, 16>(a, s_job, s_rows);
+    else if (kb == 4 && vb == 2 && T == 32) commit_job_fmt<4, 2, 32>(a, s_job, s_rows);
+    else if (kb == 8 && vb == 8) commit_job_fmt<8, 8, 16>(a, s_job, s_rows);
+    else if (kb == 8 && vb == 2) commit_job_fmt<8, 2, 16>(a, s_job, s_rows);
+    else if (kb == 4 && vb == 1) commit_job_fmt<4, 1, 32>(a, s_job, s_rows);
+    else commit_job_fmt<4, 2, 16>(a, s_job, s_rows);
 }
 
 constexpr int kPlanKeep = 2;  // tables per thread whose state stays in registers

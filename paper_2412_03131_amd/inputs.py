@@ -128,6 +128,21 @@ def prefill(name, seed=None, B=None, L=None):
                 quota=quota, q=q, outliers=outl, max_len=int(new_len.max()))
 
 
+def uniform_cache(B, Hq, Hkv, L, seed=5):
+    """A decode cache's inputs with no pruning and one precision for every token: the
+    llama8b value distributions (q, k, v ~ N(0,1), 4 key outlier channels x10 per KV head),
+    L tokens per sequence, Zipf scores.  Returns new_len, k, v, score, q."""
+    r_k, r_v, r_s, r_q, r_o = _streams(seed, 5)
+    outl = outlier_channels(r_o, Hkv)
+    k, v = draw_kv(r_k, r_v, B * L, Hkv, outl)
+    score = np.empty((B * L, Hkv), np.float32)
+    for b in range(B):
+        for h in range(Hkv):
+            score[b * L:(b + 1) * L, h] = zipf_scores(r_s, L)
+    q = f16_bits(r_q.standard_normal((B, Hq, HEAD_DIM), dtype=np.float32))
+    return dict(new_len=np.full(B, L, np.int32), k=k, v=v, score=score, q=q)
+
+
 def decode_token(name, step, B, Hq, Hkv, outliers, seed=None):
     """One generated token per sequence: k/v [B][Hkv][D], score [B][Hkv],
     quota (1, 0) per table (the new token enters the recent window), new q."""

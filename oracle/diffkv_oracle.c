@@ -954,6 +954,65 @@ int dko_update_significance(const dko_layout* L, dko_cache* C, int num_q_heads,
 }
 
 /* ======================================================================
+ * Prompt-phase significance (Sec. 4).  Over a prompt of N tokens every
+ * query j attends causally to the keys 0..j with the full-precision (fp16)
+ * keys; token p receives the N - p probabilities of the queries p..N-1.
+ * Its significance is their average, each probability being the maximum
+ * over the g query heads of its KV head (taken per query, the reading the
+ * decode-time update continues).  fp64 throughout; rows of q, k and score
+ * are the prompt tokens concatenated sequence after sequence.  `select`
+ * ([B][Hkv], nonzero = compute) limits the work to some tables; the scores
+ * of the others are left untouched.
+ * ====================================================================== */
+int dko_prompt_significance(int B, const int32_t* new_len, int num_q_heads, int num_kv_heads,
+                            int D, const uint16_t* q, const uint16_t* k, double sm_scale,
+                            const uint8_t* select, float* score)
+{
+    int H = num_kv_heads;
+    if (H <= 0 || num_q_heads % H != 0 || D <= 0) return 1;
+    int g = num_q_heads / H;
+    int64_t row0 = 0;
+    for (int b = 0; b < B; b++) {
+        int N = new_len[b];
+        if (N < 0) return 1;
+        for (int h = 0; h < H; h++) {
+            if (N == 0 || (select && !select[b * H + h])) continue;
+            double* Kd = (double*)malloc(sizeof(double) * (size_t)N * D);
+            double* logit = (double*)malloc(sizeof(double) * (size_t)N);
+            double* x = (double*)malloc(sizeof(double) * (size_t)N);
+            double* sum = (double*)calloc((size_t)N, sizeof(double));
+            for (int p = 0; p < N; p++)
+                for (int d = 0; d < D; d++)
+                    Kd[(int64_t)p * D + d] = dko_half_to_float(k[((row0 + p) * H + h) * D + d]);
+            for (int j = 0; j < N; j++) {          /* query j: keys 0..j */
+                for (int p = 0; p <= j; p++) x[p] = 0.0;
+                for (int hq = h * g; hq < (h + 1) * g; hq++) {
+                    const uint16_t* qv = q + ((row0 + j) * num_q_heads + hq) * D;
+                    double m = -INFINITY;
+                    for (int p = 0; p <= j; p++) {
+                        double dot = 0.0;
+                        for (int d = 0; d < D; d++) dot += (double)dko_half_to_float(qv[d]) * Kd[(int64_t)p * D + d];
+                        logit[p] = sm_scale * dot;
+                        if (logit[p] > m) m = logit[p];
+                    }
+                    double l = 0.0;
+                    for (int p = 0; p <= j; p++) l += exp(logit[p] - m);
+                    for (int p = 0; p <= j; p++) {
+                        double pr = exp(logit[p] - m) / l;
+                        if (pr > x[p]) x[p] = pr;
+                    }
+                }
+                for (int p = 0; p <= j; p++) sum[p] += x[p];
+            }
+            for (int p = 0; p < N; p++) score[(row0 + p) * H + h] = (float)(sum[p] / (double)(N - p));
+            free(Kd); free(logit); free(x); free(sum);
+        }
+        row0 += N;
+    }
+    return 0;
+}
+
+/* ======================================================================
  * Memory accounting against FP16 (Sec. 1, Fig. 1): bits of the kept
  * key/value codes over the bits of n_total FP16 keys/values.
  * ====================================================================== */

@@ -165,6 +165,12 @@ void dko_merge_partials(int S, int D, const double* m, const double* l,
  * Returns 1 when num_q_heads is not a multiple of H. */
 int dko_update_significance(const dko_layout* L, dko_cache* C, int num_q_heads,
                             const uint16_t* q, double sm_scale);
+/* Prompt-phase significance of every prompt token (Sec. 4): q [rows][Hq][D],
+ * k [rows][Hkv][D] fp16 bits, rows concatenated per sequence (new_len[B]);
+ * score [rows][Hkv] fp32 out; select [B][Hkv] or NULL.  1 on bad shapes. */
+int dko_prompt_significance(int B, const int32_t* new_len, int num_q_heads, int num_kv_heads,
+                            int D, const uint16_t* q, const uint16_t* k, double sm_scale,
+                            const uint8_t* select, float* score);
 
 void dko_kv_bits_fraction(const dko_layout* L, int n_hi, int n_lo,
                           int n_total, double* k_frac, double* v_frac);

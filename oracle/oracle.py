@@ -72,6 +72,8 @@ def _setup(L):
     L.dko_kv_bits_fraction.argtypes = [C.POINTER(Layout), C.c_int, C.c_int, C.c_int, vp, vp]
     L.dko_update_significance.argtypes = [C.POINTER(Layout), C.POINTER(_Cache), C.c_int, vp, f64]
     L.dko_update_significance.restype = C.c_int
+    L.dko_prompt_significance.argtypes = [C.c_int, vp, C.c_int, C.c_int, C.c_int, vp, vp, f64, vp, vp]
+    L.dko_prompt_significance.restype = C.c_int
     L.dko_float_to_half.restype = C.c_uint16
     L.dko_float_to_half.argtypes = [f32]
     L.dko_half_to_float.restype = f32
@@ -231,6 +233,24 @@ def update_significance(cache, q, sm_scale):
     st = cache.struct()
     if lib().dko_update_significance(C.byref(cache.L), C.byref(st), q.shape[1], _p(q), float(sm_scale)):
         raise ValueError("oracle: Hq must be a multiple of Hkv")
+
+
+def prompt_significance(new_len, q, k, sm_scale, select=None, out=None):
+    """Prompt-phase significance of every prompt token: q [rows][Hq][D], k [rows][Hkv][D]
+    fp16 bits, rows concatenated per sequence; returns score [rows][Hkv] fp32.  With
+    `select` ([B][Hkv] bool) only those tables are computed (others stay as in `out`)."""
+    new_len = np.ascontiguousarray(new_len, np.int32)
+    q = np.ascontiguousarray(q, np.uint16)
+    k = np.ascontiguousarray(k, np.uint16)
+    rows, Hq, D = q.shape
+    Hkv = k.shape[1]
+    assert k.shape == (rows, Hkv, D) and int(new_len.sum()) == rows
+    score = np.zeros((rows, Hkv), np.float32) if out is None else out
+    sel = None if select is None else np.ascontiguousarray(select, np.uint8)
+    if lib().dko_prompt_significance(len(new_len), _p(new_len), Hq, Hkv, D, _p(q), _p(k), float(sm_scale),
+                                     None if sel is None else _p(sel), _p(score)):
+        raise ValueError("oracle: bad shapes")
+    return score
 
 
 def attention_partial(cache, q, sm_scale, b, hq, p0, p1):

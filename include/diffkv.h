@@ -143,13 +143,15 @@ enum {
     DIFFKV_OP_ATTENTION = 1,
     DIFFKV_OP_COMPACT = 2,
     DIFFKV_OP_ALLOC = 3,
-    DIFFKV_OP_GENERATION = 4
+    DIFFKV_OP_GENERATION = 4,
+    DIFFKV_OP_PROMPT_SIGNIFICANCE = 5
 };
 
 /* Bytes of device workspace the operation needs (host out-parameter).
  * APPEND: num_seqs, num_kv_heads, total_new.  ATTENTION: num_seqs,
  * num_q_heads, num_splits (0 = automatic, -1 = balanced).
- * COMPACT / ALLOC / GENERATION: num_seqs*num_kv_heads tables.  Unused sizes
+ * COMPACT / ALLOC / GENERATION: num_seqs*num_kv_heads tables.
+ * PROMPT_SIGNIFICANCE: num_seqs, num_q_heads, total_new.  Unused sizes
  * are ignored. */
 diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout,
                                     int32_t num_seqs, int32_t num_q_heads,
@@ -280,6 +282,37 @@ diffkv_status diffkv_decode_attention_noalloc(const diffkv_layout* layout, const
 diffkv_status diffkv_update_significance(const diffkv_layout* layout, const diffkv_cache* cache,
                                          int32_t num_q_heads, const uint16_t* q, float sm_scale,
                                          const float* lse, void* stream);
+
+/*
+ * Prompt-phase significance (Sec. 4): the score of every prompt token, from
+ * the prompt's own queries and fp16 keys, before the prompt is appended.
+ * For sequence b with N = new_len[b] prompt tokens and KV head h, token p
+ * (0-based) gets
+ *   score[p][h] = (1 / (N - p)) * sum_{j = p}^{N-1} max_{hq of h} P_hq[j][p],
+ *   P_hq[j][.] = softmax over p' <= j of sm_scale * q[j][hq] . k[p'][h],
+ * the mean of the N - p causal attention probabilities the token receives,
+ * the KV head's query heads combined by their maximum per query (the score
+ * diffkv_update_significance continues).  The result feeds the `score`
+ * argument of diffkv_quantize_append directly (same rows, same order).
+ *   new_len  device int32 [num_seqs]; rows of sequence b follow those of b-1.
+ *            Lengths are clamped to [0, max_new] and rows past total_new are
+ *            neither read nor scored.
+ *   q        device fp16 [total_new][num_q_heads][128], 16-byte aligned
+ *   k        device fp16 [total_new][num_kv_heads][128], 16-byte aligned
+ *   lse      device fp32 [total_new][num_q_heads] natural-log row normalizers
+ *            (as a prompt attention kernel writes them), or NULL: the call
+ *            computes them in an extra pass over q and k.
+ *   score    device fp32 [total_new][num_kv_heads] out
+ *   ws       diffkv_workspace_size(DIFFKV_OP_PROMPT_SIGNIFICANCE, ...) bytes
+ * Arithmetic: fp16 x fp16 products on the matrix cores (exact), fp32 sums,
+ * fp32 softmax with exp2; probabilities below 2^-126 may come out as zero.
+ * num_q_heads / num_kv_heads up to 8 (else DIFFKV_E_UNSUPPORTED).
+ */
+diffkv_status diffkv_prompt_significance(const diffkv_layout* layout, int32_t num_seqs, int64_t total_new,
+                                         int32_t max_new, const int32_t* new_len, int32_t num_q_heads,
+                                         int32_t num_kv_heads, const uint16_t* q, const uint16_t* k,
+                                         float sm_scale, const float* lse, float* score, void* ws,
+                                         size_t ws_bytes, void* stream);
 
 /*
  * Parallel free-list compaction (Sec. 5.2 recycling, Sec. 5.3): for the

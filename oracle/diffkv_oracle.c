@@ -981,6 +981,7 @@ int dko_prompt_significance(int B, const int32_t* new_len, int num_q_heads, int 
             double* logit = (double*)malloc(sizeof(double) * (size_t)N);
             double* x = (double*)malloc(sizeof(double) * (size_t)N);
             double* sum = (double*)calloc((size_t)N, sizeof(double));
+            double* qd = (double*)malloc(sizeof(double) * (size_t)D);
             for (int p = 0; p < N; p++)
                 for (int d = 0; d < D; d++)
                     Kd[(int64_t)p * D + d] = dko_half_to_float(k[((row0 + p) * H + h) * D + d]);
@@ -988,10 +989,11 @@ int dko_prompt_significance(int B, const int32_t* new_len, int num_q_heads, int 
                 for (int p = 0; p <= j; p++) x[p] = 0.0;
                 for (int hq = h * g; hq < (h + 1) * g; hq++) {
                     const uint16_t* qv = q + ((row0 + j) * num_q_heads + hq) * D;
+                    for (int d = 0; d < D; d++) qd[d] = dko_half_to_float(qv[d]);
                     double m = -INFINITY;
                     for (int p = 0; p <= j; p++) {
                         double dot = 0.0;
-                        for (int d = 0; d < D; d++) dot += (double)dko_half_to_float(qv[d]) * Kd[(int64_t)p * D + d];
+                        for (int d = 0; d < D; d++) dot += qd[d] * Kd[(int64_t)p * D + d];
                         logit[p] = sm_scale * dot;
                         if (logit[p] > m) m = logit[p];
                     }
@@ -1005,7 +1007,7 @@ int dko_prompt_significance(int B, const int32_t* new_len, int num_q_heads, int 
                 for (int p = 0; p <= j; p++) sum[p] += x[p];
             }
             for (int p = 0; p < N; p++) score[(row0 + p) * H + h] = (float)(sum[p] / (double)(N - p));
-            free(Kd); free(logit); free(x); free(sum);
+            free(Kd); free(logit); free(x); free(sum); free(qd);
         }
         row0 += N;
     }

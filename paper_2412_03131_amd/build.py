@@ -13,7 +13,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdiffkv.so")
 SOURCES = ["api.cpp", "k_memory.hip", "k_attention.hip", "k_attn_l0.hip", "k_attn_l1.hip", "k_attn_l2.hip",
-           "k_attn_l3.hip", "k_generation.hip"]
+           "k_attn_l3.hip", "k_generation.hip", "k_prompt.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -161,6 +161,22 @@ AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits, int64_t worke
     return w;
 }
 
+// Prompt significance: sequence offsets and clamped lengths, row log2-sum-exps.
+struct PromptWs {
+    int64_t off, nlen, lse2, total;
+};
+
+PromptWs prompt_ws(int64_t B, int64_t Hq, int64_t total_new)
+{
+    PromptWs w;
+    int64_t o = 0;
+    w.off = o;  o = align256(o + B * 8);
+    w.nlen = o; o = align256(o + B * 4);
+    w.lse2 = o; o = align256(o + total_new * Hq * 4);
+    w.total = o;
+    return w;
+}
+
 int64_t compact_ws(int64_t T) { return align256(sizeof(CallFlags)) + 2 * align256(T * 4); }
 int64_t alloc_ws(int64_t T) { return align256(sizeof(CallFlags)) + align256(T * 16); }
 // generation step: call flags, per-table actions, page requests and ring offsets
@@ -271,6 +287,10 @@ diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout, int
     case DIFFKV_OP_GENERATION:
         if (num_kv_heads <= 0) return DIFFKV_E_INVAL;
         *bytes = (size_t)gen_ws((int64_t)num_seqs * num_kv_heads);
+        return DIFFKV_OK;
+    case DIFFKV_OP_PROMPT_SIGNIFICANCE:
+        if (num_q_heads <= 0 || total_new < 0) return DIFFKV_E_INVAL;
+        *bytes = (size_t)prompt_ws(num_seqs, num_q_heads, total_new).total;
         return DIFFKV_OK;
     default:
         return DIFFKV_E_INVAL;
@@ -386,6 +406,41 @@ diffkv_status diffkv_update_significance(const diffkv_layout* layout, const diff
     a.lse = lse;
     a.layout = layout_index(layout);
     hipError_t e = launch_significance(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
+}
+
+diffkv_status diffkv_prompt_significance(const diffkv_layout* layout, int32_t num_seqs, int64_t total_new,
+                                        int32_t max_new, const int32_t* new_len, int32_t num_q_heads,
+                                        int32_t num_kv_heads, const uint16_t* q, const uint16_t* k,
+                                        float sm_scale, const float* lse, float* score, void* ws,
+                                        size_t ws_bytes, void* stream)
+{
+    if (!layout_valid(layout) || num_seqs < 0 || total_new < 0 || max_new < 0) return DIFFKV_E_INVAL;
+    if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0) return DIFFKV_E_INVAL;
+    if (num_q_heads / num_kv_heads > 8) return DIFFKV_E_UNSUPPORTED;
+    if (num_seqs == 0 || total_new == 0 || max_new == 0) return DIFFKV_OK;
+    if (!new_len || !q || !k || !score) return DIFFKV_E_INVAL;
+    if (((uintptr_t)q | (uintptr_t)k) % 16 != 0) return DIFFKV_E_INVAL;
+    const PromptWs w = prompt_ws(num_seqs, num_q_heads, total_new);
+    if (!ws || (int64_t)ws_bytes < w.total) return DIFFKV_E_WORKSPACE;
+    PromptArgs a;
+    memset(&a, 0, sizeof(a));
+    a.B = num_seqs;
+    a.Hq = num_q_heads;
+    a.Hkv = num_kv_heads;
+    a.max_new = max_new;
+    a.total_new = total_new;
+    a.new_len = new_len;
+    a.q = q;
+    a.k = k;
+    a.lse = lse;
+    a.scale_log2 = sm_scale * 1.4426950408889634f;
+    a.score = score;
+    uint8_t* base = static_cast<uint8_t*>(ws);
+    a.off = reinterpret_cast<long long*>(base + w.off);
+    a.nlen = reinterpret_cast<int32_t*>(base + w.nlen);
+    a.lse2 = reinterpret_cast<float*>(base + w.lse2);
+    hipError_t e = launch_prompt_significance(a, num_q_heads / num_kv_heads, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? DIFFKV_OK : DIFFKV_E_LAUNCH;
 }
 

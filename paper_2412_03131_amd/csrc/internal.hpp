@@ -170,6 +170,23 @@ hipError_t launch_significance(const SigArgs& a, hipStream_t st);
 // *workers = the balanced mode's share count.
 hipError_t attention_mode(int gq, int li, long long T, int splits, int* mode, int* workers);
 
+// Prompt-phase significance: rows of q [total_new][Hq][kD] and k
+// [total_new][Hkv][kD] concatenated per sequence; score [total_new][Hkv].
+struct PromptArgs {
+    int B, Hq, Hkv, max_new;
+    long long total_new;
+    const int32_t* new_len;
+    const uint16_t* q;
+    const uint16_t* k;
+    const float* lse;    // [total_new][Hq] natural log from the caller, or null: the row pass computes it
+    float scale_log2;    // sm_scale * log2(e)
+    float* score;
+    long long* off;      // [B] first row of each sequence (workspace)
+    int32_t* nlen;       // [B] rows of each sequence, clamped to max_new and total_new (workspace)
+    float* lse2;         // [total_new][Hq] row log2-sum-exp (workspace)
+};
+hipError_t launch_prompt_significance(const PromptArgs& a, int g, hipStream_t st);
+
 // Fixed device scratch of diffkv_decode_attention_noalloc, one per device.
 constexpr long long kNoAllocScratchBytes = 8ll << 20;
 hipError_t noalloc_scratch(void** ptr);

@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(_HERE, "libdiffkv.so")
 
 OK, E_INVAL, E_UNSUPPORTED, E_WORKSPACE, E_LAUNCH, E_SCRATCH = 0, 1, 2, 3, 4, 5
 ST_OUT_OF_PAGES, ST_TABLE_OVERFLOW, ST_BAD_INPUT = 1, 2, 4
-OP_APPEND, OP_ATTENTION, OP_COMPACT, OP_ALLOC, OP_GENERATION = 0, 1, 2, 3, 4
+OP_APPEND, OP_ATTENTION, OP_COMPACT, OP_ALLOC, OP_GENERATION, OP_PROMPT_SIGNIFICANCE = 0, 1, 2, 3, 4, 5
 HIGH, LOW = 0, 1
 
 _lib = None
@@ -51,8 +51,8 @@ class CacheStruct(C.Structure):
 
 EXPORTS = ("diffkv_layout_init", "diffkv_workspace_size", "diffkv_quantize_append",
            "diffkv_decode_attention", "diffkv_decode_attention_noalloc", "diffkv_update_significance",
-           "diffkv_compact_free_list", "diffkv_alloc_pages", "diffkv_generation_step",
-           "diffkv_status_str")
+           "diffkv_prompt_significance", "diffkv_compact_free_list", "diffkv_alloc_pages",
+           "diffkv_generation_step", "diffkv_status_str")
 
 
 def lib():
@@ -72,6 +72,8 @@ def lib():
         L.diffkv_decode_attention.argtypes = [PL, PC, i32, vp, f32, vp, vp, i32, vp, sz, vp]
         L.diffkv_decode_attention_noalloc.argtypes = [PL, PC, i32, vp, f32, vp, vp, i32, vp]
         L.diffkv_update_significance.argtypes = [PL, PC, i32, vp, f32, vp, vp]
+        L.diffkv_prompt_significance.argtypes = [PL, i32, i64, i32, vp, i32, i32, vp, vp, f32, vp, vp,
+                                                 vp, sz, vp]
         L.diffkv_compact_free_list.argtypes = [PL, PC, i32, vp, vp, sz, vp]
         L.diffkv_alloc_pages.argtypes = [PL, PC, i32, vp, vp, sz, vp]
         L.diffkv_generation_step.argtypes = [PL, PC, f32, f32, i32, vp, sz, vp]
@@ -240,6 +242,26 @@ def update_significance(cache, q, sm_scale, lse, stream=None):
     _check(lib().diffkv_update_significance(C.byref(cache.L), C.byref(st), q.shape[1], _ptr(_bits16(q)),
                                             float(sm_scale), _ptr(lse), _stream(stream)),
            "diffkv_update_significance")
+
+
+def prompt_significance(L, new_len, q, k, sm_scale, lse=None, score=None, max_new=None, ws=None,
+                        stream=None):
+    """diffkv_prompt_significance: q fp16 [rows, Hq, D], k fp16 [rows, Hkv, D] (device, rows
+    concatenated per sequence), new_len int32 [B] (device); returns score fp32 [rows, Hkv].
+    lse (fp32 [rows, Hq], natural log) skips the row pass when given."""
+    rows, Hq, Hkv = q.shape[0], q.shape[1], k.shape[1]
+    B = new_len.shape[0]
+    if max_new is None:
+        max_new = int(new_len.max().item()) if B else 0
+    if score is None:
+        score = torch.empty((rows, Hkv), dtype=torch.float32, device=q.device)
+    need = workspace_size(OP_PROMPT_SIGNIFICANCE, L, B, Hq, Hkv, rows)
+    ws = _ws(need, q.device, ws)
+    _check(lib().diffkv_prompt_significance(C.byref(L), B, rows, int(max_new), _ptr(new_len), Hq, Hkv,
+                                            _ptr(_bits16(q)), _ptr(_bits16(k)), float(sm_scale), _ptr(lse),
+                                            _ptr(score), _ptr(ws), ws.numel() * ws.element_size(),
+                                            _stream(stream)), "diffkv_prompt_significance")
+    return score
 
 
 def compact_free_list(cache, release, num_tables=None, ws=None, stream=None):

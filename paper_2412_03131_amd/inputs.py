@@ -143,6 +143,14 @@ def uniform_cache(B, Hq, Hkv, L, seed=5):
     return dict(new_len=np.full(B, L, np.int32), k=k, v=v, score=score, q=q)
 
 
+def prompt_queries(name, rows, seed=None):
+    """Queries of the prompt rows of a workload: fp16 bits [rows][Hq][D], N(0,1)."""
+    cfg = CONFIGS[name]
+    seed = cfg["seed"] + 17 if seed is None else seed
+    (r_q,) = _streams(seed, 1)
+    return f16_bits(r_q.standard_normal((rows, cfg["Hq"], HEAD_DIM), dtype=np.float32))
+
+
 def decode_token(name, step, B, Hq, Hkv, outliers, seed=None):
     """One generated token per sequence: k/v [B][Hkv][D], score [B][Hkv],
     quota (1, 0) per table (the new token enters the recent window), new q."""

@@ -117,4 +117,19 @@ def test_argument_checks_enqueue_nothing(dk):
     bad.off_vcode[0] += 64
     assert lib.diffkv_compact_free_list(C.byref(bad), C.byref(st), 1, fake, fake, 1 << 20,
                                         None) == dk.E_INVAL  # not a layout diffkv_layout_init made
+    # prompt significance: shapes, alignment, group size and workspace are checked first
+    ps = lib.diffkv_prompt_significance
+    assert ps(C.byref(L), 2, 100, 60, fake, 6, 4, fake, fake, 0.1, None, fake, fake, 1 << 30,
+              None) == dk.E_INVAL  # Hq % Hkv
+    assert ps(C.byref(L), 2, 100, 60, fake, 36, 4, fake, fake, 0.1, None, fake, fake, 1 << 30,
+              None) == dk.E_UNSUPPORTED  # 9 query heads per KV head
+    assert ps(C.byref(L), 2, 100, 60, fake, 8, 4, fake + 8, fake, 0.1, None, fake, fake, 1 << 30,
+              None) == dk.E_INVAL  # q not 16-byte aligned
+    assert ps(C.byref(L), 2, 100, 60, None, 8, 4, fake, fake, 0.1, None, fake, fake, 1 << 30,
+              None) == dk.E_INVAL
+    need = dk.workspace_size(dk.OP_PROMPT_SIGNIFICANCE, L, 2, 8, 4, 100)
+    assert need >= 100 * 8 * 4 + 2 * 12
+    assert ps(C.byref(L), 2, 100, 60, fake, 8, 4, fake, fake, 0.1, None, fake, fake, need - 1,
+              None) == dk.E_WORKSPACE
+    assert ps(C.byref(L), 0, 0, 0, None, 8, 4, None, None, 0.1, None, None, None, 0, None) == dk.OK
     assert dk.status_str(dk.E_WORKSPACE) == "workspace too small"

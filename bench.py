@@ -123,11 +123,12 @@ def parse():
     ap.add_argument("--generation-steps", type=int, default=50)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=("all", "attention", "copy", "generation"), default="all",
+    ap.add_argument("--only", choices=("all", "attention", "copy", "generation", "prompt"), default="all",
                     help="profiling aids that print no benchmark line: 'attention' builds the "
                          "--config cache and times only attention calls (no flush); 'copy' runs a "
                          "plain 1 GiB device copy (the reference for scaling HBM byte counters); "
-                         "'generation' runs only the generation-step measurement")
+                         "'generation' runs only the generation-step measurement; 'prompt' only "
+                         "the prompt-phase significance measurement")
     return ap.parse_args()
 
 
@@ -388,6 +389,62 @@ def significance_bench(torch, dk, lib, dev, sptr, wl, flush, reps=30):
     return res
 
 
+MFMA_F16_PEAK = 2.5e15   # dense fp16 matrix-core peak of the MI355X, FLOP/s
+
+
+def prompt_significance_bench(torch, dk, lib, dev, sptr, reps=5):
+    """diffkv_prompt_significance over the llama8b prompt batch (B=64, Hq=32, Hkv=8,
+    prompts of 1024-4096 tokens), with the row pass (no lse given) and without it (the
+    row normalizers passed in, as a prompt attention kernel would supply them).
+    Algorithmic FLOPs per pass: 2 * 128 per causal (query head, query, key) triple."""
+    from paper_2412_03131_amd import inputs
+    w = inputs.prefill("llama8b")
+    B, Hq, Hkv = w["B"], w["Hq"], w["Hkv"]
+    nl = w["new_len"].astype(np.int64)
+    rows = int(nl.sum())
+    q = torch.from_numpy(inputs.prompt_queries("llama8b", rows).view(np.int16)).to(dev).view(torch.float16)
+    k = torch.from_numpy(w["k"].view(np.int16)).to(dev).view(torch.float16)
+    new_len = torch.from_numpy(w["new_len"].astype(np.int32)).to(dev)
+    L = dk.layout(max_seq_len=64)
+    score = torch.empty((rows, Hkv), dtype=torch.float32, device=dev)
+    ws = torch.empty(dk.workspace_size(dk.OP_PROMPT_SIGNIFICANCE, L, B, Hq, Hkv, rows), dtype=torch.uint8,
+                     device=dev)
+    lse = torch.zeros((rows, Hq), dtype=torch.float32, device=dev)
+    vp = lambda x: C.c_void_p(x.data_ptr())
+    call = lambda l: lib.diffkv_prompt_significance(C.byref(L), B, rows, int(nl.max()), vp(new_len), Hq, Hkv,
+                                                    vp(q), vp(k), float(SCALE), l, vp(score), vp(ws),
+                                                    ws.numel(), sptr)
+    rc = call(None) | call(None)
+    # (the normalizers passed in are zeros: their values do not change the work)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    for e in ev:
+        e[0].record()
+        rc |= call(None)
+        e[1].record()
+        rc |= call(vp(lse))
+        e[2].record()
+    torch.cuda.synchronize()
+    if rc:
+        raise RuntimeError("prompt significance bench: call failed")
+    pairs = int((Hq * nl * (nl + 1) // 2).sum())
+    flop_pass = 2.0 * 128 * pairs
+    full = np.array([e[0].elapsed_time(e[1]) * 1e3 for e in ev])
+    cols = np.array([e[1].elapsed_time(e[2]) * 1e3 for e in ev])
+    res = {"workload": "llama8b prompt batch: B=64, Hq=32, Hkv=8 (GQA 4), D=128, prompts of 1024-4096 "
+                       "tokens (%d rows), fp16 q/k" % rows,
+           "us_both_passes": pct(full), "us_column_pass_lse_given": pct(cols),
+           "flop_per_pass": flop_pass,
+           "tflops_both_passes": 2 * flop_pass / (full.mean() * 1e-6) / 1e12,
+           "tflops_column_pass": flop_pass / (cols.mean() * 1e-6) / 1e12,
+           "frac_of_mfma_f16_peak_both": 2 * flop_pass / (full.mean() * 1e-6) / MFMA_F16_PEAK,
+           "frac_of_mfma_f16_peak_column": flop_pass / (cols.mean() * 1e-6) / MFMA_F16_PEAK}
+    log("prompt significance (llama8b prompts, %d rows): %.0f us both passes (%.0f TFLOP/s, %.2f of the "
+        "fp16 MFMA peak), %.0f us column pass alone (%.0f TFLOP/s)"
+        % (rows, full.mean(), res["tflops_both_passes"], res["frac_of_mfma_f16_peak_both"], cols.mean(),
+           res["tflops_column_pass"]))
+    return res
+
+
 PRECISIONS = [  # (name, layout keyword arguments, section holding every token)
     ("K8V8", dict(k_bits=(8, 4), v_bits=(8, 2), tokens_per_page=(16, 32)), 0),
     ("K8V4", dict(k_bits=(8, 4), v_bits=(4, 2), tokens_per_page=(16, 32)), 0),
@@ -627,6 +684,9 @@ def main():
     if args.only == "generation":
         generation_bench(torch, dk, lib, dev, sptr, args.generation_steps)
         return
+    if args.only == "prompt":
+        prompt_significance_bench(torch, dk, lib, dev, sptr)
+        return
     flush = Flush(torch, dev)
     wl = build_decode(torch, dk, dev, args.config, args.warmup + 2 * args.steps + 8)
     if args.only == "attention":
@@ -644,6 +704,7 @@ def main():
     if args.extras == "all":
         extras["significance"] = significance_bench(torch, dk, lib, dev, sptr, wl, flush)
         extras["precisions"] = precision_bench(torch, dk, lib, dev, sptr, flush)
+        extras["prompt_significance"] = prompt_significance_bench(torch, dk, lib, dev, sptr)
         if args.config != "llama70b":
             del wl
             torch.cuda.empty_cache()

@@ -306,6 +306,7 @@ diffkv_status diffkv_update_significance(const diffkv_layout* layout, const diff
  *   ws       diffkv_workspace_size(DIFFKV_OP_PROMPT_SIGNIFICANCE, ...) bytes
  * Arithmetic: fp16 x fp16 products on the matrix cores (exact), fp32 sums,
  * fp32 softmax with exp2; probabilities below 2^-126 may come out as zero.
+ * sm_scale must be positive and finite (DIFFKV_E_INVAL otherwise).
  * num_q_heads / num_kv_heads up to 8 (else DIFFKV_E_UNSUPPORTED).
  */
 diffkv_status diffkv_prompt_significance(const diffkv_layout* layout, int32_t num_seqs, int64_t total_new,

@@ -418,6 +418,7 @@ diffkv_status diffkv_prompt_significance(const diffkv_layout* layout, int32_t nu
     if (!layout_valid(layout) || num_seqs < 0 || total_new < 0 || max_new < 0) return DIFFKV_E_INVAL;
     if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0) return DIFFKV_E_INVAL;
     if (num_q_heads / num_kv_heads > 8) return DIFFKV_E_UNSUPPORTED;
+    if (!(sm_scale > 0.0f) || sm_scale > 1e30f) return DIFFKV_E_INVAL;
     if (num_seqs == 0 || total_new == 0 || max_new == 0) return DIFFKV_OK;
     if (!new_len || !q || !k || !score) return DIFFKV_E_INVAL;
     if (((uintptr_t)q | (uintptr_t)k) % 16 != 0) return DIFFKV_E_INVAL;

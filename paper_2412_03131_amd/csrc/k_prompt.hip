@@ -48,6 +48,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 template <int G>
 struct PsShape {
+    static constexpr int QI = G <= 4 ? 32 : 16;      // query positions per LDS stage of the column pass
     static constexpr int QT = G >= 3 ? 1 : 4 / G;   // 16-position query tiles per head per wave
     static constexpr int PW = 16 * QT;               // query positions per wave
     static constexpr int PB = 4 * PW;                // query positions per workgroup
@@ -59,6 +60,8 @@ __device__ __forceinline__ f4 mfma16(h8 a, h8 b, f4 c)
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float max3f(float a, float b, float c) { return __builtin_fmaxf(__builtin_fmaxf(a, b), c); }
 
 // Logical block of workgroup i among n: XCD x = i % 8 runs the logical range
 // [x * (n / 8) + min(x, n % 8), ...) in order.  A bijection of [0, n).
@@ -146,15 +149,16 @@ __global__ __launch_bounds__(kPsThreads) void ps_rows(PromptArgs a)
 
     const int last = min(N, q0 + PB) - 1;
     const int nkb = last / kKeyBlock + 1;
-    const int srow = threadIdx.x >> 2, spart = threadIdx.x & 3;
-    h8 pre[4];
+    constexpr int kPer = kKeyBlock * 16 / kPsThreads;    // 16-byte chunks staged per thread
+    const int srow = threadIdx.x / (16 / kPer), spart = threadIdx.x % (16 / kPer);
+    h8 pre[kPer];
     auto fetch = [&](int kb) {
         const int p = kb * kKeyBlock + srow;
-        const h8* src = reinterpret_cast<const h8*>(a.k + ((off + p) * a.Hkv + h) * kD) + spart * 4;
-        for (int i = 0; i < 4; i++) pre[i] = p < N ? src[i] : zero8();
+        const h8* src = reinterpret_cast<const h8*>(a.k + ((off + p) * a.Hkv + h) * kD) + spart * kPer;
+        for (int i = 0; i < kPer; i++) pre[i] = p < N ? src[i] : zero8();
     };
     auto stash = [&](int buf) {
-        for (int i = 0; i < 4; i++) sk[buf][srow][spart * 4 + i] = pre[i];
+        for (int i = 0; i < kPer; i++) sk[buf][srow][spart * kPer + i] = pre[i];
     };
     fetch(0);
     stash(0);
@@ -168,7 +172,7 @@ __global__ __launch_bounds__(kPsThreads) void ps_rows(PromptArgs a)
         // removes keys >= N: those lie after every valid position)
         if (kbase < wq0 + PW && wq0 < N) {
             const bool need_mask = kbase + kKeyBlock - 1 > wq0;
-            for (int kt = 0; kt < 4; kt++) {
+            for (int kt = 0; kt < kKeyBlock / 16; kt++) {
                 h8 af[4];
                 for (int s = 0; s < 4; s++) af[s] = sk[buf][kt * 16 + col][4 * s + grp];
                 const int key0 = kbase + kt * 16 + 4 * grp;
@@ -177,20 +181,18 @@ __global__ __launch_bounds__(kPsThreads) void ps_rows(PromptArgs a)
                     for (int t = 0; t < G; t++) {
                         f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
                         for (int s = 0; s < 4; s++) acc = mfma16(af[s], qf[qt][t][s], acc);
-                        float x[4];
-                        for (int i = 0; i < 4; i++) {
-                            x[i] = acc[i] * c;
-                            if (need_mask && key0 + i > j) x[i] = -__builtin_huge_valf();
-                        }
-                        const float bm = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+                        if (need_mask)
+                            for (int i = 0; i < 4; i++)
+                                if (key0 + i > j) acc[i] = -__builtin_huge_valf();
+                        const float bm = max3f(acc[0], acc[1], fmaxf(acc[2], acc[3])) * c;
                         if (__builtin_amdgcn_ballot_w64(bm > m[qt][t] + kSlack)) {
                             const float mn = fmaxf(m[qt][t], bm);
                             sum[qt][t] *= fast_exp2(m[qt][t] - mn);
                             m[qt][t] = mn;
                         }
-                        const float mm = m[qt][t];
-                        sum[qt][t] += (fast_exp2(x[0] - mm) + fast_exp2(x[1] - mm)) +
-                                      (fast_exp2(x[2] - mm) + fast_exp2(x[3] - mm));
+                        const float nm = -m[qt][t];
+                        sum[qt][t] += (fast_exp2(fmaf(acc[0], c, nm)) + fast_exp2(fmaf(acc[1], c, nm))) +
+                                      (fast_exp2(fmaf(acc[2], c, nm)) + fast_exp2(fmaf(acc[3], c, nm)));
                     }
                 }
             }
@@ -216,8 +218,10 @@ __global__ __launch_bounds__(kPsThreads) void ps_rows(PromptArgs a)
 template <int G>
 __global__ __launch_bounds__(kPsThreads) void ps_cols(PromptArgs a)
 {
-    __shared__ h8 sq[2][G][16][kRowChunks];
-    __shared__ float sl[2][G][16];
+    constexpr int QI = PsShape<G>::QI;
+    constexpr int NR = G * QI * 16 / kPsThreads;     // 16-byte chunks of q staged per thread
+    __shared__ h8 sq[2][G][QI][kRowChunks];
+    __shared__ float sl[2][G][QI];
 
     const int nkb = (a.max_new + kColKeys - 1) / kColKeys;
     const long long nblk = (long long)a.B * a.Hkv * nkb;
@@ -236,6 +240,7 @@ __global__ __launch_bounds__(kPsThreads) void ps_cols(PromptArgs a)
     const int col = lane & 15, grp = lane >> 4;
     const int wk0 = k0 + w * 64;
     const float c = a.scale_log2;
+    const float inv_c = 1.0f / c;
 
     h8 kf[4][4];
     for (int kt = 0; kt < 4; kt++) {
@@ -247,19 +252,19 @@ __global__ __launch_bounds__(kPsThreads) void ps_cols(PromptArgs a)
     for (int kt = 0; kt < 4; kt++)
         for (int i = 0; i < 4; i++) cs[kt][i] = 0.0f;
 
-    const int nq = (N - k0 + 15) / 16;
-    h8 pq[G];
+    const int nq = (N - k0 + QI - 1) / QI;
+    h8 pq[NR];
     float pl = 0.0f;
     auto fetch = [&](int it) {
-        const int j0 = k0 + it * 16;
-        for (int r = 0; r < G; r++) {
+        const int j0 = k0 + it * QI;
+        for (int r = 0; r < NR; r++) {
             const int cidx = r * kPsThreads + tid;
             const int row = cidx >> 4, pos = row / G, t = row - pos * G;
             const int j = j0 + pos;
             const h8* src = reinterpret_cast<const h8*>(a.q + ((off + j) * a.Hq + h * G + t) * kD);
             pq[r] = j < N ? src[cidx & 15] : zero8();
         }
-        if (tid < 16 * G) {
+        if (tid < QI * G) {
             const int pos = tid / G, t = tid - pos * G;
             const int j = j0 + pos;
             const long long e = (off + j) * a.Hq + h * G + t;
@@ -267,12 +272,12 @@ __global__ __launch_bounds__(kPsThreads) void ps_cols(PromptArgs a)
         }
     };
     auto stash = [&](int buf) {
-        for (int r = 0; r < G; r++) {
+        for (int r = 0; r < NR; r++) {
             const int cidx = r * kPsThreads + tid;
             const int row = cidx >> 4, pos = row / G, t = row - pos * G;
             sq[buf][t][pos][cidx & 15] = pq[r];
         }
-        if (tid < 16 * G) {
+        if (tid < QI * G) {
             const int pos = tid / G, t = tid - pos * G;
             sl[buf][t][pos] = pl;
         }
@@ -283,26 +288,38 @@ __global__ __launch_bounds__(kPsThreads) void ps_cols(PromptArgs a)
     for (int it = 0; it < nq; it++) {
         const int buf = it & 1;
         if (it + 1 < nq) fetch(it + 1);
-        const int j0 = k0 + it * 16;
-        if (j0 + 15 >= wk0) {              // some query of the tile reaches the wave's keys
+        for (int sub = 0; sub < QI / 16; sub++) {
+            const int j0 = k0 + it * QI + sub * 16;
+            if (j0 + 15 < wk0 || wk0 >= N) continue;   // no query of the tile reaches the wave's keys
             const bool diag = j0 < wk0 + 63;
+            // the MFMA accumulates onto -lse/c, so acc = S - lse/c and the maximum over the
+            // heads needs no per-head arithmetic; exp2(c * max) is the group's probability
             f4 mx[4];
-            for (int kt = 0; kt < 4; kt++)
-                for (int i = 0; i < 4; i++) mx[kt][i] = -__builtin_huge_valf();
-            for (int t = 0; t < G; t++) {
-                h8 bf[4];
-                for (int s = 0; s < 4; s++) bf[s] = sq[buf][t][col][4 * s + grp];
-                const float lt = sl[buf][t][col];
+            for (int t = 0; t < G; t += 2) {
+                const bool pair = t + 1 < G;
+                h8 bf0[4], bf1[4];
+                for (int s = 0; s < 4; s++) bf0[s] = sq[buf][t][sub * 16 + col][4 * s + grp];
+                if (pair)
+                    for (int s = 0; s < 4; s++) bf1[s] = sq[buf][t + 1][sub * 16 + col][4 * s + grp];
+                const float z0 = -sl[buf][t][sub * 16 + col] * inv_c;
+                const float z1 = pair ? -sl[buf][t + 1][sub * 16 + col] * inv_c : 0.0f;
                 for (int kt = 0; kt < 4; kt++) {
-                    f4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-                    for (int s = 0; s < 4; s++) acc = mfma16(kf[kt][s], bf[s], acc);
-                    for (int i = 0; i < 4; i++) mx[kt][i] = fmaxf(mx[kt][i], fmaf(acc[i], c, -lt));
+                    f4 acc0 = {z0, z0, z0, z0};
+                    for (int s = 0; s < 4; s++) acc0 = mfma16(kf[kt][s], bf0[s], acc0);
+                    if (pair) {
+                        f4 acc1 = {z1, z1, z1, z1};
+                        for (int s = 0; s < 4; s++) acc1 = mfma16(kf[kt][s], bf1[s], acc1);
+                        for (int i = 0; i < 4; i++)
+                            mx[kt][i] = t == 0 ? fmaxf(acc0[i], acc1[i]) : max3f(mx[kt][i], acc0[i], acc1[i]);
+                    } else {
+                        for (int i = 0; i < 4; i++) mx[kt][i] = t == 0 ? acc0[i] : fmaxf(mx[kt][i], acc0[i]);
+                    }
                 }
             }
             const int j = j0 + col;
             for (int kt = 0; kt < 4; kt++)
                 for (int i = 0; i < 4; i++) {
-                    float v = fast_exp2(mx[kt][i]);
+                    float v = fast_exp2(mx[kt][i] * c);
                     if (diag && wk0 + kt * 16 + 4 * grp + i > j) v = 0.0f;
                     cs[kt][i] += v;
                 }

@@ -123,12 +123,14 @@ def parse():
     ap.add_argument("--generation-steps", type=int, default=50)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=("all", "attention", "copy", "generation", "prompt"), default="all",
+    ap.add_argument("--only", choices=("all", "attention", "copy", "generation", "prompt", "compaction"),
+                    default="all",
                     help="profiling aids that print no benchmark line: 'attention' builds the "
                          "--config cache and times only attention calls (no flush); 'copy' runs a "
                          "plain 1 GiB device copy (the reference for scaling HBM byte counters); "
                          "'generation' runs only the generation-step measurement; 'prompt' only "
-                         "the prompt-phase significance measurement")
+                         "the prompt-phase significance measurement; 'compaction' only the "
+                         "compaction workload")
     return ap.parse_args()
 
 
@@ -686,6 +688,9 @@ def main():
         return
     if args.only == "prompt":
         prompt_significance_bench(torch, dk, lib, dev, sptr)
+        return
+    if args.only == "compaction":
+        compaction_bench(torch, dk, lib, dev, sptr, args.compaction_rounds)
         return
     flush = Flush(torch, dev)
     wl = build_decode(torch, dk, dev, args.config, args.warmup + 2 * args.steps + 8)

@@ -327,7 +327,8 @@ diffkv_status diffkv_prompt_significance(const diffkv_layout* layout, int32_t nu
  * down).  Request completion = releasing every live slot of its tables.
  *   release  device uint8 [num_tables][p_max]; bytes of non-live slots are
  *            ignored.
- * Never fails on the device (released IDs always fit the ring).
+ * Never fails on the device (released IDs always fit the ring).  p_max above
+ * 8192 or more than 2^20 tables: DIFFKV_E_UNSUPPORTED.
  */
 diffkv_status diffkv_compact_free_list(const diffkv_layout* layout, const diffkv_cache* cache,
                                        int32_t num_tables, const uint8_t* release,

@@ -455,6 +455,7 @@ diffkv_status diffkv_compact_free_list(const diffkv_layout* layout, const diffkv
     if (num_tables == 0) return DIFFKV_OK;
     if (!release) return DIFFKV_E_INVAL;
     if (layout->p_max > 8192) return DIFFKV_E_UNSUPPORTED;  // LDS staging of one row
+    if ((int64_t)num_tables > (int64_t)1024 * 1024) return DIFFKV_E_UNSUPPORTED;  // count groups
     const int64_t need = compact_ws(num_tables);
     if (!ws || (int64_t)ws_bytes < need) return DIFFKV_E_WORKSPACE;
     CompactArgs a;

@@ -83,8 +83,9 @@ struct CompactArgs {
     int num_tables;
     const uint8_t* release;
     CallFlags* flags;
-    int32_t* count;
-    int32_t* offset;
+    int32_t* count;    // [num_tables] released live slots of each table
+    int32_t* offset;   // [groups] released slots of each group of group_tables tables
+    int group_tables;  // tables per compact_count workgroup
 };
 
 // per-table decision of one generation step

@@ -14,7 +14,7 @@
 //                    (new pages from the table's ring region), quantize each
 //                    token's 32-dim groups and write the page.
 // Allocation alone (alloc_plan + alloc_write) and compaction (compact_count,
-// compact_scan, compact_apply) follow the same planning/coordination split:
+// compact_apply) follow the same planning/coordination split:
 // per-table work is fully parallel, one prefix sum gives every table a
 // disjoint ring region.
 #include "internal.hpp"
@@ -825,126 +825,148 @@ __global__ __launch_bounds__(kWave) void alloc_write(AllocArgs a)
 }
 
 // ---------------------------------------------------------------------------
-// Compaction: compact_count (wave per table), compact_scan (one workgroup,
-// only above kCompactFusedTables tables), compact_apply (wave per table)
+// Compaction in two launches: compact_count (a wave per table; a workgroup
+// counts a group of group_tables tables and writes the group's total) and
+// compact_apply (a wave per table).  An apply wave finds its ring offset from
+// the totals of the groups before its own plus the counts of the earlier
+// tables of its group; groups are sized so that neither exceeds kMaxGroups
+// values, i.e. one round of loads per lane, so no scan launch runs between the
+// two at any table count.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ bool slot_live(int slot, int ph, int pl, int P)
 {
     return slot < ph || slot >= P - pl;
 }
 
-__global__ __launch_bounds__(kWave) void compact_count(CompactArgs a)
+constexpr int kCountWaves = 4;       // waves of a compact_count workgroup
+constexpr int kCompactPlanIlp = 16;  // values a lane loads at once
+constexpr int kMaxGroups = kWave * kCompactPlanIlp;
+
+// ONE: one table per wave (group_tables == kCountWaves, up to kMaxGroups * kCountWaves tables)
+template <bool ONE>
+__global__ __launch_bounds__(kCountWaves * kWave) void compact_count(CompactArgs a)
 {
-    const int t = blockIdx.x;
+    __shared__ int s_c[kCountWaves];
+    const int w = wave_index();
+    const int lane = threadIdx.x & (kWave - 1);
     const int P = a.p_max;
-    int ph = a.pages[2 * t], pl = a.pages[2 * t + 1];
-    ph = ph < 0 ? 0 : (ph > P ? P : ph);
-    pl = pl < 0 ? 0 : (pl > P - ph ? P - ph : pl);
-    const uint8_t* rel = a.release + (long long)t * P;
-    int c = 0;
-    for (int s = threadIdx.x; s < P; s += kWave) c += (rel[s] != 0 && slot_live(s, ph, pl, P));
-    c = wave_isum_w<kWave>(c);
-    if (threadIdx.x == 0) a.count[t] = c;
-    // the end pointer before the call, for an apply kernel that plans itself
-    if (t == 0 && threadIdx.x == 0) a.flags->tail_old = a.ring_ptr[1];
+    const int GT = ONE ? kCountWaves : a.group_tables;
+    const int t0 = blockIdx.x * GT;
+    const int t1 = ONE ? min(a.num_tables, t0 + w + 1) : min(a.num_tables, t0 + GT);
+    int gsum = 0;
+    for (int t = t0 + w; t < t1; t += kCountWaves) {
+        int ph = a.pages[2 * t], pl = a.pages[2 * t + 1];
+        ph = ph < 0 ? 0 : (ph > P ? P : ph);
+        pl = pl < 0 ? 0 : (pl > P - ph ? P - ph : pl);
+        const uint8_t* rel = a.release + (long long)t * P;
+        int c = 0;
+        for (int s = lane; s < P; s += kWave) c += (rel[s] != 0 && slot_live(s, ph, pl, P));
+        c = wave_isum_w<kWave>(c);
+        if (lane == 0) a.count[t] = c;
+        gsum += c;
+    }
+    if (lane == 0) s_c[w] = gsum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int g = 0;
+#pragma unroll
+        for (int i = 0; i < kCountWaves; ++i) g += s_c[i];
+        a.offset[blockIdx.x] = g;  // the group's total
+        // the end pointer before the call
+        if (blockIdx.x == 0) a.flags->tail_old = a.ring_ptr[1];
+    }
 }
 
-__global__ __launch_bounds__(kPlanThreads) void compact_scan(CompactArgs a)
+// sum of v[0 .. n) and of v[0 .. below) over the wave, n <= kMaxGroups: all
+// loads in flight together (unconditional, clamped to the last element)
+__device__ __forceinline__ void wave_sum_prefix(const int32_t* v, int n, int below, int lane, int& tot, int& pre)
 {
-    const int tid = threadIdx.x;
-    __shared__ long long s_scan[kPlanThreads / kWave + 1];
-    __shared__ long long s_tail;
-    if (tid == 0) s_tail = a.ring_ptr[1];
-    __syncthreads();
-    long long carry = 0;
-    for (int t0 = 0; t0 < a.num_tables; t0 += kPlanThreads) {
-        const int t = t0 + tid;
-        const int c = t < a.num_tables ? a.count[t] : 0;
-        long long tr;
-        long long off = block_excl_scan<long long>(c, s_scan, &tr) + carry;
-        carry += tr;
-        if (t < a.num_tables) a.offset[t] = (int)off;
-    }
-    if (tid == 0) {
-        a.flags->tail_old = s_tail;
-        a.ring_ptr[1] = s_tail + carry;
+    int cv[kCompactPlanIlp];
+#pragma unroll
+    for (int k = 0; k < kCompactPlanIlp; ++k) cv[k] = v[min(lane + k * kWave, n - 1)];
+#pragma unroll
+    for (int k = 0; k < kCompactPlanIlp; ++k) {
+        const int i = lane + k * kWave;
+        const int c = i < n ? cv[k] : 0;
+        tot += c;
+        pre += i < below ? c : 0;
     }
 }
 
 // One wave per table; the live part of the row is staged in LDS (dynamic
-// shared memory of 2*p_max ints) so the squeeze can write in place.  FUSED:
-// the wave sums every table's count itself (its ring offset and the total; the
-// wave of table 0 advances the end pointer), so no scan launch runs between
-// counting and applying; used up to kCompactFusedTables tables.
-constexpr int kCompactFusedTables = 2048;
-constexpr int kCompactPlanIlp = 16;  // counts a lane loads at once
-
-template <bool FUSED>
+// shared memory of 2*p_max ints) with each slot's release flag in the sign bit
+// of its page ID (IDs are non-negative), so the squeeze writes in place and no
+// global load sits between the ring stores (a byte load may alias them, so the
+// compiler would keep each after the last store).  The wave of table 0
+// advances the end pointer by the call's total.
+template <bool ONE>
 __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
 {
-    extern __shared__ int32_t s_row[];  // [0, P): old IDs, [P, 2P): new row
+    extern __shared__ int32_t s_row[];  // [0, P): old IDs (sign bit: released), [P, 2P): new row
     const int t = blockIdx.x;
     const int lane = threadIdx.x;
-    int my_off;
-    if constexpr (FUSED) {
-        const int NT = a.num_tables;
-        int tot = 0, below = 0;
-        for (int base = 0; base < NT; base += kWave * kCompactPlanIlp) {
-            int cv[kCompactPlanIlp];
-#pragma unroll
-            for (int k = 0; k < kCompactPlanIlp; ++k)  // unconditional: all loads in flight together
-                cv[k] = a.count[min(base + lane + k * kWave, NT - 1)];
-#pragma unroll
-            for (int k = 0; k < kCompactPlanIlp; ++k) {
-                const int i = base + lane + k * kWave;
-                const int c = i < NT ? cv[k] : 0;
-                tot += c;
-                below += i < t ? c : 0;
-            }
-        }
-        tot = wave_isum_w<kWave>(tot);
-        my_off = wave_isum_w<kWave>(below);
-        if (t == 0 && lane == 0) a.ring_ptr[1] = a.flags->tail_old + tot;
-    } else {
-        my_off = a.offset[t];
-    }
+    const int NT = a.num_tables;
     const int P = a.p_max;
     int ph = a.pages[2 * t], pl = a.pages[2 * t + 1];
+    const int len0 = a.len[2 * t], len1 = a.len[2 * t + 1];
+    const long long tail_old = a.flags->tail_old;
+    const int GT = ONE ? kCountWaves : a.group_tables;
+    const int ng = (NT + GT - 1) / GT, g = t / GT, t0 = g * GT;
+    int tot = 0, before = 0;
+    wave_sum_prefix(a.offset, ng, g, lane, tot, before);  // the groups before g
+    if (ONE) {
+        if (lane < t - t0) before += a.count[t0 + lane];  // its group's tables before t
+    } else {
+        for (int i = t0 + lane; i < t; i += kWave) before += a.count[i];
+    }
     ph = ph < 0 ? 0 : (ph > P ? P : ph);  // same clamp as compact_count
     pl = pl < 0 ? 0 : (pl > P - ph ? P - ph : pl);
-    const int len0 = a.len[2 * t], len1 = a.len[2 * t + 1];
     const int T0 = a.T[0], T1 = a.T[1];
     const uint8_t* rel = a.release + (long long)t * P;
     int32_t* row = a.page_table + (long long)t * P;
     int32_t* s_new = s_row + P;
-    const long long base = a.flags->tail_old + my_off;
+    // the whole row, without waiting for the page counts: every load of the
+    // wave is then in flight at once (slots outside the sections are not read)
+    for (int s = lane; s < P; s += kWave) s_row[s] = row[s] | (rel[s] != 0 ? (int32_t)0x80000000 : 0);
+    tot = wave_isum_w<kWave>(tot);
+    const int my_off = wave_isum_w<kWave>(before);
+    if (t == 0 && lane == 0) a.ring_ptr[1] = tail_old + tot;
+    const long long n = a.num_pages;
+    // ring position of this table's first released ID, reduced once; later
+    // positions pass n at most once (rank < released slots <= pages in the pool)
+    const long long start = (tail_old % n + my_off) % n;
     const uint64_t below = (1ull << lane) - 1ull;
-    for (int s = lane; s < ph; s += kWave) s_row[s] = row[s];
-    for (int s = P - pl + lane; s < P; s += kWave) s_row[s] = row[s];
     __syncthreads();
+    auto ring_at = [&](int k) -> int32_t& {
+        long long i = start + k;
+        i = i >= n ? i - n : i;
+        return a.ring[i];
+    };
     // released IDs to the ring in ascending slot order; kept high IDs packed left
     int rank = 0, hi_keep = 0, drop0 = 0, drop1 = 0;
     for (int c = 0; c < ph; c += kWave) {
         const int s = c + lane;
         const bool live = s < ph;
-        const bool r = live && rel[s] != 0;
+        const int32_t id = live ? s_row[s] : 0;
+        const bool r = live && id < 0;
         const uint64_t mr = __ballot(r);
         const uint64_t mk = __ballot(live && !r);
         if (r) {
-            a.ring[(base + rank + __popcll(mr & below)) % a.num_pages] = s_row[s];
+            ring_at(rank + __popcll(mr & below)) = id & 0x7fffffff;
             int f = len0 - s * T0;
             drop0 += f < 0 ? 0 : (f > T0 ? T0 : f);
         }
-        if (live && !r) s_new[hi_keep + __popcll(mk & below)] = s_row[s];
+        if (live && !r) s_new[hi_keep + __popcll(mk & below)] = id;
         rank += __popcll(mr);
         hi_keep += __popcll(mk);
     }
     for (int c = P - pl; c < P; c += kWave) {
         const int s = c + lane;
-        const bool r = s < P && rel[s] != 0;
+        const int32_t id = s < P ? s_row[s] : 0;
+        const bool r = s < P && id < 0;
         const uint64_t mr = __ballot(r);
         if (r) {
-            a.ring[(base + rank + __popcll(mr & below)) % a.num_pages] = s_row[s];
+            ring_at(rank + __popcll(mr & below)) = id & 0x7fffffff;
             int f = len1 - (P - 1 - s) * T1;
             drop1 += f < 0 ? 0 : (f > T1 ? T1 : f);
         }
@@ -955,9 +977,10 @@ __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
     for (int c = 0; c < pl; c += kWave) {
         const int k = c + lane;
         const int s = P - 1 - k;
-        const bool keep = k < pl && rel[s] == 0;
+        const int32_t id = k < pl ? s_row[s] : -1;
+        const bool keep = k < pl && id >= 0;
         const uint64_t mk = __ballot(keep);
-        if (keep) s_new[P - 1 - (lo_keep + __popcll(mk & below))] = s_row[s];
+        if (keep) s_new[P - 1 - (lo_keep + __popcll(mk & below))] = id;
         lo_keep += __popcll(mk);
     }
     __syncthreads();
@@ -995,16 +1018,23 @@ hipError_t launch_alloc(const AllocArgs& a, hipStream_t st)
     return launch1(alloc_write, (unsigned)a.num_tables, kWave, st, a);
 }
 
-hipError_t launch_compact(const CompactArgs& a, hipStream_t st)
+hipError_t launch_compact(const CompactArgs& args, hipStream_t st)
 {
-    if (a.num_tables == 0) return hipSuccess;
+    if (args.num_tables == 0) return hipSuccess;
+    CompactArgs a = args;
+    // tables per count group: at least one per wave, and few enough groups that an
+    // apply wave sums them (and its group's earlier counts) in one round of loads
+    const long long per = ((long long)a.num_tables + kMaxGroups - 1) / kMaxGroups;
+    a.group_tables = (int)(per < kCountWaves ? kCountWaves : per);
+    if (a.group_tables > kMaxGroups) return hipErrorInvalidValue;
     const size_t lds = (size_t)2 * a.p_max * sizeof(int32_t);
-    hipError_t e = launch1(compact_count, (unsigned)a.num_tables, kWave, st, a);
+    const unsigned groups = (unsigned)((a.num_tables + a.group_tables - 1) / a.group_tables);
+    const bool one = a.group_tables == kCountWaves;
+    hipError_t e = one ? launch1(compact_count<true>, groups, kCountWaves * kWave, st, a)
+                       : launch1(compact_count<false>, groups, kCountWaves * kWave, st, a);
     if (e != hipSuccess) return e;
-    if (a.num_tables <= kCompactFusedTables) return launch1(compact_apply<true>, (unsigned)a.num_tables, kWave, st, a, lds);
-    e = launch1(compact_scan, 1, kPlanThreads, st, a);
-    if (e != hipSuccess) return e;
-    return launch1(compact_apply<false>, (unsigned)a.num_tables, kWave, st, a, lds);
+    return one ? launch1(compact_apply<true>, (unsigned)a.num_tables, kWave, st, a, lds)
+               : launch1(compact_apply<false>, (unsigned)a.num_tables, kWave, st, a, lds);
 }
 
 }  // namespace dkv

@@ -398,6 +398,35 @@ def test_compaction_random_rounds_bitexact():
     assert np.array_equal(st2["table"], st["table"])
 
 
+@pytest.mark.parametrize("tables,max_len,num_pages", [(7, 40000, 12000), (5003, 100, 60000)])
+def test_compaction_wide_rows_and_many_groups(tables, max_len, num_pages):
+    """Rows of more than 2048 slots, and more than 4096 tables (the apply waves sum
+    the count groups' totals in several rounds), bit-exact."""
+    rng = np.random.default_rng(tables)
+    Lo, Ld = layouts(max_seq_len=max_len)
+    oc = orc.Cache(Lo, num_pages, tables, 1, ring=rng.permutation(num_pages), with_pool=False)
+    dc = dev_cache_from_oracle(Ld, oc, with_pool=False)
+    for rnd in range(4):
+        print("case: compaction %d tables, p_max %d, round %d" % (tables, Lo.p_max, rnd), flush=True)
+        free = int(oc.ring_ptr[1] - oc.ring_ptr[0])
+        dem = np.zeros((tables, 2), np.int32)
+        for tt in range(tables):
+            room = Lo.p_max - int(oc.pages[tt].sum())
+            a = int(rng.integers(0, max(1, min(room, 2 * free // tables) + 1)))
+            hi = int(rng.integers(0, a + 1))
+            dem[tt] = hi, a - hi
+        orc.alloc_pages(oc, dem)
+        dk.alloc_pages(dc, t(dem))
+        oc.len[:] = np.maximum(oc.pages * np.array([16, 32]) - rng.integers(0, 16, (tables, 2)), 0)
+        oc.len[oc.pages == 0] = 0
+        dc.len.copy_(t(oc.len))
+        rel = (rng.random((tables, Lo.p_max)) < 0.4).astype(np.uint8)
+        orc.compact(oc, rel)
+        dk.compact_free_list(dc, t(rel))
+        assert_state_equal(dc, oc, with_pool=False, what="%d tables round %d" % (tables, rnd))
+    assert Lo.p_max > 2048 or tables > 4096
+
+
 def test_compaction_workload_scaled():
     """The compaction workload's recipe at 1/16 scale: 2^16 pages, 256 tables, 60% held,
     Bernoulli(0.35) releases, refill, 10 rounds (the ring wraps)."""

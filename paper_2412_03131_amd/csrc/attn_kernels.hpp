@@ -397,6 +397,32 @@ __device__ __forceinline__ float xsum4(float a, float b, float c, float d)
     return __uint_as_float(uw[0]) + __uint_as_float(uw[1]);
 }
 
+// Sum over the four rows, in every row (same column).
+__device__ __forceinline__ float rows_allsum(float v)
+{
+    auto ab = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    const float u = __uint_as_float(ab[0]) + __uint_as_float(ab[1]);
+    auto uw = __builtin_amdgcn_permlane32_swap(__float_as_uint(u), __float_as_uint(u), false, false);
+    return __uint_as_float(uw[0]) + __uint_as_float(uw[1]);
+}
+
+// Whether slot s of a wave's GQ heads (heads 4s .. 4s+3, one per row) holds a
+// single head: the last slot when GQ = 4k + 1.  Its logit is then summed over
+// the rows into every row, so its weights need no gather across rows.
+template <int GQ>
+constexpr bool lone_slot(int s)
+{
+    return GQ % 4 == 1 && GQ > 1 && s == (GQ + 3) / 4 - 1;
+}
+
+// The transposed row sum of slot s: row r gets head 4s + r (a lone head: every row).
+template <int GQ>
+__device__ __forceinline__ float slot_sum(int s, const float* part)
+{
+    return lone_slot<GQ>(s) ? rows_allsum(part[4 * s])
+                            : xsum4(part[4 * s], part[4 * s + 1], part[4 * s + 2], part[4 * s + 3]);
+}
+
 // o[r] = x of row r (same column), in every lane
 __device__ __forceinline__ void gather4(float x, float* o)
 {
@@ -481,7 +507,7 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         const bool valid = jl + 16 * tk < n_valid;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            const float x = xsum4(part[4 * s], part[4 * s + 1], part[4 * s + 2], part[4 * s + 3]);
+            const float x = slot_sum<GQ>(s, part);
             lg[tk][s] = valid ? x : -INFINITY;
         }
     }
@@ -508,7 +534,10 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
             const float alpha = __builtin_amdgcn_exp2f(st.m[s] - mnew);
             st.m[s] = mnew;
             st.l[s] *= alpha;
-            gather4(alpha, al + 4 * s);
+            if (lone_slot<GQ>(s))
+                al[4 * s] = alpha;
+            else
+                gather4(alpha, al + 4 * s);
         }
 #pragma unroll
         for (int hh = 0; hh < GQ; ++hh) {
@@ -533,7 +562,12 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
     for (int tk = 0; tk < NT; ++tk) {
         float pg[4 * NS];
 #pragma unroll
-        for (int s = 0; s < NS; ++s) gather4(p[tk][s], pg + 4 * s);
+        for (int s = 0; s < NS; ++s) {
+            if (lone_slot<GQ>(s))
+                pg[4 * s] = p[tk][s];
+            else
+                gather4(p[tk][s], pg + 4 * s);
+        }
         const uint32_t vm = tk ? r.m3 : r.m2;
         const float vs = h2f(vm & 0xffffu), vz = h2f(vm >> 16);
         constexpr float centre = 0.5f * (float)((1 << VB) - 1);
@@ -1331,7 +1365,7 @@ __device__ __forceinline__ void sig_page(const SigArgs& a, uint8_t* pg, int pbyt
         float x = 0.f;
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            const float lg = xsum4(part[4 * s], part[4 * s + 1], part[4 * s + 2], part[4 * s + 3]);
+            const float lg = slot_sum<GQ>(s, part);
             const float pr = 4 * s + (int)grp < GQ ? __builtin_amdgcn_exp2f(lg - lse2[s]) : 0.f;
             x = fmax_sel(x, pr);
         }

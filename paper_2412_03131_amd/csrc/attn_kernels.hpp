@@ -297,6 +297,9 @@ typedef __attribute__((address_space(3))) uint32_t lds_u32;
 typedef __attribute__((address_space(3))) _Float16 lds_f16;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) u32x4 lds_u4;
+typedef __attribute__((address_space(3))) float lds_f32;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) f32x4 lds_f4;
 
 // Buffer loads with an LDS destination: lane L's 16 (or 4) bytes land at byte
 // m0 + 16 L (or m0 + 4 L).  Written as asm so that the compiler, which would
@@ -384,6 +387,7 @@ struct CoefLds {
     static constexpr int kRow = 16 * kH + 4;     // dwords per row (16 pairs)
     uint32_t v[kAttnWaves][4 * kRow];
 };
+static_assert(4 * CoefLds<1>::kRow >= 32 * 4, "a wave's weight area holds one slot's softmax weights");
 
 // Sum over the four rows with a transpose: row r of the result holds the sum of
 // argument r (heads a, b, c, d -> rows 0, 1, 2, 3).
@@ -412,7 +416,7 @@ __device__ __forceinline__ float rows_allsum(float v)
 template <int GQ>
 constexpr bool lone_slot(int s)
 {
-    return GQ % 4 == 1 && GQ > 1 && s == (GQ + 3) / 4 - 1;
+    return GQ % 4 == 1 && s == (GQ + 3) / 4 - 1;
 }
 
 // The transposed row sum of slot s: row r gets head 4s + r (a lone head: every row).
@@ -471,7 +475,7 @@ template <int GQ, int KB, int VB, int T>
 __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, const uint32_t (&qr)[GQ],
                                         const half2_t (&q0)[GQ],
                                         const float (&qsum)[GQ], float sl2, int n_valid, int lane,
-                                        lds_u32* coef_row)
+                                        lds_u32* coef_row, lds_f32* px)
 {
     constexpr int NS = WaveState<GQ>::NS;
     constexpr int kH = CoefLds<GQ>::kH;
@@ -556,18 +560,34 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         }
     }
     // ---- value weights of token jl + 16*tk for this lane's group (row), all
-    // heads: fp16 to LDS, zero-point and rounding terms into z
+    // heads: fp16 to LDS, zero-point and rounding terms into z.  First every
+    // slot's heads (one per row) of the lane's tokens reach every row through
+    // LDS: a write and a read on the LDS pipe instead of three lane swaps and
+    // their copies on the VALU (the wave's LDS operations complete in order, so
+    // a read sees all four rows).  The exchange uses the start of the wave's
+    // weight area, so all of it ends before the first weight is written there.
+    float pg[NT][4 * NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (lone_slot<GQ>(s)) {
+#pragma unroll
+            for (int tk = 0; tk < NT; ++tk) pg[tk][4 * s] = p[tk][s];
+            continue;
+        }
+#pragma unroll
+        for (int tk = 0; tk < NT; ++tk) px[(jl + 16 * tk) * 4 + (lane >> 4)] = p[tk][s];
+#pragma unroll
+        for (int tk = 0; tk < NT; ++tk) {
+            const f32x4 v = *reinterpret_cast<const lds_f4*>(px + (jl + 16 * tk) * 4);
+            pg[tk][4 * s] = v.x;
+            pg[tk][4 * s + 1] = v.y;
+            pg[tk][4 * s + 2] = v.z;
+            pg[tk][4 * s + 3] = v.w;
+        }
+    }
     lds_f16* crow = reinterpret_cast<lds_f16*>(coef_row);
 #pragma unroll
     for (int tk = 0; tk < NT; ++tk) {
-        float pg[4 * NS];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            if (lone_slot<GQ>(s))
-                pg[4 * s] = p[tk][s];
-            else
-                gather4(p[tk][s], pg + 4 * s);
-        }
         const uint32_t vm = tk ? r.m3 : r.m2;
         const float vs = h2f(vm & 0xffffu), vz = h2f(vm >> 16);
         constexpr float centre = 0.5f * (float)((1 << VB) - 1);
@@ -581,8 +601,8 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         lds_f16* dst = crow + pi * 2 * kH + pos;
 #pragma unroll
         for (int hh = 0; hh < GQ; ++hh) {
-            const _Float16 c = (_Float16)(pg[hh] * vs_c);
-            st.z[hh] = fmaf(pg[hh], zc, st.z[hh]);
+            const _Float16 c = (_Float16)(pg[tk][hh] * vs_c);
+            st.z[hh] = fmaf(pg[tk][hh], zc, st.z[hh]);
             st.z[hh] = fmaf(-cc, (float)c, st.z[hh]);
             dst[2 * hh] = c;
         }
@@ -805,6 +825,9 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     using LY = Lay<LI>;
     constexpr long long page_bytes = LY::page_bytes;  // (the layout check guarantees it)
     lds_u32* coef_row = (lds_u32*)(&coef->v[wave][grp * CoefLds<GQ>::kRow]);
+    // one slot's softmax weights [token][row] pass through the start of the wave's
+    // weight area before the page's weights are written there
+    lds_f32* px = (lds_f32*)(&coef->v[wave][0]);
     const int nmine = pb - pa > wave ? (pb - pa - wave + kAttnWaves - 1) / kAttnWaves : 0;
     const int32_t* trow = a.page_table + (long long)t * P;
 
@@ -897,13 +920,14 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
         if (i >= c1 || !ok) return;
         const int p = page_of(i);
-        do_page<GQ, LY::hi.kb, LY::hi.vb, LY::hi.T>(st, r, qr, q0, qsum, sl2, ti.len_hi - p * LY::hi.T, lane, coef_row);
+        do_page<GQ, LY::hi.kb, LY::hi.vb, LY::hi.T>(st, r, qr, q0, qsum, sl2, ti.len_hi - p * LY::hi.T, lane, coef_row,
+                                                   px);
     };
     auto compute_lo = [&](int i, const PageRaw& r, bool ok) {
         if (i >= c1 || !ok) return;
         const int p = page_of(i);
         do_page<GQ, LY::lo.kb, LY::lo.vb, LY::lo.T>(st, r, qr, q0, qsum, sl2, ti.len_lo - (p - ph) * LY::lo.T, lane,
-                                                   coef_row);
+                                                   coef_row, px);
     };
     // Wave priority follows the pages this wave still has: on a SIMD shared
     // with shorter work, the longest work is served first (longest-first

@@ -299,6 +299,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) u32x4 lds_u4;
 typedef __attribute__((address_space(3))) float lds_f32;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) f32x4 lds_f4;
 
 // Buffer loads with an LDS destination: lane L's 16 (or 4) bytes land at byte
@@ -599,12 +601,24 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         int pi, pos;
         coef_slot<VB, T>(tok, pi, pos);
         lds_f16* dst = crow + pi * 2 * kH + pos;
+        // weights rounded to fp16 two heads at a time (one packed conversion)
+        _Float16 c[GQ];
+#pragma unroll
+        for (int hh = 0; hh < GQ; hh += 2) {
+            if (hh + 1 < GQ) {
+                const f32x2 w2 = {pg[tk][hh] * vs_c, pg[tk][hh + 1] * vs_c};
+                const f16x2 c2 = __builtin_convertvector(w2, f16x2);
+                c[hh] = c2.x;
+                c[hh + 1] = c2.y;
+            } else {
+                c[hh] = (_Float16)(pg[tk][hh] * vs_c);
+            }
+        }
 #pragma unroll
         for (int hh = 0; hh < GQ; ++hh) {
-            const _Float16 c = (_Float16)(pg[tk][hh] * vs_c);
             st.z[hh] = fmaf(pg[tk][hh], zc, st.z[hh]);
-            st.z[hh] = fmaf(-cc, (float)c, st.z[hh]);
-            dst[2 * hh] = c;
+            st.z[hh] = fmaf(-cc, (float)c[hh], st.z[hh]);
+            dst[2 * hh] = c[hh];
         }
     }
     __builtin_amdgcn_wave_barrier();

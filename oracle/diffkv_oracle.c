@@ -1014,6 +1014,51 @@ int dko_prompt_significance(int B, const int32_t* new_len, int num_q_heads, int 
     return 0;
 }
 
+/* Prompt-phase significance of the last m tokens of one N-token prompt and
+ * KV head h: the same definition restricted to tokens N-m..N-1, which only
+ * the queries N-m..N-1 reach (each still normalized over its keys 0..j).
+ * q, k point at the prompt's first row ([N][Hq][D], [N][Hkv][D]).
+ * score_tail[i] is the score of token N-m+i, fp64. */
+int dko_prompt_significance_tail(int N, int num_q_heads, int num_kv_heads, int D, const uint16_t* q,
+                                 const uint16_t* k, double sm_scale, int h, int m, double* score_tail)
+{
+    int H = num_kv_heads;
+    if (H <= 0 || num_q_heads % H != 0 || D <= 0 || h < 0 || h >= H || m < 0 || m > N) return 1;
+    int g = num_q_heads / H;
+    int p0 = N - m;
+    double* Kd = (double*)malloc(sizeof(double) * (size_t)N * D);
+    double* logit = (double*)malloc(sizeof(double) * (size_t)N);
+    double* x = (double*)malloc(sizeof(double) * (size_t)N);
+    double* qd = (double*)malloc(sizeof(double) * (size_t)D);
+    for (int p = 0; p < N; p++)
+        for (int d = 0; d < D; d++) Kd[(int64_t)p * D + d] = dko_half_to_float(k[((int64_t)p * H + h) * D + d]);
+    for (int i = 0; i < m; i++) score_tail[i] = 0.0;
+    for (int j = p0; j < N; j++) {
+        for (int p = p0; p <= j; p++) x[p] = 0.0;
+        for (int hq = h * g; hq < (h + 1) * g; hq++) {
+            const uint16_t* qv = q + ((int64_t)j * num_q_heads + hq) * D;
+            for (int d = 0; d < D; d++) qd[d] = dko_half_to_float(qv[d]);
+            double mx = -INFINITY;
+            for (int p = 0; p <= j; p++) {
+                double dot = 0.0;
+                for (int d = 0; d < D; d++) dot += qd[d] * Kd[(int64_t)p * D + d];
+                logit[p] = sm_scale * dot;
+                if (logit[p] > mx) mx = logit[p];
+            }
+            double l = 0.0;
+            for (int p = 0; p <= j; p++) l += exp(logit[p] - mx);
+            for (int p = p0; p <= j; p++) {
+                double pr = exp(logit[p] - mx) / l;
+                if (pr > x[p]) x[p] = pr;
+            }
+        }
+        for (int p = p0; p <= j; p++) score_tail[p - p0] += x[p];
+    }
+    for (int p = p0; p < N; p++) score_tail[p - p0] /= (double)(N - p);
+    free(Kd); free(logit); free(x); free(qd);
+    return 0;
+}
+
 /* ======================================================================
  * Memory accounting against FP16 (Sec. 1, Fig. 1): bits of the kept
  * key/value codes over the bits of n_total FP16 keys/values.

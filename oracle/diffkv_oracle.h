@@ -171,6 +171,10 @@ int dko_update_significance(const dko_layout* L, dko_cache* C, int num_q_heads,
 int dko_prompt_significance(int B, const int32_t* new_len, int num_q_heads, int num_kv_heads,
                             int D, const uint16_t* q, const uint16_t* k, double sm_scale,
                             const uint8_t* select, float* score);
+/* Scores (fp64) of the last m tokens of one N-token prompt for KV head h; q
+ * and k point at the prompt's first row.  1 on bad arguments. */
+int dko_prompt_significance_tail(int N, int num_q_heads, int num_kv_heads, int D, const uint16_t* q,
+                                 const uint16_t* k, double sm_scale, int h, int m, double* score_tail);
 
 void dko_kv_bits_fraction(const dko_layout* L, int n_hi, int n_lo,
                           int n_total, double* k_frac, double* v_frac);

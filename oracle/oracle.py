@@ -74,6 +74,8 @@ def _setup(L):
     L.dko_update_significance.restype = C.c_int
     L.dko_prompt_significance.argtypes = [C.c_int, vp, C.c_int, C.c_int, C.c_int, vp, vp, f64, vp, vp]
     L.dko_prompt_significance.restype = C.c_int
+    L.dko_prompt_significance_tail.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, vp, vp, f64, C.c_int, C.c_int, vp]
+    L.dko_prompt_significance_tail.restype = C.c_int
     L.dko_float_to_half.restype = C.c_uint16
     L.dko_float_to_half.argtypes = [f32]
     L.dko_half_to_float.restype = f32
@@ -251,6 +253,19 @@ def prompt_significance(new_len, q, k, sm_scale, select=None, out=None):
                                      None if sel is None else _p(sel), _p(score)):
         raise ValueError("oracle: bad shapes")
     return score
+
+
+def prompt_significance_tail(q, k, sm_scale, h, m):
+    """Scores (fp64) of the last m tokens of one prompt (q [N][Hq][D], k [N][Hkv][D]
+    fp16 bits) for KV head h."""
+    q = np.ascontiguousarray(q, np.uint16)
+    k = np.ascontiguousarray(k, np.uint16)
+    N, Hq, D = q.shape
+    out = np.zeros(m)
+    if lib().dko_prompt_significance_tail(N, Hq, k.shape[1], D, _p(q), _p(k), float(sm_scale), int(h), int(m),
+                                          _p(out)):
+        raise ValueError("oracle: bad arguments")
+    return out
 
 
 def attention_partial(cache, q, sm_scale, b, hq, p0, p1):

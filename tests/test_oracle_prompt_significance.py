@@ -185,3 +185,18 @@ def test_decode_update_continues_the_prompt_scores(orc):
             _, _, sc, p = orc.read_token(c, h, 0, u)
             got[p] = sc
         assert np.allclose(got, s_n1[:, h], rtol=2e-6, atol=1e-12), h
+
+
+def test_tail_equals_the_full_scores(orc):
+    """The tail function (only the last m queries) gives the full function's scores of
+    the last m tokens, bit for bit after rounding to fp32."""
+    rng = np.random.default_rng(250)
+    N, Hkv, g = 90, 2, 3
+    q = f16(rng.standard_normal((N, Hkv * g, D)))
+    k = f16(rng.standard_normal((N, Hkv, D)) * 2)
+    full = orc.prompt_significance(np.array([N], np.int32), q, k, SCALE)
+    for h in range(Hkv):
+        for m in (1, 7, N):
+            tail = orc.prompt_significance_tail(q, k, SCALE, h, m)
+            assert np.array_equal(tail.astype(np.float32), full[N - m:, h]), (h, m)
+    assert orc.prompt_significance_tail(q, k, SCALE, 0, 1)[0] > 0.0

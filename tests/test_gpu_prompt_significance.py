@@ -8,7 +8,8 @@ flushed to zero on the GPU).  Cases: every group size 1-8 over ragged prompts th
 several query and key blocks with ragged tails; lengths 0, 1 and block multiples;
 row normalizers passed in (the row pass skipped); rows cut at total_new; the full
 llama8b prompt batch (B=64, Hq=32, Hkv=8, prompts of 1024-4096 tokens) on sampled
-tables, plus a row-sum property over every table with one head per KV head.
+tables, plus a row-sum property over every table with one head per KV head; two
+32768-token prompts at the long32k head shape on the last tokens of sampled tables.
 """
 import numpy as np
 import pytest
@@ -159,3 +160,27 @@ def test_row_sums_one_head_per_kv_head_full_size():
         N = int(new_len[b])
         tot = (s[off[b]:off[b + 1]] * (N - np.arange(N))[:, None]).sum(axis=0)
         assert np.allclose(tot, N, rtol=1e-4), (b, tot)
+
+
+def test_long_context_prompt_tail():
+    """Two 32768-token prompts at the long32k head shape (Hq=40, Hkv=8): the last 48
+    tokens of three tables against the oracle (they depend only on the last 48
+    queries, each over its whole causal row), every score finite and in (0, 1]."""
+    cfg = inputs.CONFIGS["long32k"]
+    N, Hq, Hkv = 32768, cfg["Hq"], cfg["Hkv"]
+    w = inputs.prefill("long32k", B=2)
+    new_len = w["new_len"]
+    assert list(new_len) == [N, N]
+    rows = 2 * N
+    q = inputs.prompt_queries("long32k", rows)
+    print("case: prompt significance, two 32768-token prompts (Hq %d, Hkv %d)" % (Hq, Hkv), flush=True)
+    got = dk.prompt_significance(LD, t(new_len), t(q).view(torch.float16), t(w["k"]).view(torch.float16), SCALE)
+    torch.cuda.synchronize()
+    g = got.cpu().numpy()
+    assert np.all(np.isfinite(g)) and np.all(g >= 0) and np.all(g <= 1.0 + 1e-6)
+    m = 48
+    for b, h in ((0, 0), (1, 3), (1, 7)):
+        print("case: oracle tail, sequence %d head %d" % (b, h), flush=True)
+        r0 = b * N
+        want = orc.prompt_significance_tail(q[r0:r0 + N], w["k"][r0:r0 + N], SCALE, h, m)
+        _close(g[r0 + N - m:r0 + N, h], want, "32k tail (%d, %d)" % (b, h))

@@ -225,8 +225,9 @@ diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_c
  *        ranges, merged the same way (S = 1: no split, no merge).  Results
  *        are deterministic for a given mode and device.
  *   ws   device workspace of diffkv_workspace_size(DIFFKV_OP_ATTENTION, ...)
- *        bytes (always needed: it holds the work bookkeeping and partial
- *        states).
+ *        bytes (always needed: it holds the split tables' partial states and
+ *        one arrival word per table, which each call tags as its own, so the
+ *        workspace needs no clearing between calls).
  * num_q_heads must be a multiple of num_kv_heads, with at most 8 query heads
  * per KV head.
  * Precision: q . k_hat is exact up to fp32 summation (codes and q enter fp16
@@ -246,7 +247,7 @@ diffkv_status diffkv_decode_attention(const diffkv_layout* layout, const diffkv_
  * diffkv_decode_attention without a workspace, for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc).  Same arguments, minus ws / ws_bytes, and
- * the same kernels and results, bit for bit.  The work bookkeeping and split
+ * the same kernels and results, bit for bit.  The arrival words and split
  * partial states go to a fixed 8 MiB array in the library's device memory, one
  * per device, held from the library's load until the process ends; its device
  * address is looked up on the first call on each device and kept (the one

@@ -140,11 +140,12 @@ AppendWs append_ws(int64_t B, int64_t Hkv, int64_t total_new)
     return w;
 }
 
-// Attention workspace: automatic (0) or balanced (-1) mode: per-table first
-// unit, the unit total and one partial state per (share, table) slot k + t;
-// split mode (S > 1): S partial states per table; S = 1 needs none.
+// Attention workspace: one arrival word per table (split tables count their
+// shares' partial states in it), then the partial states: automatic (0) or
+// balanced (-1) mode one per (share, table) slot k + t; split mode (S > 1) S
+// per table; S = 1 needs none.
 struct AttnWs {
-    int64_t ustart, utot, part, total, nparts;
+    int64_t arrive, part, total, nparts;
 };
 
 AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits, int64_t workers)
@@ -154,8 +155,7 @@ AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits, int64_t worke
     const int64_t gq = Hkv > 0 ? Hq / Hkv : 1;
     w.nparts = splits <= 0 ? workers + T : (splits > 1 ? T * splits : 0);
     int64_t o = 0;
-    w.ustart = o; o = align256(o + T * 8);
-    w.utot = o;   o = align256(o + 8);
+    w.arrive = o; o = align256(o + T * 8);
     w.part = o;   o = align256(o + w.nparts * gq * (kD + 2) * 4);
     w.total = o;
     return w;
@@ -242,8 +242,7 @@ diffkv_status attention_call(const diffkv_layout* layout, const diffkv_cache* ca
     a.lse = lse;
     a.splits = num_splits;
     uint8_t* base = static_cast<uint8_t*>(ws);
-    a.ustart = reinterpret_cast<long long*>(base + w.ustart);
-    a.utot = reinterpret_cast<long long*>(base + w.utot);
+    a.arrive = reinterpret_cast<unsigned long long*>(base + w.arrive);
     a.part = reinterpret_cast<float*>(base + w.part);
     a.layout = layout_index(layout);
     hipError_t e = launch_attention(a, static_cast<hipStream_t>(stream));

@@ -21,12 +21,11 @@ constexpr bool layout_wide_values(int li)
 }
 constexpr int attn_blocks_per_cu(int gq, int li) { return gq <= (layout_wide_values(li) ? 5 : 6) ? 2 : 1; }
 constexpr int kPartStride = kD + 2;
-constexpr int kMergeThreads = 256;
 constexpr int kSigWaves = 4;
 constexpr int kSigPages = 16;  // pages per workgroup of attn_significance
 
 // Kernel entry points of layout n (k_attn_l<n>.hip): which = 0 attn_decode,
-// 1 attn_significance, 2 attn_merge (gq ignored); nullptr for an unknown gq.
+// 1 attn_significance; nullptr for an unknown gq.
 const void* attn_kernel_l0(int gq, int which);
 const void* attn_kernel_l1(int gq, int which);
 const void* attn_kernel_l2(int gq, int which);

@@ -6,7 +6,8 @@
 // one eight-wave workgroup for all GQ query heads that read them, or -- in the
 // balanced mode -- every table's pages are laid end to end and cut into one
 // equal share per resident workgroup, so the spread of table lengths costs
-// nothing; tables that straddle shares are merged by attn_merge.  Inside a
+// nothing; a table that straddles shares is merged by the last of them to
+// finish (split tables below).  Inside a
 // workgroup each wave takes every eighth page, one register buffer per wave:
 // with two workgroups per CU four waves share each SIMD, so the waves hide
 // each other's page loads, and a table left alone on its CU still runs two
@@ -778,6 +779,11 @@ struct AttnShared {
     int t_first;
     int len_first[2];  // section lengths of t_first (longest-first ranking)
     long long u_first;
+    int last;          // this workgroup is the last of a split table's shares
+    unsigned long long tag;  // this call's tag (arrival words)
+    long long units;         // balanced mode: the unit total of all tables
+    int pend_t[2];           // balanced mode: split tables of this share, and
+    long long pend_u[2];     // their first units (arrivals after the walk)
 };
 
 // Exclusive prefix sum of one 64-bit value per thread of the workgroup.
@@ -813,6 +819,160 @@ __device__ __forceinline__ void write_empty(const AttnArgs& a, int t, int gq)
         a.out[row * kD + d] = 0.f;
         if (d == 0 && a.lse) a.lse[row] = -INFINITY;
     }
+}
+
+// The same from one thread (an empty table met by one thread of the balanced
+// mode's table scan).
+__device__ __forceinline__ void write_empty_one(const AttnArgs& a, int t, int gq)
+{
+    const int b = t / a.Hkv, h = t - b * a.Hkv;
+    for (int hh = 0; hh < gq; ++hh) {
+        const long long row = (long long)b * a.Hq + h * gq + hh;
+        float4* o = reinterpret_cast<float4*>(a.out + row * kD);
+        for (int i = 0; i < kD / 4; ++i) o[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (a.lse) a.lse[row] = -INFINITY;
+    }
+}
+
+// ---- split tables: merged by the last of their shares -------------------
+// A table whose pages went to n > 1 workgroups is merged inside the launch
+// by the last of them to finish.  Each writes its partial state {max, sum,
+// acc} per head with agent-scope stores (written through to memory, where
+// every XCD's accesses meet), waits until they are done, and counts itself in
+// the table's arrival word with agent-scope atomics; the one that brings the
+// count to n reads the n states back with agent-scope loads, in page order,
+// and writes the output.  Every byte that crosses workgroups goes through
+// agent-scope accesses, so no cache-wide release or acquire (an L2 writeback
+// and invalidate per workgroup) is needed.
+//
+// An arrival word is a 44-bit call tag above a 20-bit count (n is at most
+// 65535 split ranges or the share count plus one), and a word whose tag is not
+// this call's counts as zero: the workspace needs no clearing, and what an
+// earlier call left there is never taken for this one's.  The tag is the
+// dispatch's packet index in its hardware queue (32 bits) with 12 bits of the
+// queue's address (queues count their packets separately).
+extern "C" __device__ unsigned long long dkv_dispatch_id() __asm("llvm.amdgcn.dispatch.id");
+
+__device__ __forceinline__ unsigned long long call_tag()
+{
+    const unsigned long long q = (unsigned long long)(size_t)__builtin_amdgcn_queue_ptr();
+    return (dkv_dispatch_id() & 0xffffffffull) | ((((q >> 12) ^ (q >> 24)) & 0xfffull) << 32);
+}
+
+constexpr int kArriveCountBits = 20;
+
+__device__ __forceinline__ void put_part(float* p, float v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 get_part2(const float* p)  // p 8-byte aligned
+{
+    const unsigned long long v = __hip_atomic_load(reinterpret_cast<unsigned long long*>(const_cast<float*>(p)),
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+
+// The kernel's arguments read afresh from the kernel argument segment (the
+// attention kernel's one argument sits at its start), through a pointer the
+// compiler cannot see through: what the code after the page loops reads from
+// it is loaded there, not at the kernel's start and kept in registers across
+// the loops.
+__device__ __forceinline__ const AttnArgs& late_args()
+{
+    typedef const __attribute__((address_space(4))) AttnArgs* karg_ptr;
+    karg_ptr p = (karg_ptr)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(p));
+    return *(const AttnArgs*)p;
+}
+
+// After the workgroup wrote its partial state of table t: whether it is the
+// n-th of the table's shares to arrive (uniform over the workgroup).
+template <int GQ>
+__device__ __forceinline__ bool arrive_last(const AttnArgs& a, AttnShared<GQ>& sh, int t, int n)
+{
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's partial stores are done
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long* w = a.arrive + t;
+        const unsigned long long tag = sh.tag;
+        constexpr unsigned long long kCount = (1ull << kArriveCountBits) - 1;
+        // One add counts this arrival when the word already carries this
+        // call's tag (every arrival but, normally, a table's first).  An add
+        // that lands on another call's word counts nothing: the word is then
+        // taken over by compare-and-swap (tag, 1), or, once another arrival
+        // has done that, counted in by compare-and-swap as well.
+        unsigned long long old = __hip_atomic_fetch_add(w, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        unsigned long long cnt;
+        if ((old >> kArriveCountBits) == tag) {
+            cnt = old & kCount;
+        } else {
+            old += 1;
+            for (;;) {
+                cnt = (old >> kArriveCountBits) == tag ? (old & kCount) : 0ull;
+                const unsigned long long nw = (tag << kArriveCountBits) | (cnt + 1);
+                if (__hip_atomic_compare_exchange_strong(w, &old, nw, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT))
+                    break;
+            }
+        }
+        sh.last = cnt + 1 == (unsigned long long)n;
+    }
+    __syncthreads();
+    return __builtin_amdgcn_readfirstlane(sh.last) != 0;
+}
+
+// Output of table t from the partial states of its nsl share slots at `base`
+// (slot j at base + j * GQ * kPartStride; wrote(j): slot j holds a state), in
+// page order.  One wave per query head, lane = dims 2*lane, 2*lane+1; the
+// first kPre slots' loads are all issued before any is used (one round trip
+// for the usual two to five shares of a table).
+template <int GQ, typename Wrote>
+__device__ __forceinline__ void merge_parts(const AttnArgs& a, int t, const float* base, int nsl, Wrote wrote)
+{
+    const int b = t / a.Hkv, h = t - b * a.Hkv;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int hh = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const long long stride = (long long)GQ * kPartStride;
+    static_assert(GQ <= kAttnWaves, "one wave per query head");
+    if (hh < GQ) {
+        const float* pr = base + hh * kPartStride;
+        constexpr int kPre = 8;
+        float2 ml[kPre], o[kPre];
+#pragma unroll
+        for (int j = 0; j < kPre; ++j) {
+            const bool ok = j < nsl && wrote(j);
+            ml[j] = ok ? get_part2(pr + j * stride) : make_float2(-INFINITY, 0.f);
+            o[j] = ok ? get_part2(pr + j * stride + 2 + 2 * lane) : make_float2(0.f, 0.f);
+        }
+        float M = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < kPre; ++j) M = fmax_sel(M, ml[j].x);
+        for (int j = kPre; j < nsl; ++j)
+            if (wrote(j)) M = fmax_sel(M, get_part2(pr + j * stride).x);
+        float L = 0.f, O0 = 0.f, O1 = 0.f;
+        if (M != -INFINITY) {
+#pragma unroll
+            for (int j = 0; j < kPre; ++j) {
+                const float f = __builtin_amdgcn_exp2f(ml[j].x - M);  // 0 for slots without a state
+                L = fmaf(ml[j].y, f, L);
+                O0 = fmaf(o[j].x, f, O0);
+                O1 = fmaf(o[j].y, f, O1);
+            }
+            for (int j = kPre; j < nsl; ++j) {
+                if (!wrote(j)) continue;
+                const float2 mj = get_part2(pr + j * stride), oj = get_part2(pr + j * stride + 2 + 2 * lane);
+                const float f = __builtin_amdgcn_exp2f(mj.x - M);
+                L = fmaf(mj.y, f, L);
+                O0 = fmaf(oj.x, f, O0);
+                O1 = fmaf(oj.y, f, O1);
+            }
+        }
+        const long long row = (long long)b * a.Hq + h * GQ + hh;
+        *reinterpret_cast<float2*>(a.out + row * kD + 2 * lane) =
+            (L > 0.f) ? make_float2(O0 / L, O1 / L) : make_float2(0.f, 0.f);
+        if (lane == 0 && a.lse) a.lse[row] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
+    }
+    __syncthreads();  // sh.last is read again by the next arrival
 }
 
 // ---------------------------------------------------------------------------
@@ -1022,10 +1182,10 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
             if (d == 0 && a.lse) a.lse[row] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
         } else {
             float* pr = part + hh * kPartStride;
-            pr[2 + d] = O;
+            put_part(pr + 2 + d, O);
             if (d == 0) {
-                pr[0] = M;
-                pr[1] = L;
+                put_part(pr, M);
+                put_part(pr + 1, L);
             }
         }
     }
@@ -1042,7 +1202,8 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
 //    prefix sum over the tables' units, then walks its tables.  A table lying
 //    inside one share is finished in place; otherwise share k writes its
 //    partial state to slot k + t (distinct for every (share, table) pair met
-//    in this walk) and attn_merge combines them.
+//    in this walk) and the last of the table's shares to arrive merges them.
+//    An empty table's output is written by workgroup t % W.
 // ---------------------------------------------------------------------------
 // Table of rank j when the tables are ordered by decreasing work units
 // (bucketed into 1024 bins, ties by index): workgroups are dispatched in
@@ -1161,6 +1322,9 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
     __shared__ AttnShared<GQ> sh;
     __shared__ CoefLds<GQ> coef;
     __shared__ PageStage<Lay<LI>::nv> stage[kAttnWaves];
+    // the call tag goes to LDS at once, so the registers it comes in are free
+    // for the rest of the kernel (read after the workgroup's first barrier)
+    if (threadIdx.x == 0) sh.tag = call_tag();
     const int T = a.B * a.Hkv;
     if (a.splits > 0) {
         const int j = blockIdx.x / a.splits, c = blockIdx.x - j * a.splits;
@@ -1173,8 +1337,13 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
         }
         if (c >= n) return;
         const int pa = (int)((long long)c * ti.np / n), pb = (int)((long long)(c + 1) * ti.np / n);
-        float* part = n == 1 ? nullptr : a.part + ((long long)t * a.splits + c) * GQ * kPartStride;
+        float* base = a.part + (long long)t * a.splits * GQ * kPartStride;
+        float* part = n == 1 ? nullptr : base + (long long)c * GQ * kPartStride;
         run_segment<GQ, LI>(a, sh, &coef, stage, t, ti, pa, pb, part);
+        if (part != nullptr) {
+            const AttnArgs& al = late_args();
+            if (arrive_last<GQ>(al, sh, t, n)) merge_parts<GQ>(al, t, base, n, [](int) { return true; });
+        }
         return;
     }
     // ---- balanced shares -------------------------------------------------
@@ -1197,12 +1366,18 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
         for (int i = 0; i < kKeep; ++i) {
             units[i] = t0 + i < t1 ? table_info_of<LI>(a, lh[i], ll[i]).units : 0;
             mine += units[i];
+            // an empty table's output comes from workgroup t % W
+            if (t0 + i < t1 && units[i] == 0 && (t0 + i) % W == k) write_empty_one(a, t0 + i, GQ);
         }
     }
-    for (int t = t0 + kKeep; t < t1; ++t) mine += table_info<LI>(a, t).units;
+    for (int t = t0 + kKeep; t < t1; ++t) {
+        const long long u = table_info<LI>(a, t).units;
+        mine += u;
+        if (u == 0 && t % W == k) write_empty_one(a, t, GQ);
+    }
     long long total;
     const long long before = wg_excl_scan(mine, sh.scan, &total);
-    if (k == 0 && threadIdx.x == 0) a.utot[0] = total;
+    if (threadIdx.x == 0) sh.units = total;  // read back by the arrival (not kept in registers)
     const long long b_lo = k * total / W, b_hi = (k + 1) * total / W;
     if (b_lo >= b_hi) return;
     long long u = before;
@@ -1221,122 +1396,49 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
     __syncthreads();
     int t = __builtin_amdgcn_readfirstlane(sh.t_first);
     long long ut = read_lane<long long>(sh.u_first, 0);
+    // A share holds at most two split tables, its first and its last (the
+    // tables between lie inside it); their arrivals wait until the walk is
+    // done, which delays no merge, since the shares end together, and keeps
+    // the merge code out of the walk's registers.
+    int npend = 0;
     while (t < T && ut < b_hi) {
         const TableInfo ti = table_info<LI>(a, t);
         if (ti.units > 0) {
             const int pa = page_at_unit<LI>(b_lo - ut, ti.ph, ti.np);
             const int pb = page_at_unit<LI>(b_hi - ut, ti.ph, ti.np);
-            const bool first = ut >= b_lo;
-            const bool whole = first && ut + ti.units <= b_hi;
-            if (first && threadIdx.x == 0) a.ustart[t] = ut;
+            const bool whole = ut >= b_lo && ut + ti.units <= b_hi;
             run_segment<GQ, LI>(a, sh, &coef, stage, t, ti, pa, pb, whole ? nullptr : a.part + (k + t) * GQ * kPartStride);
+            if (!whole) {
+                if (threadIdx.x == 0) {
+                    sh.pend_t[npend] = t;
+                    sh.pend_u[npend] = ut;
+                }
+                ++npend;
+            }
         }
         ut += ti.units;
         ++t;
     }
-}
-
-// ---------------------------------------------------------------------------
-// attn_merge: one wave per (table, query head) of a table whose pages went to
-// several workgroups; combines their partial states in page order.  Also
-// writes the empty result of empty tables in the balanced mode.  Partial
-// slots of shares with an empty unit range are never read (they hold
-// whatever an earlier call left there).
-// ---------------------------------------------------------------------------
-
-template <int LI>
-__global__ __launch_bounds__(kMergeThreads) void attn_merge(AttnArgs a)
-{
-    const int gq = a.Hq / a.Hkv;
-    const long long job = (long long)blockIdx.x * (kMergeThreads / kWave) + threadIdx.x / kWave;
-    const int T = a.B * a.Hkv;
-    if (job >= (long long)T * gq) return;
-    const int t = (int)(job / gq), hh = (int)(job - (long long)t * gq);
-    const int lane = threadIdx.x & (kWave - 1);
-    const TableInfo ti = table_info<LI>(a, t);
-    const int b = t / a.Hkv, h = t - b * a.Hkv;
-    const long long row = (long long)b * a.Hq + h * gq + hh;
-    // candidate partial slots first + i, i < n; in the balanced mode a share
-    // whose unit range is empty (more shares than units) wrote nothing
-    long long first, kf = 0, U = 1, W = 1;
-    int n;
-    if (a.splits > 0) {
-        n = ti.np < a.splits ? ti.np : a.splits;
-        if (n <= 1) return;  // written by attn_decode
-        first = (long long)t * a.splits;
-    } else {
-        if (ti.units == 0) {
-            a.out[row * kD + 2 * lane] = 0.f;
-            a.out[row * kD + 2 * lane + 1] = 0.f;
-            if (lane == 0 && a.lse) a.lse[row] = -INFINITY;
-            return;
+    const AttnArgs& al = late_args();
+    for (int i = 0; i < npend; ++i) {
+        __syncthreads();
+        const int tp = __builtin_amdgcn_readfirstlane(sh.pend_t[i]);
+        const long long up = read_lane<long long>(sh.pend_u[i], 0);
+        const long long U = read_lane<long long>(sh.units, 0);
+        const long long units = table_info<LI>(al, tp).units;
+        // shares kf .. kl own the table's units (the owner of unit x is the
+        // largest k with k*U/W <= x); with fewer units than shares some of
+        // them own none and wrote nothing
+        const long long kf = ((up + 1) * W - 1) / U, kl = ((up + units) * W - 1) / U;
+        const int nsl = (int)(kl - kf + 1);
+        auto wrote = [&](int j) { return U >= W || (kf + j) * U / W != (kf + j + 1) * U / W; };
+        int n = nsl;
+        if (U < W) {
+            n = 0;
+            for (int j = 0; j < nsl; ++j) n += wrote(j) ? 1 : 0;
         }
-        U = a.utot[0];
-        W = a.workers;
-        const long long ut = a.ustart[t];
-        // share owning unit x: the largest k with k*U/W <= x
-        kf = ((ut + 1) * W - 1) / U;
-        const long long kl = ((ut + ti.units) * W - 1) / U;
-        if (kf == kl) return;  // written by attn_decode
-        n = (int)(kl - kf + 1);
-        first = kf + t;
+        if (arrive_last<GQ>(al, sh, tp, n)) merge_parts<GQ>(al, tp, al.part + (kf + tp) * GQ * kPartStride, nsl, wrote);
     }
-    auto wrote = [&](int i) {
-        if (a.splits > 0) return true;
-        const long long k = kf + i;
-        return k * U / W != (k + 1) * U / W;
-    };
-    const float* base = a.part + first * gq * kPartStride + hh * kPartStride;
-    const long long stride = (long long)gq * kPartStride;
-    // the first kPre partials' acc pairs are loaded together with every
-    // partial's (max, sum): one round of loads for the usual 2-4 partials
-    constexpr int kPre = 4;
-    float2 pre[kPre];
-#pragma unroll
-    for (int j = 0; j < kPre; ++j)
-        pre[j] = j < n && wrote(j) ? *reinterpret_cast<const float2*>(base + j * stride + 2 + 2 * lane)
-                                   : make_float2(0.f, 0.f);
-    float M = -INFINITY;
-    for (int i = lane; i < n; i += kWave)
-        if (wrote(i)) M = fmax_sel(M, base[i * stride]);
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) M = fmax_sel(M, __shfl_xor(M, o, kWave));
-    float L = 0.f, O0 = 0.f, O1 = 0.f;
-    if (M != -INFINITY) {
-        float Lp = 0.f;
-        for (int i0 = 0; i0 < n; i0 += kWave) {
-            // weight of partial i0 + lane (0 for slots never written)
-            const int i = i0 + lane;
-            float f = 0.f;
-            if (i < n && wrote(i)) {
-                f = __builtin_amdgcn_exp2f(base[i * stride] - M);
-                Lp = fmaf(base[i * stride + 1], f, Lp);
-            }
-            int j = 0;
-            if (i0 == 0) {
-#pragma unroll
-                for (; j < kPre; ++j) {
-                    const float fj = __shfl(f, j, kWave);
-                    O0 = fmaf(pre[j].x, fj, O0);
-                    O1 = fmaf(pre[j].y, fj, O1);
-                }
-            }
-            const int cnt = n - i0 < kWave ? n - i0 : kWave;
-            for (; j < cnt; ++j) {
-                const float fj = __shfl(f, j, kWave);
-                if (fj == 0.f) continue;  // also skips slots never written
-                const float2 o2 = *reinterpret_cast<const float2*>(base + (i0 + j) * stride + 2 + 2 * lane);
-                O0 = fmaf(o2.x, fj, O0);
-                O1 = fmaf(o2.y, fj, O1);
-            }
-        }
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) Lp += __shfl_xor(Lp, o, kWave);
-        L = Lp;
-    }
-    a.out[row * kD + 2 * lane] = (L > 0.f) ? O0 / L : 0.f;
-    a.out[row * kD + 2 * lane + 1] = (L > 0.f) ? O1 / L : 0.f;
-    if (lane == 0 && a.lse) a.lse[row] = (L > 0.f) ? (M + __log2f(L)) * 0.69314718055994530942f : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------
@@ -1477,7 +1579,7 @@ __global__ __launch_bounds__(kSigWaves * kWave) void attn_significance(SigArgs a
 
 
 // Kernel entry points of layout LI (host-side stubs): which = 0 attn_decode,
-// 1 attn_significance, 2 attn_merge (gq ignored).
+// 1 attn_significance.
 template <int LI>
 const void* attn_kernel_of(int gq, int which)
 {
@@ -1485,7 +1587,6 @@ const void* attn_kernel_of(int gq, int which)
     case G:                                                                                \
         return which == 0 ? reinterpret_cast<const void*>(&attn_decode<G, LI>)             \
                           : reinterpret_cast<const void*>(&attn_significance<G, LI>);
-    if (which == 2) return reinterpret_cast<const void*>(&attn_merge<LI>);
     switch (gq) {
         DKV_ATTN_CASE(1)
         DKV_ATTN_CASE(2)

@@ -131,9 +131,7 @@ struct AttnArgs {
     float* out;
     float* lse;
     int splits;          // 0: balanced shares; S >= 1: min(S, pages) ranges per table
-    int workers;         // balanced mode: shares (= workgroups of attn_decode)
-    long long* ustart;   // [T] first work unit of each table (balanced mode)
-    long long* utot;     // [1] total work units (balanced mode)
+    unsigned long long* arrive;  // [T] arrival words of split tables (call tag, count)
     float* part;         // partial states {max, sum, acc[kD]} per head
     int layout;          // index into kLayoutFmts
 };

@@ -11,7 +11,7 @@ namespace dkv {
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-// Kernel entry points of layout li: which = 0 decode, 1 significance, 2 merge.
+// Kernel entry points of layout li: which = 0 decode, 1 significance.
 static const void* attn_kernel_ptr(int li, int gq, int which)
 {
     switch (li) {
@@ -53,7 +53,7 @@ hipError_t attention_mode(int gq, int li, long long T, int splits, int* mode, in
     return hipSuccess;
 }
 
-// The no-allocation entry point's scratch: work bookkeeping and split partial
+// The no-allocation entry point's scratch: arrival words and split partial
 // states of one attention call.  In host code `scratch` names a host-side
 // stand-in, so its device address is looked up once per device (with that
 // device current) and only that address is handed to kernels.
@@ -82,27 +82,15 @@ hipError_t launch_attention(AttnArgs a, hipStream_t st)
 {
     const int gq = a.Hq / a.Hkv;
     const void* kern = attn_kernel_ptr(a.layout, gq, 0);
-    const void* merge = attn_kernel_ptr(a.layout, gq, 2);
-    if (!kern || !merge) return hipErrorInvalidValue;
+    if (!kern) return hipErrorInvalidValue;
     const long long T = (long long)a.B * a.Hkv;
     int workers = 0;
     hipError_t e = attention_mode(gq, a.layout, T, a.splits, &a.splits, &workers);
     if (e != hipSuccess) return e;
-    long long grid;
-    if (a.splits > 0) {
-        grid = T * a.splits;
-        a.workers = 0;
-    } else {
-        a.workers = workers;
-        grid = a.workers;
-    }
+    const long long grid = a.splits > 0 ? T * a.splits : workers;
     if (grid < 1 || grid > INT32_MAX) return hipErrorInvalidValue;
     void* args[] = {&a};
-    e = hipLaunchKernel(kern, dim3((unsigned)grid), dim3(kAttnThreads), args, 0, st);
-    if (e != hipSuccess || a.splits == 1) return e;
-    const long long jobs = T * gq;
-    const long long mgrid = (jobs + kMergeThreads / kWave - 1) / (kMergeThreads / kWave);
-    return hipLaunchKernel(merge, dim3((unsigned)mgrid), dim3(kMergeThreads), args, 0, st);
+    return hipLaunchKernel(kern, dim3((unsigned)grid), dim3(kAttnThreads), args, 0, st);
 }
 
 

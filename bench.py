@@ -762,7 +762,7 @@ def main():
         "config": {"workload": WORKLOADS[args.config], "global_batch": int(wl_B(args.config)),
                    "attention_splits": args.splits},
         "roofline": {
-            "kernel": "diffkv_decode_attention (attn_decode, plus attn_merge when the mode splits tables)",
+            "kernel": "diffkv_decode_attention (attn_decode; split tables merged in the same launch)",
             "bound": "hbm",
             "achieved": head["achieved"],
             "peak": HBM_PEAK_GBPS,

@@ -716,13 +716,15 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
 // ---------------------------------------------------------------------------
 // A table's pages in attention order: high pages 0 .. ph-1 (slots 0 ..), then
 // low pages ph .. np-1 (slots p_max-1 downward).  For balancing, a high page
-// is kHighUnits units of work and a low page kLowUnits (twice the tokens; the
-// measured time per page is about 5:3): page p starts at unit kHighUnits*p
-// (p < ph) or kHighUnits*ph + kLowUnits*(p - ph).
+// is kHighUnits units of work and a low page kLowUnits: the page loops are
+// bound by VALU issue, and a 32-token low page issues twice the instructions
+// of a 16-token high page (both bytes per page being equal), a 16-token low
+// page about as many: page p starts at unit kHighUnits*p (p < ph) or
+// kHighUnits*ph + kLowUnits*(p - ph).
 template <int LI>
 struct Units {
     static constexpr int hi = 3;
-    static constexpr int lo = Lay<LI>::lo.T == 32 ? 5 : 3;
+    static constexpr int lo = Lay<LI>::lo.T == 32 ? 6 : 3;
 };
 
 struct TableInfo {
@@ -986,7 +988,7 @@ __device__ __forceinline__ void merge_parts(const AttnArgs& a, int t, const floa
 template <int GQ, int LI>
 __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& sh, CoefLds<GQ>* coef,
                                             PageStage<Lay<LI>::nv>* stage, int t, const TableInfo& ti, int pa,
-                                            int pb, float* part)
+                                            int pb, float* part, int& done, int target)
 {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -1103,14 +1105,30 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         do_page<GQ, LY::lo.kb, LY::lo.vb, LY::lo.T>(st, r, qr, q0, qsum, sl2, ti.len_lo - (p - ph) * LY::lo.T, lane,
                                                    coef_row, px);
     };
-    // Wave priority follows the pages this wave still has: on a SIMD shared
-    // with shorter work, the longest work is served first (longest-first
-    // scheduling at the wave level; ties go to the older wave).
-    auto set_prio = [&](int rem) {
-        if (rem > 12) __builtin_amdgcn_s_setprio(3);
-        else if (rem > 6) __builtin_amdgcn_s_setprio(2);
-        else if (rem > 2) __builtin_amdgcn_s_setprio(1);
-        else __builtin_amdgcn_s_setprio(0);
+    // Wave priority.  One workgroup per table or range (target 0): it follows
+    // the pages this wave still has, so on a SIMD shared with shorter work the
+    // longest work is served first (longest-first scheduling at the wave
+    // level).  Balanced shares (equal work, target = the wave's part of its
+    // share in units): it follows the part still ahead of the wave, falling
+    // at 60, 30 and 10 % left, so whichever of the waves on a SIMD is further
+    // behind goes first and the two workgroups of a CU finish together; with
+    // one level for all, issue goes to the older wave, and the workgroup
+    // dispatched first ran ahead while its partner finished alone, two waves
+    // per SIMD.  `done` counts the units of the wave's pages taken so far.
+    auto set_prio = [&](int rem, int units) {
+        if (target > 0) {
+            const int left = target - done;
+            if (left * 10 > target * 6) __builtin_amdgcn_s_setprio(3);
+            else if (left * 10 > target * 3) __builtin_amdgcn_s_setprio(2);
+            else if (left * 10 > target) __builtin_amdgcn_s_setprio(1);
+            else __builtin_amdgcn_s_setprio(0);
+            done += units;
+        } else {
+            if (rem > 12) __builtin_amdgcn_s_setprio(3);
+            else if (rem > 6) __builtin_amdgcn_s_setprio(2);
+            else if (rem > 2) __builtin_amdgcn_s_setprio(1);
+            else __builtin_amdgcn_s_setprio(0);
+        }
     };
     // Page i comes out of the LDS slot into registers, page i + 1 goes into the
     // slot, then page i is computed: one page is always in flight while the
@@ -1124,12 +1142,12 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
         const int nh = nhi < c1 ? nhi : c1;  // high pages end (within this chunk)
         int i = c0;
         for (; i < nh; ++i) {
-            set_prio(nmine - i);
+            set_prio(nmine - i, Units<LI>::hi);
             next(i);
             compute_hi(i, buf0, ok0);
         }
         for (; i < c1; ++i) {
-            set_prio(nmine - i);
+            set_prio(nmine - i, Units<LI>::lo);
             next(i);
             compute_lo(i, buf0, ok0);
         }
@@ -1339,7 +1357,8 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
         const int pa = (int)((long long)c * ti.np / n), pb = (int)((long long)(c + 1) * ti.np / n);
         float* base = a.part + (long long)t * a.splits * GQ * kPartStride;
         float* part = n == 1 ? nullptr : base + (long long)c * GQ * kPartStride;
-        run_segment<GQ, LI>(a, sh, &coef, stage, t, ti, pa, pb, part);
+        int done = 0;
+        run_segment<GQ, LI>(a, sh, &coef, stage, t, ti, pa, pb, part, done, 0);
         if (part != nullptr) {
             const AttnArgs& al = late_args();
             if (arrive_last<GQ>(al, sh, t, n)) merge_parts<GQ>(al, t, base, n, [](int) { return true; });
@@ -1401,13 +1420,16 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
     // done, which delays no merge, since the shares end together, and keeps
     // the merge code out of the walk's registers.
     int npend = 0;
+    int done = 0;
+    const int target = (int)((b_hi - b_lo + kAttnWaves - 1) / kAttnWaves);
     while (t < T && ut < b_hi) {
         const TableInfo ti = table_info<LI>(a, t);
         if (ti.units > 0) {
             const int pa = page_at_unit<LI>(b_lo - ut, ti.ph, ti.np);
             const int pb = page_at_unit<LI>(b_hi - ut, ti.ph, ti.np);
             const bool whole = ut >= b_lo && ut + ti.units <= b_hi;
-            run_segment<GQ, LI>(a, sh, &coef, stage, t, ti, pa, pb, whole ? nullptr : a.part + (k + t) * GQ * kPartStride);
+            run_segment<GQ, LI>(a, sh, &coef, stage, t, ti, pa, pb, whole ? nullptr : a.part + (k + t) * GQ * kPartStride,
+                                done, target);
             if (!whole) {
                 if (threadIdx.x == 0) {
                     sh.pend_t[npend] = t;

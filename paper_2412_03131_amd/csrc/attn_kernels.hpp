@@ -719,12 +719,16 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
 // is kHighUnits units of work and a low page kLowUnits: the page loops are
 // bound by VALU issue, and a 32-token low page issues twice the instructions
 // of a 16-token high page (both bytes per page being equal), a 16-token low
-// page about as many: page p starts at unit kHighUnits*p (p < ph) or
-// kHighUnits*ph + kLowUnits*(p - ph).
+// page about as many.  A table's first page also carries kSegUnits, the cost
+// of starting a segment (its query, page-ID and first-page loads, the waves'
+// merge, an arrival), so a balanced share that crosses a table boundary gets
+// fewer pages: page 0 starts at unit 0, page p > 0 at kSegUnits + kHighUnits*p
+// (p <= ph) or kSegUnits + kHighUnits*ph + kLowUnits*(p - ph).
 template <int LI>
 struct Units {
     static constexpr int hi = 3;
     static constexpr int lo = Lay<LI>::lo.T == 32 ? 6 : 3;
+    static constexpr int seg = 80;
 };
 
 struct TableInfo {
@@ -749,7 +753,7 @@ __device__ __forceinline__ TableInfo table_info_of(const AttnArgs& a, int len_hi
     pl = pl < 0 ? 0 : (pl > P - ph ? P - ph : pl);
     ti.ph = ph;
     ti.np = ph + pl;
-    ti.units = (long long)kHighUnits * ph + (long long)kLowUnits * pl;
+    ti.units = ti.np > 0 ? Units<LI>::seg + (long long)kHighUnits * ph + (long long)kLowUnits * pl : 0;
     return ti;
 }
 // t uniform: the section lengths come through scalar loads (the attention
@@ -767,6 +771,8 @@ __device__ __forceinline__ int page_at_unit(long long x, int ph, int np)
 {
     constexpr int kHighUnits = Units<LI>::hi, kLowUnits = Units<LI>::lo;
     if (x <= 0) return 0;
+    x -= Units<LI>::seg;
+    if (x <= 0) return np > 0 ? 1 : 0;
     const long long xh = (long long)kHighUnits * ph;
     const long long p = x <= xh ? (x + kHighUnits - 1) / kHighUnits : ph + (x - xh + kLowUnits - 1) / kLowUnits;
     return p > np ? np : (int)p;
@@ -1251,7 +1257,7 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
         const int lane = threadIdx.x;
         const int t0 = lane * per, t1 = t0 + per < T ? t0 + per : T;
         int shift = 0;
-        while (((Units<LI>::lo * a.p_max) >> shift) >= kBins) ++shift;
+        while (((Units<LI>::lo * a.p_max + Units<LI>::seg) >> shift) >= kBins) ++shift;
         int lh[kRankPer], ll[kRankPer], bin[kRankPer];
 #pragma unroll
         for (int i = 0; i < kRankPer; ++i) {

@@ -6,20 +6,22 @@
 
 namespace dkv {
 
-constexpr int kAttnWaves = 8;  // single page buffer: GQ <= 6 fits two workgroups per CU
-constexpr int kAttnThreads = kAttnWaves * kWave;
-// Workgroups of attn_decode<GQ, LI> each CU holds at once; the launch bounds
-// make the compiler fit that residency (at most 128 VGPRs for two eight-wave
-// workgroups).  GQ 7-8 need more registers: four waves per SIMD there spilled
-// and measured slower, so they run one workgroup per CU.  Layouts with 8-bit
-// values stage two value rows per lane, which leaves LDS for two workgroups
-// per CU only up to GQ 5.
+// Workgroups of attn_decode<GQ, LI> each CU holds at once: two eight-wave
+// workgroups (four waves per SIMD, at most 128 VGPRs) up to GQ 5; from GQ 6
+// the kernel needs more registers (129-153), and one twelve-wave workgroup per
+// CU keeps three waves per SIMD.  Layouts with 8-bit values stage two value
+// rows per lane (more LDS per wave).
 constexpr bool layout_wide_values(int li)
 {
     return 2 * kLayoutFmts[li].hi.T * kLayoutFmts[li].hi.vb / 8 > 16 ||
            2 * kLayoutFmts[li].lo.T * kLayoutFmts[li].lo.vb / 8 > 16;
 }
-constexpr int attn_blocks_per_cu(int gq, int li) { return gq <= (layout_wide_values(li) ? 5 : 6) ? 2 : 1; }
+constexpr int attn_blocks_per_cu(int gq, int li) { return gq <= 5 ? 2 : 1; }
+// Waves per workgroup: eight (two per SIMD) where two workgroups share a CU,
+// twelve (three per SIMD) where one workgroup has the CU: the registers of
+// the larger group sizes (at most 168 VGPRs) allow three waves per SIMD, and
+// the page loops need the waves to cover each other's waits.
+constexpr int attn_waves(int gq, int li) { return attn_blocks_per_cu(gq, li) == 2 ? 8 : 12; }
 constexpr int kPartStride = kD + 2;
 constexpr int kSigWaves = 4;
 constexpr int kSigPages = 16;  // pages per workgroup of attn_significance

@@ -384,13 +384,13 @@ struct WaveState {
 // LDS for the value weights of one page: [row = value group][token pair][head]
 // as fp16 pairs; rows padded by four dwords so the four rows' broadcast reads
 // hit different banks.
-template <int GQ>
+template <int GQ, int NW>
 struct CoefLds {
     static constexpr int kH = GQ <= 4 ? 4 : 8;  // heads per pair entry (dwords)
     static constexpr int kRow = 16 * kH + 4;     // dwords per row (16 pairs)
-    uint32_t v[kAttnWaves][4 * kRow];
+    uint32_t v[NW][4 * kRow];
 };
-static_assert(4 * CoefLds<1>::kRow >= 32 * 4, "a wave's weight area holds one slot's softmax weights");
+static_assert(4 * CoefLds<1, 8>::kRow >= 32 * 4, "a wave's weight area holds one slot's softmax weights");
 
 // Sum over the four rows with a transpose: row r of the result holds the sum of
 // argument r (heads a, b, c, d -> rows 0, 1, 2, 3).
@@ -481,7 +481,7 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
                                         lds_u32* coef_row, lds_f32* px)
 {
     constexpr int NS = WaveState<GQ>::NS;
-    constexpr int kH = CoefLds<GQ>::kH;
+    constexpr int kH = CoefLds<GQ, 8>::kH;
     constexpr int NT = T / 16;
     static_assert(KB == 4 || NT == 1, "8-bit keys: 16 tokens per page");
     const int jl = lane & 15;
@@ -778,12 +778,12 @@ __device__ __forceinline__ int page_at_unit(long long x, int ph, int np)
     return p > np ? np : (int)p;
 }
 
-template <int GQ>
+template <int GQ, int NW>
 struct AttnShared {
-    float m[kAttnWaves][8];
-    float l[kAttnWaves][8];
-    float acc[kAttnWaves][GQ][kD];
-    long long scan[kAttnWaves + 1];
+    float m[NW][8];
+    float l[NW][8];
+    float acc[NW][GQ][kD];
+    long long scan[NW + 1];
     int t_first;
     int len_first[2];  // section lengths of t_first (longest-first ranking)
     long long u_first;
@@ -794,7 +794,8 @@ struct AttnShared {
     long long pend_u[2];     // their first units (arrivals after the walk)
 };
 
-// Exclusive prefix sum of one 64-bit value per thread of the workgroup.
+// Exclusive prefix sum of one 64-bit value per thread of an NW-wave workgroup.
+template <int NW>
 __device__ __forceinline__ long long wg_excl_scan(long long x, long long* lds, long long* total)
 {
     const int l = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
@@ -808,7 +809,7 @@ __device__ __forceinline__ long long wg_excl_scan(long long x, long long* lds, l
     __syncthreads();
     long long before = 0, tot = 0;
 #pragma unroll
-    for (int i = 0; i < kAttnWaves; ++i) {
+    for (int i = 0; i < NW; ++i) {
         const long long v = lds[i];
         before += i < w ? v : 0;
         tot += v;
@@ -895,8 +896,8 @@ __device__ __forceinline__ const AttnArgs& late_args()
 
 // After the workgroup wrote its partial state of table t: whether it is the
 // n-th of the table's shares to arrive (uniform over the workgroup).
-template <int GQ>
-__device__ __forceinline__ bool arrive_last(const AttnArgs& a, AttnShared<GQ>& sh, int t, int n)
+template <int GQ, int NW>
+__device__ __forceinline__ bool arrive_last(const AttnArgs& a, AttnShared<GQ, NW>& sh, int t, int n)
 {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's partial stores are done
     __syncthreads();
@@ -941,7 +942,7 @@ __device__ __forceinline__ void merge_parts(const AttnArgs& a, int t, const floa
     const int lane = threadIdx.x & (kWave - 1);
     const int hh = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const long long stride = (long long)GQ * kPartStride;
-    static_assert(GQ <= kAttnWaves, "one wave per query head");
+    static_assert(GQ <= 8, "one wave per query head (eight or more waves)");
     if (hh < GQ) {
         const float* pr = base + hh * kPartStride;
         constexpr int kPre = 8;
@@ -991,8 +992,8 @@ __device__ __forceinline__ void merge_parts(const AttnArgs& a, int t, const floa
 // into the output (part == nullptr) or into a partial state {max, sum, acc}
 // per head at `part` (pa == pb gives the empty state).
 // ---------------------------------------------------------------------------
-template <int GQ, int LI>
-__device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& sh, CoefLds<GQ>* coef,
+template <int GQ, int LI, int NW = attn_waves(GQ, LI)>
+__device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW>& sh, CoefLds<GQ, NW>* coef,
                                             PageStage<Lay<LI>::nv>* stage, int t, const TableInfo& ti, int pa,
                                             int pb, float* part, int& done, int target)
 {
@@ -1006,18 +1007,18 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     const long long npool = a.num_pages;
     using LY = Lay<LI>;
     constexpr long long page_bytes = LY::page_bytes;  // (the layout check guarantees it)
-    lds_u32* coef_row = (lds_u32*)(&coef->v[wave][grp * CoefLds<GQ>::kRow]);
+    lds_u32* coef_row = (lds_u32*)(&coef->v[wave][grp * CoefLds<GQ, NW>::kRow]);
     // one slot's softmax weights [token][row] pass through the start of the wave's
     // weight area before the page's weights are written there
     lds_f32* px = (lds_f32*)(&coef->v[wave][0]);
-    const int nmine = pb - pa > wave ? (pb - pa - wave + kAttnWaves - 1) / kAttnWaves : 0;
+    const int nmine = pb - pa > wave ? (pb - pa - wave + NW - 1) / NW : 0;
     const int32_t* trow = a.page_table + (long long)t * P;
 
     // The wave's pages run in chunks of 64: lane k holds the ID of chunk page
     // c0 + k (one vector load per chunk), and a page's ID is read into a scalar
     // register when its loads are issued.  Chunk bounds [c0, c1); past c1 the
     // index is clamped to the chunk's last page.
-    auto page_of = [&](int i) { return pa + wave + kAttnWaves * i; };
+    auto page_of = [&](int i) { return pa + wave + NW * i; };
     auto slot_of = [&](int p) { return p < ph ? p : P - 1 - (p - ph); };
     int c0 = 0, c1 = 0, c_last = 0, ids_v = 0;
     auto clamp_i = [&](int i) { return i < c_last ? i : c_last; };
@@ -1098,7 +1099,7 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     // low pages run in loops of their own (no per-page branch between two
     // different updates of the softmax state); the prefetch crosses from one
     // loop to the next.
-    const int nhi = ph - pa - wave > 0 ? min(nmine, (ph - pa - wave + kAttnWaves - 1) / kAttnWaves) : 0;
+    const int nhi = ph - pa - wave > 0 ? min(nmine, (ph - pa - wave + NW - 1) / NW) : 0;
     auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
         if (i >= c1 || !ok) return;
         const int p = page_of(i);
@@ -1186,15 +1187,15 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
     }
     __syncthreads();
     // ---- merge the waves: final output, or this segment's partial state ---
-    for (int i = threadIdx.x; i < GQ * kD; i += kAttnThreads) {
+    for (int i = threadIdx.x; i < GQ * kD; i += NW * kWave) {
         const int hh = i / kD, d = i - hh * kD;
         float M = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < kAttnWaves; ++w) M = fmax_sel(M, sh.m[w][hh]);
+        for (int w = 0; w < NW; ++w) M = fmax_sel(M, sh.m[w][hh]);
         float L = 0.f, O = 0.f;
         if (M != -INFINITY) {
 #pragma unroll
-            for (int w = 0; w < kAttnWaves; ++w) {
+            for (int w = 0; w < NW; ++w) {
                 const float f = __builtin_amdgcn_exp2f(sh.m[w][hh] - M);
                 L = fmaf(sh.l[w][hh], f, L);
                 O = fmaf(sh.acc[w][hh][d], f, O);
@@ -1241,8 +1242,8 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ>& s
 constexpr int kKeep = 8;     // tables per thread whose units stay in registers (balanced mode)
 constexpr int kRankPer = 16;  // tables per lane of the ranking wave
 
-template <int GQ, int LI>
-__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& sh, CoefLds<GQ>* coef, int T, int j,
+template <int GQ, int LI, int NW>
+__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ, NW>& sh, CoefLds<GQ, NW>* coef, int T, int j,
                                              TableInfo* ti)
 {
     constexpr int kBins = 1024;
@@ -1251,7 +1252,7 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
         *ti = table_info<LI>(a, j);
         return j;
     }
-    static_assert(sizeof(CoefLds<GQ>) >= kBins * sizeof(int), "histogram lives in the weight LDS");
+    static_assert(sizeof(CoefLds<GQ, NW>) >= kBins * sizeof(int), "histogram lives in the weight LDS");
     if (threadIdx.x < kWave) {
         int* hist = reinterpret_cast<int*>(coef);  // free until the page loop
         const int lane = threadIdx.x;
@@ -1341,11 +1342,13 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ>& 
 }
 
 template <int GQ, int LI>
-__global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn_decode(AttnArgs a)
+__global__ __launch_bounds__(attn_waves(GQ, LI) * kWave, attn_blocks_per_cu(GQ, LI)) void attn_decode(AttnArgs a)
 {
-    __shared__ AttnShared<GQ> sh;
-    __shared__ CoefLds<GQ> coef;
-    __shared__ PageStage<Lay<LI>::nv> stage[kAttnWaves];
+    constexpr int NW = attn_waves(GQ, LI);
+    constexpr int NT = NW * kWave;
+    __shared__ AttnShared<GQ, NW> sh;
+    __shared__ CoefLds<GQ, NW> coef;
+    __shared__ PageStage<Lay<LI>::nv> stage[NW];
     // the call tag goes to LDS at once, so the registers it comes in are free
     // for the rest of the kernel (read after the workgroup's first barrier)
     if (threadIdx.x == 0) sh.tag = call_tag();
@@ -1373,7 +1376,7 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
     }
     // ---- balanced shares -------------------------------------------------
     const long long k = blockIdx.x, W = gridDim.x;
-    const int per = (T + kAttnThreads - 1) / kAttnThreads;
+    const int per = (T + NT - 1) / NT;
     const int t0 = threadIdx.x * per;
     const int t1 = t0 + per < T ? t0 + per : T;
     long long units[kKeep];
@@ -1401,7 +1404,7 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
         if (u == 0 && t % W == k) write_empty_one(a, t, GQ);
     }
     long long total;
-    const long long before = wg_excl_scan(mine, sh.scan, &total);
+    const long long before = wg_excl_scan<NW>(mine, sh.scan, &total);
     if (threadIdx.x == 0) sh.units = total;  // read back by the arrival (not kept in registers)
     const long long b_lo = k * total / W, b_hi = (k + 1) * total / W;
     if (b_lo >= b_hi) return;
@@ -1427,7 +1430,7 @@ __global__ __launch_bounds__(kAttnThreads, attn_blocks_per_cu(GQ, LI)) void attn
     // the merge code out of the walk's registers.
     int npend = 0;
     int done = 0;
-    const int target = (int)((b_hi - b_lo + kAttnWaves - 1) / kAttnWaves);
+    const int target = (int)((b_hi - b_lo + NW - 1) / NW);
     while (t < T && ut < b_hi) {
         const TableInfo ti = table_info<LI>(a, t);
         if (ti.units > 0) {

@@ -90,7 +90,7 @@ hipError_t launch_attention(AttnArgs a, hipStream_t st)
     const long long grid = a.splits > 0 ? T * a.splits : workers;
     if (grid < 1 || grid > INT32_MAX) return hipErrorInvalidValue;
     void* args[] = {&a};
-    return hipLaunchKernel(kern, dim3((unsigned)grid), dim3(kAttnThreads), args, 0, st);
+    return hipLaunchKernel(kern, dim3((unsigned)grid), dim3((unsigned)(attn_waves(gq, a.layout) * kWave)), args, 0, st);
 }
 
 

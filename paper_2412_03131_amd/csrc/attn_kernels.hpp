@@ -477,7 +477,7 @@ __device__ __forceinline__ void coef_slot(int t, int& pi, int& pos)
 template <int GQ, int KB, int VB, int T>
 __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, const uint32_t (&qr)[GQ],
                                         const half2_t (&q0)[GQ],
-                                        const float (&qsum)[GQ], float sl2, int n_valid, int lane,
+                                        const float (&qs2)[GQ], float sl2, int n_valid, int lane,
                                         lds_u32* coef_row, lds_f32* px)
 {
     constexpr int NS = WaveState<GQ>::NS;
@@ -491,7 +491,10 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
 #pragma unroll
     for (int tk = 0; tk < NT; ++tk) {
         const uint32_t km = tk ? r.m1 : r.m0;
-        const float ks = h2f(km & 0xffffu) * (kTwo24 * sl2), kz = h2f(km >> 16) * sl2;
+        // the zero term takes the fp16 zero as it is (a mixed-precision fma),
+        // qs2 = sum(q) * scale_log2 per head
+        const float ks = h2f(km & 0xffffu) * (kTwo24 * sl2);
+        const float kz = (float)__builtin_bit_cast(f16x2, km).y;
         float dlo[GQ], dhi[GQ];
         if constexpr (KB == 8) {
             const uint32_t w[8] = {r.k0.x, r.k0.y, r.k0.z, r.k0.w, r.k1.x, r.k1.y, r.k1.z, r.k1.w};
@@ -506,7 +509,7 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         for (int hh = 0; hh < 4 * NS; ++hh) {
             if (hh < GQ) {
                 const float d = KB == 8 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
-                part[hh] = fmaf(ks, d, kz * qsum[hh]);
+                part[hh] = fmaf(kz, qs2[hh], ks * d);
             } else {
                 part[hh] = 0.f;
             }
@@ -602,8 +605,12 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         int pi, pos;
         coef_slot<VB, T>(tok, pi, pos);
         lds_f16* dst = crow + pi * 2 * kH + pos;
-        // weights rounded to fp16 two heads at a time (one packed conversion)
+        // weights rounded to fp16 two heads at a time (one packed conversion);
+        // the second of a pair goes to LDS straight from the high half
+        // (ds_write_b16_d16_hi: the wave's LDS operations stay in order, and
+        // the asm orders itself against the compiler's memory accesses)
         _Float16 c[GQ];
+        uint32_t cpk[(GQ + 1) / 2];
 #pragma unroll
         for (int hh = 0; hh < GQ; hh += 2) {
             if (hh + 1 < GQ) {
@@ -611,15 +618,20 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
                 const f16x2 c2 = __builtin_convertvector(w2, f16x2);
                 c[hh] = c2.x;
                 c[hh + 1] = c2.y;
+                cpk[hh / 2] = __builtin_bit_cast(uint32_t, c2);
             } else {
                 c[hh] = (_Float16)(pg[tk][hh] * vs_c);
             }
         }
+        const uint32_t dst_addr = (uint32_t)(size_t)dst;
 #pragma unroll
         for (int hh = 0; hh < GQ; ++hh) {
             st.z[hh] = fmaf(pg[tk][hh], zc, st.z[hh]);
             st.z[hh] = fmaf(-cc, (float)c[hh], st.z[hh]);
-            dst[2 * hh] = c[hh];
+            if (hh % 2 == 1)
+                asm volatile("ds_write_b16_d16_hi %0, %1 offset:%2" ::"v"(dst_addr), "v"(cpk[hh / 2]), "i"(4 * hh) : "memory");
+            else
+                dst[2 * hh] = c[hh];
         }
     }
     __builtin_amdgcn_wave_barrier();
@@ -1067,11 +1079,11 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW
     }
 
     // q of this lane's group as fp16 pairs (d, d+4), one pair per lane (read
-    // by the others through DPP), pair 0 (dims 0, 4) in every lane; qsum = the
-    // group's sum (row sum)
+    // by the others through DPP), pair 0 (dims 0, 4) in every lane; qs2 = the
+    // group's sum (row sum) times scale_log2
     uint32_t qr[GQ];
     half2_t q0[GQ];
-    float qsum[GQ];
+    float qs2[GQ];
     constexpr uint32_t kOnes = 0x3C003C00u;  // fp16 pair (1, 1)
     {
         const uint32_t sel = (qa & 1) ? 0x07060302u : 0x05040100u;
@@ -1079,7 +1091,7 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW
         for (int hh = 0; hh < GQ; ++hh) {
             qr[hh] = __builtin_amdgcn_perm(qraw[hh][1], qraw[hh][0], sel);
             q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(qraw[hh][3], qraw[hh][2], 0x05040100u));
-            qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f));
+            qs2[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f)) * sl2;
         }
     }
 
@@ -1103,13 +1115,13 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW
     auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
         if (i >= c1 || !ok) return;
         const int p = page_of(i);
-        do_page<GQ, LY::hi.kb, LY::hi.vb, LY::hi.T>(st, r, qr, q0, qsum, sl2, ti.len_hi - p * LY::hi.T, lane, coef_row,
+        do_page<GQ, LY::hi.kb, LY::hi.vb, LY::hi.T>(st, r, qr, q0, qs2, sl2, ti.len_hi - p * LY::hi.T, lane, coef_row,
                                                    px);
     };
     auto compute_lo = [&](int i, const PageRaw& r, bool ok) {
         if (i >= c1 || !ok) return;
         const int p = page_of(i);
-        do_page<GQ, LY::lo.kb, LY::lo.vb, LY::lo.T>(st, r, qr, q0, qsum, sl2, ti.len_lo - (p - ph) * LY::lo.T, lane,
+        do_page<GQ, LY::lo.kb, LY::lo.vb, LY::lo.T>(st, r, qr, q0, qs2, sl2, ti.len_lo - (p - ph) * LY::lo.T, lane,
                                                    coef_row, px);
     };
     // Wave priority.  One workgroup per table or range (target 0): it follows
@@ -1511,7 +1523,8 @@ __device__ __forceinline__ void sig_page(const SigArgs& a, uint8_t* pg, int pbyt
 #pragma unroll
     for (int tk = 0; tk < NT; ++tk) {
         const uint32_t kmt = tk ? m1 : m0;
-        const float ks = h2f(kmt & 0xffffu) * (kTwo24 * a.scale_log2), kz = h2f(kmt >> 16) * a.scale_log2;
+        const float ks = h2f(kmt & 0xffffu) * (kTwo24 * a.scale_log2);
+        const float kz = (float)__builtin_bit_cast(f16x2, kmt).y;
         float dlo[GQ], dhi[GQ];
         if constexpr (KB == 8) {
             const uint32_t w[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
@@ -1526,7 +1539,7 @@ __device__ __forceinline__ void sig_page(const SigArgs& a, uint8_t* pg, int pbyt
         for (int hh = 0; hh < 4 * NS; ++hh) {
             if (hh < GQ) {
                 const float d = KB == 8 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
-                part[hh] = fmaf(ks, d, kz * qsum[hh]);
+                part[hh] = fmaf(kz, qsum[hh], ks * d);
             } else {
                 part[hh] = 0.f;
             }
@@ -1586,7 +1599,7 @@ __global__ __launch_bounds__(kSigWaves * kWave) void attn_significance(SigArgs a
         const int o = 4 * qm + ((qa & 2) ? 1 : 0);
         qr[hh] = __builtin_amdgcn_perm(qd[o + 2], qd[o], sel);
         q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(qd[2], qd[0], 0x05040100u));
-        qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f));
+        qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f)) * a.scale_log2;  // times scale_log2
     }
     float lse2[NS];
 #pragma unroll

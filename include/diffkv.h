@@ -213,10 +213,13 @@ diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_c
  *   lse  device fp32 [num_seqs][num_q_heads] (natural log of the softmax
  *        denominator incl. the max) or NULL.  An empty table gives out = 0,
  *        lse = -inf.
- *   num_splits  0 = automatic (default): one workgroup per table when there
- *        are at least as many tables as workgroups the device holds at once
- *        (waves with more pages left get issue priority, so the longest
- *        tables are served first), otherwise the balanced mode.
+ *   num_splits  0 = automatic (default): no table is split when there are
+ *        at least as many tables as eight-wave workgroups the device holds at
+ *        once -- up to 5 query heads per KV head each workgroup takes two
+ *        tables (one long, one short: ranks j and T-1-j by decreasing work)
+ *        and splits its waves between them by their work; above, one
+ *        workgroup per table (waves with more pages left get issue priority)
+ *        -- otherwise the balanced mode.
  *        -1 = balanced: the page lists of all tables, in table order, form one
  *        list of work units (a high page 3, a 32-token low page 6, a 16-token
  *        low page 3, a table's start 80) cut into one equal

@@ -153,7 +153,7 @@ AttnWs attn_ws(int64_t B, int64_t Hq, int64_t Hkv, int64_t splits, int64_t worke
     AttnWs w;
     const int64_t T = B * Hkv;
     const int64_t gq = Hkv > 0 ? Hq / Hkv : 1;
-    w.nparts = splits <= 0 ? workers + T : (splits > 1 ? T * splits : 0);
+    w.nparts = (splits == 0 || splits == -1) ? workers + T : (splits > 1 ? T * splits : 0);
     int64_t o = 0;
     w.arrive = o; o = align256(o + T * 8);
     w.part = o;   o = align256(o + w.nparts * gq * (kD + 2) * 4);

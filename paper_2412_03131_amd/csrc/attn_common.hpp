@@ -22,12 +22,18 @@ constexpr int attn_blocks_per_cu(int gq, int li) { return gq <= 5 ? 2 : 1; }
 // the larger group sizes (at most 168 VGPRs) allow three waves per SIMD, and
 // the page loops need the waves to cover each other's waits.
 constexpr int attn_waves(int gq, int li) { return attn_blocks_per_cu(gq, li) == 2 ? 8 : 12; }
+// The paired-table kernel: sixteen waves, one workgroup per CU, up to GQ 5
+// (at most 128 VGPRs, four waves per SIMD).
+constexpr int kPairWaves = 16;
+constexpr int kPairMaxGq = 5;
+constexpr int kModePair = -2;  // launch mode of attn_pair (internal; never a caller's num_splits)
 constexpr int kPartStride = kD + 2;
 constexpr int kSigWaves = 4;
 constexpr int kSigPages = 16;  // pages per workgroup of attn_significance
 
 // Kernel entry points of layout n (k_attn_l<n>.hip): which = 0 attn_decode,
-// 1 attn_significance; nullptr for an unknown gq.
+// 1 attn_significance, 2 attn_pair; nullptr for an unknown gq (and for
+// attn_pair above kPairMaxGq).
 const void* attn_kernel_l0(int gq, int which);
 const void* attn_kernel_l1(int gq, int which);
 const void* attn_kernel_l2(int gq, int which);

@@ -797,8 +797,9 @@ struct AttnShared {
     float acc[NW][GQ][kD];
     long long scan[NW + 1];
     int t_first;
-    int len_first[2];  // section lengths of t_first (longest-first ranking)
     long long u_first;
+    int rk_t[2];       // tables of the ranks searched (longest-first ranking)
+    int rk_len[2][2];  // and their section lengths
     int last;          // this workgroup is the last of a split table's shares
     unsigned long long tag;  // this call's tag (arrival words)
     long long units;         // balanced mode: the unit total of all tables
@@ -998,19 +999,22 @@ __device__ __forceinline__ void merge_parts(const AttnArgs& a, int t, const floa
 
 // ---------------------------------------------------------------------------
 // One segment: pages [pa, pb) of table t for all GQ query heads of its KV
-// head.  The eight waves take every eighth page, each loading a page and
-// then computing it (the other waves on its SIMD cover the wait).  Their
-// (max, sum, acc) states merge through LDS
-// into the output (part == nullptr) or into a partial state {max, sum, acc}
-// per head at `part` (pa == pb gives the empty state).
+// head, taken by waves w0 .. w0+nw-1 of the workgroup: wave w0 + i takes every
+// nw-th page from pa + i, each loading a page and then computing it (the other
+// waves on its SIMD cover the wait).  seg_pages leaves each wave's (max, sum,
+// acc) state in LDS (no workgroup barrier inside, so the waves of a workgroup
+// may work on different tables); seg_merge combines the states of waves
+// w0 .. w0+nw-1 into the output (part == nullptr) or into a partial state
+// {max, sum, acc} per head at `part` (pa == pb gives the empty state).
 // ---------------------------------------------------------------------------
-template <int GQ, int LI, int NW = attn_waves(GQ, LI)>
-__device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW>& sh, CoefLds<GQ, NW>* coef,
-                                            PageStage<Lay<LI>::nv>* stage, int t, const TableInfo& ti, int pa,
-                                            int pb, float* part, int& done, int target)
+template <int GQ, int LI, int NW>
+__device__ __forceinline__ void seg_pages(const AttnArgs& a, AttnShared<GQ, NW>& sh, CoefLds<GQ, NW>* coef,
+                                          PageStage<Lay<LI>::nv>* stage, int t, const TableInfo& ti, int pa,
+                                          int pb, int w0, int nw, int& done, int target)
 {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wv = wave - w0;  // this wave's place among the segment's waves
     const int grp = lane >> 4;
     const int P = a.p_max;
     const int b = t / a.Hkv, h = t - b * a.Hkv;
@@ -1023,14 +1027,14 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW
     // one slot's softmax weights [token][row] pass through the start of the wave's
     // weight area before the page's weights are written there
     lds_f32* px = (lds_f32*)(&coef->v[wave][0]);
-    const int nmine = pb - pa > wave ? (pb - pa - wave + NW - 1) / NW : 0;
+    const int nmine = pb - pa > wv ? (pb - pa - wv + nw - 1) / nw : 0;
     const int32_t* trow = a.page_table + (long long)t * P;
 
     // The wave's pages run in chunks of 64: lane k holds the ID of chunk page
     // c0 + k (one vector load per chunk), and a page's ID is read into a scalar
     // register when its loads are issued.  Chunk bounds [c0, c1); past c1 the
     // index is clamped to the chunk's last page.
-    auto page_of = [&](int i) { return pa + wave + NW * i; };
+    auto page_of = [&](int i) { return pa + wv + nw * i; };
     auto slot_of = [&](int p) { return p < ph ? p : P - 1 - (p - ph); };
     int c0 = 0, c1 = 0, c_last = 0, ids_v = 0;
     auto clamp_i = [&](int i) { return i < c_last ? i : c_last; };
@@ -1111,7 +1115,7 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW
     // low pages run in loops of their own (no per-page branch between two
     // different updates of the softmax state); the prefetch crosses from one
     // loop to the next.
-    const int nhi = ph - pa - wave > 0 ? min(nmine, (ph - pa - wave + NW - 1) / NW) : 0;
+    const int nhi = ph - pa - wv > 0 ? min(nmine, (ph - pa - wv + nw - 1) / nw) : 0;
     auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
         if (i >= c1 || !ok) return;
         const int p = page_of(i);
@@ -1197,17 +1201,25 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW
         sh.acc[wave][hh][2 * lane] = fmaf(st.acc[hh][0], kTwo24, z);
         sh.acc[wave][hh][2 * lane + 1] = fmaf(st.acc[hh][1], kTwo24, z);
     }
-    __syncthreads();
+}
+
+template <int GQ, int NW>
+__device__ __forceinline__ void seg_merge(const AttnArgs& a, AttnShared<GQ, NW>& sh, int t, int w0, int nw,
+                                          float* part)
+{
     // ---- merge the waves: final output, or this segment's partial state ---
+    const int b = t / a.Hkv, h = t - b * a.Hkv;
     for (int i = threadIdx.x; i < GQ * kD; i += NW * kWave) {
         const int hh = i / kD, d = i - hh * kD;
         float M = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) M = fmax_sel(M, sh.m[w][hh]);
+        for (int w = 0; w < NW; ++w)
+            if (w >= w0 && w < w0 + nw) M = fmax_sel(M, sh.m[w][hh]);
         float L = 0.f, O = 0.f;
         if (M != -INFINITY) {
 #pragma unroll
             for (int w = 0; w < NW; ++w) {
+                if (w < w0 || w >= w0 + nw) continue;
                 const float f = __builtin_amdgcn_exp2f(sh.m[w][hh] - M);
                 L = fmaf(sh.l[w][hh], f, L);
                 O = fmaf(sh.acc[w][hh][d], f, O);
@@ -1226,6 +1238,17 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW
             }
         }
     }
+}
+
+// One segment by all waves of the workgroup: the pages, then the merge.
+template <int GQ, int LI, int NW = attn_waves(GQ, LI)>
+__device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW>& sh, CoefLds<GQ, NW>* coef,
+                                            PageStage<Lay<LI>::nv>* stage, int t, const TableInfo& ti, int pa,
+                                            int pb, float* part, int& done, int target)
+{
+    seg_pages<GQ, LI, NW>(a, sh, coef, stage, t, ti, pa, pb, 0, NW, done, target);
+    __syncthreads();
+    seg_merge<GQ, NW>(a, sh, t, 0, NW, part);
     __syncthreads();  // LDS is reused by the next segment
 }
 
@@ -1242,27 +1265,32 @@ __device__ __forceinline__ void run_segment(const AttnArgs& a, AttnShared<GQ, NW
 //    in this walk) and the last of the table's shares to arrive merges them.
 //    An empty table's output is written by workgroup t % W.
 // ---------------------------------------------------------------------------
-// Table of rank j when the tables are ordered by decreasing work units
-// (bucketed into 1024 bins, ties by index): workgroups are dispatched in
-// index order and two share a CU for the whole launch, so taking the tables
-// longest first spreads the long ones over the CUs and starts them first
-// (longest-processing-time-first order).  Every workgroup derives the same
-// order from the section lengths; wave 0 does it alone (wave-level scans, no
-// workgroup barrier until the result).  Beyond kRankPer tables per lane the
-// order is the identity.  *ti gets the table's pages and units, from the
-// lengths the ranking wave already holds.
+// Tables of ranks rank[0 .. NR) when the tables are ordered by decreasing
+// work units (bucketed into 1024 bins, ties by index): workgroups are
+// dispatched in index order and two share a CU for the whole launch, so
+// taking the tables longest first spreads the long ones over the CUs and
+// starts them first (longest-processing-time-first order).  Every workgroup
+// derives the same order from the section lengths; wave 0 does it alone
+// (wave-level scans, no workgroup barrier until the result).  Beyond kRankPer
+// tables per lane the order is the identity.  ti[k] gets the table's pages and
+// units, from the lengths the ranking wave already holds.
 constexpr int kKeep = 8;     // tables per thread whose units stay in registers (balanced mode)
 constexpr int kRankPer = 16;  // tables per lane of the ranking wave
 
-template <int GQ, int LI, int NW>
-__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ, NW>& sh, CoefLds<GQ, NW>* coef, int T, int j,
-                                             TableInfo* ti)
+template <int GQ, int LI, int NW, int NR>
+__device__ __forceinline__ void rank_tables(const AttnArgs& a, AttnShared<GQ, NW>& sh, CoefLds<GQ, NW>* coef, int T,
+                                            const int (&rank)[NR], int (&tab)[NR], TableInfo (&ti)[NR])
 {
+    static_assert(NR <= 2, "two ranks at most");
     constexpr int kBins = 1024;
     const int per = (T + kWave - 1) / kWave;
     if (per > kRankPer) {
-        *ti = table_info<LI>(a, j);
-        return j;
+#pragma unroll
+        for (int k = 0; k < NR; ++k) {
+            tab[k] = rank[k];
+            ti[k] = table_info<LI>(a, rank[k]);
+        }
+        return;
     }
     static_assert(sizeof(CoefLds<GQ, NW>) >= kBins * sizeof(int), "histogram lives in the weight LDS");
     if (threadIdx.x < kWave) {
@@ -1301,56 +1329,76 @@ __device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ, N
 #pragma unroll
         for (int q = 0; q < 16; ++q) s16 += c16[q];
         const int incl = wave_incl_scan(s16);
-        int at = incl - s16, b = 0, r = 0;
-        bool found = false;
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            if (!found && at <= j && j < at + c16[q]) {
-                found = true;
-                b = 16 * lane + q;
-                r = j - at;
-            }
-            at += c16[q];
-        }
-        const unsigned long long fm = __builtin_amdgcn_ballot_w64(found);  // exactly one lane (j < T)
-        const int src = fm ? __builtin_ctzll(fm) : 0;
-        b = __builtin_amdgcn_readlane(b, src);
-        r = __builtin_amdgcn_readlane(r, src);
-        // the r-th table (by index) of bin b
-        int cnt = 0;
+        for (int k = 0; k < NR; ++k) {
+            const int j = rank[k];
+            int at = incl - s16, b = 0, r = 0;
+            bool found = false;
 #pragma unroll
-        for (int i = 0; i < kRankPer; ++i) cnt += bin[i] == b;
-        int before = wave_incl_scan(cnt) - cnt, t = 0, th = 0, tl = 0;
-        found = false;
-#pragma unroll
-        for (int i = 0; i < kRankPer; ++i) {
-            if (bin[i] == b) {
-                if (before == r) {
+            for (int q = 0; q < 16; ++q) {
+                if (!found && at <= j && j < at + c16[q]) {
                     found = true;
-                    t = t0 + i;
-                    th = lh[i];
-                    tl = ll[i];
+                    b = 16 * lane + q;
+                    r = j - at;
                 }
-                ++before;
+                at += c16[q];
             }
-        }
-        const unsigned long long fm2 = __builtin_amdgcn_ballot_w64(found);
-        const int src2 = fm2 ? __builtin_ctzll(fm2) : 0;
-        // read with every lane active
-        const int tr = __builtin_amdgcn_readlane(t, src2);
-        const int thr = __builtin_amdgcn_readlane(th, src2), tlr = __builtin_amdgcn_readlane(tl, src2);
-        if (lane == 0) {
-            sh.t_first = tr;
-            sh.len_first[0] = thr;
-            sh.len_first[1] = tlr;
+            const unsigned long long fm = __builtin_amdgcn_ballot_w64(found);  // exactly one lane (j < T)
+            const int src = fm ? __builtin_ctzll(fm) : 0;
+            b = __builtin_amdgcn_readlane(b, src);
+            r = __builtin_amdgcn_readlane(r, src);
+            // the r-th table (by index) of bin b
+            int cnt = 0;
+#pragma unroll
+            for (int i = 0; i < kRankPer; ++i) cnt += bin[i] == b;
+            int before = wave_incl_scan(cnt) - cnt, t = 0, th = 0, tl = 0;
+            found = false;
+#pragma unroll
+            for (int i = 0; i < kRankPer; ++i) {
+                if (bin[i] == b) {
+                    if (before == r) {
+                        found = true;
+                        t = t0 + i;
+                        th = lh[i];
+                        tl = ll[i];
+                    }
+                    ++before;
+                }
+            }
+            const unsigned long long fm2 = __builtin_amdgcn_ballot_w64(found);
+            const int src2 = fm2 ? __builtin_ctzll(fm2) : 0;
+            // read with every lane active
+            const int tr = __builtin_amdgcn_readlane(t, src2);
+            const int thr = __builtin_amdgcn_readlane(th, src2), tlr = __builtin_amdgcn_readlane(tl, src2);
+            if (lane == 0) {
+                sh.rk_t[k] = tr;
+                sh.rk_len[k][0] = thr;
+                sh.rk_len[k][1] = tlr;
+            }
         }
     }
     __syncthreads();
-    // (uniform values read back from LDS: readfirstlane keeps the table's
+    // (uniform values read back from LDS: readfirstlane keeps the tables'
     // loads and addresses scalar)
-    *ti = table_info_of<LI>(a, __builtin_amdgcn_readfirstlane(sh.len_first[0]),
-                            __builtin_amdgcn_readfirstlane(sh.len_first[1]));
-    return __builtin_amdgcn_readfirstlane(sh.t_first);  // (not written again in this mode)
+#pragma unroll
+    for (int k = 0; k < NR; ++k) {
+        ti[k] = table_info_of<LI>(a, __builtin_amdgcn_readfirstlane(sh.rk_len[k][0]),
+                                  __builtin_amdgcn_readfirstlane(sh.rk_len[k][1]));
+        tab[k] = __builtin_amdgcn_readfirstlane(sh.rk_t[k]);
+    }
+}
+
+// The table of rank j (see rank_tables).
+template <int GQ, int LI, int NW>
+__device__ __forceinline__ int longest_first(const AttnArgs& a, AttnShared<GQ, NW>& sh, CoefLds<GQ, NW>* coef, int T, int j,
+                                             TableInfo* ti)
+{
+    const int rank[1] = {j};
+    int tab[1];
+    TableInfo tis[1];
+    rank_tables<GQ, LI, NW, 1>(a, sh, coef, T, rank, tab, tis);
+    *ti = tis[0];
+    return tab[0];
 }
 
 template <int GQ, int LI>
@@ -1481,6 +1529,52 @@ __global__ __launch_bounds__(attn_waves(GQ, LI) * kWave, attn_blocks_per_cu(GQ, 
             for (int j = 0; j < nsl; ++j) n += wrote(j) ? 1 : 0;
         }
         if (arrive_last<GQ>(al, sh, tp, n)) merge_parts<GQ>(al, tp, al.part + (kf + tp) * GQ * kPartStride, nsl, wrote);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// attn_pair: the automatic mode when the tables alone fill the device (up to
+// GQ 5).  Workgroup j of ceil(T/2), sixteen waves and the whole CU, takes the
+// tables of ranks j and T-1-j by decreasing work: a long table with a short
+// one, so every CU carries about the average work.  The waves are split
+// between the two tables in proportion to their units and take the progress
+// priority of the balanced mode, so both tables end together; a long table
+// is not left with half a CU once its partner is done, as with one eight-wave
+// workgroup per table.  No partial states: each table is finished in place.
+// ---------------------------------------------------------------------------
+template <int GQ, int LI>
+__global__ __launch_bounds__(kPairWaves * kWave, 1) void attn_pair(AttnArgs a)
+{
+    constexpr int NW = kPairWaves;
+    __shared__ AttnShared<GQ, NW> sh;
+    __shared__ CoefLds<GQ, NW> coef;
+    __shared__ PageStage<Lay<LI>::nv> stage[NW];
+    const int T = a.B * a.Hkv;
+    const int rank[2] = {(int)blockIdx.x, T - 1 - (int)blockIdx.x};
+    int tab[2];
+    TableInfo ti[2];
+    rank_tables<GQ, LI, NW, 2>(a, sh, &coef, T, rank, tab, ti);
+    const bool two = rank[1] != rank[0];
+    const long long u0 = ti[0].units, u1 = two ? ti[1].units : 0;
+    // waves of the first table: round(NW * u0 / (u0 + u1)), at least one each
+    int n0 = NW;
+    if (two && u1 > 0) {
+        n0 = (int)((2 * NW * u0 + u0 + u1) / (2 * (u0 + u1)));
+        n0 = n0 < 1 ? 1 : (n0 > NW - 1 ? NW - 1 : n0);
+    }
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const bool first = wave < n0;
+    const int tw = first ? tab[0] : tab[1];
+    const TableInfo tiw = first ? ti[0] : ti[1];
+    const int w0 = first ? 0 : n0, nw = first ? n0 : NW - n0;
+    int done = 0;
+    const int target = (int)((tiw.units + nw - 1) / nw);
+    seg_pages<GQ, LI, NW>(a, sh, &coef, stage, tw, tiw, 0, tiw.np, w0, nw, done, target > 0 ? target : 1);
+    __syncthreads();
+    seg_merge<GQ, NW>(a, sh, tab[0], 0, n0, nullptr);
+    if (two) {
+        if (n0 < NW) seg_merge<GQ, NW>(a, sh, tab[1], n0, NW - n0, nullptr);
+        else write_empty(a, tab[1], GQ);  // no units
     }
 }
 
@@ -1623,12 +1717,13 @@ __global__ __launch_bounds__(kSigWaves * kWave) void attn_significance(SigArgs a
 
 
 // Kernel entry points of layout LI (host-side stubs): which = 0 attn_decode,
-// 1 attn_significance.
+// 1 attn_significance, 2 attn_pair (nullptr above GQ 5).
 template <int LI>
 const void* attn_kernel_of(int gq, int which)
 {
 #define DKV_ATTN_CASE(G)                                                                   \
     case G:                                                                                \
+        if (which == 2) return G <= kPairMaxGq ? reinterpret_cast<const void*>(&attn_pair<(G <= kPairMaxGq ? G : 1), LI>) : nullptr; \
         return which == 0 ? reinterpret_cast<const void*>(&attn_decode<G, LI>)             \
                           : reinterpret_cast<const void*>(&attn_significance<G, LI>);
     switch (gq) {

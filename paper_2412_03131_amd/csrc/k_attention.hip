@@ -11,7 +11,7 @@ namespace dkv {
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-// Kernel entry points of layout li: which = 0 decode, 1 significance.
+// Kernel entry points of layout li: which = 0 decode, 1 significance, 2 paired tables.
 static const void* attn_kernel_ptr(int li, int gq, int which)
 {
     switch (li) {
@@ -45,11 +45,13 @@ hipError_t attention_mode(int gq, int li, long long T, int splits, int* mode, in
 {
     hipError_t e = balanced_workers(gq, li, workers);
     if (e != hipSuccess) return e;
-    // automatic: one workgroup per table when the tables alone fill the device
-    // (their spread is absorbed by wave priorities and by the hardware
-    // dispatching further tables as workgroups finish), balanced shares when
-    // there are fewer tables than resident workgroups
-    *mode = splits != 0 ? splits : (T >= *workers ? 1 : -1);
+    // automatic: when the tables alone fill the device, no table is split --
+    // pairs of tables (a long one with a short one) per sixteen-wave workgroup
+    // up to GQ 5, one workgroup per table above (their spread is absorbed by
+    // wave priorities and by the hardware dispatching further workgroups as
+    // others finish); balanced shares when there are fewer tables than
+    // resident workgroups
+    *mode = splits != 0 ? splits : (T >= *workers ? (gq <= kPairMaxGq ? kModePair : 1) : -1);
     return hipSuccess;
 }
 
@@ -87,9 +89,16 @@ hipError_t launch_attention(AttnArgs a, hipStream_t st)
     int workers = 0;
     hipError_t e = attention_mode(gq, a.layout, T, a.splits, &a.splits, &workers);
     if (e != hipSuccess) return e;
+    void* args[] = {&a};
+    if (a.splits == kModePair) {
+        const void* pair = attn_kernel_ptr(a.layout, gq, 2);
+        if (!pair) return hipErrorInvalidValue;
+        const long long pgrid = (T + 1) / 2;
+        if (pgrid < 1 || pgrid > INT32_MAX) return hipErrorInvalidValue;
+        return hipLaunchKernel(pair, dim3((unsigned)pgrid), dim3((unsigned)(kPairWaves * kWave)), args, 0, st);
+    }
     const long long grid = a.splits > 0 ? T * a.splits : workers;
     if (grid < 1 || grid > INT32_MAX) return hipErrorInvalidValue;
-    void* args[] = {&a};
     return hipLaunchKernel(kern, dim3((unsigned)grid), dim3((unsigned)(attn_waves(gq, a.layout) * kWave)), args, 0, st);
 }
 

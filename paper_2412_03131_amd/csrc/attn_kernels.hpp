@@ -376,6 +376,7 @@ template <int GQ>
 struct WaveState {
     static constexpr int NS = (GQ + 3) / 4;  // head slots per lane in the softmax layout
     float m[NS];       // running max of head 4s + row (log2 domain), row-uniform
+    float mt[NS];      // m + kSlack: the raise threshold on pages that take the slack
     float l[NS];       // this lane's share of the running sum of head 4s + row
     float z[GQ];       // this lane's share of the zero-point term of head hh (group = row)
     float acc[GQ][2];  // dims 2*lane, 2*lane+1, in units of 2^-24
@@ -514,12 +515,16 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
                 part[hh] = 0.f;
             }
         }
-        const bool valid = jl + 16 * tk < n_valid;
 #pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            const float x = slot_sum<GQ>(s, part);
-            lg[tk][s] = valid ? x : -INFINITY;
-        }
+        for (int s = 0; s < NS; ++s) lg[tk][s] = slot_sum<GQ>(s, part);
+    }
+    // tokens past the section's end (only on its last page: a uniform branch)
+    if (n_valid < T) {
+#pragma unroll
+        for (int tk = 0; tk < NT; ++tk)
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                if (jl + 16 * tk >= n_valid) lg[tk][s] = -INFINITY;
     }
     // ---- online softmax with a lazily raised max (one head per lane and slot).
     // The value weights p * s_v are rounded to fp16, so they must stay below
@@ -527,12 +532,18 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
     // p <= 2^8 (weights <= 2^15); a page with a larger V scale takes no slack,
     // so its weights are p <= 1 times an fp16 scale.
     const bool big_v = (r.m2 & 0xffffu) > kVScaleSlackMax || (NT == 2 && (r.m3 & 0xffffu) > kVScaleSlackMax);
-    const float slack = __builtin_amdgcn_ballot_w64(big_v) ? 0.f : kSlack;
     bool raise = false;
+    if (__builtin_amdgcn_ballot_w64(big_v)) {
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
+        for (int s = 0; s < NS; ++s)
 #pragma unroll
-        for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.m[s] + slack;
+            for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.m[s];
+    } else {
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+            for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.mt[s];
+    }
     if (__builtin_amdgcn_ballot_w64(raise)) {
         float al[4 * NS];
 #pragma unroll
@@ -543,6 +554,7 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
             const float mnew = fmax_sel(st.m[s], mx);
             const float alpha = __builtin_amdgcn_exp2f(st.m[s] - mnew);
             st.m[s] = mnew;
+            st.mt[s] = mnew + kSlack;
             st.l[s] *= alpha;
             if (lone_slot<GQ>(s))
                 al[4 * s] = alpha;
@@ -1103,6 +1115,7 @@ __device__ __forceinline__ void seg_pages(const AttnArgs& a, AttnShared<GQ, NW>&
 #pragma unroll
     for (int s = 0; s < WaveState<GQ>::NS; ++s) {
         st.m[s] = -INFINITY;
+        st.mt[s] = -INFINITY;
         st.l[s] = 0.f;
     }
 #pragma unroll

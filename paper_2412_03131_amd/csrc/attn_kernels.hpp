@@ -3,17 +3,19 @@
 // for gfx950 (DiffKV Eq. (1) of Sec. 2.1, kernel structure of Sec. 6.2).
 //
 // Work: a table's pages (high pages first, then low pages) are processed by
-// one eight-wave workgroup for all GQ query heads that read them, or -- in the
-// balanced mode -- every table's pages are laid end to end and cut into one
-// equal share per resident workgroup, so the spread of table lengths costs
-// nothing; a table that straddles shares is merged by the last of them to
-// finish (split tables below).  Inside a
-// workgroup each wave takes every eighth page, one register buffer per wave:
-// with two workgroups per CU four waves share each SIMD, so the waves hide
-// each other's page loads, and a table left alone on its CU still runs two
-// waves per SIMD.  A wave's page IDs arrive as one vector per 64 pages and
-// each page is loaded through a buffer resource over that page (scalar
-// address, hardware bounds).
+// one workgroup for all GQ query heads that read them (eight waves up to GQ
+// 5, two workgroups per CU; twelve waves, one per CU, above), or by half of a
+// sixteen-wave workgroup that takes two tables, a long one and a short one,
+// with its waves split by their work (attn_pair, the automatic mode when the
+// tables fill the device), or -- in the balanced mode -- every table's pages
+// are laid end to end and cut into one equal share per resident workgroup, so
+// the spread of table lengths costs nothing; a table that straddles shares is
+// merged by the last of them to finish (split tables below).  Inside a
+// workgroup each wave of a segment takes every nw-th page, one register
+// buffer per wave and the next page staged in LDS: with four (three) waves per
+// SIMD the waves hide each other's page loads.  A wave's page IDs arrive as
+// one vector per 64 pages and each page is loaded through a buffer resource
+// over that page (scalar address, hardware bounds).
 //
 // Lane mapping inside a wave (64 lanes = 4 rows of 16):
 //   key phase    lane = grp*16 + j: token j (and j+16 on 32-token pages),
@@ -27,14 +29,14 @@
 //                row r, so the softmax costs one exp2 per (token, head).
 //   softmax      online, base 2, with a lazily raised max: the page max (DPP
 //                row ops) is only taken when a logit exceeds the running max
-//                by more than 2^8.
+//                by more than 8 (weights up to 2^8).
 //   value phase  lane owns dims 2*lane, 2*lane+1 (its row's group).  The
 //                weights p*s_v of the row's tokens, rounded to fp16, go
 //                through LDS (one broadcast read per token pair for all heads)
 //                into v_dot2_f32_f16 with two tokens' codes as fp16 denormals;
 //                the zero-point term and the weights' rounding error (charged
 //                at the centre code) are accumulated per lane and added once.
-// The eight waves' (max, sum, acc) states merge through LDS.
+// The waves' (max, sum, acc) states merge through LDS.
 #include <cstddef>
 #include <utility>
 

@@ -1571,11 +1571,20 @@ __global__ __launch_bounds__(kPairWaves * kWave, 1) void attn_pair(AttnArgs a)
     rank_tables<GQ, LI, NW, 2>(a, sh, &coef, T, rank, tab, ti);
     const bool two = rank[1] != rank[0];
     const long long u0 = ti[0].units, u1 = two ? ti[1].units : 0;
-    // waves of the first table: round(NW * u0 / (u0 + u1)), at least one each
+    // waves of the first table: of the two integer splits around NW * u0 /
+    // (u0 + u1), the one with the smaller larger load per wave (u / waves), at
+    // least one wave each
     int n0 = NW;
     if (two && u1 > 0) {
-        n0 = (int)((2 * NW * u0 + u0 + u1) / (2 * (u0 + u1)));
-        n0 = n0 < 1 ? 1 : (n0 > NW - 1 ? NW - 1 : n0);
+        int lo = (int)(NW * u0 / (u0 + u1));
+        lo = lo < 1 ? 1 : (lo > NW - 1 ? NW - 1 : lo);
+        const int hi = lo < NW - 1 ? lo + 1 : lo;
+        // max(u0/lo, u1/(NW-lo)) <= max(u0/hi, u1/(NW-hi)), compared exactly by cross-multiplying
+        auto worse = [&](int n) {  // larger load of split n, as a fraction num/den
+            return u0 * (NW - n) >= u1 * n ? std::make_pair(u0, (long long)n) : std::make_pair(u1, (long long)(NW - n));
+        };
+        const auto wl = worse(lo), wh = worse(hi);
+        n0 = wl.first * wh.second <= wh.first * wl.second ? lo : hi;
     }
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const bool first = wave < n0;

@@ -72,6 +72,24 @@ def test_noalloc_matches_workspace_entry_point(splits):
         assert np.isfinite(o2.cpu().numpy()).all()
 
 
+def test_noalloc_paired_mode():
+    """The automatic mode with at least as many tables as the device holds eight-wave
+    workgroups (two per CU) pairs the tables in sixteen-wave workgroups; its only
+    scratch is the arrival words.  Two such calls in a row, the second on fewer and
+    shorter tables."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    b_min = -(-2 * cus // 8) + 1   # llama8b: eight KV heads per sequence
+    big = _cache(b_min + 20, (20, 300), 33)
+    small = _cache(b_min, (1, 60), 34)
+    for what, (dc, q) in (("first call, %d tables" % (8 * (b_min + 20)), big),
+                          ("second call, %d tables" % (8 * b_min), small)):
+        print("case: no-alloc attention, paired mode, %s" % what, flush=True)
+        (o1, l1), (o2, l2) = _both(dc, q, 0)
+        assert torch.equal(o1, o2), what
+        assert torch.equal(l1, l2), what
+        assert np.isfinite(o2.cpu().numpy()).all()
+
+
 def test_noalloc_refuses_calls_beyond_its_scratch():
     """Balanced shares over 2000 tables of GQ 8: (resident workgroups + 2000) x 8 heads x
     520 B of partial states is more than the 8 MiB scratch; the call is refused and the

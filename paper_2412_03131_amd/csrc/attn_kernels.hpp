@@ -185,6 +185,16 @@ __device__ __forceinline__ void kdone(float (&d)[GQ])
     for (int hh = 0; hh < GQ; ++hh) asm volatile("" : "+v"(d[hh]));
 }
 
+// A query pair times 1/16 (both halves, fp16, rounded to nearest): the
+// factor of the K4 pairs whose codes are taken as 16 * code.  Exact unless a
+// half falls below 2^-10 in magnitude, where the fp16 denormal spacing rounds
+// it by at most 2^-25 (2^-21 of the unscaled value).
+__device__ __forceinline__ uint32_t q_by16(uint32_t q)
+{
+    const half2_t s = {(_Float16)0.0625f, (_Float16)0.0625f};
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2_t, q) * s);
+}
+
 // v_perm selector of pair a of an 8-dim block: bytes [w_lo.byte a, 0, w_hi.byte a, 0]
 constexpr uint32_t kPermSel(int a) { return 0x0C000C00u | ((uint32_t)(4 + a) << 16) | (uint32_t)a; }
 
@@ -225,46 +235,42 @@ __device__ __forceinline__ void kdots_k8(const uint32_t (&w)[8], const uint32_t 
 }
 
 // K4 token: pairs 4m + a (a = 0..3) of dword w[m] are its nibbles (a, a+4)
-// (a even) or 16 * nibbles (a, a+4) (a odd); even pairs sum into dlo, odd ones
-// into dhi (scaled by 1/16 afterwards).  The two chains alternate, so a
-// chain's steps are 2*GQ-1 dots and two AND steps apart (one in the last
-// step); a code pair is formed GQ dots and one AND step before its use.
+// (a even) or 16 * nibbles (a, a+4) (a odd: one AND, no shift); odd pairs take
+// the query pairs scaled by 1/16 (qr16), so all sixteen pairs sum into one
+// chain per head, with the timing of the K8 sequence (an AND in place of each
+// v_perm).
 template <int GQ>
-__device__ __forceinline__ void kdots_k4(const uint32_t (&w)[4], const uint32_t (&qr)[GQ], const half2_t (&q0)[GQ],
-                                         float (&dlo)[GQ], float (&dhi)[GQ])
+__device__ __forceinline__ void kdots_k4(const uint32_t (&w)[4], const uint32_t (&qr)[GQ], const uint32_t (&qr16)[GQ],
+                                         const half2_t (&q0)[GQ], float (&d)[GQ])
 {
     kwait<5>();
     uint32_t w8[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) w8[m] = w[m] >> 8;
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) kzero(dhi[hh]);
     uint32_t x = kand(w[0], 0x000F000Fu);
     static_for<16>([&](auto i) {
+        constexpr int step = i < 15 ? 1 : 0;
+        constexpr int pad = i > 0 ? kMax0((i == 1 ? 3 : 2) - (GQ - 1 + step)) : 0;
         constexpr int n = i + 1, m = n / 4, a = n % 4;
-        constexpr int pad = i > 0 ? kMax0(2 - (GQ + (i < 15 ? 1 : 0))) : 0;
         constexpr uint32_t mask = (a & 1) ? 0x00F000F0u : 0x000F000Fu;
+        const uint32_t(&q)[GQ] = (i % 2) ? qr16 : qr;
         uint32_t xn = 0;
         if constexpr (i > 0 && i < 15 && pad == 0) {
-            float(&acc)[GQ] = (i % 2 == 0) ? dlo : dhi;
-            xn = kand_dot<(i > 0 ? i : 1)>(a >= 2 ? w8[m] : w[m], mask, acc[0], qr[0], x);
+            xn = kand_dot<(i > 0 ? i : 1)>(a >= 2 ? w8[m] : w[m], mask, d[0], q[0], x);
 #pragma unroll
-            for (int hh = 1; hh < GQ; ++hh) kdot_bcast<(i > 0 ? i : 1)>(acc[hh], qr[hh], x);
+            for (int hh = 1; hh < GQ; ++hh) kdot_bcast<(i > 0 ? i : 1)>(d[hh], q[hh], x);
         } else {
             if constexpr (i < 15) xn = kand(a >= 2 ? w8[m] : w[m], mask);
             kwait<pad>();
 #pragma unroll
             for (int hh = 0; hh < GQ; ++hh) {
-                if constexpr (i == 0) kdot_first(dlo[hh], q0[hh], x);
-                else if constexpr (i % 2 == 0) kdot_bcast<(i > 0 ? i : 1)>(dlo[hh], qr[hh], x);
-                else kdot_bcast<(i > 0 ? i : 1)>(dhi[hh], qr[hh], x);
+                if constexpr (i == 0) kdot_first(d[hh], q0[hh], x);
+                else kdot_bcast<(i > 0 ? i : 1)>(d[hh], q[hh], x);
             }
         }
         x = xn;
     });
-    kwait<3>();
-#pragma unroll
-    for (int hh = 0; hh < GQ; ++hh) asm volatile("" : "+v"(dlo[hh]), "+v"(dhi[hh]));
+    kdone<GQ>(d);
 }
 
 constexpr float kTwo24 = 16777216.0f;
@@ -479,7 +485,7 @@ __device__ __forceinline__ void coef_slot(int t, int& pi, int& pos)
 
 template <int GQ, int KB, int VB, int T>
 __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, const uint32_t (&qr)[GQ],
-                                        const half2_t (&q0)[GQ],
+                                        const uint32_t (&qr16)[GQ], const half2_t (&q0)[GQ],
                                         const float (&qs2)[GQ], float sl2, int n_valid, int lane,
                                         lds_u32* coef_row, lds_f32* px)
 {
@@ -498,21 +504,20 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         // qs2 = sum(q) * scale_log2 per head
         const float ks = h2f(km & 0xffffu) * (kTwo24 * sl2);
         const float kz = (float)__builtin_bit_cast(f16x2, km).y;
-        float dlo[GQ], dhi[GQ];
+        float dk[GQ];
         if constexpr (KB == 8) {
             const uint32_t w[8] = {r.k0.x, r.k0.y, r.k0.z, r.k0.w, r.k1.x, r.k1.y, r.k1.z, r.k1.w};
-            kdots_k8<GQ>(w, qr, q0, dlo);
+            kdots_k8<GQ>(w, qr, q0, dk);
         } else {
             const uint4 kk = tk ? r.k1 : r.k0;
             const uint32_t w[4] = {kk.x, kk.y, kk.z, kk.w};
-            kdots_k4<GQ>(w, qr, q0, dlo, dhi);
+            kdots_k4<GQ>(w, qr, qr16, q0, dk);
         }
         float part[4 * NS];
 #pragma unroll
         for (int hh = 0; hh < 4 * NS; ++hh) {
             if (hh < GQ) {
-                const float d = KB == 8 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
-                part[hh] = fmaf(kz, qs2[hh], ks * d);
+                part[hh] = fmaf(kz, qs2[hh], ks * dk[hh]);
             } else {
                 part[hh] = 0.f;
             }
@@ -520,8 +525,10 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
 #pragma unroll
         for (int s = 0; s < NS; ++s) lg[tk][s] = slot_sum<GQ>(s, part);
     }
-    // tokens past the section's end (only on its last page: a uniform branch)
+    // tokens past the section's end (only on its last page: a uniform branch,
+    // kept a branch by the empty asm, which the compiler does not speculate)
     if (n_valid < T) {
+        asm volatile("");
 #pragma unroll
         for (int tk = 0; tk < NT; ++tk)
 #pragma unroll
@@ -534,19 +541,21 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
     // p <= 2^8 (weights <= 2^15); a page with a larger V scale takes no slack,
     // so its weights are p <= 1 times an fp16 scale.
     const bool big_v = (r.m2 & 0xffffu) > kVScaleSlackMax || (NT == 2 && (r.m3 & 0xffffu) > kVScaleSlackMax);
-    bool raise = false;
+    // one wave-wide compare mask per logit, or-ed on the scalar unit
+    unsigned long long raise = 0;
     if (__builtin_amdgcn_ballot_w64(big_v)) {
+        asm volatile("");
 #pragma unroll
         for (int s = 0; s < NS; ++s)
 #pragma unroll
-            for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.m[s];
+            for (int tk = 0; tk < NT; ++tk) raise |= __builtin_amdgcn_ballot_w64(lg[tk][s] > st.m[s]);
     } else {
 #pragma unroll
         for (int s = 0; s < NS; ++s)
 #pragma unroll
-            for (int tk = 0; tk < NT; ++tk) raise |= lg[tk][s] > st.mt[s];
+            for (int tk = 0; tk < NT; ++tk) raise |= __builtin_amdgcn_ballot_w64(lg[tk][s] > st.mt[s]);
     }
-    if (__builtin_amdgcn_ballot_w64(raise)) {
+    if (raise) {
         float al[4 * NS];
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
@@ -613,7 +622,8 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         constexpr float centre = 0.5f * (float)((1 << VB) - 1);
         const int tok = jl + 16 * tk;
         const bool by4 = VB == 2 && (tok & 1);
-        const float vs_c = by4 ? vs * 0.25f : vs;
+        // s_v times the lane's code factor in one mixed-precision fma
+        const float vs_c = fmaf(vs, by4 ? 0.25f : 1.0f, 0.0f);
         const float cc = by4 ? 4.f * centre : centre;
         const float zc = fmaf(centre, vs, vz);
         int pi, pos;
@@ -1099,7 +1109,7 @@ __device__ __forceinline__ void seg_pages(const AttnArgs& a, AttnShared<GQ, NW>&
     // q of this lane's group as fp16 pairs (d, d+4), one pair per lane (read
     // by the others through DPP), pair 0 (dims 0, 4) in every lane; qs2 = the
     // group's sum (row sum) times scale_log2
-    uint32_t qr[GQ];
+    uint32_t qr[GQ], qr16[GQ];
     half2_t q0[GQ];
     float qs2[GQ];
     constexpr uint32_t kOnes = 0x3C003C00u;  // fp16 pair (1, 1)
@@ -1108,6 +1118,7 @@ __device__ __forceinline__ void seg_pages(const AttnArgs& a, AttnShared<GQ, NW>&
 #pragma unroll
         for (int hh = 0; hh < GQ; ++hh) {
             qr[hh] = __builtin_amdgcn_perm(qraw[hh][1], qraw[hh][0], sel);
+            qr16[hh] = q_by16(qr[hh]);
             q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(qraw[hh][3], qraw[hh][2], 0x05040100u));
             qs2[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f)) * sl2;
         }
@@ -1134,13 +1145,13 @@ __device__ __forceinline__ void seg_pages(const AttnArgs& a, AttnShared<GQ, NW>&
     auto compute_hi = [&](int i, const PageRaw& r, bool ok) {
         if (i >= c1 || !ok) return;
         const int p = page_of(i);
-        do_page<GQ, LY::hi.kb, LY::hi.vb, LY::hi.T>(st, r, qr, q0, qs2, sl2, ti.len_hi - p * LY::hi.T, lane, coef_row,
+        do_page<GQ, LY::hi.kb, LY::hi.vb, LY::hi.T>(st, r, qr, qr16, q0, qs2, sl2, ti.len_hi - p * LY::hi.T, lane, coef_row,
                                                    px);
     };
     auto compute_lo = [&](int i, const PageRaw& r, bool ok) {
         if (i >= c1 || !ok) return;
         const int p = page_of(i);
-        do_page<GQ, LY::lo.kb, LY::lo.vb, LY::lo.T>(st, r, qr, q0, qs2, sl2, ti.len_lo - (p - ph) * LY::lo.T, lane,
+        do_page<GQ, LY::lo.kb, LY::lo.vb, LY::lo.T>(st, r, qr, qr16, q0, qs2, sl2, ti.len_lo - (p - ph) * LY::lo.T, lane,
                                                    coef_row, px);
     };
     // Wave priority.  One workgroup per table or range (target 0): it follows
@@ -1616,8 +1627,9 @@ __global__ __launch_bounds__(kPairWaves * kWave, 1) void attn_pair(AttnArgs a)
 
 template <int GQ, int KB, int T>
 __device__ __forceinline__ void sig_page(const SigArgs& a, uint8_t* pg, int pbytes, SecOffsets O,
-                                         const uint32_t (&qr)[GQ], const half2_t (&q0)[GQ], const float (&qsum)[GQ],
-                                         const float (&lse2)[(GQ + 3) / 4], int n_valid, int N, int lane)
+                                         const uint32_t (&qr)[GQ], const uint32_t (&qr16)[GQ], const half2_t (&q0)[GQ],
+                                         const float (&qsum)[GQ], const float (&lse2)[(GQ + 3) / 4], int n_valid,
+                                         int N, int lane)
 {
     constexpr int NS = (GQ + 3) / 4;
     constexpr int NT = T / 16;
@@ -1643,21 +1655,20 @@ __device__ __forceinline__ void sig_page(const SigArgs& a, uint8_t* pg, int pbyt
         const uint32_t kmt = tk ? m1 : m0;
         const float ks = h2f(kmt & 0xffffu) * (kTwo24 * a.scale_log2);
         const float kz = (float)__builtin_bit_cast(f16x2, kmt).y;
-        float dlo[GQ], dhi[GQ];
+        float dk[GQ];
         if constexpr (KB == 8) {
             const uint32_t w[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
-            kdots_k8<GQ>(w, qr, q0, dlo);
+            kdots_k8<GQ>(w, qr, q0, dk);
         } else {
             const uint4 kk = tk ? k1 : k0;
             const uint32_t w[4] = {kk.x, kk.y, kk.z, kk.w};
-            kdots_k4<GQ>(w, qr, q0, dlo, dhi);
+            kdots_k4<GQ>(w, qr, qr16, q0, dk);
         }
         float part[4 * NS];
 #pragma unroll
         for (int hh = 0; hh < 4 * NS; ++hh) {
             if (hh < GQ) {
-                const float d = KB == 8 ? dlo[hh] : fmaf(dhi[hh], 0.0625f, dlo[hh]);
-                part[hh] = fmaf(kz, qsum[hh], ks * d);
+                part[hh] = fmaf(kz, qsum[hh], ks * dk[hh]);
             } else {
                 part[hh] = 0.f;
             }
@@ -1706,7 +1717,7 @@ __global__ __launch_bounds__(kSigWaves * kWave) void attn_significance(SigArgs a
     // q pairs as in run_segment: lane k of a row holds its group's pair k
     // (dims d, d+4), pair 0 whole in every lane, the group's sum
     const int qm = (lane & 15) >> 2, qa = lane & 3;
-    uint32_t qr[GQ];
+    uint32_t qr[GQ], qr16[GQ];
     half2_t q0[GQ];
     float qsum[GQ];
     constexpr uint32_t kOnes = 0x3C003C00u;
@@ -1716,6 +1727,7 @@ __global__ __launch_bounds__(kSigWaves * kWave) void attn_significance(SigArgs a
         const uint32_t* qd = reinterpret_cast<const uint32_t*>(a.q + ((long long)b * a.Hq + h * GQ + hh) * kD + grp * kG);
         const int o = 4 * qm + ((qa & 2) ? 1 : 0);
         qr[hh] = __builtin_amdgcn_perm(qd[o + 2], qd[o], sel);
+        qr16[hh] = q_by16(qr[hh]);
         q0[hh] = __builtin_bit_cast(half2_t, __builtin_amdgcn_perm(qd[2], qd[0], 0x05040100u));
         qsum[hh] = row_sum16(dot2(__builtin_bit_cast(half2_t, qr[hh]), kOnes, 0.f)) * a.scale_log2;  // times scale_log2
     }
@@ -1731,10 +1743,10 @@ __global__ __launch_bounds__(kSigWaves * kWave) void attn_significance(SigArgs a
         if ((unsigned long long)(unsigned)id >= (unsigned long long)a.num_pages) continue;  // never outside the pool
         uint8_t* pg = a.pool + (long long)id * LY::page_bytes;
         if (p < ph)
-            sig_page<GQ, LY::hi.kb, LY::hi.T>(a, pg, LY::page_bytes, LY::ohi, qr, q0, qsum, lse2, len_hi - p * LY::hi.T, N,
+            sig_page<GQ, LY::hi.kb, LY::hi.T>(a, pg, LY::page_bytes, LY::ohi, qr, qr16, q0, qsum, lse2, len_hi - p * LY::hi.T, N,
                                              lane);
         else
-            sig_page<GQ, LY::lo.kb, LY::lo.T>(a, pg, LY::page_bytes, LY::olo, qr, q0, qsum, lse2,
+            sig_page<GQ, LY::lo.kb, LY::lo.T>(a, pg, LY::page_bytes, LY::olo, qr, qr16, q0, qsum, lse2,
                                              len_lo - (p - ph) * LY::lo.T, N, lane);
     }
 }

@@ -622,8 +622,8 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
         constexpr float centre = 0.5f * (float)((1 << VB) - 1);
         const int tok = jl + 16 * tk;
         const bool by4 = VB == 2 && (tok & 1);
-        // s_v times the lane's code factor in one mixed-precision fma
-        const float vs_c = fmaf(vs, by4 ? 0.25f : 1.0f, 0.0f);
+        // s_v times the lane's code factor (2-bit values) in one mixed-precision fma
+        const float vs_c = VB == 2 ? fmaf(vs, by4 ? 0.25f : 1.0f, 0.0f) : vs;
         const float cc = by4 ? 4.f * centre : centre;
         const float zc = fmaf(centre, vs, vz);
         int pi, pos;

@@ -222,7 +222,7 @@ diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_c
  *        -- otherwise the balanced mode.
  *        -1 = balanced: the page lists of all tables, in table order, form one
  *        list of work units (a high page 3, a 32-token low page 6, a 16-token
- *        low page 3, a table's start 80) cut into one equal
+ *        low page 3, a table's start 50) cut into one equal
  *        share per resident workgroup; a table spread over several shares has
  *        their (max, sum, acc) states merged in page order (Sec. 6.2 sequence
  *        split).  S >= 1: each table is cut into min(S, pages) equal page

@@ -755,16 +755,20 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
 // is kHighUnits units of work and a low page kLowUnits: the page loops are
 // bound by VALU issue, and a 32-token low page issues twice the instructions
 // of a 16-token high page (both bytes per page being equal), a 16-token low
-// page about as many.  A table's first page also carries kSegUnits, the cost
-// of starting a segment (its query, page-ID and first-page loads, the waves'
-// merge, an arrival), so a balanced share that crosses a table boundary gets
-// fewer pages: page 0 starts at unit 0, page p > 0 at kSegUnits + kHighUnits*p
-// (p <= ph) or kSegUnits + kHighUnits*ph + kLowUnits*(p - ph).
+// page about as many.  A table's first page also carries `seg` units, the
+// cost of starting a segment (its query, page-ID and first-page loads, the
+// waves' merge, an arrival), so a balanced share that crosses a table boundary
+// gets fewer pages: page 0 starts at unit 0, page p > 0 at seg + hi*p
+// (p <= ph) or seg + hi*ph + lo*(p - ph).  Ranking tables by work and
+// splitting a paired workgroup's waves count a table's start as `seg_pair`
+// units instead (each measured best for its own use: the balanced shares with
+// 50, the pairs with 80).
 template <int LI>
 struct Units {
     static constexpr int hi = 3;
     static constexpr int lo = Lay<LI>::lo.T == 32 ? 6 : 3;
-    static constexpr int seg = 80;
+    static constexpr int seg = 50;
+    static constexpr int seg_pair = 80;
 };
 
 struct TableInfo {
@@ -791,6 +795,12 @@ __device__ __forceinline__ TableInfo table_info_of(const AttnArgs& a, int len_hi
     ti.np = ph + pl;
     ti.units = ti.np > 0 ? Units<LI>::seg + (long long)kHighUnits * ph + (long long)kLowUnits * pl : 0;
     return ti;
+}
+// A table's work as ranking and pairing count it (start cost seg_pair).
+template <int LI>
+__device__ __forceinline__ long long pair_units(const TableInfo& ti)
+{
+    return ti.np > 0 ? ti.units - Units<LI>::seg + Units<LI>::seg_pair : 0;
 }
 // t uniform: the section lengths come through scalar loads (the attention
 // kernels never write them), so everything derived from them stays scalar.
@@ -1324,7 +1334,7 @@ __device__ __forceinline__ void rank_tables(const AttnArgs& a, AttnShared<GQ, NW
         const int lane = threadIdx.x;
         const int t0 = lane * per, t1 = t0 + per < T ? t0 + per : T;
         int shift = 0;
-        while (((Units<LI>::lo * a.p_max + Units<LI>::seg) >> shift) >= kBins) ++shift;
+        while (((Units<LI>::lo * a.p_max + Units<LI>::seg_pair) >> shift) >= kBins) ++shift;
         int lh[kRankPer], ll[kRankPer], bin[kRankPer];
 #pragma unroll
         for (int i = 0; i < kRankPer; ++i) {
@@ -1340,7 +1350,7 @@ __device__ __forceinline__ void rank_tables(const AttnArgs& a, AttnShared<GQ, NW
         for (int i = 0; i < kRankPer; ++i) {
             bin[i] = -1;
             if (t0 + i < t1) {
-                const long long u = table_info_of<LI>(a, lh[i], ll[i]).units >> shift;
+                const long long u = pair_units<LI>(table_info_of<LI>(a, lh[i], ll[i])) >> shift;
                 bin[i] = kBins - 1 - (int)(u < kBins - 1 ? u : kBins - 1);  // bin 0 holds the longest
                 atomicAdd(&hist[bin[i]], 1);
             }
@@ -1581,7 +1591,7 @@ __global__ __launch_bounds__(kPairWaves * kWave, 1) void attn_pair(AttnArgs a)
     TableInfo ti[2];
     rank_tables<GQ, LI, NW, 2>(a, sh, &coef, T, rank, tab, ti);
     const bool two = rank[1] != rank[0];
-    const long long u0 = ti[0].units, u1 = two ? ti[1].units : 0;
+    const long long u0 = pair_units<LI>(ti[0]), u1 = two ? pair_units<LI>(ti[1]) : 0;
     // waves of the first table: of the two integer splits around NW * u0 /
     // (u0 + u1), the one with the smaller larger load per wave (u / waves), at
     // least one wave each
@@ -1603,7 +1613,7 @@ __global__ __launch_bounds__(kPairWaves * kWave, 1) void attn_pair(AttnArgs a)
     const TableInfo tiw = first ? ti[0] : ti[1];
     const int w0 = first ? 0 : n0, nw = first ? n0 : NW - n0;
     int done = 0;
-    const int target = (int)((tiw.units + nw - 1) / nw);
+    const int target = (int)((pair_units<LI>(tiw) + nw - 1) / nw);
     seg_pages<GQ, LI, NW>(a, sh, &coef, stage, tw, tiw, 0, tiw.np, w0, nw, done, target > 0 ? target : 1);
     __syncthreads();
     seg_merge<GQ, NW>(a, sh, tab[0], 0, n0, nullptr);

@@ -901,21 +901,8 @@ __device__ __forceinline__ void write_empty_one(const AttnArgs& a, int t, int gq
 // agent-scope accesses, so no cache-wide release or acquire (an L2 writeback
 // and invalidate per workgroup) is needed.
 //
-// An arrival word is a 44-bit call tag above a 20-bit count (n is at most
-// 65535 split ranges or the share count plus one), and a word whose tag is not
-// this call's counts as zero: the workspace needs no clearing, and what an
-// earlier call left there is never taken for this one's.  The tag is the
-// dispatch's packet index in its hardware queue (32 bits) with 12 bits of the
-// queue's address (queues count their packets separately).
-extern "C" __device__ unsigned long long dkv_dispatch_id() __asm("llvm.amdgcn.dispatch.id");
-
-__device__ __forceinline__ unsigned long long call_tag()
-{
-    const unsigned long long q = (unsigned long long)(size_t)__builtin_amdgcn_queue_ptr();
-    return (dkv_dispatch_id() & 0xffffffffull) | ((((q >> 12) ^ (q >> 24)) & 0xfffull) << 32);
-}
-
-constexpr int kArriveCountBits = 20;
+// The arrival words (call_tag, arrive_count) count at most 65535 split ranges
+// or the share count plus one per table.
 
 __device__ __forceinline__ void put_part(float* p, float v)
 {
@@ -948,31 +935,7 @@ __device__ __forceinline__ bool arrive_last(const AttnArgs& a, AttnShared<GQ, NW
 {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's partial stores are done
     __syncthreads();
-    if (threadIdx.x == 0) {
-        unsigned long long* w = a.arrive + t;
-        const unsigned long long tag = sh.tag;
-        constexpr unsigned long long kCount = (1ull << kArriveCountBits) - 1;
-        // One add counts this arrival when the word already carries this
-        // call's tag (every arrival but, normally, a table's first).  An add
-        // that lands on another call's word counts nothing: the word is then
-        // taken over by compare-and-swap (tag, 1), or, once another arrival
-        // has done that, counted in by compare-and-swap as well.
-        unsigned long long old = __hip_atomic_fetch_add(w, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        unsigned long long cnt;
-        if ((old >> kArriveCountBits) == tag) {
-            cnt = old & kCount;
-        } else {
-            old += 1;
-            for (;;) {
-                cnt = (old >> kArriveCountBits) == tag ? (old & kCount) : 0ull;
-                const unsigned long long nw = (tag << kArriveCountBits) | (cnt + 1);
-                if (__hip_atomic_compare_exchange_strong(w, &old, nw, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT))
-                    break;
-            }
-        }
-        sh.last = cnt + 1 == (unsigned long long)n;
-    }
+    if (threadIdx.x == 0) sh.last = arrive_count(a.arrive + t, sh.tag) == (unsigned long long)n;
     __syncthreads();
     return __builtin_amdgcn_readfirstlane(sh.last) != 0;
 }

@@ -67,6 +67,7 @@ struct CallFlags {
     int32_t njobs;      // quantize jobs (append)
     int64_t head_old;   // ring head before this call
     int64_t tail_old;   // ring tail before this call
+    unsigned long long arrive;  // arrival word of the one-token append (arrive_claim, arrive_count)
 };
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
@@ -183,6 +184,71 @@ __device__ __forceinline__ TInt block_excl_scan(TInt x, TInt* lds, TInt* total, 
     *total = read_lane<TInt>(tinc, nw - 1);
     __syncthreads();
     return below + inc - x;
+}
+
+// ---- arrival words --------------------------------------------------------
+// Workgroups of one launch that must find out which of them comes last count
+// themselves in a 64-bit word of the caller's workspace: a 44-bit call tag
+// above a 20-bit count.  A word whose tag is not this call's counts as zero,
+// so the workspace needs no clearing and what an earlier call left there is
+// never taken for this one's.  The tag is the dispatch's packet index in its
+// hardware queue (32 bits) with 12 bits of the queue's address (queues count
+// their packets separately).
+extern "C" __device__ unsigned long long dkv_dispatch_id() __asm("llvm.amdgcn.dispatch.id");
+
+__device__ __forceinline__ unsigned long long call_tag()
+{
+    const unsigned long long q = (unsigned long long)(size_t)__builtin_amdgcn_queue_ptr();
+    return (dkv_dispatch_id() & 0xffffffffull) | ((((q >> 12) ^ (q >> 24)) & 0xfffull) << 32);
+}
+
+constexpr int kArriveCountBits = 20;
+
+// The count before this arrival once the add that returned `old` has landed on
+// another call's word (where it counts nothing): the word is taken over by
+// compare-and-swap (tag, 1), or, once another arrival has done that, counted in
+// by compare-and-swap as well.
+__device__ __forceinline__ unsigned long long arrive_takeover(unsigned long long* w, unsigned long long old,
+                                                              unsigned long long tag)
+{
+    constexpr unsigned long long kCount = (1ull << kArriveCountBits) - 1;
+    unsigned long long cnt;
+    old += 1;
+    for (;;) {
+        cnt = (old >> kArriveCountBits) == tag ? (old & kCount) : 0ull;
+        const unsigned long long nw = (tag << kArriveCountBits) | (cnt + 1);
+        if (__hip_atomic_compare_exchange_strong(w, &old, nw, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT))
+            return cnt;
+    }
+}
+
+// Count one arrival of the call tagged `tag` in word w (agent-scope atomics);
+// returns the count including it (1 .. 2^20 - 1).  One add counts the arrival
+// when the word already carries this call's tag (every arrival but, normally,
+// the first); otherwise arrive_takeover.
+__device__ __forceinline__ unsigned long long arrive_count(unsigned long long* w, unsigned long long tag)
+{
+    constexpr unsigned long long kCount = (1ull << kArriveCountBits) - 1;
+    const unsigned long long old = __hip_atomic_fetch_add(w, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return ((old >> kArriveCountBits) == tag ? (old & kCount) : arrive_takeover(w, old, tag)) + 1;
+}
+
+// Put this call's tag on word w with count 0 unless it already carries it.
+// Done by one workgroup as a call starts, long before the arrivals of a word
+// that many workgroups share: they then find the tag and count with one add
+// each instead of taking the word over together (one compare-and-swap retry
+// per concurrent arrival).  An arrival that still comes first takes the word
+// over itself (arrive_takeover), and the claim never replaces a word that
+// already carries the tag, so no counted arrival is lost.
+__device__ __forceinline__ void arrive_claim(unsigned long long* w, unsigned long long tag)
+{
+    unsigned long long old = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    while ((old >> kArriveCountBits) != tag) {
+        if (__hip_atomic_compare_exchange_strong(w, &old, tag << kArriveCountBits, __ATOMIC_RELAXED,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+            break;
+    }
 }
 
 // Block-wide sum of a true 64-bit value and OR of flag bits (all threads get

@@ -13,6 +13,9 @@
 //                    all take (table, section, page) jobs: resolve the page ID
 //                    (new pages from the table's ring region), quantize each
 //                    token's 32-dim groups and write the page.
+//   append_one       a call of at most one new token per sequence (a decode
+//                    step) in one launch: classes, plan and page jobs, the
+//                    state written by the last workgroup to finish.
 // Allocation alone (alloc_plan + alloc_write) and compaction (compact_count,
 // compact_apply) follow the same planning/coordination split:
 // per-table work is fully parallel, one prefix sum gives every table a
@@ -352,6 +355,9 @@ __device__ __forceinline__ long long plan_word(const TablePlan& tp)  // new page
 struct JobDesc {
     int t, sec, p, u0, u1, lold, n, tslot;
     long long ring_idx;  // ring position of a new page, -1 for a page already held
+    // one-token append: the sequence's row offset and length before the call
+    // come with the job (no classify results); otherwise `one` is 0
+    int one, off_b, sold;
 };
 
 // Job `job` of table t (its plan tp, its exclusive prefix pre = new pages |
@@ -374,6 +380,9 @@ __device__ __forceinline__ void describe_job(JobDesc& d, int t, const TState& s,
     d.n = s.n;
     d.tslot = sec ? P - 1 - p : p;
     d.ring_idx = p < s.pold[sec] ? -1 : head_old + (pre & 0xffffffffll) + (sec ? tp.need[0] : 0) + (p - s.pold[sec]);
+    d.one = 0;
+    d.off_b = 0;
+    d.sold = 0;
 }
 
 // One page job: resolve the page ID (a new page from the table's ring region),
@@ -415,7 +424,9 @@ __device__ __forceinline__ void commit_job_fmt(const AppendArgs& a, const JobDes
     // this wave's tokens u0 + wave + kQuantWaves*i, all loaded up front; token
     // u of the section is row ord[u - lold] (high, rank order) or
     // ord[n - 1 - (u - lold)] (low ranks are stored from the back)
-    const int off_b = a.row_off[b];
+    const bool one = __builtin_amdgcn_readfirstlane(s_job.one) != 0;  // the job's one token is row 0 of its sequence
+    const int off_b = one ? __builtin_amdgcn_readfirstlane(s_job.off_b) : a.row_off[b];
+    const int sold = one ? __builtin_amdgcn_readfirstlane(s_job.sold) : a.sold[b];
     const int32_t* ord = a.ord + (long long)off_b * H + (long long)h * n;
     int jj[kTokLoad];
     uint32_t kx[kTokLoad], vx[kTokLoad];
@@ -423,7 +434,7 @@ __device__ __forceinline__ void commit_job_fmt(const AppendArgs& a, const JobDes
     for (int i = 0; i < kTokLoad; ++i) {
         const int u = u0 + wave + i * kQuantWaves;
         const int r = (u < u1 ? u : u0) - lold;
-        jj[i] = sec ? ord[n - 1 - r] : ord[r];
+        jj[i] = one ? 0 : (sec ? ord[n - 1 - r] : ord[r]);
     }
 #pragma unroll
     for (int i = 0; i < kTokLoad; ++i) {
@@ -509,7 +520,7 @@ __device__ __forceinline__ void commit_job_fmt(const AppendArgs& a, const JobDes
             }
             if (lane == 0) {
                 reinterpret_cast<float*>(pg + a.off_score[sec])[sl] = a.score[row];
-                reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[sl] = a.sold[b] + jj[pass * kTokIlp + i];
+                reinterpret_cast<int32_t*>(pg + a.off_pos[sec])[sl] = sold + jj[pass * kTokIlp + i];
             }
         }
     }
@@ -751,6 +762,177 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit_planned(AppendAr
         commit_job(a, s_job, s_rows);
         if (job + (int)gridDim.x < njobs) __syncthreads();  // s_job and s_rows are reused by the next job
     }
+}
+
+// ---------------------------------------------------------------------------
+// append_one: the whole append of a call in which every sequence takes at most
+// one new token (max_new <= 1) over at most kAppendPlanTables tables -- a
+// decode step -- in one launch, one workgroup per table.  One token needs no
+// selection: inside the recent window it is high; in the quota form it is
+// high when the high quota (clamped to the one token) is 1, else low when the
+// low quota is; in the threshold form its score is compared with alpha / N as
+// in append_classify.  So every workgroup derives every table's class, the
+// plan (page demand, one prefix sum over tables) and the all-or-nothing
+// verdict from the state before the call, then does its own table's page job
+// (at most one: one token lies on one page).  No workgroup writes what another
+// reads: the state after the call (lengths, pages, seq_len, ring head) is
+// written by the workgroup that arrives last (arrive_count), after every
+// workgroup has read the state before the call.
+// ---------------------------------------------------------------------------
+constexpr int kOnePer = (kAppendPlanTables + kCommitThreads - 1) / kCommitThreads;  // tables per thread
+
+inline bool append_one_call(const AppendArgs& a) { return a.max_new <= 1 && !append_planned(a.B, a.Hkv); }
+
+__global__ __launch_bounds__(kCommitThreads) void append_one(AppendArgs a)
+{
+    const int tid = threadIdx.x;
+    const int H = a.Hkv, B = a.B, NT = B * H, P = a.p_max;
+    __shared__ long long s_scan[kCommitThreads / kWave];
+    __shared__ uint32_t s_bits[kCommitThreads / kWave];
+    __shared__ JobDesc s_job;
+    __shared__ uint32_t s_rows[kQuantWaves][kWave][kRowWords];
+    __shared__ int s_off[kAppendPlanTables];  // row offset of each sequence (new tokens of the lower ones)
+    __shared__ int s_job_here, s_last;
+    const unsigned long long tag = call_tag();
+    if (blockIdx.x == 0 && tid == 0) arrive_claim(&a.flags->arrive, tag);  // before any arrival, as a rule
+    const long long head_old = a.ring_ptr[0], tail_old = a.ring_ptr[1];
+    if (tid == 0) s_job_here = 0;
+
+    // ---- row offsets; each thread a run of sequences (B <= NT <= kAppendPlanTables)
+    const int pb = (B + kCommitThreads - 1) / kCommitThreads;
+    const int b0 = tid * pb;
+    int nb[kOnePer];
+    long long nsum = 0;
+    uint32_t bad = 0;
+#pragma unroll
+    for (int i = 0; i < kOnePer; ++i) {
+        nb[i] = 0;
+        if (i < pb && b0 + i < B) {
+            const int v = a.new_len[b0 + i];
+            if (v < 0 || v > a.max_new) bad = 1;
+            nb[i] = v < 0 ? 0 : (v > 1 ? 1 : v);
+            nsum += nb[i];
+        }
+    }
+    long long ntot;
+    uint32_t any_bad;
+    long long off = block_excl_scan<long long>(nsum, s_scan, &ntot, bad, s_bits, &any_bad);
+#pragma unroll
+    for (int i = 0; i < kOnePer; ++i) {
+        if (i < pb && b0 + i < B) {
+            s_off[b0 + i] = (int)off;
+            off += nb[i];
+        }
+    }
+    __syncthreads();
+    // every count in [0, max_new] and their sum total_new: the classify
+    // kernel's per-sequence row checks, taken for the whole call
+    const bool bad_call = any_bad != 0 || ntot != a.total_new;
+
+    // ---- classes and plans of every table; each thread a run of tables
+    const int pt = (NT + kCommitThreads - 1) / kCommitThreads;
+    const int t0 = tid * pt;
+    const bool quota = a.quota != nullptr;
+    TState st[kOnePer];
+    long long packed = 0;
+    uint32_t bits = 0;
+#pragma unroll
+    for (int i = 0; i < kOnePer; ++i) {
+        TState& s = st[i];
+        s.cnt[0] = s.cnt[1] = 0;
+        s.lold[0] = s.lold[1] = s.pold[0] = s.pold[1] = 0;
+        s.ring_off = 0;
+        s.n = 0;
+        const int t = t0 + i;
+        if (i < pt && t < NT) {
+            const int b = t / H, h = t - b * H;
+            const int v = a.new_len[b];
+            const int n = v < 0 ? 0 : (v > 1 ? 1 : v);
+            s.n = n;
+            s.lold[0] = a.len[2 * t];
+            s.lold[1] = a.len[2 * t + 1];
+            s.pold[0] = a.pages[2 * t];
+            s.pold[1] = a.pages[2 * t + 1];
+            if (n == 1 && !bad_call) {  // (a bad call's row offsets may lie past total_new)
+                if (a.window >= 1) {
+                    s.cnt[0] = 1;
+                } else if (quota) {
+                    const int q0 = a.quota[2 * t], q1 = a.quota[2 * t + 1];
+                    const int nh = q0 < 0 ? 0 : (q0 > 1 ? 1 : q0);
+                    const int nl = q1 < 0 ? 0 : (q1 > 1 - nh ? 1 - nh : q1);
+                    s.cnt[0] = nh;
+                    s.cnt[1] = nl;
+                } else {
+                    const float sc = a.score[(long long)s_off[b] * H + h];
+                    const float N = (float)(a.seq_len[b] + n);
+                    const float thr_h = a.alpha_h / N, thr_l = a.alpha_l / N;
+                    const bool a0 = sc >= thr_h;
+                    const bool a1 = a0 || sc >= thr_l;
+                    s.cnt[0] = a0 ? 1 : 0;
+                    s.cnt[1] = (a1 && !a0) ? 1 : 0;
+                }
+            }
+            const TablePlan tp = table_plan(s, P, a.tsh);
+            if (tp.held_over) bits |= DIFFKV_ST_TABLE_OVERFLOW;
+            packed += plan_word(tp);
+        }
+    }
+    long long tot;
+    uint32_t all_bits;
+    const long long before = block_excl_scan<long long>(packed, s_scan, &tot, bits, s_bits, &all_bits);
+    bits = all_bits & DIFFKV_ST_TABLE_OVERFLOW;
+    const long long total_need = tot & 0xffffffffll;
+    if (bad_call) bits = DIFFKV_ST_BAD_INPUT;
+    else if (total_need > tail_old - head_old) bits |= DIFFKV_ST_OUT_OF_PAGES;
+    if (bits) {  // all or nothing: no state, table or page changes
+        if (blockIdx.x == 0 && tid == 0) atomicOr(a.status, bits);
+        return;
+    }
+
+    // ---- this workgroup's table: its page job, if its token is kept
+    {
+        long long pre = before;
+#pragma unroll
+        for (int i = 0; i < kOnePer; ++i) {
+            const int t = t0 + i;
+            if (i < pt && t < NT) {
+                const TablePlan tp = table_plan(st[i], P, a.tsh);
+                if (t == (int)blockIdx.x && tp.jobs[0] + tp.jobs[1] > 0) {
+                    describe_job(s_job, t, st[i], tp, pre, (int)(pre >> 32), P, head_old, a.tsh);
+                    const int b = t / H;
+                    s_job.one = 1;
+                    s_job.off_b = s_off[b];
+                    s_job.sold = a.seq_len[b];
+                    s_job_here = 1;
+                }
+                pre += plan_word(tp);
+            }
+        }
+    }
+    __syncthreads();
+    if (s_job_here) commit_job(a, s_job, s_rows);
+
+    // ---- the workgroup arriving last writes the state after the call
+    __syncthreads();
+    if (tid == 0) s_last = arrive_count(&a.flags->arrive, tag) == (unsigned long long)gridDim.x;
+    __syncthreads();
+    if (!s_last) return;
+#pragma unroll
+    for (int i = 0; i < kOnePer; ++i) {
+        const int t = t0 + i;
+        if (i < pt && t < NT) {
+            const TablePlan tp = table_plan(st[i], P, a.tsh);
+#pragma unroll
+            for (int sec = 0; sec < 2; ++sec) {
+                a.len[2 * t + sec] = st[i].lold[sec] + st[i].cnt[sec];
+                a.pages[2 * t + sec] = st[i].pold[sec] + tp.need[sec];
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kOnePer; ++i)  // no other workgroup writes seq_len: this is still the length before the call
+        if (i < pb && b0 + i < B) a.seq_len[b0 + i] = a.seq_len[b0 + i] + nb[i];
+    if (tid == 0) a.ring_ptr[0] = head_old + total_need;
 }
 
 // ---------------------------------------------------------------------------
@@ -1001,6 +1183,7 @@ __global__ __launch_bounds__(kWave) void compact_apply(CompactArgs a)
 // ---------------------------------------------------------------------------
 hipError_t launch_append(const AppendArgs& a, int grid_quant, hipStream_t st)
 {
+    if (append_one_call(a)) return launch1(append_one, (unsigned)(a.Hkv * a.B), kCommitThreads, st, a);
     hipError_t e = launch1(append_classify, (unsigned)(a.Hkv * a.B), kClsThreads, st, a);
     if (e != hipSuccess) return e;
     if (append_planned(a.B, a.Hkv)) {

@@ -106,6 +106,151 @@ def test_append_decode_steps_into_partial_pages():
     assert_state_equal(dc, oc, what="decode end")
 
 
+def test_append_one_token_steps_every_form():
+    """Steps of at most one new token per sequence (one launch: every workgroup
+    classes every table's token, plans, does its own table's page job; the state
+    is written by the last workgroup to finish): quota form with quotas clamped
+    to the one token, threshold form around alpha / N, the recent window, and
+    sequences without a token, bit for bit against the oracle after every step."""
+    w = inputs.prefill("llama8b", B=5, L=(20, 70))
+    B, Hkv = w["B"], w["Hkv"]
+    Lo, Ld, oc, dc = _pair(300, B, Hkv, 160, seed=21)
+    _append_both(oc, dc, w["new_len"], w["k"], w["v"], w["score"], quota=w["quota"])
+    assert_state_equal(dc, oc, what="prefill")
+    rng = np.random.default_rng(22)
+    for step in range(32):
+        nl = (rng.random(B) < 0.7).astype(np.int32)
+        n = int(nl.sum())
+        k = (rng.standard_normal((n, Hkv, 128)) * 2).astype(np.float16).view(np.uint16)
+        v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+        score = (rng.random((n, Hkv)) * 0.04).astype(np.float32)
+        form = step % 4
+        if form == 0:
+            kw = dict(quota=rng.integers(0, 3, (B, Hkv, 2)).astype(np.int32))
+        elif form == 1:  # thresholds alpha / N around the scores (N ~ 50-110)
+            kw = dict(alpha_h=float(rng.uniform(0.5, 2.5)), alpha_l=float(rng.uniform(0.1, 0.8)))
+        elif form == 2:
+            kw = dict(quota=np.zeros((B, Hkv, 2), np.int32), window=int(rng.integers(1, 4)))
+        else:
+            kw = dict(alpha_h=float(rng.uniform(0.5, 2.5)), alpha_l=0.0, window=int(rng.integers(0, 2)))
+        print("case: one-token step %d, form %d, %d tokens" % (step, form, n), flush=True)
+        _append_both(oc, dc, nl, k, v, score, **kw)
+        assert_state_equal(dc, oc, what="one-token step %d" % step)
+
+
+def test_append_one_token_refusals():
+    """The one-launch step's all-or-nothing refusals: out of pages, a table past
+    p_max, and bad counts (above max_new, a sum other than total_new, negative),
+    each leaving every state byte as it was; an empty step changes nothing."""
+    from gpu_util import snapshot
+    rng = np.random.default_rng(23)
+    B, Hkv = 2, 2
+
+    def kv(n):
+        return (rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16),
+                rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16),
+                rng.random((n, Hkv)).astype(np.float32))
+
+    print("case: one-token step out of pages", flush=True)
+    Lo, Ld, oc, dc = _pair(4, B, Hkv, 64, seed=24)  # four pages: one full high page per table
+    k, v, sc = kv(32)
+    _append_both(oc, dc, np.array([16, 16], np.int32), k, v, sc, quota=np.full((B, Hkv, 2), [16, 0], np.int32))
+    assert_state_equal(dc, oc, what="full pool")
+    k, v, sc = kv(2)
+    _append_both(oc, dc, np.array([1, 1], np.int32), k, v, sc, quota=np.full((B, Hkv, 2), [1, 0], np.int32))
+    s = assert_state_equal(dc, oc, what="one-token oop")
+    assert s["status"][0] == dk.ST_OUT_OF_PAGES
+
+    print("case: one-token step past p_max", flush=True)
+    Lo, Ld, oc, dc = _pair(64, B, Hkv, 32, seed=25)
+    full = 16 * Lo.p_max
+    k, v, sc = kv(2 * full)
+    _append_both(oc, dc, np.array([full, full], np.int32), k, v, sc,
+                 quota=np.full((B, Hkv, 2), [full, 0], np.int32))
+    assert_state_equal(dc, oc, what="full tables")
+    k, v, sc = kv(1)
+    _append_both(oc, dc, np.array([1, 0], np.int32), k, v, sc, quota=np.full((B, Hkv, 2), [1, 0], np.int32))
+    s = assert_state_equal(dc, oc, what="one-token overflow")
+    assert s["status"][0] == dk.ST_TABLE_OVERFLOW
+
+    for what, nl, total in (("a count above max_new", [2, 0], 2), ("counts summing past total_new", [1, 1], 1),
+                            ("a negative count", [-1, 1], 0)):
+        print("case: one-token step, %s" % what, flush=True)
+        Lo, Ld, oc, dc = _pair(64, B, Hkv, 64, seed=26)
+        before = snapshot(dc)
+        k, v, sc = kv(max(total, 1))
+        dk.quantize_append(dc, t(np.array(nl, np.int32)), t(k), t(v), t(sc),
+                           quota=t(np.full((B, Hkv, 2), [1, 0], np.int32)), total_new=total, max_new=1)
+        after = snapshot(dc)
+        assert after["status"][0] == dk.ST_BAD_INPUT, what
+        for f in ("table", "pages", "len", "seq_len", "ring", "ring_ptr", "pool"):
+            assert np.array_equal(after[f], before[f]), (what, f)
+
+    print("case: empty one-token step", flush=True)
+    Lo, Ld, oc, dc = _pair(64, B, Hkv, 64, seed=27)
+    k, v, sc = kv(20)
+    _append_both(oc, dc, np.array([7, 3], np.int32), k, v, sc, quota=np.full((B, Hkv, 2), [4, 3], np.int32))
+    k, v, sc = kv(0)
+    _append_both(oc, dc, np.array([0, 0], np.int32), k, v, sc, quota=np.full((B, Hkv, 2), [1, 0], np.int32))
+    s = assert_state_equal(dc, oc, what="empty step")
+    assert s["status"][0] == 0
+
+
+def test_append_one_token_workspace_contents():
+    """The one-launch step counts its workgroups in an arrival word of the caller's
+    workspace (call tag above a 20-bit count).  Whatever that word holds beforehand
+    -- zero, a small count under tag 0, another call's tag, a count about to carry
+    into the tag -- every step is bit-exact against the oracle (the last workgroup
+    to arrive, and only it, writes the state after the call)."""
+    w = inputs.prefill("llama8b", B=24, L=(10, 60))
+    B, Hkv = w["B"], w["Hkv"]
+    Lo, Ld, oc, dc = _pair(1200, B, Hkv, 128, seed=31)
+    _append_both(oc, dc, w["new_len"], w["k"], w["v"], w["score"], quota=w["quota"])
+    need = dk.workspace_size(dk.OP_APPEND, Ld, B, 0, Hkv, B)
+    ws = torch.empty((max(need, 256) + 7) // 8, dtype=torch.int64, device=DEV)
+    rng = np.random.default_rng(32)
+    word = 3  # the arrival word: bytes 24..31 of the call flags at the workspace's start
+    for i, fill in enumerate([0, 5, (1 << 20) - 1, 0x123456789 << 20, (0xabcdef << 20) | ((1 << 20) - 2), -1, 7]):
+        ws.fill_(int(rng.integers(0, 1 << 62)))
+        ws[word] = fill
+        nl = (rng.random(B) < 0.8).astype(np.int32)
+        n = int(nl.sum())
+        k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+        v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+        sc = rng.random((n, Hkv)).astype(np.float32)
+        quota = rng.integers(0, 2, (B, Hkv, 2)).astype(np.int32)
+        print("case: one-token step, arrival word %#x" % (fill & ((1 << 64) - 1)), flush=True)
+        orc.quantize_append(oc, nl, k, v, sc, quota=quota)
+        dk.quantize_append(dc, t(nl), t(k), t(v), t(sc), quota=t(quota), total_new=n, max_new=1, ws=ws)
+        assert_state_equal(dc, oc, what="arrival word case %d" % i)
+
+
+def test_append_one_token_at_the_table_limit():
+    """1024 tables (the most a one-launch step takes; more plan in their own launch):
+    a prompt, then four one-token steps with some sequences idle, bit for bit."""
+    B, Hkv = 128, 8
+    rng = np.random.default_rng(28)
+    Lo, Ld, oc, dc = _pair(8 * B * Hkv, B, Hkv, 96, seed=29, garbage=False)
+    nl = rng.integers(0, 40, B).astype(np.int32)
+    n = int(nl.sum())
+    k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+    sc = rng.random((n, Hkv)).astype(np.float32)
+    quota = np.stack([(nl[:, None] * rng.uniform(0, 0.6, (B, Hkv))).astype(np.int32),
+                      (nl[:, None] * rng.uniform(0, 0.4, (B, Hkv))).astype(np.int32)], axis=2)
+    print("case: 1024-table prompt", flush=True)
+    _append_both(oc, dc, nl, k, v, sc, quota=quota)
+    for step in range(4):
+        nl = (rng.random(B) < 0.9).astype(np.int32)
+        n = int(nl.sum())
+        k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+        v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
+        sc = rng.random((n, Hkv)).astype(np.float32)
+        print("case: 1024-table one-token step %d" % step, flush=True)
+        _append_both(oc, dc, nl, k, v, sc, quota=rng.integers(0, 2, (B, Hkv, 2)).astype(np.int32))
+        assert_state_equal(dc, oc, what="1024 tables, step %d" % step)
+
+
 def test_append_all_or_nothing_on_device():
     rng = np.random.default_rng(14)
     B, Hkv = 2, 2

@@ -108,9 +108,9 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64, help="timed decode steps (per pass)")
-    ap.add_argument("--warmup", type=int, default=64,
-                    help="untimed decode steps first (after only 8, the next 64 back-to-back steps "
-                         "measured about 13 us per step slower than later ones)")
+    ap.add_argument("--warmup", type=int, default=320,
+                    help="untimed decode steps first: back-to-back steps reach their steady time only "
+                         "after ~25 ms of them (64 warmup steps: 110 us per long32k step; 320: 97-99 us)")
     ap.add_argument("--config", choices=("long32k", "llama70b", "llama8b"), default="long32k",
                     help="headline decode workload")
     ap.add_argument("--splits", type=int, default=0,

@@ -135,7 +135,6 @@ def test_the_model_catches_a_dropped_tag_check():
         w.v = (old + 1) & M64
         yield
         return (old & MASK) + 1
-    rng = random.Random(9)
     w = Word((123 << CB) | 5)
     tag = 456
     gens = [bad_count(w, tag) for _ in range(3)]

@@ -192,7 +192,9 @@ diffkv_status diffkv_workspace_size(int32_t op, const diffkv_layout* layout,
  *   after the demands of all lower tables, high pages first; head advances
  *   by the total.  Raises OUT_OF_PAGES / TABLE_OVERFLOW all-or-nothing.
  * Updates pool, page_table, pages, len, seq_len (+= new_len), ring_ptr[0].
- * Workspace: diffkv_workspace_size(DIFFKV_OP_APPEND, ...).
+ * Workspace: diffkv_workspace_size(DIFFKV_OP_APPEND, ...); it needs no
+ * clearing between calls.  A call with max_new <= 1 over at most 1024 tables
+ * (a decode step) runs as one launch.
  */
 diffkv_status diffkv_quantize_append(const diffkv_layout* layout, const diffkv_cache* cache,
                                      int64_t total_new, int32_t max_new,

@@ -777,7 +777,9 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit_planned(AppendAr
 // (at most one: one token lies on one page).  No workgroup writes what another
 // reads: the state after the call (lengths, pages, seq_len, ring head) is
 // written by the workgroup that arrives last (arrive_count), after every
-// workgroup has read the state before the call.
+// workgroup has read the state before the call.  Workgroup 0 claims the
+// arrival word with the call's tag as it starts (arrive_claim), so the
+// arrivals, all at about the same time, count with one add each.
 // ---------------------------------------------------------------------------
 constexpr int kOnePer = (kAppendPlanTables + kCommitThreads - 1) / kCommitThreads;  // tables per thread
 

@@ -149,7 +149,6 @@ __device__ __forceinline__ uint32_t kand(uint32_t v, uint32_t mask)
     asm volatile("v_and_b32 %0, %2, %1" : "=v"(x) : "v"(v), "s"(mask));
     return x;
 }
-__device__ __forceinline__ void kzero(float& c) { asm volatile("v_mov_b32 %0, 0" : "=v"(c)); }
 // The next code pair's v_perm / v_and and the first head's dot in one asm
 // statement (the compiler pads between separate asm statements).
 template <int L>

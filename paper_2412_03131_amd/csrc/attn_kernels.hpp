@@ -522,7 +522,18 @@ __device__ __forceinline__ void do_page(WaveState<GQ>& st, const PageRaw& r, con
             }
         }
 #pragma unroll
-        for (int s = 0; s < NS; ++s) lg[tk][s] = slot_sum<GQ>(s, part);
+        for (int s = 0; s < NS; ++s) {
+            if (lone_slot<GQ>(s)) {
+                // a lone head's row sum through the wave's exchange area: one
+                // write, one read and three adds instead of two copies, two
+                // swaps and two adds (same order: (r0 + r1) + (r2 + r3))
+                px[(jl + 16 * tk) * 4 + (lane >> 4)] = part[4 * s];
+                const f32x4 v = *reinterpret_cast<const lds_f4*>(px + (jl + 16 * tk) * 4);
+                lg[tk][s] = (v.x + v.y) + (v.z + v.w);
+            } else {
+                lg[tk][s] = slot_sum<GQ>(s, part);
+            }
+        }
     }
     // tokens past the section's end (only on its last page: a uniform branch,
     // kept a branch by the empty asm, which the compiler does not speculate)

@@ -68,7 +68,9 @@ struct CallFlags {
     int64_t head_old;   // ring head before this call
     int64_t tail_old;   // ring tail before this call
     unsigned long long arrive;  // arrival word of the one-token append (arrive_claim, arrive_count)
+    unsigned long long arrive_group[16];  // its first level: one word per group of workgroups
 };
+static_assert(sizeof(CallFlags) <= 256, "call flags fit the 256 B every workspace reserves for them");
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 

@@ -776,12 +776,14 @@ __global__ __launch_bounds__(kCommitThreads) void append_commit_planned(AppendAr
 // verdict from the state before the call, then does its own table's page job
 // (at most one: one token lies on one page).  No workgroup writes what another
 // reads: the state after the call (lengths, pages, seq_len, ring head) is
-// written by the workgroup that arrives last (arrive_count), after every
-// workgroup has read the state before the call.  Workgroup 0 claims the
-// arrival word with the call's tag as it starts (arrive_claim), so the
-// arrivals, all at about the same time, count with one add each.
+// written by the workgroup that arrives last (arrive_count, on two levels of
+// words), after every workgroup has read the state before the call.
+// Workgroup 0 claims the arrival words with the call's tag as it starts
+// (arrive_claim), so the arrivals, all at about the same time, count with one
+// add each.
 // ---------------------------------------------------------------------------
 constexpr int kOnePer = (kAppendPlanTables + kCommitThreads - 1) / kCommitThreads;  // tables per thread
+constexpr int kOneGroups = 16;  // first-level arrival words
 
 inline bool append_one_call(const AppendArgs& a) { return a.max_new <= 1 && !append_planned(a.B, a.Hkv); }
 
@@ -796,7 +798,8 @@ __global__ __launch_bounds__(kCommitThreads) void append_one(AppendArgs a)
     __shared__ int s_off[kAppendPlanTables];  // row offset of each sequence (new tokens of the lower ones)
     __shared__ int s_job_here, s_last;
     const unsigned long long tag = call_tag();
-    if (blockIdx.x == 0 && tid == 0) arrive_claim(&a.flags->arrive, tag);  // before any arrival, as a rule
+    if (blockIdx.x == 0 && tid <= kOneGroups)  // before any arrival, as a rule
+        arrive_claim(tid < kOneGroups ? &a.flags->arrive_group[tid] : &a.flags->arrive, tag);
     const long long head_old = a.ring_ptr[0], tail_old = a.ring_ptr[1];
     if (tid == 0) s_job_here = 0;
 
@@ -916,7 +919,17 @@ __global__ __launch_bounds__(kCommitThreads) void append_one(AppendArgs a)
 
     // ---- the workgroup arriving last writes the state after the call
     __syncthreads();
-    if (tid == 0) s_last = arrive_count(&a.flags->arrive, tag) == (unsigned long long)gridDim.x;
+    if (tid == 0) {
+        // two levels, so that no word takes more than a few dozen concurrent
+        // adds: workgroup j counts in group j % kOneGroups, the last of a
+        // group in the top word
+        const int ng = NT < kOneGroups ? NT : kOneGroups, g = (int)blockIdx.x % kOneGroups;
+        const unsigned long long gsize = NT / kOneGroups + (g < NT % kOneGroups ? 1 : 0);
+        bool last = false;
+        if (arrive_count(&a.flags->arrive_group[g], tag) == gsize)
+            last = arrive_count(&a.flags->arrive, tag) == (unsigned long long)ng;
+        s_last = last;
+    }
     __syncthreads();
     if (!s_last) return;
 #pragma unroll

@@ -165,6 +165,53 @@ def to_dev(torch, dev, a):
     return torch.from_numpy(a).to(dev)
 
 
+class HipEvent:
+    """A HIP timing event recorded on the launch stream without system-scope fences
+    (hipEventDisableSystemFence).  An event of the default kind (what torch.cuda.Event
+    creates) records with a system-scope release and acquire; measured on MI355X, each
+    such record delays the next launch on the stream by 5.7 us, against 4.4 us for
+    this kind (the marker itself), and that delay falls inside the timed interval.
+    The stream stays in order: the record still waits for the work before it.  Same
+    interface as torch.cuda.Event: record(), elapsed_time(end) in ms."""
+    hip = None
+    stream = None
+
+    @classmethod
+    def setup(cls, stream_ptr):
+        """Bind to the HIP runtime that torch loaded (the one libdiffkv.so links to) and
+        to the stream the library launches on; call after torch has initialised HIP."""
+        path = None
+        with open("/proc/self/maps") as f:
+            for line in f:
+                if "libamdhip64.so" in line:
+                    path = line.split()[-1]
+                    break
+        if path is None:
+            raise RuntimeError("the HIP runtime is not loaded")
+        cls.hip = C.CDLL(path)
+        cls.hip.hipEventCreateWithFlags.argtypes = [C.POINTER(C.c_void_p), C.c_uint]
+        cls.hip.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+        cls.hip.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        cls.stream = stream_ptr
+
+    def __init__(self):
+        self.e = C.c_void_p()
+        self._check(self.hip.hipEventCreateWithFlags(C.byref(self.e), 0x20000000), "create")
+
+    @staticmethod
+    def _check(rc, what):
+        if rc != 0:
+            raise RuntimeError("hipEvent %s failed (%d)" % (what, rc))
+
+    def record(self):
+        self._check(self.hip.hipEventRecord(self.e, self.stream), "record")
+
+    def elapsed_time(self, end):
+        ms = C.c_float()
+        self._check(self.hip.hipEventElapsedTime(C.byref(ms), self.e, end.e), "elapsed time")
+        return ms.value
+
+
 class Flush:
     """Evicts the Infinity Cache and the L2s with clean lines: a reduction that reads
     1 GiB.  (A fill kernel would leave dirty lines whose write-back then lands inside
@@ -238,7 +285,7 @@ def decode_headline(torch, dk, lib, dev, sptr, wl, args, flush):
     # warm-up: W - F attention calls on the cache as the prompt left it (they bring
     # the GPU to its steady clock without growing the cache), then F full steps
     F = min(W, 8)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(2 * K)]  # passes 2, 3
+    ev = [[HipEvent() for _ in range(3)] for _ in range(2 * K)]  # passes 2, 3
 
     def step(s, e=None):
         if e is not None:
@@ -332,7 +379,7 @@ def attention_modes(torch, dk, lib, dev, sptr, wl, reps, flush, modes=(1, 0, -1)
                 ws.numel(), sptr)
         for _ in range(5):
             lib.diffkv_decode_attention(*args)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        ev = [(HipEvent(), HipEvent()) for _ in range(reps)]
         rc = 0
         for e in ev:
             flush()
@@ -375,8 +422,8 @@ def significance_bench(torch, dk, lib, dev, sptr, wl, flush, reps=30):
     att = (C.byref(L), C.byref(cs), Hq, C.c_void_p(q.data_ptr()), float(SCALE), C.c_void_p(out.data_ptr()),
            C.c_void_p(lse.data_ptr()), 0, C.c_void_p(ws.data_ptr()), ws.numel(), sptr)
     upd = (C.byref(L), C.byref(cs), Hq, C.c_void_p(q.data_ptr()), float(SCALE), C.c_void_p(lse.data_ptr()), sptr)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
-    ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+    ev = [[HipEvent() for _ in range(3)] for _ in range(reps)]
+    ev2 = [[HipEvent() for _ in range(2)] for _ in range(reps)]
     rc = 0
     for _ in range(3):
         rc |= lib.diffkv_decode_attention(*att)
@@ -436,7 +483,7 @@ def prompt_significance_bench(torch, dk, lib, dev, sptr, reps=5):
                                                     ws.numel(), sptr)
     rc = call(None) | call(None)
     # (the normalizers passed in are zeros: their values do not change the work)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    ev = [[HipEvent() for _ in range(3)] for _ in range(reps)]
     for e in ev:
         e[0].record()
         rc |= call(None)
@@ -503,7 +550,7 @@ def precision_bench(torch, dk, lib, dev, sptr, flush, B=64, Hq=32, Hkv=8, L=2048
                 C.c_void_p(out.data_ptr()), C.c_void_p(lse.data_ptr()), 0, C.c_void_p(ws.data_ptr()), ws.numel(), sptr)
         for _ in range(3):
             lib.diffkv_decode_attention(*args)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        ev = [(HipEvent(), HipEvent()) for _ in range(reps)]
         rc = 0
         for e in ev:
             flush()
@@ -610,7 +657,7 @@ def serving_step(torch, dk, lib, dev, sptr, args):
     comp_args = [(Lp, C.byref(call_struct), NL * B * Hkv, vp(m), vp(ws_c), ws_c.numel(), sptr)
                  for m in masks]
     seq_rows = [torch.arange(r, NL * B, B, device=dev) for r in range(B)]
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    ev = [[HipEvent() for _ in range(4)] for _ in range(K)]
 
     def run_step(s, e=None):
         si = steps_in[s]
@@ -704,6 +751,7 @@ def main():
     lib = dk.lib()
     stream = torch.cuda.current_stream()
     sptr = C.c_void_p(stream.cuda_stream)
+    HipEvent.setup(sptr)
     if args.only == "generation":
         generation_bench(torch, dk, lib, dev, sptr, args.generation_steps)
         return
@@ -779,7 +827,8 @@ def main():
             "traffic": measured_traffic(args.config),
             "bytes_per_launch": head["bytes_per_launch"],
             "us_per_launch": head["us_per_launch"],
-            "timing": "HIP events on the launch stream around each step's attention call, Infinity "
+            "timing": "HIP events (no system-scope fences) on the launch stream around each step's "
+                      "attention call, Infinity "
                       "Cache and L2 evicted before every step (outside the events); mean over K "
                       "steps run right after the back-to-back timed steps, which carry no events",
         },
@@ -816,7 +865,7 @@ def compaction_bench(torch, dk, lib, dev, sptr, rounds):
     cs = c.struct()
     Lp = C.byref(L)
     live = int(demand.sum())
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(rounds)]
+    ev = [[HipEvent() for _ in range(3)] for _ in range(rounds)]
     before = torch.empty_like(c.pages)
     lost = torch.empty_like(c.pages)
     torch.cuda.synchronize()
@@ -914,7 +963,7 @@ def memory_management_bench(torch, dk, lib, dev, sptr, batches=(8, 32, 128), ste
         ws_a = torch.empty(dk.workspace_size(dk.OP_ALLOC, L, B, 0, H), dtype=torch.uint8, device=dev)
         cs = c.struct()
         Lp = C.byref(L)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        ev = [(HipEvent(), HipEvent()) for _ in range(steps)]
         torch.cuda.synchronize()
         torch.cuda._sleep(int(2.4e9 * 1e-4 * steps) + 1)   # the host enqueues ahead of the GPU
         rc = 0
@@ -989,7 +1038,7 @@ def generation_bench(torch, dk, lib, dev, sptr, steps, window=64):
         app.append((Lp, C.byref(cs), B, 1, vp(ones), vp(t[0]), vp(t[1]), vp(t[2]), vp(t[3]),
                     0.0, 0.0, window, vp(ws_a), ws_a.numel(), sptr))
     gen = (Lp, C.byref(cs), C.c_float(1.0), C.c_float(0.5), window, vp(ws_g), ws_g.numel(), sptr)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    ev = [(HipEvent(), HipEvent())
           for _ in range(steps)]
     torch.cuda.synchronize()
     lens0, pages0 = c.len.cpu().numpy().copy(), c.pages.cpu().numpy().copy()

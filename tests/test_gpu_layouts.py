@@ -109,6 +109,39 @@ def test_layout_append_attention_significance(name):
     assert e.value.code == dk.E_UNSUPPORTED
 
 
+@pytest.mark.parametrize("name", ["K8V4-K4V2"] + list(LAYOUTS))
+def test_layout_append_planned(name):
+    """Every layout on the path for more than 1024 tables (the plan in a launch of its
+    own, then page jobs of fewer waves each): two long prompts among short ones, then
+    decode steps into either section, bit-exact against the oracle."""
+    kw = LAYOUTS.get(name, dict(k_bits=(8, 4), v_bits=(4, 2), tokens_per_page=(16, 32)))
+    rng = np.random.default_rng(300 + len(name))
+    B, Hkv = 130, 8
+    new_len = rng.integers(0, 30, B).astype(np.int32)
+    new_len[[5, 77]] = [700, 333]
+    Lo, Ld = layouts(max_seq_len=760, **kw)
+    npages = 6000
+    oc = orc.Cache(Lo, npages, B, Hkv, ring=rng.permutation(npages))
+    oc.pool[:] = rng.integers(0, 256, oc.pool.shape, dtype=np.uint8)
+    dc = dev_cache_from_oracle(Ld, oc)
+    print("case: layout %s, planned prompt append, %d tables" % (name, B * Hkv), flush=True)
+    k, v, score, quota = _prompt(rng, B, Hkv, new_len)
+    _append_both(oc, dc, new_len, k, v, score, quota)
+    assert oc.status[0] == 0
+    assert_state_equal(dc, oc, what="%s planned prompt" % name)
+    for step in range(3):
+        nl = (rng.random(B) < 0.9).astype(np.int32)
+        m = int(nl.sum())
+        kd = rng.standard_normal((m, Hkv, 128)).astype(np.float16).view(np.uint16)
+        vd = rng.standard_normal((m, Hkv, 128)).astype(np.float16).view(np.uint16)
+        sd = rng.random((m, Hkv)).astype(np.float32)
+        qa = np.where(rng.random((B, Hkv, 1)) < 0.5, [[1, 0]], [[0, 1]]).astype(np.int32)
+        print("case: layout %s, planned decode step %d" % (name, step), flush=True)
+        _append_both(oc, dc, nl, kd, vd, sd, qa)
+        assert oc.status[0] == 0
+        assert_state_equal(dc, oc, what="%s planned step %d" % (name, step))
+
+
 def test_unsupported_layouts_are_refused():
     for kw in (dict(k_bits=(8, 8), v_bits=(8, 8), tokens_per_page=(16, 16)),
                dict(k_bits=(4, 4), v_bits=(4, 2), tokens_per_page=(16, 32)),

@@ -225,11 +225,13 @@ def test_append_one_token_workspace_contents():
         assert_state_equal(dc, oc, what="arrival word case %d" % i)
 
 
-@pytest.mark.parametrize("B,Hkv", [(128, 8), (1024, 1)])
+@pytest.mark.parametrize("B,Hkv", [(128, 8), (1024, 1), (5, 3), (17, 1), (11, 3)])
 def test_append_one_token_at_the_table_limit(B, Hkv):
     """1024 tables (the most a one-launch step takes; more plan in their own launch):
     a prompt, then four one-token steps with some sequences idle, bit for bit; with
-    one KV head, every thread of the step's workgroups counts four sequences."""
+    one KV head, every thread of the step's workgroups counts four sequences.  15, 17
+    and 33 tables: the step's first-level arrival groups (16 of them, workgroup b in
+    group b mod 16) are unevenly filled or partly empty."""
     rng = np.random.default_rng(28)
     Lo, Ld, oc, dc = _pair(8 * B * Hkv, B, Hkv, 96, seed=29, garbage=False)
     nl = rng.integers(0, 40, B).astype(np.int32)
@@ -239,7 +241,7 @@ def test_append_one_token_at_the_table_limit(B, Hkv):
     sc = rng.random((n, Hkv)).astype(np.float32)
     quota = np.stack([(nl[:, None] * rng.uniform(0, 0.6, (B, Hkv))).astype(np.int32),
                       (nl[:, None] * rng.uniform(0, 0.4, (B, Hkv))).astype(np.int32)], axis=2)
-    print("case: 1024-table prompt, B %d, Hkv %d" % (B, Hkv), flush=True)
+    print("case: %d-table prompt, B %d, Hkv %d" % (B * Hkv, B, Hkv), flush=True)
     _append_both(oc, dc, nl, k, v, sc, quota=quota)
     for step in range(4):
         nl = (rng.random(B) < 0.9).astype(np.int32)
@@ -247,12 +249,12 @@ def test_append_one_token_at_the_table_limit(B, Hkv):
         k = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
         v = rng.standard_normal((n, Hkv, 128)).astype(np.float16).view(np.uint16)
         sc = rng.random((n, Hkv)).astype(np.float32)
-        print("case: 1024-table one-token step %d" % step, flush=True)
+        print("case: %d-table one-token step %d" % (B * Hkv, step), flush=True)
         if step % 2 == 0:
             _append_both(oc, dc, nl, k, v, sc, quota=rng.integers(0, 2, (B, Hkv, 2)).astype(np.int32))
         else:  # threshold form: the scores are read at the row offsets the step computes
             _append_both(oc, dc, nl, k, v, sc, alpha_h=20.0, alpha_l=5.0)
-        assert_state_equal(dc, oc, what="1024 tables, step %d" % step)
+        assert_state_equal(dc, oc, what="%d tables, step %d" % (B * Hkv, step))
 
 
 def test_append_all_or_nothing_on_device():
